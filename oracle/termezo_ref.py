@@ -1,0 +1,365 @@
+"""TerMeZO CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain, slow, obviously-correct statement of the TerMeZO sparse zeroth-order
+step (Algorithm 1 with K = 1 and the full-precision parameters theta frozen),
+composed from the C primitives in ``termezo_oracle.c``.  Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
+this module.  It shares no code with the HIP library.
+
+Step by step (paper section in brackets):
+  * thresholds tau^l = 0.5 (gamma^l + delta), gamma^l = mean |w^l|   [Sec. 3, eq. quant]
+  * distances d_i = min(|w_i - tau|, |w_i + tau|)                    [eq. distance]
+  * S_0 = the rho_0 fraction of all latents with the smallest d,
+    xi_0 the largest selected distance                               [eq. selection_init]
+  * perturbed evaluation at w +/- eps m (.) z, with z regenerated from
+    the seed, requantised with the perturbed layer's own threshold    [Algorithm 1]
+  * BitLinear: per-token absmax int8 activations x ternary codes     [Sec. 1, Sec. 3]
+  * g = (F+ - F-) / (2 eps); w <- w - lr g m (.) z                   [eq. spsa, Algorithm 1]
+  * S_{t+1} = {i in S_t : d_i(w_{t+1}) <= xi_0}                      [eq. selection_]
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+OK, ERR_INVALID, ERR_STATE, ERR_NUMERIC = 0, 1, 2, 5
+
+
+def lib():
+    """Load (building on first use if absent) the C oracle library."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build_oracle  # type: ignore
+        build_oracle.build()
+    L = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i64, u64, u32, f32, i32 = (ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint32,
+                               ctypes.c_float, ctypes.c_int)
+    sig = {
+        "orc_philox4x32_10": (None, [P, P, P]),
+        "orc_ln": (f32, [f32]),
+        "orc_ln_array": (None, [P, i64, P]),
+        "orc_sincos_turn24": (None, [u32, P, P]),
+        "orc_sincos_turn24_array": (None, [P, i64, P, P]),
+        "orc_gauss_one": (f32, [u64, u32, u64]),
+        "orc_gauss": (None, [u64, u32, P, i64, P]),
+        "orc_gauss_range": (None, [u64, u32, i64, i64, P]),
+        "orc_fix_abs": (i64, [f32]),
+        "orc_layer_abs_sum": (i32, [P, i64, P]),
+        "orc_threshold": (None, [i64, i64, f32, P, P]),
+        "orc_quantize": (None, [P, i64, f32, P]),
+        "orc_distance": (None, [P, i64, f32, P]),
+        "orc_select": (i32, [P, i64, i64, i32, P, i64, P, P]),
+        "orc_perturbed_layer": (None, [P, i64, P, i64, i64, u64, f32, i32, P]),
+        "orc_act_quant": (None, [P, i64, i64, P, P]),
+        "orc_bitlinear": (None, [P, P, P, f32, i64, i64, i64, P, P]),
+        "orc_bf16_round_array": (None, [P, i64, P]),
+        "orc_update_layer": (None, [P, P, i64, i64, u64, f32, f32, i32]),
+        "orc_shrink_layer": (i64, [P, P, i64, f32, f32]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _p(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+# --------------------------------------------------------------------------
+# Generator primitives
+# --------------------------------------------------------------------------
+def philox4x32_10(ctr: Sequence[int], key: Sequence[int]) -> Tuple[int, int, int, int]:
+    c = (ctypes.c_uint32 * 4)(*[int(v) & 0xFFFFFFFF for v in ctr])
+    k = (ctypes.c_uint32 * 2)(*[int(v) & 0xFFFFFFFF for v in key])
+    o = (ctypes.c_uint32 * 4)()
+    lib().orc_philox4x32_10(c, k, o)
+    return tuple(int(v) for v in o)  # type: ignore
+
+
+def ln(x: np.ndarray) -> np.ndarray:
+    x = _f32(x)
+    y = np.empty_like(x)
+    lib().orc_ln_array(_p(x), x.size, _p(y))
+    return y
+
+
+def sincos_turn24(j: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    j = np.ascontiguousarray(j, dtype=np.uint32)
+    s = np.empty(j.shape, np.float32)
+    c = np.empty(j.shape, np.float32)
+    lib().orc_sincos_turn24_array(_p(j), j.size, _p(s), _p(c))
+    return s, c
+
+
+def gauss(seed: int, gids, stream: int = 0) -> np.ndarray:
+    """z_i for the given global ids (fp32), regenerated from (seed, stream)."""
+    g = _i64(gids)
+    z = np.empty(g.shape, np.float32)
+    lib().orc_gauss(seed & (2**64 - 1), stream, _p(g), g.size, _p(z))
+    return z
+
+
+def gauss_range(seed: int, gid0: int, n: int, stream: int = 0) -> np.ndarray:
+    z = np.empty(n, np.float32)
+    lib().orc_gauss_range(seed & (2**64 - 1), stream, gid0, n, _p(z))
+    return z
+
+
+# --------------------------------------------------------------------------
+# Quantiser primitives (Sec. 3)
+# --------------------------------------------------------------------------
+def layer_abs_sum(w: np.ndarray) -> int:
+    """Exact S = sum floor(|w| 2^36); raises on |w| >= 4 or non-finite."""
+    w = _f32(w).ravel()
+    out = ctypes.c_int64()
+    rc = lib().orc_layer_abs_sum(_p(w), w.size, ctypes.byref(out))
+    if rc != OK:
+        raise FloatingPointError("latent out of the fixed-point range (|w| >= 4 or non-finite)")
+    return int(out.value)
+
+
+def threshold(S: int, n: int, delta: float) -> Tuple[float, float]:
+    """(tau, beta) as fp32 from the exact sum S of a layer with n weights."""
+    tau = ctypes.c_float()
+    beta = ctypes.c_float()
+    lib().orc_threshold(int(S), int(n), float(delta), ctypes.byref(tau), ctypes.byref(beta))
+    return float(np.float32(tau.value)), float(np.float32(beta.value))
+
+
+def quantize(w: np.ndarray, tau: float) -> np.ndarray:
+    w = _f32(w)
+    c = np.empty(w.shape, np.int8)
+    lib().orc_quantize(_p(w), w.size, float(tau), _p(c))
+    return c
+
+
+def distance(w: np.ndarray, tau: float) -> np.ndarray:
+    w = _f32(w)
+    d = np.empty(w.shape, np.float32)
+    lib().orc_distance(_p(w), w.size, float(tau), _p(d))
+    return d
+
+
+def select(d_all: np.ndarray, k: int, inclusive: bool = False) -> Tuple[np.ndarray, float]:
+    """Sorted gids of the k smallest (d, gid) pairs, and xi0 (the k-th d)."""
+    d_all = _f32(d_all).ravel()
+    cap = d_all.size
+    out = np.empty(cap, np.int64)
+    n = ctypes.c_int64()
+    xi = ctypes.c_float()
+    rc = lib().orc_select(_p(d_all), d_all.size, int(k), int(bool(inclusive)), _p(out), cap,
+                          ctypes.byref(n), ctypes.byref(xi))
+    if rc != OK:
+        raise ValueError(f"selection failed (status {rc})")
+    return out[: n.value].copy(), float(np.float32(xi.value))
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    x = _f32(x)
+    y = np.empty_like(x)
+    lib().orc_bf16_round_array(_p(x), x.size, _p(y))
+    return y
+
+
+# --------------------------------------------------------------------------
+# BitLinear (8-bit activations x ternary weights)
+# --------------------------------------------------------------------------
+def act_quant(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    x = _f32(x)
+    M, K = x.shape
+    xq = np.empty((M, K), np.int8)
+    s = np.empty(M, np.float32)
+    lib().orc_act_quant(_p(x), M, K, _p(xq), _p(s))
+    return xq, s
+
+
+def bitlinear(xq: np.ndarray, s: np.ndarray, codes: np.ndarray, beta: float,
+              want_acc: bool = True) -> Tuple[Optional[np.ndarray], np.ndarray]:
+    """Plain triple loop: acc = x_q c^T (int32), y = acc * (beta / s_m)."""
+    xq = np.ascontiguousarray(xq, np.int8)
+    s = _f32(s)
+    codes = np.ascontiguousarray(codes, np.int8)
+    M, K = xq.shape
+    N = codes.shape[0]
+    assert codes.shape[1] == K
+    acc = np.empty((M, N), np.int32) if want_acc else None
+    y = np.empty((M, N), np.float32)
+    lib().orc_bitlinear(_p(xq), _p(s), _p(codes), float(beta), M, K, N,
+                        _p(acc) if acc is not None else None, _p(y))
+    return acc, y
+
+
+def bitlinear_matmul(xq: np.ndarray, s: np.ndarray, codes: np.ndarray, beta: float):
+    """Same result as ``bitlinear`` with the integer contraction done by a
+    library fp32 matmul.  Exact: every term is an integer of magnitude <= 128
+    and every partial sum is bounded by 128 K < 2^24 for K < 131072, so all
+    fp32 additions (in any order, with or without fma) are exact."""
+    M, K = xq.shape
+    assert K < 131072
+    accf = np.matmul(xq.astype(np.float32), codes.astype(np.float32).T)
+    acc = accf.astype(np.int32)
+    r = (np.float32(beta) / _f32(s)).astype(np.float32)
+    y = (acc.astype(np.float32) * r[:, None]).astype(np.float32)
+    return acc, y
+
+
+def mse(y: np.ndarray, target: np.ndarray) -> float:
+    """Config-1 loss: e = y - t and e^2 in fp32, the mean accumulated in fp64."""
+    e = (_f32(y) - _f32(target)).astype(np.float32)
+    e2 = (e * e).astype(np.float32)
+    return float(np.float32(np.sum(e2.astype(np.float64)) / e2.size))
+
+
+def projected_grad(f_plus: float, f_minus: float, eps: float) -> float:
+    """g = (F+ - F-) / (2 eps) in fp32 (eq. spsa, Algorithm 1)."""
+    fp, fm, e = np.float32(f_plus), np.float32(f_minus), np.float32(eps)
+    return float(np.float32(np.float32(fp - fm) / np.float32(np.float32(2.0) * e)))
+
+
+# --------------------------------------------------------------------------
+# Algorithm-1 state
+# --------------------------------------------------------------------------
+@dataclass
+class Layer:
+    d_out: int
+    d_in: int
+
+    @property
+    def n(self) -> int:
+        return self.d_out * self.d_in
+
+
+@dataclass
+class TerMeZOOracle:
+    """Latent weights of the ternary projections and the TerMeZO state.
+
+    ``w`` holds every latent in global-id order as fp32 (bf16 latents are held
+    widened, and updates round back to bf16)."""
+    layers: List[Layer]
+    w: np.ndarray
+    bf16: bool = False
+    delta: float = 1e-5
+    offsets: np.ndarray = field(init=False)
+    S: List[int] = field(init=False)          # exact fixed-point |w| sums (clean)
+    tau: List[float] = field(init=False)
+    beta: List[float] = field(init=False)
+    active: List[np.ndarray] = field(init=False)  # ascending local indices per layer
+    xi0: Optional[float] = None
+    k0: int = 0
+    last_seed: Optional[int] = None
+    last_eps: Optional[float] = None
+
+    def __post_init__(self):
+        self.w = _f32(self.w).ravel().copy()
+        sizes = [l.n for l in self.layers]
+        self.offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+        assert self.offsets[-1] == self.w.size
+        if self.bf16:
+            assert np.array_equal(bf16_round(self.w), self.w), "bf16 latents must be bf16 values"
+        self.active = [np.empty(0, np.int64) for _ in self.layers]
+        self._refresh_thresholds()
+
+    # -- helpers ----------------------------------------------------------
+    @property
+    def D(self) -> int:
+        return int(self.offsets[-1])
+
+    def layer_w(self, l: int) -> np.ndarray:
+        return self.w[self.offsets[l]: self.offsets[l + 1]]
+
+    def _refresh_thresholds(self):
+        self.S, self.tau, self.beta = [], [], []
+        for l, L in enumerate(self.layers):
+            S = layer_abs_sum(self.layer_w(l))
+            tau, beta = threshold(S, L.n, self.delta)
+            self.S.append(S)
+            self.tau.append(tau)
+            self.beta.append(beta)
+
+    def clean_codes(self, l: int) -> np.ndarray:
+        L = self.layers[l]
+        return quantize(self.layer_w(l), self.tau[l]).reshape(L.d_out, L.d_in)
+
+    @property
+    def k(self) -> int:
+        return int(sum(a.size for a in self.active))
+
+    # -- eq. selection_init --------------------------------------------------
+    def build_mask(self, rho0: float, inclusive: bool = False) -> Tuple[int, float]:
+        self._refresh_thresholds()
+        d_all = np.concatenate([distance(self.layer_w(l), self.tau[l])
+                                for l in range(len(self.layers))])
+        k0 = int(np.floor(np.float64(np.float32(rho0)) * np.float64(self.D)))
+        if k0 <= 0:
+            raise ValueError("rho0 * D rounds down to an empty mask")
+        gids, xi0 = select(d_all, k0, inclusive)
+        self.active = []
+        for l in range(len(self.layers)):
+            lo, hi = self.offsets[l], self.offsets[l + 1]
+            sel = gids[(gids >= lo) & (gids < hi)] - lo
+            self.active.append(sel.astype(np.int64))
+        self.xi0, self.k0 = xi0, int(gids.size)
+        return self.k0, xi0
+
+    # -- Algorithm 1: perturbed evaluation ----------------------------------
+    def perturbed_layer(self, l: int, seed: int, eps: float, sign: int) -> np.ndarray:
+        L = self.layers[l]
+        w = self.layer_w(l)
+        out = np.empty_like(w)
+        act = _i64(self.active[l])
+        lib().orc_perturbed_layer(_p(w), w.size, _p(act), act.size, int(self.offsets[l]),
+                                  seed & (2**64 - 1), float(eps), int(sign), _p(out))
+        return out
+
+    def perturb(self, seed: int, eps: float, sign: int):
+        """Codes, tau' and beta' of every layer at w + sign eps m (.) z(seed)."""
+        codes, taus, betas = [], [], []
+        for l, L in enumerate(self.layers):
+            wp = self.perturbed_layer(l, seed, eps, sign)
+            S = layer_abs_sum(wp)
+            tau, beta = threshold(S, L.n, self.delta)
+            codes.append(quantize(wp, tau).reshape(L.d_out, L.d_in))
+            taus.append(tau)
+            betas.append(beta)
+        self.last_seed, self.last_eps = seed, eps
+        return codes, taus, betas
+
+    # -- Algorithm 1: update, then eq. selection_ ---------------------------
+    def update(self, g: float, lr: float) -> int:
+        assert self.last_seed is not None, "update needs a preceding perturbation"
+        for l in range(len(self.layers)):
+            w = self.layer_w(l)
+            act = _i64(self.active[l])
+            lib().orc_update_layer(_p(w), _p(act), act.size, int(self.offsets[l]),
+                                   self.last_seed & (2**64 - 1), float(lr), float(g),
+                                   int(self.bf16))
+        self._refresh_thresholds()
+        for l in range(len(self.layers)):
+            act = _i64(self.active[l]).copy()
+            n = lib().orc_shrink_layer(_p(self.layer_w(l)), _p(act), act.size,
+                                       float(self.tau[l]), float(self.xi0))
+            self.active[l] = act[:n].copy()
+        self.last_seed = None
+        return self.k
