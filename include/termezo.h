@@ -1,0 +1,181 @@
+/*
+ * termezo.h -- C ABI of the MI355X (gfx950) TerMeZO sparse zeroth-order step.
+ *
+ * TerMeZO (Sec. 3 and Algorithm 1 of the paper) fine-tunes the latent weights
+ * w of a BitNet model's ternary linear projections with two-point SPSA
+ * (eq. spsa), perturbing and updating only a mask of latents that lie close
+ * to the ternary quantiser's decision boundaries (eq. distance,
+ * eq. selection_init, eq. selection_).  This library holds the hot path of one
+ * step on one GPU: mask construction, seed-regenerated perturbation with
+ * absmean requantisation, BitLinear forward (per-token absmax int8 activations
+ * x ternary weights, int32 accumulation, rescale) and the masked update.
+ *
+ * Conventions shared by every call
+ *   - All functions return a termezo_status; no C++ exception crosses the ABI.
+ *     A call that fails validation changes no state; termezo_last_error()
+ *     returns a message for the last failure on a context.
+ *   - A context is not thread-safe.  All device work is ordered on the HIP
+ *     stream given at creation.  Only the calls that return host values
+ *     (build_mask, update with k_out, mse_loss, model_loss, sync and the
+ *     exports) wait for the stream; they also report a deferred NUMERIC error
+ *     raised by an earlier kernel on that context.
+ *   - Device pointers are plain device addresses of memory owned by the
+ *     caller (for example PyTorch tensors); host pointers are noted as such.
+ *   - Latent weights are BORROWED: the caller owns them and they must outlive
+ *     the context.  The library writes them only in termezo_update, and only
+ *     at the active indices.
+ *   - Global ids: layers are enumerated in registration order; inside a layer
+ *     the latent matrix is row-major [d_out][d_in]; gid = (sum of the sizes
+ *     of the earlier layers) + row * d_in + col.
+ *   - Gaussian directions z are regenerated from the 64-bit seed with
+ *     Philox4x32-10 (counter = (gid >> 2, stream 0)) and the Box-Muller
+ *     transform; they are never stored.
+ */
+#ifndef TERMEZO_H_
+#define TERMEZO_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TERMEZO_OK = 0,
+  TERMEZO_ERR_INVALID_ARG = 1, /* bad argument; nothing was done            */
+  TERMEZO_ERR_STATE = 2,       /* call not valid in the current state       */
+  TERMEZO_ERR_DEVICE = 3,      /* no usable HIP device / HIP runtime error  */
+  TERMEZO_ERR_OOM = 4,         /* device allocation failed                  */
+  TERMEZO_ERR_NUMERIC = 5      /* non-finite value or |w| >= 4 in a latent  */
+} termezo_status;
+
+typedef enum {
+  TERMEZO_F32 = 0,
+  TERMEZO_BF16 = 1,
+  TERMEZO_I8 = 2,
+  TERMEZO_I32 = 3
+} termezo_dtype;
+
+/* One ternary linear projection (Sec. 3: q, k, v, o and every MLP linear).
+ * latent: device pointer to d_out * d_in latent weights, row-major, 16-byte
+ * aligned, of the context's latent dtype.  d_in must be a multiple of 16 and
+ * d_out * d_in must not exceed 2^25 (the fixed-point |w| sum stays exact). */
+typedef struct {
+  void* latent;
+  int64_t d_out;
+  int64_t d_in;
+} termezo_layer;
+
+typedef struct termezo_ctx termezo_ctx;
+
+/* Register the latent weights of n_layers projections (latent_dtype F32 or
+ * BF16) and allocate the library-owned state: packed 2-bit ternary codes
+ * (d_out * d_in / 4 bytes per layer), per-layer thresholds and fixed-point
+ * sums, and mask storage.  hip_stream: a hipStream_t (NULL = default stream).
+ * Errors: INVALID_ARG (null pointers, n_layers <= 0, d_in % 16 != 0,
+ * misaligned latent, layer too large, bad dtype), DEVICE, OOM. */
+termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
+                              termezo_dtype latent_dtype, void* hip_stream,
+                              termezo_ctx** out);
+
+/* Free every library-owned buffer.  Never frees the latents.  NULL is a no-op. */
+void termezo_destroy(termezo_ctx* ctx);
+
+/* Message describing the last failure on ctx ("" if none).  Owned by ctx. */
+const char* termezo_last_error(const termezo_ctx* ctx);
+
+/* Initial mask (Sec. 3, eq. distance and eq. selection_init; Algorithm 1,
+ * first two statements).  Computes tau^l = 0.5 (mean|w^l| + delta) per layer,
+ * the distance d_i = min(|w_i - tau|, |w_i + tau|) of every latent, the global
+ * budget k0 = floor(rho0 * D) and xi0, the k0-th smallest distance over all
+ * layers (ties at xi0 broken by ascending gid; tie_inclusive != 0 keeps every
+ * distance <= xi0 instead).  Also sets the current codes to Q(w) (clean).
+ * k0_out, xi0_out: host pointers (nullable) receiving the mask size and xi0.
+ * Waits for the stream.  Rebuilding discards the previous mask.
+ * Errors: INVALID_ARG (rho0 not in (0, 1], delta <= 0 or not finite),
+ * STATE (k0 == 0), NUMERIC (a latent non-finite or |w| >= 4). */
+termezo_status termezo_build_mask(termezo_ctx* ctx, float rho0, float delta,
+                                  int32_t tie_inclusive, int64_t* k0_out,
+                                  float* xi0_out);
+
+/* Perturbed evaluation point (Algorithm 1: w +/- eps m (.) z).  Sets the
+ * current ternary codes and scales of every layer to the requantisation of
+ * w' = w + sign * eps * m (.) z(seed): w'_i = fma(sign * eps, z_i, w_i) on the
+ * active set, w'_i = w_i elsewhere; tau' and beta' = 2 tau' are recomputed from
+ * w' (the quantiser is applied on the fly to the perturbed latents, eq.
+ * objective).  The latents themselves are not modified.  sign = 0 gives the
+ * clean codes.  Records (seed, eps) for the following termezo_update.
+ * Errors: INVALID_ARG (sign not in {-1, 0, 1}; eps <= 0 or not finite),
+ * STATE (no mask).  A perturbed |w'| >= 4 raises a deferred NUMERIC. */
+termezo_status termezo_perturb(termezo_ctx* ctx, uint64_t seed, float eps,
+                               int32_t sign);
+
+/* BitLinear forward of one projection on its current codes (Sec. 1 and 3:
+ * ternary weights with 8-bit activations).  x: device [M][d_in] (F32 or BF16);
+ * y: device [M][d_out] (F32 or BF16).  Per token row m: a_m = max_k |x[m][k]|,
+ * s_m = 127 / max(a_m, 1e-5), x_q = clamp(round_half_even(x * s_m), -128, 127);
+ * acc[m][n] = sum_k x_q[m][k] * c[n][k] exactly in int32;
+ * y[m][n] = float(acc) * (beta' / s_m) (rounded to bf16 if y is BF16).
+ * xq_out [M][d_in] int8, xscale_out [M] fp32 (s_m), acc_out [M][d_out] int32:
+ * optional device outputs (nullable) for inspection.
+ * Errors: INVALID_ARG (layer out of range, M <= 0, bad dtype, null x or y),
+ * STATE (no current codes: before build_mask or after update). */
+termezo_status termezo_bitlinear_forward(termezo_ctx* ctx, int32_t layer,
+                                         const void* x, termezo_dtype x_dtype,
+                                         int64_t M, void* y, termezo_dtype y_dtype,
+                                         int8_t* xq_out, float* xscale_out,
+                                         int32_t* acc_out);
+
+/* Masked projected-gradient update (Algorithm 1, last loop, K = 1) followed by
+ * the shrink-only set update (eq. selection_).  With the seed of the last
+ * termezo_perturb: for every active i, w_i <- round(fma(-(lr * g), z_i, w_i))
+ * (round = to nearest-even bf16 for BF16 latents, identity for F32); unmasked
+ * latents are untouched.  Then tau^l is recomputed from the updated latents and
+ * the active set keeps only the i with d_i <= xi0 (order preserved).
+ * proj_grad is g = (F+ - F-) / (2 eps) (eq. spsa).  k_out: host pointer
+ * (nullable) receiving the new mask size; when non-NULL the call waits.
+ * Invalidates the current codes.  Errors: INVALID_ARG (g or lr not finite),
+ * STATE (no perturbation since the last update or mask build). */
+termezo_status termezo_update(termezo_ctx* ctx, float proj_grad, float lr,
+                              int64_t* k_out);
+
+/* ---- inspection and support calls (not part of the four hot-path calls) ---- */
+
+/* Wait for the context's stream; reports a deferred NUMERIC error. */
+termezo_status termezo_sync(termezo_ctx* ctx);
+
+/* Copy one layer's ascending active local indices (row * d_in + col) to the
+ * host buffer idx (capacity cap entries); *n receives the count.
+ * Errors: INVALID_ARG (layer range, null n, cap < count), STATE (no mask). */
+termezo_status termezo_mask_export(termezo_ctx* ctx, int32_t layer, uint32_t* idx,
+                                   int64_t cap, int64_t* n);
+
+/* Unpack one layer's current ternary codes to host int8 [d_out][d_in]. */
+termezo_status termezo_codes_export(termezo_ctx* ctx, int32_t layer, int8_t* codes);
+
+/* Host copies of one layer's clean (tau, beta, fixed-point sum) and current
+ * (tau', beta') scales; any pointer may be NULL. */
+termezo_status termezo_layer_stats(termezo_ctx* ctx, int32_t layer, float* tau,
+                                   float* beta, int64_t* abs_sum_fix,
+                                   float* tau_cur, float* beta_cur);
+
+/* Mean squared error of device fp32 y against device fp32 target over n
+ * elements: e = y - t and e*e in fp32, the sum in fp64, mean rounded to fp32.
+ * out: host pointer.  Waits for the stream. */
+termezo_status termezo_mse_loss(termezo_ctx* ctx, const float* y, const float* target,
+                                int64_t n, float* out);
+
+/* Gaussian directions z_i for n global ids (device uint64 gids, device fp32
+ * z), exactly as the perturbation and the update regenerate them from seed.
+ * hip_stream: a hipStream_t (NULL = default stream); no synchronisation. */
+termezo_status termezo_gauss(void* hip_stream, uint64_t seed, const uint64_t* gids, int64_t n,
+                             float* z);
+
+/* Number of active latents (host value; waits for the stream). */
+termezo_status termezo_active_count(termezo_ctx* ctx, int64_t* k);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TERMEZO_H_ */

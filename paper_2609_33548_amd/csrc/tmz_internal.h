@@ -1,0 +1,166 @@
+// Host-side internals shared by the TerMeZO library sources.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/termezo.h"
+
+namespace tmz {
+
+constexpr int kTile = 8192;          // elements per streaming tile (never straddles layers)
+constexpr int kBlock = 256;          // threads per block for streaming kernels
+constexpr int kHistBins = 2048;      // radix-select histogram width (11 bits)
+
+struct LayerHost {
+  void* w;
+  int64_t d_out, d_in, n, gid0;
+  int64_t code_off;                  // offset of the layer's packed codes, in 32-bit words
+  int64_t tile0, ntiles;             // tile range of the layer
+};
+
+// Device-side view of the registered layers and the per-layer state.
+struct DevState {
+  const void* const* w;              // [L] latent pointers
+  const int64_t* n;                  // [L]
+  const int64_t* gid0;               // [L]
+  const int64_t* code_off;           // [L]
+  const int32_t* tile_layer;         // [T]
+  const int64_t* tile_start;         // [T] layer-local start element
+  uint32_t* codes;                   // packed codes, all layers
+  int64_t* S_clean;                  // [L] fixed-point sum of |w|
+  int64_t* S_cur;                    // [L] fixed-point sum of |w'| of the current codes
+  float* tau;                        // [L] clean threshold
+  float* beta;                       // [L]
+  float* tau_cur;                    // [L] threshold of the current codes
+  float* beta_cur;                   // [L]
+  int32_t* err;                      // deferred numeric error flag
+  int32_t L;
+  int64_t T;                         // number of tiles
+};
+
+struct SelectState {                 // radix-select bookkeeping (device)
+  unsigned long long k0;             // budget
+  unsigned long long less;           // keys strictly below the current prefix bucket
+  uint32_t prefix;                   // key bits fixed so far
+  uint32_t pad;
+};
+
+}  // namespace tmz
+
+struct termezo_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  termezo_dtype dtype = TERMEZO_F32;
+  int32_t L = 0;
+  int64_t D = 0;
+  std::vector<tmz::LayerHost> layers;
+  std::vector<int64_t> tile_start_host;
+  int64_t T = 0;
+
+  // device buffers
+  void** d_wptr = nullptr;
+  int64_t* d_n = nullptr;
+  int64_t* d_gid0 = nullptr;
+  int64_t* d_code_off = nullptr;
+  int32_t* d_tile_layer = nullptr;
+  int64_t* d_tile_start = nullptr;
+  uint32_t* d_codes = nullptr;
+  int64_t* d_S_clean = nullptr;
+  int64_t* d_S_cur = nullptr;
+  float* d_tau = nullptr;
+  float* d_beta = nullptr;
+  float* d_tau_cur = nullptr;
+  float* d_beta_cur = nullptr;
+  int32_t* d_err = nullptr;
+
+  // mask
+  uint32_t* d_act = nullptr;         // active local indices, ascending, layer after layer
+  uint32_t* d_act_tmp = nullptr;     // compaction target
+  int64_t act_cap = 0;
+  int64_t* d_act_off = nullptr;      // [L+1]
+  int64_t* d_act_off_tmp = nullptr;  // [L+1]
+  std::vector<int64_t> h_act_off;    // host copy, valid when act_off_host_valid
+  bool act_off_host_valid = false;
+  float* d_wp = nullptr;             // perturbed values at the actives (act_cap)
+
+  // scratch
+  unsigned long long* d_hist = nullptr;      // kHistBins
+  tmz::SelectState* d_sel = nullptr;
+  uint32_t* d_tile_cnt = nullptr;            // 2 * T  (less, equal) per tile
+  int64_t* d_tile_out = nullptr;             // T      output offset per tile
+  int64_t* d_tile_eqb = nullptr;             // T      equal keys before the tile
+  int64_t* d_blk_cnt = nullptr;              // shrink block counts
+  int64_t blk_cap = 0;
+  double* d_loss = nullptr;                  // loss accumulators
+  int8_t* d_xq = nullptr;                    // activation-quantisation scratch
+  int64_t xq_cap = 0;
+  float* d_xs = nullptr;
+  int64_t xs_cap = 0;
+
+  // state
+  bool has_mask = false;
+  bool codes_valid = false;
+  bool pending_perturb = false;
+  uint64_t last_seed = 0;
+  float last_eps = 0.f;
+  float delta = 1e-5f;
+  float xi0 = 0.f;
+  int64_t k0 = 0;
+  int64_t k_bound = 0;               // upper bound of the active count (exact after a sync)
+  int tie_inclusive = 0;
+
+  std::string last_error;
+
+  tmz::DevState dev() const {
+    tmz::DevState s;
+    s.w = (const void* const*)d_wptr;
+    s.n = d_n;
+    s.gid0 = d_gid0;
+    s.code_off = d_code_off;
+    s.tile_layer = d_tile_layer;
+    s.tile_start = d_tile_start;
+    s.codes = d_codes;
+    s.S_clean = d_S_clean;
+    s.S_cur = d_S_cur;
+    s.tau = d_tau;
+    s.beta = d_beta;
+    s.tau_cur = d_tau_cur;
+    s.beta_cur = d_beta_cur;
+    s.err = d_err;
+    s.L = L;
+    s.T = T;
+    return s;
+  }
+};
+
+namespace tmz {
+
+// Launchers (stream-ordered, no synchronisation).  Return hipSuccess or the
+// launch error.
+hipError_t launch_abs_sum(termezo_ctx* c, int64_t* S_out);
+hipError_t launch_thresholds(termezo_ctx* c, const int64_t* S, float* tau, float* beta);
+hipError_t launch_fill_u64(unsigned long long* p, int64_t n, unsigned long long v, hipStream_t s);
+hipError_t launch_copy_i64(int64_t* dst, const int64_t* src, int64_t n, hipStream_t s);
+hipError_t launch_select(termezo_ctx* c, int64_t k0);     // three radix passes -> d_sel
+hipError_t launch_mask_compact_counts(termezo_ctx* c, int inclusive);  // -> act_off
+hipError_t launch_mask_compact_write(termezo_ctx* c, int inclusive);   // -> act
+hipError_t launch_requant_dense(termezo_ctx* c);          // codes of w with tau_cur
+hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se);
+hipError_t launch_patch_codes(termezo_ctx* c, int64_t k);
+hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed, float a);
+hipError_t launch_shrink(termezo_ctx* c, int64_t k);      // d_act -> d_act_tmp, offsets -> tmp
+hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);
+hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z, hipStream_t s);
+hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hipStream_t s);
+
+// BitLinear
+hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
+                            float* s, hipStream_t st);
+hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
+                                 const float* beta_dev, int64_t M, int64_t K, int64_t N,
+                                 void* y, termezo_dtype ydt, int32_t* acc, hipStream_t st);
+
+}  // namespace tmz

@@ -1,0 +1,464 @@
+// C ABI of the TerMeZO library: validation, buffer ownership, launch order.
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "tmz_internal.h"
+
+using namespace tmz;
+
+namespace {
+
+termezo_status fail(termezo_ctx* c, termezo_status st, const std::string& msg) {
+  if (c) c->last_error = msg;
+  return st;
+}
+
+termezo_status hip_fail(termezo_ctx* c, hipError_t e, const char* what) {
+  const termezo_status st = e == hipErrorOutOfMemory ? TERMEZO_ERR_OOM : TERMEZO_ERR_DEVICE;
+  return fail(c, st, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define TMZ_HIP(c, expr)                                 \
+  do {                                                   \
+    hipError_t _e = (expr);                              \
+    if (_e != hipSuccess) return hip_fail((c), _e, #expr); \
+  } while (0)
+
+template <typename P>
+hipError_t dalloc(P** p, size_t count) {
+  void* v = nullptr;
+  hipError_t e = hipMalloc(&v, count * sizeof(P) > 0 ? count * sizeof(P) : 1);
+  *p = static_cast<P*>(v);
+  return e;
+}
+
+template <typename P>
+void dfree(P*& p) {
+  if (p) (void)hipFree((void*)p);
+  p = nullptr;
+}
+
+size_t dtype_size(termezo_dtype t) {
+  switch (t) {
+    case TERMEZO_F32: return 4;
+    case TERMEZO_BF16: return 2;
+    case TERMEZO_I8: return 1;
+    case TERMEZO_I32: return 4;
+  }
+  return 0;
+}
+
+// Wait for the stream and surface a deferred numeric error.
+termezo_status sync_and_check(termezo_ctx* c) {
+  TMZ_HIP(c, hipStreamSynchronize(c->stream));
+  int32_t err = 0;
+  TMZ_HIP(c, hipMemcpy(&err, c->d_err, sizeof(err), hipMemcpyDeviceToHost));
+  if (err) {
+    const int32_t zero = 0;
+    TMZ_HIP(c, hipMemcpy(c->d_err, &zero, sizeof(zero), hipMemcpyHostToDevice));
+    return fail(c, TERMEZO_ERR_NUMERIC,
+                "a latent (or perturbed latent) is non-finite or has |w| >= 4");
+  }
+  return TERMEZO_OK;
+}
+
+termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
+  if (k <= c->act_cap && c->d_act) return TERMEZO_OK;
+  dfree(c->d_act);
+  dfree(c->d_act_tmp);
+  dfree(c->d_wp);
+  dfree(c->d_blk_cnt);
+  c->act_cap = 0;
+  const int64_t cap = k > 0 ? k : 1;
+  TMZ_HIP(c, dalloc(&c->d_act, (size_t)cap));
+  TMZ_HIP(c, dalloc(&c->d_act_tmp, (size_t)cap));
+  TMZ_HIP(c, dalloc(&c->d_wp, (size_t)cap));
+  c->blk_cap = cap / 4096 + 2;
+  TMZ_HIP(c, dalloc(&c->d_blk_cnt, (size_t)c->blk_cap));
+  c->act_cap = cap;
+  return TERMEZO_OK;
+}
+
+termezo_status ensure_xq_capacity(termezo_ctx* c, int64_t M, int64_t K) {
+  const int64_t need = M * K;
+  if (need > c->xq_cap) {
+    dfree(c->d_xq);
+    c->xq_cap = 0;
+    TMZ_HIP(c, dalloc(&c->d_xq, (size_t)need));
+    c->xq_cap = need;
+  }
+  if (M > c->xs_cap) {
+    dfree(c->d_xs);
+    c->xs_cap = 0;
+    TMZ_HIP(c, dalloc(&c->d_xs, (size_t)M));
+    c->xs_cap = M;
+  }
+  return TERMEZO_OK;
+}
+
+void free_all(termezo_ctx* c) {
+  dfree(c->d_wptr);
+  dfree(c->d_n);
+  dfree(c->d_gid0);
+  dfree(c->d_code_off);
+  dfree(c->d_tile_layer);
+  dfree(c->d_tile_start);
+  dfree(c->d_codes);
+  dfree(c->d_S_clean);
+  dfree(c->d_S_cur);
+  dfree(c->d_tau);
+  dfree(c->d_beta);
+  dfree(c->d_tau_cur);
+  dfree(c->d_beta_cur);
+  dfree(c->d_err);
+  dfree(c->d_act);
+  dfree(c->d_act_tmp);
+  dfree(c->d_act_off);
+  dfree(c->d_act_off_tmp);
+  dfree(c->d_wp);
+  dfree(c->d_hist);
+  dfree(c->d_sel);
+  dfree(c->d_tile_cnt);
+  dfree(c->d_tile_out);
+  dfree(c->d_tile_eqb);
+  dfree(c->d_blk_cnt);
+  dfree(c->d_loss);
+  dfree(c->d_xq);
+  dfree(c->d_xs);
+}
+
+bool finite(float v) { return std::isfinite(v); }
+
+}  // namespace
+
+extern "C" {
+
+termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
+                              termezo_dtype latent_dtype, void* hip_stream, termezo_ctx** out) {
+  if (!out) return TERMEZO_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!layers || n_layers <= 0) return TERMEZO_ERR_INVALID_ARG;
+  if (latent_dtype != TERMEZO_F32 && latent_dtype != TERMEZO_BF16) return TERMEZO_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const termezo_layer& L = layers[l];
+    if (!L.latent || L.d_out <= 0 || L.d_in <= 0 || L.d_in % 16 != 0) return TERMEZO_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(L.latent) & 15u) != 0) return TERMEZO_ERR_INVALID_ARG;
+    if (L.d_out > (int64_t(1) << 25) / L.d_in) return TERMEZO_ERR_INVALID_ARG;  // n <= 2^25
+  }
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) return TERMEZO_ERR_DEVICE;
+
+  termezo_ctx* c = new (std::nothrow) termezo_ctx();
+  if (!c) return TERMEZO_ERR_OOM;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return TERMEZO_ERR_DEVICE;
+  }
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->dtype = latent_dtype;
+  c->L = n_layers;
+
+  std::vector<void*> wptr(n_layers);
+  std::vector<int64_t> n(n_layers), gid0(n_layers), code_off(n_layers);
+  std::vector<int32_t> tile_layer;
+  int64_t D = 0, words = 0;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    LayerHost h;
+    h.w = layers[l].latent;
+    h.d_out = layers[l].d_out;
+    h.d_in = layers[l].d_in;
+    h.n = h.d_out * h.d_in;
+    h.gid0 = D;
+    h.code_off = words;
+    h.tile0 = (int64_t)tile_layer.size();
+    h.ntiles = (h.n + kTile - 1) / kTile;
+    for (int64_t t = 0; t < h.ntiles; ++t) {
+      tile_layer.push_back(l);
+      c->tile_start_host.push_back(t * kTile);
+    }
+    c->layers.push_back(h);
+    wptr[l] = h.w;
+    n[l] = h.n;
+    gid0[l] = h.gid0;
+    code_off[l] = h.code_off;
+    D += h.n;
+    words += h.n / 16;
+  }
+  c->D = D;
+  c->T = (int64_t)tile_layer.size();
+
+  termezo_status st = TERMEZO_OK;
+  auto chk = [&](hipError_t e, const char* what) {
+    if (e != hipSuccess && st == TERMEZO_OK) st = hip_fail(c, e, what);
+  };
+  chk(dalloc(&c->d_wptr, n_layers), "alloc");
+  chk(dalloc(&c->d_n, n_layers), "alloc");
+  chk(dalloc(&c->d_gid0, n_layers), "alloc");
+  chk(dalloc(&c->d_code_off, n_layers), "alloc");
+  chk(dalloc(&c->d_tile_layer, (size_t)c->T), "alloc");
+  chk(dalloc(&c->d_tile_start, (size_t)c->T), "alloc");
+  chk(dalloc(&c->d_codes, (size_t)words), "alloc codes");
+  chk(dalloc(&c->d_S_clean, n_layers), "alloc");
+  chk(dalloc(&c->d_S_cur, n_layers), "alloc");
+  chk(dalloc(&c->d_tau, n_layers), "alloc");
+  chk(dalloc(&c->d_beta, n_layers), "alloc");
+  chk(dalloc(&c->d_tau_cur, n_layers), "alloc");
+  chk(dalloc(&c->d_beta_cur, n_layers), "alloc");
+  chk(dalloc(&c->d_err, 1), "alloc");
+  chk(dalloc(&c->d_act_off, (size_t)n_layers + 1), "alloc");
+  chk(dalloc(&c->d_act_off_tmp, (size_t)n_layers + 1), "alloc");
+  chk(dalloc(&c->d_hist, kHistBins), "alloc");
+  chk(dalloc(&c->d_sel, 1), "alloc");
+  chk(dalloc(&c->d_tile_cnt, (size_t)(2 * c->T)), "alloc");
+  chk(dalloc(&c->d_tile_out, (size_t)c->T), "alloc");
+  chk(dalloc(&c->d_tile_eqb, (size_t)c->T), "alloc");
+  chk(dalloc(&c->d_loss, 4), "alloc");
+  if (st == TERMEZO_OK) {
+    chk(hipMemcpy(c->d_wptr, wptr.data(), n_layers * sizeof(void*), hipMemcpyHostToDevice), "copy");
+    chk(hipMemcpy(c->d_n, n.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice), "copy");
+    chk(hipMemcpy(c->d_gid0, gid0.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice), "copy");
+    chk(hipMemcpy(c->d_code_off, code_off.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice),
+        "copy");
+    chk(hipMemcpy(c->d_tile_layer, tile_layer.data(), c->T * sizeof(int32_t), hipMemcpyHostToDevice),
+        "copy");
+    chk(hipMemcpy(c->d_tile_start, c->tile_start_host.data(), c->T * sizeof(int64_t),
+                  hipMemcpyHostToDevice),
+        "copy");
+    const int32_t zero = 0;
+    chk(hipMemcpy(c->d_err, &zero, sizeof(zero), hipMemcpyHostToDevice), "copy");
+  }
+  if (st != TERMEZO_OK) {
+    free_all(c);
+    delete c;
+    return st;
+  }
+  *out = c;
+  return TERMEZO_OK;
+}
+
+void termezo_destroy(termezo_ctx* ctx) {
+  if (!ctx) return;
+  (void)hipStreamSynchronize(ctx->stream);
+  free_all(ctx);
+  delete ctx;
+}
+
+const char* termezo_last_error(const termezo_ctx* ctx) {
+  return ctx ? ctx->last_error.c_str() : "null context";
+}
+
+termezo_status termezo_sync(termezo_ctx* c) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  return sync_and_check(c);
+}
+
+termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32_t tie_inclusive,
+                                  int64_t* k0_out, float* xi0_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!finite(rho0) || !(rho0 > 0.0f) || rho0 > 1.0f)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "rho0 must lie in (0, 1]");
+  if (!finite(delta) || !(delta > 0.0f))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "delta must be positive and finite");
+  const int64_t k0 = (int64_t)std::floor((double)rho0 * (double)c->D);
+  if (k0 <= 0) return fail(c, TERMEZO_ERR_STATE, "rho0 * D rounds down to an empty mask");
+
+  c->has_mask = false;
+  c->codes_valid = false;
+  c->pending_perturb = false;
+  c->delta = delta;
+  TMZ_HIP(c, launch_abs_sum(c, c->d_S_clean));
+  TMZ_HIP(c, launch_thresholds(c, c->d_S_clean, c->d_tau, c->d_beta));
+  termezo_status st = sync_and_check(c);
+  if (st != TERMEZO_OK) return st;
+
+  TMZ_HIP(c, launch_select(c, k0));
+  // counts and offsets first: the inclusive reading may admit more than k0
+  const int inclusive = tie_inclusive ? 1 : 0;
+  TMZ_HIP(c, launch_mask_compact_counts(c, inclusive));
+  int64_t total = 0;
+  TMZ_HIP(c, hipMemcpyAsync(&total, c->d_act_off + c->L, sizeof(int64_t), hipMemcpyDeviceToHost,
+                            c->stream));
+  TMZ_HIP(c, hipStreamSynchronize(c->stream));
+  st = ensure_active_capacity(c, total);
+  if (st != TERMEZO_OK) return st;
+  TMZ_HIP(c, launch_mask_compact_write(c, inclusive));
+
+  // clean codes: current = clean
+  TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
+  TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
+  TMZ_HIP(c, launch_requant_dense(c));
+
+  SelectState sel;
+  TMZ_HIP(c, hipMemcpyAsync(&sel, c->d_sel, sizeof(sel), hipMemcpyDeviceToHost, c->stream));
+  st = sync_and_check(c);
+  if (st != TERMEZO_OK) return st;
+  float xi0;
+  std::memcpy(&xi0, &sel.prefix, sizeof(float));
+  c->xi0 = xi0;
+  c->k0 = total;
+  c->k_bound = total;
+  c->tie_inclusive = inclusive;
+  c->has_mask = true;
+  c->codes_valid = true;
+  if (k0_out) *k0_out = total;
+  if (xi0_out) *xi0_out = xi0;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t sign) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (sign < -1 || sign > 1) return fail(c, TERMEZO_ERR_INVALID_ARG, "sign must be -1, 0 or 1");
+  if (!finite(eps) || !(eps > 0.0f)) return fail(c, TERMEZO_ERR_INVALID_ARG, "eps must be > 0");
+  if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "perturb before build_mask");
+  const float se = (float)sign * eps;
+  TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
+  TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se));
+  TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
+  TMZ_HIP(c, launch_requant_dense(c));
+  TMZ_HIP(c, launch_patch_codes(c, c->k_bound));
+  c->codes_valid = true;
+  c->pending_perturb = true;
+  c->last_seed = seed;
+  c->last_eps = eps;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const void* x,
+                                         termezo_dtype x_dtype, int64_t M, void* y,
+                                         termezo_dtype y_dtype, int8_t* xq_out, float* xscale_out,
+                                         int32_t* acc_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= c->L) return fail(c, TERMEZO_ERR_INVALID_ARG, "layer out of range");
+  if (M <= 0 || !x || !y) return fail(c, TERMEZO_ERR_INVALID_ARG, "M <= 0 or null x / y");
+  if ((x_dtype != TERMEZO_F32 && x_dtype != TERMEZO_BF16) ||
+      (y_dtype != TERMEZO_F32 && y_dtype != TERMEZO_BF16))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "x and y must be F32 or BF16");
+  if ((reinterpret_cast<uintptr_t>(x) & 15u) != 0)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "x must be 16-byte aligned");
+  if (xq_out && (reinterpret_cast<uintptr_t>(xq_out) & 15u) != 0)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "xq_out must be 16-byte aligned");
+  if (!c->codes_valid) return fail(c, TERMEZO_ERR_STATE, "no current codes (perturb first)");
+  const LayerHost& L = c->layers[layer];
+  int8_t* xq = xq_out;
+  float* xs = xscale_out;
+  if (!xq || !xs) {
+    termezo_status st = ensure_xq_capacity(c, M, L.d_in);
+    if (st != TERMEZO_OK) return st;
+    if (!xq) xq = c->d_xq;
+    if (!xs) xs = c->d_xs;
+  }
+  TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->stream));
+  TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
+                                   L.d_in, L.d_out, y, y_dtype, acc_out, c->stream));
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_update(termezo_ctx* c, float proj_grad, float lr, int64_t* k_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!finite(proj_grad) || !finite(lr))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "projected gradient and lr must be finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  const float a = -(lr * proj_grad);
+  TMZ_HIP(c, launch_update(c, c->k_bound, c->last_seed, a));
+  TMZ_HIP(c, launch_thresholds(c, c->d_S_clean, c->d_tau, c->d_beta));
+  TMZ_HIP(c, launch_shrink(c, c->k_bound));
+  std::swap(c->d_act, c->d_act_tmp);
+  std::swap(c->d_act_off, c->d_act_off_tmp);
+  c->codes_valid = false;
+  c->pending_perturb = false;
+  if (k_out) {
+    int64_t k = 0;
+    TMZ_HIP(c, hipMemcpyAsync(&k, c->d_act_off + c->L, sizeof(int64_t), hipMemcpyDeviceToHost,
+                              c->stream));
+    termezo_status st = sync_and_check(c);
+    if (st != TERMEZO_OK) return st;
+    c->k_bound = k;
+    *k_out = k;
+  }
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_gauss(void* hip_stream, uint64_t seed, const uint64_t* gids, int64_t n,
+                             float* z) {
+  if (n < 0 || (n > 0 && (!gids || !z))) return TERMEZO_ERR_INVALID_ARG;
+  if (n == 0) return TERMEZO_OK;
+  return launch_gauss(seed, gids, n, z, static_cast<hipStream_t>(hip_stream)) == hipSuccess
+             ? TERMEZO_OK
+             : TERMEZO_ERR_DEVICE;
+}
+
+termezo_status termezo_active_count(termezo_ctx* c, int64_t* k) {
+  if (!c || !k) return TERMEZO_ERR_INVALID_ARG;
+  if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "no mask");
+  int64_t v = 0;
+  TMZ_HIP(c, hipMemcpyAsync(&v, c->d_act_off + c->L, sizeof(int64_t), hipMemcpyDeviceToHost,
+                            c->stream));
+  termezo_status st = sync_and_check(c);
+  if (st != TERMEZO_OK) return st;
+  c->k_bound = v;
+  *k = v;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_mask_export(termezo_ctx* c, int32_t layer, uint32_t* idx, int64_t cap,
+                                   int64_t* n) {
+  if (!c || !n) return TERMEZO_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= c->L) return fail(c, TERMEZO_ERR_INVALID_ARG, "layer out of range");
+  if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "no mask");
+  std::vector<int64_t> off(c->L + 1);
+  TMZ_HIP(c, hipMemcpyAsync(off.data(), c->d_act_off, (c->L + 1) * sizeof(int64_t),
+                            hipMemcpyDeviceToHost, c->stream));
+  termezo_status st = sync_and_check(c);
+  if (st != TERMEZO_OK) return st;
+  const int64_t cnt = off[layer + 1] - off[layer];
+  *n = cnt;
+  if (cnt > cap || (cnt > 0 && !idx))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "index buffer too small");
+  if (cnt > 0)
+    TMZ_HIP(c, hipMemcpy(idx, c->d_act + off[layer], cnt * sizeof(uint32_t), hipMemcpyDeviceToHost));
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_codes_export(termezo_ctx* c, int32_t layer, int8_t* codes) {
+  if (!c || !codes) return TERMEZO_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= c->L) return fail(c, TERMEZO_ERR_INVALID_ARG, "layer out of range");
+  if (!c->codes_valid) return fail(c, TERMEZO_ERR_STATE, "no current codes");
+  const LayerHost& L = c->layers[layer];
+  int8_t* tmp = nullptr;
+  TMZ_HIP(c, dalloc(&tmp, (size_t)L.n));
+  hipError_t e = launch_unpack_layer(c, layer, tmp);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e == hipSuccess) e = hipMemcpy(codes, tmp, (size_t)L.n, hipMemcpyDeviceToHost);
+  (void)hipFree(tmp);
+  if (e != hipSuccess) return hip_fail(c, e, "codes export");
+  return sync_and_check(c);
+}
+
+termezo_status termezo_layer_stats(termezo_ctx* c, int32_t layer, float* tau, float* beta,
+                                   int64_t* abs_sum_fix, float* tau_cur, float* beta_cur) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= c->L) return fail(c, TERMEZO_ERR_INVALID_ARG, "layer out of range");
+  TMZ_HIP(c, hipStreamSynchronize(c->stream));
+  if (tau) TMZ_HIP(c, hipMemcpy(tau, c->d_tau + layer, 4, hipMemcpyDeviceToHost));
+  if (beta) TMZ_HIP(c, hipMemcpy(beta, c->d_beta + layer, 4, hipMemcpyDeviceToHost));
+  if (abs_sum_fix) TMZ_HIP(c, hipMemcpy(abs_sum_fix, c->d_S_clean + layer, 8, hipMemcpyDeviceToHost));
+  if (tau_cur) TMZ_HIP(c, hipMemcpy(tau_cur, c->d_tau_cur + layer, 4, hipMemcpyDeviceToHost));
+  if (beta_cur) TMZ_HIP(c, hipMemcpy(beta_cur, c->d_beta_cur + layer, 4, hipMemcpyDeviceToHost));
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_mse_loss(termezo_ctx* c, const float* y, const float* target, int64_t n,
+                                float* out) {
+  if (!c || !y || !target || !out || n <= 0) return TERMEZO_ERR_INVALID_ARG;
+  TMZ_HIP(c, launch_mse(y, target, n, c->d_loss, c->stream));
+  double sum = 0.0;
+  TMZ_HIP(c, hipMemcpyAsync(&sum, c->d_loss, sizeof(double), hipMemcpyDeviceToHost, c->stream));
+  termezo_status st = sync_and_check(c);
+  if (st != TERMEZO_OK) return st;
+  *out = (float)(sum / (double)n);
+  return TERMEZO_OK;
+}
+
+}  // extern "C"

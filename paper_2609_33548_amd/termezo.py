@@ -1,0 +1,213 @@
+"""Python binding of the TerMeZO C ABI (libtermezo.so).
+
+Argument marshalling only: every step of the TerMeZO path runs in the HIP
+kernels of libtermezo.so.  PyTorch tensors supply device memory and the HIP
+stream.  The library must be built (``python -m paper_2609_33548_amd.build``);
+importing this module without it raises ImportError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtermezo.so")
+
+OK, ERR_INVALID_ARG, ERR_STATE, ERR_DEVICE, ERR_OOM, ERR_NUMERIC = range(6)
+F32, BF16, I8, I32 = range(4)
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "STATE", 3: "DEVICE", 4: "OOM", 5: "NUMERIC"}
+
+
+class TermezoError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"termezo {STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("latent", ctypes.c_void_p), ("d_out", ctypes.c_int64), ("d_in", ctypes.c_int64)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_33548_amd.build`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_P = ctypes.c_void_p
+_i32, _i64, _u64, _f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
+_SIGS = {
+    "termezo_create": [ctypes.POINTER(Layer), _i32, _i32, _P, ctypes.POINTER(_P)],
+    "termezo_destroy": [_P],
+    "termezo_last_error": [_P],
+    "termezo_build_mask": [_P, _f32, _f32, _i32, ctypes.POINTER(_i64), ctypes.POINTER(_f32)],
+    "termezo_perturb": [_P, _u64, _f32, _i32],
+    "termezo_bitlinear_forward": [_P, _i32, _P, _i32, _i64, _P, _i32, _P, _P, _P],
+    "termezo_update": [_P, _f32, _f32, ctypes.POINTER(_i64)],
+    "termezo_sync": [_P],
+    "termezo_mask_export": [_P, _i32, _P, _i64, ctypes.POINTER(_i64)],
+    "termezo_codes_export": [_P, _i32, _P],
+    "termezo_layer_stats": [_P, _i32, ctypes.POINTER(_f32), ctypes.POINTER(_f32),
+                            ctypes.POINTER(_i64), ctypes.POINTER(_f32), ctypes.POINTER(_f32)],
+    "termezo_mse_loss": [_P, _P, _P, _i64, ctypes.POINTER(_f32)],
+    "termezo_active_count": [_P, ctypes.POINTER(_i64)],
+    "termezo_gauss": [_P, _u64, _P, _i64, _P],
+}
+for _name, _args in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.argtypes = _args
+    _fn.restype = None if _name == "termezo_destroy" else (
+        ctypes.c_char_p if _name == "termezo_last_error" else ctypes.c_int)
+
+lib = _lib
+
+
+def _ptr(t) -> Optional[int]:
+    """Device address of a torch tensor (None passes NULL)."""
+    return None if t is None else int(t.data_ptr())
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+# --------------------------------------------------------------------------
+# Thin wrappers with the C names
+# --------------------------------------------------------------------------
+def termezo_create(layers: Sequence[Tuple[int, int, int]], latent_dtype: int, stream: Optional[int]):
+    arr = (Layer * len(layers))(*[Layer(p, o, i) for p, o, i in layers])
+    out = _P()
+    st = _lib.termezo_create(arr, len(layers), latent_dtype, stream, ctypes.byref(out))
+    if st != OK:
+        raise TermezoError(st, "termezo_create failed")
+    return out.value
+
+
+class Context:
+    """A registered set of ternary projections and its TerMeZO state.
+
+    ``latents`` are torch device tensors [d_out, d_in] (all fp32 or all bf16)
+    that the caller keeps alive; the library updates them in place."""
+
+    def __init__(self, latents, stream=None):
+        import torch
+        if not latents:
+            raise ValueError("at least one layer")
+        dt = latents[0].dtype
+        for w in latents:
+            if w.dtype != dt or w.dim() != 2 or not w.is_contiguous() or not w.is_cuda:
+                raise ValueError("latents must be contiguous 2-D device tensors of one dtype")
+        self.latents = list(latents)
+        self.dtype_code = _dtype_code(latents[0])
+        self.shapes = [tuple(w.shape) for w in latents]
+        self._stream = stream if stream is not None else torch.cuda.current_stream()
+        self.handle = termezo_create([(w.data_ptr(), w.shape[0], w.shape[1]) for w in latents],
+                                     self.dtype_code, int(self._stream.cuda_stream))
+
+    def _check(self, st: int, what: str):
+        if st != OK:
+            msg = _lib.termezo_last_error(self.handle)
+            raise TermezoError(st, f"{what}: {msg.decode() if msg else ''}")
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _lib.termezo_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- the four hot-path calls ----------------------------------------------
+    def build_mask(self, rho0: float, delta: float = 1e-5, tie_inclusive: bool = False):
+        k0 = _i64()
+        xi0 = _f32()
+        self._check(_lib.termezo_build_mask(self.handle, rho0, delta, int(tie_inclusive),
+                                            ctypes.byref(k0), ctypes.byref(xi0)), "build_mask")
+        return int(k0.value), float(np.float32(xi0.value))
+
+    def perturb(self, seed: int, eps: float, sign: int):
+        self._check(_lib.termezo_perturb(self.handle, seed & (2**64 - 1), eps, sign), "perturb")
+
+    def bitlinear_forward(self, layer: int, x, y, xq_out=None, xscale_out=None, acc_out=None):
+        M = x.shape[0]
+        self._check(_lib.termezo_bitlinear_forward(
+            self.handle, layer, _ptr(x), _dtype_code(x), M, _ptr(y), _dtype_code(y),
+            _ptr(xq_out), _ptr(xscale_out), _ptr(acc_out)), "bitlinear_forward")
+
+    def update(self, proj_grad: float, lr: float, want_k: bool = True) -> Optional[int]:
+        k = _i64()
+        self._check(_lib.termezo_update(self.handle, proj_grad, lr,
+                                        ctypes.byref(k) if want_k else None), "update")
+        return int(k.value) if want_k else None
+
+    # -- support calls ----------------------------------------------------------
+    def sync(self):
+        self._check(_lib.termezo_sync(self.handle), "sync")
+
+    def active_count(self) -> int:
+        k = _i64()
+        self._check(_lib.termezo_active_count(self.handle, ctypes.byref(k)), "active_count")
+        return int(k.value)
+
+    def mask(self, layer: int) -> np.ndarray:
+        n = _i64()
+        d_out, d_in = self.shapes[layer]
+        buf = np.empty(max(1, d_out * d_in), np.uint32)
+        self._check(_lib.termezo_mask_export(self.handle, layer, buf.ctypes.data, buf.size,
+                                             ctypes.byref(n)), "mask_export")
+        return buf[: n.value].astype(np.int64)
+
+    def codes(self, layer: int) -> np.ndarray:
+        d_out, d_in = self.shapes[layer]
+        buf = np.empty((d_out, d_in), np.int8)
+        self._check(_lib.termezo_codes_export(self.handle, layer, buf.ctypes.data), "codes_export")
+        return buf
+
+    def layer_stats(self, layer: int):
+        tau, beta, tc, bc = _f32(), _f32(), _f32(), _f32()
+        S = _i64()
+        self._check(_lib.termezo_layer_stats(self.handle, layer, ctypes.byref(tau), ctypes.byref(beta),
+                                             ctypes.byref(S), ctypes.byref(tc), ctypes.byref(bc)),
+                    "layer_stats")
+        f = lambda v: float(np.float32(v.value))
+        return {"tau": f(tau), "beta": f(beta), "S": int(S.value), "tau_cur": f(tc), "beta_cur": f(bc)}
+
+    def mse_loss(self, y, target) -> float:
+        out = _f32()
+        self._check(_lib.termezo_mse_loss(self.handle, _ptr(y), _ptr(target), y.numel(),
+                                          ctypes.byref(out)), "mse_loss")
+        return float(np.float32(out.value))
+
+
+def gauss(seed: int, gids, stream=None):
+    """z at the given global ids (torch int64 device tensor) as a device fp32 tensor."""
+    import torch
+    g = gids.to(torch.int64).contiguous()
+    z = torch.empty(g.shape, dtype=torch.float32, device=g.device)
+    st = _lib.termezo_gauss(_stream_handle(stream), seed & (2**64 - 1), g.data_ptr(), g.numel(),
+                            z.data_ptr())
+    if st != OK:
+        raise TermezoError(st, "termezo_gauss failed")
+    return z
+
+
+def projected_grad(f_plus: float, f_minus: float, eps: float) -> float:
+    """g = (F+ - F-) / (2 eps) in fp32 (eq. spsa); host scalar arithmetic."""
+    fp, fm, e = np.float32(f_plus), np.float32(f_minus), np.float32(eps)
+    return float(np.float32(np.float32(fp - fm) / np.float32(np.float32(2.0) * e)))
