@@ -1,0 +1,118 @@
+"""Pins of the decoder oracle (the BitNet forward around the ternary
+projections) against textbook definitions in independent library routines
+(torch CPU, fp64) and invariants (rotation norms, relative positions,
+causality, uniform logits)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import decoder_ref as dec
+from paper_2609_33548_amd import synth
+
+
+def test_rmsnorm_matches_torch():
+    h = synth.activations(1, 7, 96) * np.float32(3.0)
+    ref = F.rms_norm(torch.from_numpy(h).double(), (96,), eps=1e-5).numpy()
+    assert np.allclose(dec.rmsnorm(h, 1e-5), ref, rtol=1e-6, atol=1e-7)
+
+
+def test_rope_is_complex_rotation_and_relative():
+    M, H, hd = 6, 3, 16
+    x = synth.activations(2, M, H * hd).astype(np.float64)
+    pos = np.array([0, 1, 5, 17, 100, 511])
+    got = dec.rope(x, pos, H, hd, 10000.0)
+    half = hd // 2
+    xc = x.reshape(M, H, 2, half)
+    z = xc[:, :, 0, :] + 1j * xc[:, :, 1, :]
+    theta = 10000.0 ** (-np.arange(half) * 2.0 / hd)
+    zr = z * np.exp(1j * pos[:, None, None] * theta[None, None, :])
+    ref = np.concatenate([zr.real, zr.imag], axis=-1).reshape(M, H * hd)
+    assert np.allclose(got, ref, atol=1e-12)
+    assert np.allclose(np.linalg.norm(got, axis=1), np.linalg.norm(x, axis=1))
+    q = synth.activations(3, 1, hd).astype(np.float64)
+    k = synth.activations(4, 1, hd).astype(np.float64)
+    dots = [float((dec.rope(q, np.array([p + 7]), 1, hd, 1e4) @ dec.rope(k, np.array([p]), 1, hd, 1e4).T)[0, 0])
+            for p in (0, 3, 50)]
+    assert np.allclose(dots, dots[0])
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (4, 1), (6, 2)])
+def test_attention_matches_torch_sdpa(Hq, Hkv):
+    B, S, hd = 2, 9, 8
+    q = synth.activations(5, B * S, Hq * hd)
+    k = synth.activations(6, B * S, Hkv * hd)
+    v = synth.activations(7, B * S, Hkv * hd)
+    got = dec.attention(q, k, v, B, S, Hq, Hkv, hd)
+    tq = torch.from_numpy(q).double().reshape(B, S, Hq, hd).transpose(1, 2)
+    tk = torch.from_numpy(k).double().reshape(B, S, Hkv, hd).transpose(1, 2)
+    tv = torch.from_numpy(v).double().reshape(B, S, Hkv, hd).transpose(1, 2)
+    tk = tk.repeat_interleave(Hq // Hkv, dim=1)
+    tv = tv.repeat_interleave(Hq // Hkv, dim=1)
+    ref = F.scaled_dot_product_attention(tq, tk, tv, is_causal=True)
+    ref = ref.transpose(1, 2).reshape(B * S, Hq * hd).numpy()
+    assert np.allclose(got, ref, atol=1e-12)
+
+
+def test_silu_mul_matches_torch():
+    g = synth.activations(8, 5, 33)
+    u = synth.activations(9, 5, 33)
+    ref = (F.silu(torch.from_numpy(g).double()) * torch.from_numpy(u).double()).numpy()
+    assert np.allclose(dec.silu_mul(g, u), ref, rtol=1e-6, atol=1e-7)
+
+
+def _tiny(bf16=False):
+    cfg = dec.DecoderConfig(n_blocks=2, d_model=64, n_heads=4, n_kv_heads=2, d_ffn=96,
+                            vocab=50, bf16=bf16)
+    shapes = cfg.layer_shapes()
+    rng = np.random.default_rng(0)
+    codes = [rng.integers(-1, 2, size=s).astype(np.int8) for s in shapes]
+    betas = [0.016] * len(shapes)
+    emb = synth.latents(11, [cfg.vocab * cfg.d_model], bf16=bf16).reshape(cfg.vocab, cfg.d_model)
+    return cfg, codes, betas, emb
+
+
+def test_cross_entropy_matches_torch_and_causality():
+    cfg, codes, betas, emb = _tiny()
+    tok = synth.tokens(1, 2, 12, cfg.vocab)
+    rows = dec.forward_row_losses(cfg, emb, tok, codes, betas)
+    assert np.all(rows[:, -1] == 0.0) and np.all(rows[:, :-1] > 0)
+    # changing the last input token changes only the last labelled position
+    tok2 = tok.copy()
+    tok2[:, -1] = (tok2[:, -1] + 1) % cfg.vocab
+    rows2 = dec.forward_row_losses(cfg, emb, tok2, codes, betas)
+    assert np.array_equal(rows[:, :-2], rows2[:, :-2])
+    assert not np.array_equal(rows[:, -2], rows2[:, -2])
+    # changing a middle token leaves every earlier position untouched
+    tok3 = tok.copy()
+    tok3[:, 6] = (tok3[:, 6] + 3) % cfg.vocab
+    rows3 = dec.forward_row_losses(cfg, emb, tok3, codes, betas)
+    assert np.array_equal(rows[:, :5], rows3[:, :5])
+    assert dec.mean_loss(rows) == pytest.approx(rows.sum() / (2 * 11), rel=1e-6)
+
+
+def test_loss_is_log_vocab_for_uniform_logits():
+    cfg, codes, betas, _ = _tiny()
+    emb = np.ones((cfg.vocab, cfg.d_model), np.float32) * np.float32(0.02)
+    tok = synth.tokens(2, 2, 8, cfg.vocab)
+    rows = dec.forward_row_losses(cfg, emb, tok, codes, betas)
+    assert np.allclose(rows[:, :-1], math.log(cfg.vocab), rtol=1e-12)
+
+
+def test_cross_entropy_rows_match_torch():
+    logits = synth.activations(12, 20, 77).astype(np.float64) * 3.0
+    labels = synth.tokens(13, 1, 20, 77)[0].astype(np.int64)
+    ref = F.cross_entropy(torch.from_numpy(logits), torch.from_numpy(labels), reduction="none")
+    assert np.allclose(dec.cross_entropy_rows(logits, labels), ref.numpy(), rtol=1e-12)
+
+
+def test_bf16_storage_rounds_every_stored_activation():
+    cfg, codes, betas, emb = _tiny(bf16=True)
+    tok = synth.tokens(4, 2, 8, cfg.vocab)
+    r16 = dec.forward_row_losses(cfg, emb, tok, codes, betas)
+    cfg32 = dec.DecoderConfig(**{**cfg.__dict__, "bf16": False})
+    r32 = dec.forward_row_losses(cfg32, emb, tok, codes, betas)
+    assert not np.array_equal(r16, r32)
+    assert np.allclose(r16, r32, rtol=2e-2)
