@@ -139,6 +139,58 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* ctx, int32_t layer,
 termezo_status termezo_update(termezo_ctx* ctx, float proj_grad, float lr,
                               int64_t* k_out);
 
+/* Device-side projected gradient and update (Algorithm 1: g = (F+ - F-) / (2 eps),
+ * then the same update and shrink as termezo_update) without a host round
+ * trip: loss_plus and loss_minus are device fp32 scalars (for example written
+ * by termezo_model_loss).  g is formed in fp32 on the device as
+ * (F+ - F-) / (2 eps).  A non-finite g skips the latent update and raises a
+ * deferred NUMERIC.  Never waits.  Errors: INVALID_ARG (null pointers, eps or
+ * lr not positive/finite), STATE as for termezo_update. */
+termezo_status termezo_update_from_losses(termezo_ctx* ctx, const float* loss_plus,
+                                          const float* loss_minus, float eps, float lr);
+
+/* ---- BitNet decoder around the registered projections (Sec. 3) ----------------
+ * The context's layers must be the ternary projections of n_blocks decoder
+ * blocks in the order q, k, v, o, gate, up, down (shapes [n_heads*hd][d],
+ * [n_kv_heads*hd][d] twice, [d][n_heads*hd], [d_ffn][d] twice, [d][d_ffn],
+ * hd = d_model / n_heads).  The full-precision parameters are frozen: the
+ * token embedding (tied to the LM head) is the caller's device matrix
+ * [vocab][d_model] in act_dtype; RMSNorm weights are one.  Blocks are pre-norm:
+ * h += o(attn(rope(q(x)), rope(k(x)), v(x))), x = rmsnorm(h); then
+ * h += down(silu(gate(x)) * up(x)).  Attention is causal grouped-query with
+ * scale 1/sqrt(hd); rotary pairs are (i, i + hd/2) with angle
+ * p * rope_base^(-2i/hd).  Activations are stored in act_dtype between kernels;
+ * BitLinear inputs are quantised per token as in termezo_bitlinear_forward. */
+typedef struct {
+  int32_t n_blocks, d_model, n_heads, n_kv_heads, d_ffn, vocab;
+  float rope_base;          /* e.g. 10000 */
+  float norm_eps;           /* e.g. 1e-5  */
+  termezo_dtype act_dtype;  /* F32 or BF16 */
+} termezo_model_config;
+
+typedef struct termezo_model termezo_model;
+
+/* Bind a decoder to ctx (which must outlive it).  embedding: device pointer,
+ * 16-byte aligned, borrowed.  Errors: INVALID_ARG (shapes do not match the
+ * registered layers, unsupported head_dim for BF16 (64, 96, 128), d_model or
+ * d_ffn above 8192, bad dtype). */
+termezo_status termezo_model_create(termezo_ctx* ctx, const termezo_model_config* cfg,
+                                    const void* embedding, termezo_model** out);
+/* Free the model's activation buffers (it does not touch the context, which
+ * may already have been destroyed).  NULL is a no-op. */
+void termezo_model_destroy(termezo_model* model);
+
+/* Batch loss of eq. objective_est with next-token cross-entropy: the mean over
+ * the batch * (seq - 1) labelled positions of logsumexp(logits) - logit[next
+ * token], with the current codes (clean or perturbed).  tokens: device int32
+ * [batch][seq].  Outputs (all optional): loss_dev (device fp32 scalar),
+ * row_loss_dev (device fp32 [batch*seq], 0 at each sequence's last position),
+ * loss_host (host; the call then waits).  Errors: INVALID_ARG, STATE (no
+ * current codes), OOM. */
+termezo_status termezo_model_loss(termezo_model* model, const int32_t* tokens, int32_t batch,
+                                  int32_t seq, float* loss_dev, float* row_loss_dev,
+                                  float* loss_host);
+
 /* ---- inspection and support calls (not part of the four hot-path calls) ---- */
 
 /* Wait for the context's stream; reports a deferred NUMERIC error. */

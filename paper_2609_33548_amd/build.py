@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libtermezo.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["tmz_runtime.hip", "tmz_step.hip", "tmz_bitlinear.hip"]
+SOURCES = ["tmz_runtime.hip", "tmz_step.hip", "tmz_bitlinear.hip", "tmz_model.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",

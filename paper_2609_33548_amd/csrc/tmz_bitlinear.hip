@@ -79,19 +79,24 @@ __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int6
 constexpr int kBM = 128, kBN = 128, kBK = 64;
 constexpr int kLdsStride = 80;   // bytes per LDS row (64 data + 16 pad)
 
-__device__ __forceinline__ void store_out(float* y, int64_t i, float v) { y[i] = v; }
-__device__ __forceinline__ void store_out(uint16_t* y, int64_t i, float v) { y[i] = f32_to_bf16_rne(v); }
+__device__ __forceinline__ float load_act(const float* p) { return *p; }
+__device__ __forceinline__ float load_act(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ void store_act(float* p, float v) { *p = v; }
+__device__ __forceinline__ void store_act(uint16_t* p, float v) { *p = f32_to_bf16_rne(v); }
+__device__ __forceinline__ float round_act(const float*, float v) { return v; }
+__device__ __forceinline__ float round_act(const uint16_t*, float v) {
+  return bf16_to_f32(f32_to_bf16_rne(v));
+}
 
-template <typename TY>
+template <typename TY, int MODE>
 __global__ void __launch_bounds__(256) k_gemm_i8(const int8_t* __restrict__ xq,
                                                  const float* __restrict__ s,
-                                                 const uint32_t* __restrict__ codes,
-                                                 const float* __restrict__ beta_dev, int64_t M,
-                                                 int64_t K, int64_t N, TY* __restrict__ y,
+                                                 const uint32_t* __restrict__ codes, int64_t M,
+                                                 int64_t K, int64_t N, GemmOut out,
                                                  int32_t* __restrict__ acc_out) {
   __shared__ __attribute__((aligned(16))) int8_t As[kBM * kLdsStride];
   __shared__ __attribute__((aligned(16))) int8_t Bs[kBN * kLdsStride];
-  __shared__ float rrow[kBM];
+  __shared__ float rrow[kMaxSeg][kBM];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
@@ -99,10 +104,10 @@ __global__ void __launch_bounds__(256) k_gemm_i8(const int8_t* __restrict__ xq,
   const int64_t m0 = (int64_t)blockIdx.y * kBM, n0 = (int64_t)blockIdx.x * kBN;
   const int64_t KW = K / 16;  // code words per row
 
-  const float beta = *beta_dev;
-  for (int i = tid; i < kBM; i += 256) {
-    const int64_t m = m0 + i;
-    rrow[i] = m < M ? __fdiv_rn(beta, s[m]) : 0.0f;
+  for (int i = tid; i < kMaxSeg * kBM; i += 256) {
+    const int sg = i / kBM, r = i % kBM;
+    const int64_t m = m0 + r;
+    rrow[sg][r] = (sg < out.nseg && m < M) ? __fdiv_rn(*out.beta[sg], s[m]) : 0.0f;
   }
 
   v16i acc[2][2];
@@ -163,22 +168,36 @@ __global__ void __launch_bounds__(256) k_gemm_i8(const int8_t* __restrict__ xq,
     __syncthreads();
   }
 
-  // ---- epilogue: y = float(acc) * (beta / s_m) ----
+  // ---- epilogue: y = float(acc) * (beta_seg / s_m); segments split N ----
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int b = 0; b < 2; ++b) {
+    const int64_t n = n0 + wn * 64 + b * 32 + (lane & 31);
+    if (n >= N) continue;
+    int sg = 0;
+    if (out.nseg > 1 && n >= out.nstart[1]) sg = 1;
+    if (out.nseg > 2 && n >= out.nstart[2]) sg = 2;
+    TY* y = reinterpret_cast<TY*>(out.y[sg]);
+    const int64_t ld = out.ld[sg];
+    const int64_t nl = n - out.nstart[sg];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int li = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         const int64_t m = m0 + li;
-        const int64_t n = n0 + wn * 64 + b * 32 + (lane & 31);
-        if (m < M && n < N) {
+        if (m < M) {
           const int32_t v = acc[a][b][r];
-          store_out(y, m * N + n, (float)v * rrow[li]);
+          const float yv = (float)v * rrow[sg][li];
+          TY* p = y + m * ld + nl;
+          if (MODE == kGemmStore) {
+            store_act(p, yv);
+          } else {  // residual: h <- round(h + round(y))
+            store_act(p, load_act(p) + round_act(p, yv));
+          }
           if (acc_out) acc_out[m * N + n] = v;
         }
       }
+  }
 }
 
 // ===========================================================================
@@ -192,17 +211,39 @@ hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t
   return hipGetLastError();
 }
 
+hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
+                          int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
+                          int32_t* acc, hipStream_t st) {
+  dim3 grid((unsigned)((N + kBN - 1) / kBN), (unsigned)((M + kBM - 1) / kBM));
+  if (ydt == TERMEZO_F32) {
+    if (mode == kGemmStore)
+      hipLaunchKernelGGL((k_gemm_i8<float, kGemmStore>), grid, dim3(256), 0, st, xq, s, codes, M, K,
+                         N, out, acc);
+    else
+      hipLaunchKernelGGL((k_gemm_i8<float, kGemmResidual>), grid, dim3(256), 0, st, xq, s, codes, M,
+                         K, N, out, acc);
+  } else {
+    if (mode == kGemmStore)
+      hipLaunchKernelGGL((k_gemm_i8<uint16_t, kGemmStore>), grid, dim3(256), 0, st, xq, s, codes, M,
+                         K, N, out, acc);
+    else
+      hipLaunchKernelGGL((k_gemm_i8<uint16_t, kGemmResidual>), grid, dim3(256), 0, st, xq, s, codes,
+                         M, K, N, out, acc);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
                                  const float* beta_dev, int64_t M, int64_t K, int64_t N, void* y,
                                  termezo_dtype ydt, int32_t* acc, hipStream_t st) {
-  dim3 grid((unsigned)((N + kBN - 1) / kBN), (unsigned)((M + kBM - 1) / kBM));
-  if (ydt == TERMEZO_F32)
-    hipLaunchKernelGGL(k_gemm_i8<float>, grid, dim3(256), 0, st, xq, s, codes, beta_dev, M, K, N,
-                       (float*)y, acc);
-  else
-    hipLaunchKernelGGL(k_gemm_i8<uint16_t>, grid, dim3(256), 0, st, xq, s, codes, beta_dev, M, K,
-                       N, (uint16_t*)y, acc);
-  return hipGetLastError();
+  GemmOut out = {};
+  out.nseg = 1;
+  out.y[0] = y;
+  out.ld[0] = N;
+  out.beta[0] = beta_dev;
+  out.nstart[0] = 0;
+  out.nstart[1] = N;
+  return launch_gemm_i8(xq, s, codes, M, K, N, out, ydt, kGemmStore, acc, st);
 }
 
 }  // namespace tmz

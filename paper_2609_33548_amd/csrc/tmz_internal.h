@@ -41,6 +41,20 @@ struct DevState {
   int64_t T;                         // number of tiles
 };
 
+// Output description of a BitLinear GEMM whose N columns may be split in up
+// to kMaxSeg segments (fused projections sharing one input), each with its
+// own scale beta', destination and row stride.
+constexpr int kMaxSeg = 3;
+constexpr int kGemmStore = 0;      // y = round(acc * beta / s)
+constexpr int kGemmResidual = 1;   // y <- round(y + round(acc * beta / s))
+struct GemmOut {
+  void* y[kMaxSeg];
+  int64_t ld[kMaxSeg];
+  const float* beta[kMaxSeg];
+  int64_t nstart[kMaxSeg + 1];
+  int nseg;
+};
+
 struct SelectState {                 // radix-select bookkeeping (device)
   unsigned long long k0;             // budget
   unsigned long long less;           // keys strictly below the current prefix bucket
@@ -95,6 +109,7 @@ struct termezo_ctx {
   int64_t* d_blk_cnt = nullptr;              // shrink block counts
   int64_t blk_cap = 0;
   double* d_loss = nullptr;                  // loss accumulators
+  float* d_scal = nullptr;                   // [0] update coefficient a, [1] g
   int8_t* d_xq = nullptr;                    // activation-quantisation scratch
   int64_t xq_cap = 0;
   float* d_xs = nullptr;
@@ -150,7 +165,10 @@ hipError_t launch_mask_compact_write(termezo_ctx* c, int inclusive);   // -> act
 hipError_t launch_requant_dense(termezo_ctx* c);          // codes of w with tau_cur
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se);
 hipError_t launch_patch_codes(termezo_ctx* c, int64_t k);
-hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed, float a);
+hipError_t launch_set_coeff(termezo_ctx* c, float a);
+hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float* fm, float eps,
+                                    float lr);
+hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed);   // a from d_scal[0]
 hipError_t launch_shrink(termezo_ctx* c, int64_t k);      // d_act -> d_act_tmp, offsets -> tmp
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);
 hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z, hipStream_t s);
@@ -159,6 +177,9 @@ hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hi
 // BitLinear
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, hipStream_t st);
+hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
+                          int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
+                          int32_t* acc, hipStream_t st);
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
                                  const float* beta_dev, int64_t M, int64_t K, int64_t N,
                                  void* y, termezo_dtype ydt, int32_t* acc, hipStream_t st);

@@ -1,0 +1,835 @@
+// BitNet decoder forward around the ternary BitLinear projections, and the
+// next-token cross-entropy that TerMeZO evaluates at w +/- eps z (Sec. 3,
+// eq. objective_est).  The full-precision parameters (token embedding tied to
+// the LM head, unit-weight RMSNorms) are frozen.  Activations are stored in
+// fp32 or bf16 between kernels; the RMSNorm output and the SwiGLU product are
+// handed to the int8 activation quantiser in fp32 without being stored.
+#include <algorithm>
+#include <cmath>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "tmz_device.h"
+#include "tmz_internal.h"
+
+namespace tmz {
+
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float ld_act(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ld_act(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+__device__ __forceinline__ void st_act(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void st_act(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16_rne(v); }
+
+__device__ __forceinline__ float wsum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ float wmax(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// Block (256 threads) reductions through a 4-entry LDS scratch.
+__device__ __forceinline__ float bsum(float v, float* red) {
+  v = wsum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+__device__ __forceinline__ float bmax(float v, float* red) {
+  v = wmax(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+__device__ __forceinline__ int8_t q8(float x, float s) {
+  return (int8_t)fminf(fmaxf(__builtin_rintf(x * s), -128.0f), 127.0f);
+}
+
+constexpr int kRowMax = 32;  // per-thread register budget: rows up to 256 * 32 elements
+
+// ---------------------------------------------------------------------------
+// h[m] = E[tok[m]]
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, int64_t d, T* h) {
+  const int64_t m = blockIdx.x;
+  const T* src = E + (int64_t)tok[m] * d;
+  for (int64_t i = threadIdx.x; i < d; i += 256) h[m * d + i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// RMSNorm (unit weight) fused with the 8-bit activation quantiser:
+// x = h / sqrt(mean(h^2) + eps) in fp32, then x_q, s as in BitLinear.
+// With xf != nullptr the normalised row is stored instead (final norm).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) k_rmsnorm_quant(const T* h, int64_t d, float eps,
+                                                       int8_t* xq, float* xs, T* xf) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  float v[kRowMax];
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kRowMax; ++j) {
+    const int64_t i = threadIdx.x + 256 * j;
+    v[j] = i < d ? ld_act(h, m * d + i) : 0.0f;
+    ss = fmaf(v[j], v[j], ss);
+  }
+  ss = bsum(ss, red);
+  const float r = __fdiv_rn(1.0f, sqrt_rn(ss / (float)d + eps));
+  float a = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kRowMax; ++j) {
+    v[j] = v[j] * r;
+    a = fmaxf(a, fabsf(v[j]));
+  }
+  if (xf) {
+#pragma unroll
+    for (int j = 0; j < kRowMax; ++j) {
+      const int64_t i = threadIdx.x + 256 * j;
+      if (i < d) st_act(xf, m * d + i, v[j]);
+    }
+    return;
+  }
+  a = bmax(a, red);
+  const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
+  if (threadIdx.x == 0) xs[m] = sc;
+#pragma unroll
+  for (int j = 0; j < kRowMax; ++j) {
+    const int64_t i = threadIdx.x + 256 * j;
+    if (i < d) xq[m * d + i] = q8(v[j], sc);
+  }
+}
+
+// SwiGLU fused with the activation quantiser: a = silu(g) * u (fp32).
+template <typename T>
+__global__ void __launch_bounds__(256) k_swiglu_quant(const T* g, const T* u, int64_t F,
+                                                      int8_t* xq, float* xs) {
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;
+  float v[kRowMax];
+  float a = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kRowMax; ++j) {
+    const int64_t i = threadIdx.x + 256 * j;
+    float x = 0.0f;
+    if (i < F) {
+      const float gv = ld_act(g, m * F + i);
+      x = gv / (1.0f + expf(-gv)) * ld_act(u, m * F + i);
+    }
+    v[j] = x;
+    a = fmaxf(a, fabsf(x));
+  }
+  a = bmax(a, red);
+  const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
+  if (threadIdx.x == 0) xs[m] = sc;
+#pragma unroll
+  for (int j = 0; j < kRowMax; ++j) {
+    const int64_t i = threadIdx.x + 256 * j;
+    if (i < F) xq[m * F + i] = q8(v[j], sc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Rotary embedding in place on x [M][H * hd]; pairs (i, i + hd/2) rotated by
+// the angle pos * base^(-2i/hd), cos/sin from a table [S][hd/2].
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) k_rope(T* x, int64_t M, int H, int hd, int S,
+                                              const float* cs, const float* sn) {
+  const int half = hd / 2;
+  const int64_t total = M * H * half;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * 256) {
+    const int i = (int)(t % half);
+    const int64_t mh = t / half;
+    const int64_t m = mh / H;
+    const int h = (int)(mh % H);
+    const int p = (int)(m % S);
+    const float c = cs[p * half + i], s = sn[p * half + i];
+    const int64_t base = m * (int64_t)H * hd + (int64_t)h * hd;
+    const float a = ld_act(x, base + i), b = ld_act(x, base + i + half);
+    st_act(x, base + i, a * c - b * s);
+    st_act(x, base + i + half, a * s + b * c);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Causal GQA attention, fp32 activations (small shapes): one block per
+// (query row, head); scores staged in LDS.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_attn_f32(const float* q, const float* k, const float* v,
+                                                  float* o, int S, int Hq, int Hkv, int hd,
+                                                  float scale) {
+  extern __shared__ float sc[];  // S scores
+  __shared__ float red[4];
+  const int64_t m = blockIdx.x;  // b * S + p
+  const int h = blockIdx.y;
+  const int p = (int)(m % S);
+  const int64_t b0 = m - p;
+  const int kh = h / (Hq / Hkv);
+  const float* qr = q + m * (int64_t)Hq * hd + (int64_t)h * hd;
+  float mx = -INFINITY;
+  for (int j = threadIdx.x; j <= p; j += 256) {
+    const float* kr = k + (b0 + j) * (int64_t)Hkv * hd + (int64_t)kh * hd;
+    float acc = 0.0f;
+    for (int e = 0; e < hd; ++e) acc = fmaf(qr[e], kr[e], acc);
+    sc[j] = acc * scale;
+    mx = fmaxf(mx, sc[j]);
+  }
+  mx = bmax(mx, red);
+  float sum = 0.0f;
+  for (int j = threadIdx.x; j <= p; j += 256) {
+    const float e = expf(sc[j] - mx);
+    sc[j] = e;
+    sum += e;
+  }
+  sum = bsum(sum, red);
+  __syncthreads();
+  for (int e = threadIdx.x; e < hd; e += 256) {
+    float acc = 0.0f;
+    for (int j = 0; j <= p; ++j) acc = fmaf(sc[j], v[(b0 + j) * (int64_t)Hkv * hd + (int64_t)kh * hd + e], acc);
+    o[m * (int64_t)Hq * hd + (int64_t)h * hd + e] = acc / sum;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Causal GQA flash attention on bf16 matrix cores (v_mfma_f32_16x16x32_bf16).
+// Block = 64 queries of one (batch, head); wave w owns 16 queries.  For each
+// 64-key tile: S^T = K Q^T (K from LDS as the A operand, Q^T from registers as
+// B), online softmax per query column (the query is the lane's column, so the
+// row statistics stay in the lane), then O^T += V^T P^T with P^T taken straight
+// from the S^T accumulators (K index of the 32-key step: group g, element j ->
+// key 16 (j / 4) + 4 g + j % 4) and V^T read from a transposed LDS copy.
+// ---------------------------------------------------------------------------
+template <int HD>
+__global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ q,
+                                                   const uint16_t* __restrict__ k,
+                                                   const uint16_t* __restrict__ v,
+                                                   uint16_t* __restrict__ o, int S, int Hq,
+                                                   int Hkv, float scale_log2) {
+  constexpr int KT = 64;               // keys per tile
+  constexpr int KS = HD + 8;           // K tile row stride (bf16)
+  constexpr int VS = KT + 8;           // V^T tile row stride (bf16)
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * VS];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c = lane & 15, g = lane >> 4;
+  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int kh = h / (Hq / Hkv);
+  const int64_t rowq = (int64_t)Hq * HD, rowkv = (int64_t)Hkv * HD;
+  const int64_t base = (int64_t)b * S;
+  const int qpos = qt * 64 + w * 16 + c;        // this lane's query position
+
+  // Q^T fragments: lane holds Q[qpos][32 s + 8 g .. +7]
+  v8bf qf[HD / 32];
+#pragma unroll
+  for (int s = 0; s < HD / 32; ++s) {
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (qpos < S)
+      raw = *reinterpret_cast<const uint4*>(q + (base + qpos) * rowq + (int64_t)h * HD + 32 * s + 8 * g);
+    qf[s] = __builtin_bit_cast(v8bf, raw);
+  }
+
+  v4f ot[HD / 16];
+#pragma unroll
+  for (int t = 0; t < HD / 16; ++t) ot[t] = v4f{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.0f;
+
+  const int last_tile = min(qt, (S - 1) / KT);
+  for (int kt = 0; kt <= last_tile; ++kt) {
+    const int k0 = kt * KT;
+    // ---- stage K [64][HD] and V^T [HD][64] ----
+    for (int e = tid; e < KT * HD / 8; e += 256) {
+      const int kr = e / (HD / 8), dc = (e % (HD / 8)) * 8;
+      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+      if (k0 + kr < S) {
+        const int64_t off = (base + k0 + kr) * rowkv + (int64_t)kh * HD + dc;
+        kv = *reinterpret_cast<const uint4*>(k + off);
+        vv = *reinterpret_cast<const uint4*>(v + off);
+      }
+      *reinterpret_cast<uint4*>(Ks + kr * KS + dc) = kv;
+      const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        Vt[(dc + 2 * j) * VS + kr] = (uint16_t)(vw[j] & 0xFFFFu);
+        Vt[(dc + 2 * j + 1) * VS + kr] = (uint16_t)(vw[j] >> 16);
+      }
+    }
+    __syncthreads();
+
+    // ---- S^T for the 4 key sub-tiles ----
+    v4f st[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      st[t] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < HD / 32; ++s) {
+        const uint4 raw = *reinterpret_cast<const uint4*>(Ks + (16 * t + c) * KS + 32 * s + 8 * g);
+        st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, raw), qf[s], st[t],
+                                                        0, 0, 0);
+      }
+    }
+    // st[t][i] = score(query c of this wave, key k0 + 16 t + 4 g + i)
+    float mx = mrun;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = k0 + 16 * t + 4 * g + i;
+        float sv = st[t][i] * scale_log2;
+        if (key > qpos || key >= S) sv = -INFINITY;
+        st[t][i] = sv;
+        mx = fmaxf(mx, sv);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mnew = mx;
+    const float alpha = (mrun == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mrun - mnew);
+    mrun = mnew;
+    float psum = 0.0f;
+    v8bf pf[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      uint32_t pk[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        // elements j = 2 jj, 2 jj + 1 -> sub-tile 2 hh + j / 4, register j % 4
+        const int j0 = 2 * jj, j1 = 2 * jj + 1;
+        const float p0 = st[2 * hh + j0 / 4][j0 % 4] == -INFINITY
+                             ? 0.0f
+                             : __builtin_amdgcn_exp2f(st[2 * hh + j0 / 4][j0 % 4] - mnew);
+        const float p1 = st[2 * hh + j1 / 4][j1 % 4] == -INFINITY
+                             ? 0.0f
+                             : __builtin_amdgcn_exp2f(st[2 * hh + j1 / 4][j1 % 4] - mnew);
+        psum += p0 + p1;
+        pk[jj] = (uint32_t)f32_to_bf16_rne(p0) | ((uint32_t)f32_to_bf16_rne(p1) << 16);
+      }
+      pf[hh] = __builtin_bit_cast(v8bf, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+    }
+    lrun = lrun * alpha + psum;
+#pragma unroll
+    for (int t = 0; t < HD / 16; ++t) {
+      ot[t] *= alpha;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        // A = V^T rows d = 16 t + c, keys 32 hh + {4g..4g+3} and 32 hh + 16 + {4g..4g+3}
+        const uint16_t* vr = Vt + (16 * t + c) * VS + 32 * hh + 4 * g;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        const v8bf af = __builtin_bit_cast(v8bf, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        ot[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, pf[hh], ot[t], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  // the partial sums of the 4 lanes sharing a query
+  lrun += __shfl_xor(lrun, 16, 64);
+  lrun += __shfl_xor(lrun, 32, 64);
+  if (qpos < S) {
+    const float inv = 1.0f / lrun;
+    uint16_t* orow = o + (base + qpos) * rowq + (int64_t)h * HD;
+#pragma unroll
+    for (int t = 0; t < HD / 16; ++t) {
+      const uint32_t w0 = (uint32_t)f32_to_bf16_rne(ot[t][0] * inv) |
+                          ((uint32_t)f32_to_bf16_rne(ot[t][1] * inv) << 16);
+      const uint32_t w1 = (uint32_t)f32_to_bf16_rne(ot[t][2] * inv) |
+                          ((uint32_t)f32_to_bf16_rne(ot[t][3] * inv) << 16);
+      *reinterpret_cast<uint2*>(orow + 16 * t + 4 * g) = make_uint2(w0, w1);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Tied LM head with cross-entropy partials.  For a tile of rows and 128 vocab
+// columns: the row maximum of the logits and the sum of exp(logit - max) over
+// the tile, plus the label logit when the label falls in the tile.
+// ---------------------------------------------------------------------------
+constexpr int kVT = 128;   // vocab columns per tile
+
+// fp32 activations: one thread per (row, column).
+__global__ void __launch_bounds__(256) k_lmhead_f32(const float* x, const float* E, int64_t M,
+                                                    int64_t d, int64_t V, const int32_t* labels,
+                                                    float* pmax, float* psum, float* lab,
+                                                    int64_t nvt) {
+  __shared__ float red[2][4];
+  const int64_t m = (int64_t)blockIdx.y * 2 + (threadIdx.x >> 7);
+  const int64_t n = (int64_t)blockIdx.x * kVT + (threadIdx.x & 127);
+  float logit = -INFINITY;
+  if (m < M && n < V) {
+    float acc = 0.0f;
+    for (int64_t e = 0; e < d; ++e) acc = fmaf(x[m * d + e], E[n * d + e], acc);
+    logit = acc;
+    if (labels[m] == n) lab[m] = acc;
+  }
+  // per half-block (one row) reductions: 2 waves per row
+  const int half = threadIdx.x >> 7, wv = (threadIdx.x >> 6) & 1;
+  float mx = wmax(logit);
+  if ((threadIdx.x & 63) == 0) red[half][wv] = mx;
+  __syncthreads();
+  mx = fmaxf(red[half][0], red[half][1]);
+  __syncthreads();
+  float e = (logit == -INFINITY) ? 0.0f : expf(logit - mx);
+  e = wsum(e);
+  if ((threadIdx.x & 63) == 0) red[half][2 + wv] = e;
+  __syncthreads();
+  if ((threadIdx.x & 127) == 0 && m < M) {
+    pmax[m * nvt + blockIdx.x] = mx;
+    psum[m * nvt + blockIdx.x] = red[half][2] + red[half][3];
+  }
+}
+
+// bf16 activations and embedding: 128 x 128 tile on v_mfma_f32_32x32x16_bf16,
+// logits staged in LDS for the row statistics.
+constexpr int kLStride = 80;   // bytes per staged row (32 bf16 + pad)
+__global__ void __launch_bounds__(256) k_lmhead_bf16(const uint16_t* __restrict__ x,
+                                                     const uint16_t* __restrict__ E, int64_t M,
+                                                     int64_t d, int64_t V,
+                                                     const int32_t* __restrict__ labels,
+                                                     float* pmax, float* psum, float* lab,
+                                                     int64_t nvt) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[128 * 129 * 4];
+  uint8_t* As = smem;
+  uint8_t* Bs = smem + 128 * kLStride;
+  float* Ls = reinterpret_cast<float*>(smem);   // reused after the main loop: [128][129]
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  const int64_t m0 = (int64_t)blockIdx.y * 128, n0 = (int64_t)blockIdx.x * kVT;
+  v16f acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][bb][r] = 0.0f;
+
+  for (int64_t k0 = 0; k0 < d; k0 += 32) {
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int cidx = tid + 256 * it;
+      const int row = cidx >> 2, c4 = cidx & 3;
+      const int64_t kk = k0 + 8 * c4;
+      uint4 av = make_uint4(0, 0, 0, 0), bv = make_uint4(0, 0, 0, 0);
+      if (m0 + row < M && kk < d) av = *reinterpret_cast<const uint4*>(x + (m0 + row) * d + kk);
+      if (n0 + row < V && kk < d) bv = *reinterpret_cast<const uint4*>(E + (n0 + row) * d + kk);
+      *reinterpret_cast<uint4*>(As + row * kLStride + 16 * c4) = av;
+      *reinterpret_cast<uint4*>(Bs + row * kLStride + 16 * c4) = bv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int kb = 32 * ks + 16 * (lane >> 5);   // byte offset: 16 bf16 per step
+      v8bf af[2], bf[2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+        af[a] = __builtin_bit_cast(
+            v8bf, *reinterpret_cast<const uint4*>(As + (wm * 64 + a * 32 + (lane & 31)) * kLStride + kb));
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+        bf[bb] = __builtin_bit_cast(
+            v8bf, *reinterpret_cast<const uint4*>(Bs + (wn * 64 + bb * 32 + (lane & 31)) * kLStride + kb));
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+          acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[bb], acc[a][bb], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  // stage logits: Ls[row][col]
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int li = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int lj = wn * 64 + bb * 32 + (lane & 31);
+        Ls[li * 129 + lj] = acc[a][bb][r];
+      }
+  __syncthreads();
+  // two threads per row, 64 columns each
+  const int row = tid >> 1, hf = tid & 1;
+  const int64_t m = m0 + row;
+  float mx = -INFINITY;
+  for (int j = 0; j < 64; ++j) {
+    const int64_t n = n0 + 64 * hf + j;
+    if (n < V) mx = fmaxf(mx, Ls[row * 129 + 64 * hf + j]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+  float se = 0.0f;
+  const int lbl = m < M ? labels[m] : -1;
+  for (int j = 0; j < 64; ++j) {
+    const int64_t n = n0 + 64 * hf + j;
+    if (n < V) {
+      const float lv = Ls[row * 129 + 64 * hf + j];
+      se += __builtin_amdgcn_exp2f((lv - mx) * 1.4426950408889634f);
+      if (n == lbl) lab[m] = lv;
+    }
+  }
+  se += __shfl_xor(se, 1, 64);
+  if (hf == 0 && m < M) {
+    pmax[m * nvt + blockIdx.x] = mx;
+    psum[m * nvt + blockIdx.x] = se;
+  }
+}
+
+// Row loss = logsumexp - label logit; the last position of each sequence has
+// no label (0).  One thread per row.
+__global__ void k_ce_combine(const float* pmax, const float* psum, const float* lab, int64_t M,
+                             int64_t nvt, int S, float* row_loss) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  float mx = -INFINITY;
+  for (int64_t t = 0; t < nvt; ++t) mx = fmaxf(mx, pmax[m * nvt + t]);
+  float s = 0.0f;
+  for (int64_t t = 0; t < nvt; ++t) s += psum[m * nvt + t] * expf(pmax[m * nvt + t] - mx);
+  const bool labelled = (m % S) != S - 1;
+  row_loss[m] = labelled ? (mx + logf(s)) - lab[m] : 0.0f;
+}
+
+// Mean over the labelled positions, fp64 accumulation in a fixed order.
+__global__ void __launch_bounds__(256) k_loss_mean(const float* row_loss, int64_t M, int64_t count,
+                                                   float* out_f32, double* out_f64) {
+  __shared__ double lds[256];
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < M; i += 256) acc += (double)row_loss[i];
+  lds[threadIdx.x] = acc;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) lds[threadIdx.x] += lds[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double mean = lds[0] / (double)count;
+    if (out_f64) *out_f64 = mean;
+    if (out_f32) *out_f32 = (float)mean;
+  }
+}
+
+__global__ void k_labels(const int32_t* tok, int64_t M, int S, int32_t* labels) {
+  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  labels[m] = ((m % S) != S - 1) ? tok[m + 1] : -1;
+}
+
+}  // namespace tmz
+
+// ===========================================================================
+// Model runtime
+// ===========================================================================
+using namespace tmz;
+
+struct termezo_model {
+  termezo_ctx* ctx = nullptr;
+  hipStream_t stream = nullptr;   // copy of the context's stream (destroy never reads ctx)
+  termezo_model_config cfg{};
+  const void* emb = nullptr;
+  int hd = 0;
+  int64_t cap_M = 0;
+  int cap_S = 0;
+  void *h = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *attn = nullptr, *g = nullptr,
+       *u = nullptr, *xf = nullptr;
+  int8_t* xq = nullptr;
+  float* xs = nullptr;
+  float *pmax = nullptr, *psum = nullptr, *lab = nullptr, *row = nullptr;
+  int32_t* labels = nullptr;
+  float *rope_c = nullptr, *rope_s = nullptr;
+  double* loss64 = nullptr;
+  float* loss32 = nullptr;
+};
+
+namespace {
+
+void mfree(void*& p) {
+  if (p) (void)hipFree(p);
+  p = nullptr;
+}
+
+void model_free_buffers(termezo_model* m) {
+  mfree(m->h); mfree(m->q); mfree(m->k); mfree(m->v); mfree(m->attn); mfree(m->g); mfree(m->u);
+  mfree(m->xf);
+  void* p;
+  p = m->xq; mfree(p); m->xq = nullptr;
+  p = m->xs; mfree(p); m->xs = nullptr;
+  p = m->pmax; mfree(p); m->pmax = nullptr;
+  p = m->psum; mfree(p); m->psum = nullptr;
+  p = m->lab; mfree(p); m->lab = nullptr;
+  p = m->row; mfree(p); m->row = nullptr;
+  p = m->labels; mfree(p); m->labels = nullptr;
+  p = m->rope_c; mfree(p); m->rope_c = nullptr;
+  p = m->rope_s; mfree(p); m->rope_s = nullptr;
+  p = m->loss64; mfree(p); m->loss64 = nullptr;
+  p = m->loss32; mfree(p); m->loss32 = nullptr;
+  m->cap_M = 0;
+  m->cap_S = 0;
+}
+
+termezo_status model_reserve(termezo_model* m, int64_t M, int S) {
+  if (M <= m->cap_M && S == m->cap_S) return TERMEZO_OK;
+  model_free_buffers(m);
+  const termezo_model_config& c = m->cfg;
+  const size_t es = c.act_dtype == TERMEZO_BF16 ? 2 : 4;
+  const int64_t dq = (int64_t)c.n_heads * m->hd, dkv = (int64_t)c.n_kv_heads * m->hd;
+  const int64_t kmax = std::max<int64_t>(std::max<int64_t>(c.d_model, dq), c.d_ffn);
+  const int64_t nvt = (c.vocab + kVT - 1) / kVT;
+  hipError_t e = hipSuccess;
+  auto A = [&](void** p, size_t bytes) {
+    if (e == hipSuccess) e = hipMalloc(p, bytes > 0 ? bytes : 1);
+  };
+  A(&m->h, M * c.d_model * es);
+  A(&m->q, M * dq * es);
+  A(&m->k, M * dkv * es);
+  A(&m->v, M * dkv * es);
+  A(&m->attn, M * dq * es);
+  A(&m->g, M * c.d_ffn * es);
+  A(&m->u, M * c.d_ffn * es);
+  A(&m->xf, M * c.d_model * es);
+  A((void**)&m->xq, M * kmax);
+  A((void**)&m->xs, M * 4);
+  A((void**)&m->pmax, M * nvt * 4);
+  A((void**)&m->psum, M * nvt * 4);
+  A((void**)&m->lab, M * 4);
+  A((void**)&m->row, M * 4);
+  A((void**)&m->labels, M * 4);
+  A((void**)&m->rope_c, (size_t)S * (m->hd / 2) * 4);
+  A((void**)&m->rope_s, (size_t)S * (m->hd / 2) * 4);
+  A((void**)&m->loss64, 8);
+  A((void**)&m->loss32, 4);
+  if (e != hipSuccess) {
+    model_free_buffers(m);
+    return e == hipErrorOutOfMemory ? TERMEZO_ERR_OOM : TERMEZO_ERR_DEVICE;
+  }
+  // rotary table: angle p * base^(-2i/hd), evaluated in fp64 and rounded to fp32
+  const int half = m->hd / 2;
+  std::vector<float> cs((size_t)S * half), sn((size_t)S * half);
+  for (int p = 0; p < S; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * std::pow((double)c.rope_base, -2.0 * i / (double)m->hd);
+      cs[(size_t)p * half + i] = (float)std::cos(ang);
+      sn[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  e = hipMemcpy(m->rope_c, cs.data(), cs.size() * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(m->rope_s, sn.data(), sn.size() * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    model_free_buffers(m);
+    return TERMEZO_ERR_DEVICE;
+  }
+  m->cap_M = M;
+  m->cap_S = S;
+  return TERMEZO_OK;
+}
+
+hipError_t run_attention(termezo_model* m, int B, int S, hipStream_t st) {
+  const termezo_model_config& c = m->cfg;
+  const int64_t M = (int64_t)B * S;
+  if (c.act_dtype == TERMEZO_F32) {
+    hipLaunchKernelGGL(k_attn_f32, dim3((unsigned)M, c.n_heads), dim3(256), S * sizeof(float), st,
+                       (const float*)m->q, (const float*)m->k, (const float*)m->v, (float*)m->attn,
+                       S, c.n_heads, c.n_kv_heads, m->hd, 1.0f / std::sqrt((float)m->hd));
+    return hipGetLastError();
+  }
+  const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)m->hd));
+  dim3 grid((unsigned)((S + 63) / 64), c.n_heads, B);
+#define TMZ_ATTN(HDV)                                                                        \
+  hipLaunchKernelGGL(k_attn_bf16<HDV>, grid, dim3(256), 0, st, (const uint16_t*)m->q,          \
+                     (const uint16_t*)m->k, (const uint16_t*)m->v, (uint16_t*)m->attn, S,      \
+                     c.n_heads, c.n_kv_heads, sl2)
+  switch (m->hd) {
+    case 64: TMZ_ATTN(64); break;
+    case 96: TMZ_ATTN(96); break;
+    case 128: TMZ_ATTN(128); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TMZ_ATTN
+  return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+termezo_status termezo_model_create(termezo_ctx* ctx, const termezo_model_config* cfg,
+                                    const void* embedding, termezo_model** out) {
+  if (!out) return TERMEZO_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!ctx || !cfg || !embedding) return TERMEZO_ERR_INVALID_ARG;
+  const termezo_model_config& c = *cfg;
+  if (c.n_blocks <= 0 || c.d_model <= 0 || c.n_heads <= 0 || c.n_kv_heads <= 0 ||
+      c.d_ffn <= 0 || c.vocab <= 0 || c.d_model % c.n_heads != 0 || c.n_heads % c.n_kv_heads != 0)
+    return TERMEZO_ERR_INVALID_ARG;
+  if (c.act_dtype != TERMEZO_F32 && c.act_dtype != TERMEZO_BF16) return TERMEZO_ERR_INVALID_ARG;
+  if (!(c.norm_eps > 0.0f) || !(c.rope_base > 1.0f)) return TERMEZO_ERR_INVALID_ARG;
+  const int hd = c.d_model / c.n_heads;
+  if (hd % 2 != 0 || c.d_model % 16 != 0 || c.d_ffn % 16 != 0) return TERMEZO_ERR_INVALID_ARG;
+  if (c.act_dtype == TERMEZO_BF16 && hd != 64 && hd != 96 && hd != 128)
+    return TERMEZO_ERR_INVALID_ARG;
+  if (std::max(c.d_model, c.d_ffn) > 256 * kRowMax) return TERMEZO_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(embedding) & 15u) != 0) return TERMEZO_ERR_INVALID_ARG;
+  if (ctx->L != 7 * c.n_blocks) return TERMEZO_ERR_INVALID_ARG;
+  const int64_t dq = (int64_t)c.n_heads * hd, dkv = (int64_t)c.n_kv_heads * hd;
+  const int64_t shp[7][2] = {{dq, c.d_model}, {dkv, c.d_model}, {dkv, c.d_model}, {c.d_model, dq},
+                             {c.d_ffn, c.d_model}, {c.d_ffn, c.d_model}, {c.d_model, c.d_ffn}};
+  for (int l = 0; l < ctx->L; ++l)
+    if (ctx->layers[l].d_out != shp[l % 7][0] || ctx->layers[l].d_in != shp[l % 7][1])
+      return TERMEZO_ERR_INVALID_ARG;
+  termezo_model* m = new (std::nothrow) termezo_model();
+  if (!m) return TERMEZO_ERR_OOM;
+  m->ctx = ctx;
+  m->stream = ctx->stream;
+  m->cfg = c;
+  m->emb = embedding;
+  m->hd = hd;
+  *out = m;
+  return TERMEZO_OK;
+}
+
+void termezo_model_destroy(termezo_model* m) {
+  if (!m) return;
+  (void)hipStreamSynchronize(m->stream);
+  model_free_buffers(m);
+  delete m;
+}
+
+termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32_t batch,
+                                  int32_t seq, float* loss_dev, float* row_loss_dev,
+                                  float* loss_host) {
+  if (!m || !tokens || batch <= 0 || seq < 2) return TERMEZO_ERR_INVALID_ARG;
+  termezo_ctx* c = m->ctx;
+  if (!c->codes_valid) {
+    c->last_error = "model_loss: no current codes (perturb first)";
+    return TERMEZO_ERR_STATE;
+  }
+  const termezo_model_config& cf = m->cfg;
+  const int64_t M = (int64_t)batch * seq;
+  termezo_status st = model_reserve(m, M, seq);
+  if (st != TERMEZO_OK) return st;
+  hipStream_t s = c->stream;
+  const bool bf = cf.act_dtype == TERMEZO_BF16;
+  const int64_t d = cf.d_model, F = cf.d_ffn, dq = (int64_t)cf.n_heads * m->hd,
+                dkv = (int64_t)cf.n_kv_heads * m->hd;
+  const int64_t nvt = (cf.vocab + kVT - 1) / kVT;
+  hipError_t e = hipSuccess;
+  auto chk = [&](hipError_t x) {
+    if (e == hipSuccess) e = x;
+  };
+  const termezo_dtype adt = cf.act_dtype;
+
+  if (bf)
+    hipLaunchKernelGGL(k_embed<uint16_t>, dim3((unsigned)M), dim3(256), 0, s, tokens,
+                       (const uint16_t*)m->emb, d, (uint16_t*)m->h);
+  else
+    hipLaunchKernelGGL(k_embed<float>, dim3((unsigned)M), dim3(256), 0, s, tokens,
+                       (const float*)m->emb, d, (float*)m->h);
+  chk(hipGetLastError());
+  hipLaunchKernelGGL(k_labels, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, tokens, M, seq,
+                     m->labels);
+  auto rmsq = [&](int8_t* xq, float* xs, void* xf) {
+    if (bf)
+      hipLaunchKernelGGL(k_rmsnorm_quant<uint16_t>, dim3((unsigned)M), dim3(256), 0, s,
+                         (const uint16_t*)m->h, d, cf.norm_eps, xq, xs, (uint16_t*)xf);
+    else
+      hipLaunchKernelGGL(k_rmsnorm_quant<float>, dim3((unsigned)M), dim3(256), 0, s,
+                         (const float*)m->h, d, cf.norm_eps, xq, xs, (float*)xf);
+    chk(hipGetLastError());
+  };
+  for (int blk = 0; blk < cf.n_blocks; ++blk) {
+    const int l0 = 7 * blk;
+    const LayerHost* Ls = &c->layers[l0];
+    // attention sub-block
+    rmsq(m->xq, m->xs, nullptr);
+    GemmOut o3 = {};
+    o3.nseg = 3;
+    o3.y[0] = m->q; o3.ld[0] = dq; o3.beta[0] = c->d_beta_cur + l0;
+    o3.y[1] = m->k; o3.ld[1] = dkv; o3.beta[1] = c->d_beta_cur + l0 + 1;
+    o3.y[2] = m->v; o3.ld[2] = dkv; o3.beta[2] = c->d_beta_cur + l0 + 2;
+    o3.nstart[0] = 0; o3.nstart[1] = dq; o3.nstart[2] = dq + dkv; o3.nstart[3] = dq + 2 * dkv;
+    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
+                       kGemmStore, nullptr, s));
+    const unsigned rg = (unsigned)std::min<int64_t>(8192, (M * cf.n_heads * (m->hd / 2) + 255) / 256);
+    if (bf) {
+      hipLaunchKernelGGL(k_rope<uint16_t>, dim3(rg), dim3(256), 0, s, (uint16_t*)m->q, M,
+                         cf.n_heads, m->hd, seq, m->rope_c, m->rope_s);
+      hipLaunchKernelGGL(k_rope<uint16_t>, dim3(rg), dim3(256), 0, s, (uint16_t*)m->k, M,
+                         cf.n_kv_heads, m->hd, seq, m->rope_c, m->rope_s);
+    } else {
+      hipLaunchKernelGGL(k_rope<float>, dim3(rg), dim3(256), 0, s, (float*)m->q, M, cf.n_heads,
+                         m->hd, seq, m->rope_c, m->rope_s);
+      hipLaunchKernelGGL(k_rope<float>, dim3(rg), dim3(256), 0, s, (float*)m->k, M,
+                         cf.n_kv_heads, m->hd, seq, m->rope_c, m->rope_s);
+    }
+    chk(hipGetLastError());
+    chk(run_attention(m, batch, seq, s));
+    chk(launch_act_quant(m->attn, adt, M, dq, m->xq, m->xs, s));
+    GemmOut oo = {};
+    oo.nseg = 1;
+    oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = c->d_beta_cur + l0 + 3;
+    oo.nstart[0] = 0; oo.nstart[1] = d;
+    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
+                       nullptr, s));
+    // MLP sub-block
+    rmsq(m->xq, m->xs, nullptr);
+    GemmOut o2 = {};
+    o2.nseg = 2;
+    o2.y[0] = m->g; o2.ld[0] = F; o2.beta[0] = c->d_beta_cur + l0 + 4;
+    o2.y[1] = m->u; o2.ld[1] = F; o2.beta[1] = c->d_beta_cur + l0 + 5;
+    o2.nstart[0] = 0; o2.nstart[1] = F; o2.nstart[2] = 2 * F;
+    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt, kGemmStore,
+                       nullptr, s));
+    if (bf)
+      hipLaunchKernelGGL(k_swiglu_quant<uint16_t>, dim3((unsigned)M), dim3(256), 0, s,
+                         (const uint16_t*)m->g, (const uint16_t*)m->u, F, m->xq, m->xs);
+    else
+      hipLaunchKernelGGL(k_swiglu_quant<float>, dim3((unsigned)M), dim3(256), 0, s,
+                         (const float*)m->g, (const float*)m->u, F, m->xq, m->xs);
+    chk(hipGetLastError());
+    GemmOut od = {};
+    od.nseg = 1;
+    od.y[0] = m->h; od.ld[0] = d; od.beta[0] = c->d_beta_cur + l0 + 6;
+    od.nstart[0] = 0; od.nstart[1] = d;
+    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
+                       nullptr, s));
+  }
+  rmsq(nullptr, nullptr, m->xf);
+  if (bf)
+    hipLaunchKernelGGL(k_lmhead_bf16, dim3((unsigned)nvt, (unsigned)((M + 127) / 128)), dim3(256), 0,
+                       s, (const uint16_t*)m->xf, (const uint16_t*)m->emb, M, d,
+                       (int64_t)cf.vocab, m->labels, m->pmax, m->psum, m->lab, nvt);
+  else
+    hipLaunchKernelGGL(k_lmhead_f32, dim3((unsigned)nvt, (unsigned)((M + 1) / 2)), dim3(256), 0, s,
+                       (const float*)m->xf, (const float*)m->emb, M, d, (int64_t)cf.vocab,
+                       m->labels, m->pmax, m->psum, m->lab, nvt);
+  chk(hipGetLastError());
+  float* rows = row_loss_dev ? row_loss_dev : m->row;
+  hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, m->pmax,
+                     m->psum, m->lab, M, nvt, seq, rows);
+  hipLaunchKernelGGL(k_loss_mean, dim3(1), dim3(256), 0, s, rows, M,
+                     (int64_t)batch * (seq - 1), loss_dev ? loss_dev : m->loss32, m->loss64);
+  chk(hipGetLastError());
+  if (e != hipSuccess) {
+    c->last_error = std::string("model_loss: ") + hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? TERMEZO_ERR_OOM : TERMEZO_ERR_DEVICE;
+  }
+  if (loss_host) {
+    double v = 0.0;
+    if (hipMemcpyAsync(&v, m->loss64, 8, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return TERMEZO_ERR_DEVICE;
+    *loss_host = (float)v;
+  }
+  return TERMEZO_OK;
+}
+
+}  // extern "C"

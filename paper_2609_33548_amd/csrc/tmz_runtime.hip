@@ -125,6 +125,7 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_tile_eqb);
   dfree(c->d_blk_cnt);
   dfree(c->d_loss);
+  dfree(c->d_scal);
   dfree(c->d_xq);
   dfree(c->d_xs);
 }
@@ -215,6 +216,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_tile_out, (size_t)c->T), "alloc");
   chk(dalloc(&c->d_tile_eqb, (size_t)c->T), "alloc");
   chk(dalloc(&c->d_loss, 4), "alloc");
+  chk(dalloc(&c->d_scal, 4), "alloc");
   if (st == TERMEZO_OK) {
     chk(hipMemcpy(c->d_wptr, wptr.data(), n_layers * sizeof(void*), hipMemcpyHostToDevice), "copy");
     chk(hipMemcpy(c->d_n, n.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice), "copy");
@@ -355,13 +357,11 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
   return TERMEZO_OK;
 }
 
-termezo_status termezo_update(termezo_ctx* c, float proj_grad, float lr, int64_t* k_out) {
-  if (!c) return TERMEZO_ERR_INVALID_ARG;
-  if (!finite(proj_grad) || !finite(lr))
-    return fail(c, TERMEZO_ERR_INVALID_ARG, "projected gradient and lr must be finite");
-  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
-  const float a = -(lr * proj_grad);
-  TMZ_HIP(c, launch_update(c, c->k_bound, c->last_seed, a));
+namespace {
+// Update at the actives with the coefficient already in d_scal, then the new
+// thresholds and the shrink; the compacted list replaces the old one.
+termezo_status finish_update(termezo_ctx* c, int64_t* k_out) {
+  TMZ_HIP(c, launch_update(c, c->k_bound, c->last_seed));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_clean, c->d_tau, c->d_beta));
   TMZ_HIP(c, launch_shrink(c, c->k_bound));
   std::swap(c->d_act, c->d_act_tmp);
@@ -378,6 +378,28 @@ termezo_status termezo_update(termezo_ctx* c, float proj_grad, float lr, int64_t
     *k_out = k;
   }
   return TERMEZO_OK;
+}
+}  // namespace
+
+termezo_status termezo_update(termezo_ctx* c, float proj_grad, float lr, int64_t* k_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!finite(proj_grad) || !finite(lr))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "projected gradient and lr must be finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  const float a = -(lr * proj_grad);
+  TMZ_HIP(c, launch_set_coeff(c, a));
+  return finish_update(c, k_out);
+}
+
+termezo_status termezo_update_from_losses(termezo_ctx* c, const float* loss_plus,
+                                          const float* loss_minus, float eps, float lr) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!loss_plus || !loss_minus) return fail(c, TERMEZO_ERR_INVALID_ARG, "null loss pointer");
+  if (!finite(eps) || !(eps > 0.0f) || !finite(lr))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "eps must be > 0 and lr finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  TMZ_HIP(c, launch_coeff_from_losses(c, loss_plus, loss_minus, eps, lr));
+  return finish_update(c, nullptr);
 }
 
 termezo_status termezo_gauss(void* hip_stream, uint64_t seed, const uint64_t* gids, int64_t n,

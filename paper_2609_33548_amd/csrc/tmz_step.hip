@@ -452,9 +452,27 @@ __global__ void __launch_bounds__(256) k_patch_codes(DevState st, const uint32_t
 // Masked update: w_i <- round(fma(a, z_i, w_i)), a = -(lr g); exact delta of
 // the clean fixed-point sum.
 // ---------------------------------------------------------------------------
+__global__ void k_set_coeff(float* scal, float a) {
+  scal[0] = a;
+  scal[1] = 0.0f;
+}
+
+// g = (F+ - F-) / (2 eps) and a = -(lr g), in fp32 (eq. spsa).
+__global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps, float lr,
+                                    float* scal, int32_t* err) {
+  const float g = __fdiv_rn(*fp - *fm, 2.0f * eps);
+  const float a = -(lr * g);
+  scal[0] = a;
+  scal[1] = g;
+  if (!isfinite(a)) atomicOr(err, 2);
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* act,
-                                                const int64_t* act_off, uint64_t seed, float a) {
+                                                const int64_t* act_off, uint64_t seed,
+                                                const float* scal) {
+  const float a = scal[0];
+  if (!isfinite(a)) return;   // reported by the coefficient kernel; latents untouched
   const int64_t k = act_off[st.L];
   const int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kRun;
   int l = j0 < k ? layer_of(act_off, st.L, j0) : 0;
@@ -721,16 +739,28 @@ hipError_t launch_patch_codes(termezo_ctx* c, int64_t k) {
   return hipGetLastError();
 }
 
-hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed, float a) {
+hipError_t launch_set_coeff(termezo_ctx* c, float a) {
+  hipLaunchKernelGGL(k_set_coeff, dim3(1), dim3(1), 0, c->stream, c->d_scal, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float* fm, float eps,
+                                    float lr) {
+  hipLaunchKernelGGL(k_coeff_from_losses, dim3(1), dim3(1), 0, c->stream, fp, fm, eps, lr,
+                     c->d_scal, c->d_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed) {
   if (k <= 0) return hipSuccess;
   const int64_t threads = (k + kRun - 1) / kRun;
   const int64_t g = (threads + 255) / 256;
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, a);
+                       c->d_act_off, seed, (const float*)c->d_scal);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, a);
+                       c->d_act_off, seed, (const float*)c->d_scal);
   return hipGetLastError();
 }
 

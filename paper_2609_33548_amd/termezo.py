@@ -7,8 +7,11 @@ importing this module without it raises ImportError.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import sys
+import weakref
 from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -29,6 +32,14 @@ class TermezoError(RuntimeError):
 
 class Layer(ctypes.Structure):
     _fields_ = [("latent", ctypes.c_void_p), ("d_out", ctypes.c_int64), ("d_in", ctypes.c_int64)]
+
+
+class ModelConfig(ctypes.Structure):
+    _fields_ = [("n_blocks", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("rope_base", ctypes.c_float), ("norm_eps", ctypes.c_float),
+                ("act_dtype", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -53,14 +64,31 @@ _SIGS = {
     "termezo_mse_loss": [_P, _P, _P, _i64, ctypes.POINTER(_f32)],
     "termezo_active_count": [_P, ctypes.POINTER(_i64)],
     "termezo_gauss": [_P, _u64, _P, _i64, _P],
+    "termezo_update_from_losses": [_P, _P, _P, _f32, _f32],
+    "termezo_model_create": [_P, _P, _P, ctypes.POINTER(_P)],
+    "termezo_model_destroy": [_P],
+    "termezo_model_loss": [_P, _P, _i32, _i32, _P, _P, ctypes.POINTER(_f32)],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
     _fn.argtypes = _args
-    _fn.restype = None if _name == "termezo_destroy" else (
+    _fn.restype = None if _name in ("termezo_destroy", "termezo_model_destroy") else (
         ctypes.c_char_p if _name == "termezo_last_error" else ctypes.c_int)
 
 lib = _lib
+
+# Contexts still open; closed (models first) before interpreter teardown, while
+# the HIP runtime is still alive.
+_LIVE = weakref.WeakSet()
+
+
+@atexit.register
+def _close_all():
+    for ctx in list(_LIVE):
+        try:
+            ctx.close()
+        except Exception:
+            pass
 
 
 def _ptr(t) -> Optional[int]:
@@ -116,6 +144,8 @@ class Context:
         self._stream = stream if stream is not None else torch.cuda.current_stream()
         self.handle = termezo_create([(w.data_ptr(), w.shape[0], w.shape[1]) for w in latents],
                                      self.dtype_code, int(self._stream.cuda_stream))
+        self._models = weakref.WeakSet()
+        _LIVE.add(self)
 
     def _check(self, st: int, what: str):
         if st != OK:
@@ -123,11 +153,15 @@ class Context:
             raise TermezoError(st, f"{what}: {msg.decode() if msg else ''}")
 
     def close(self):
+        for m in list(getattr(self, "_models", ())):
+            m.close()
         if getattr(self, "handle", None):
             _lib.termezo_destroy(self.handle)
             self.handle = None
 
     def __del__(self):
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
@@ -188,11 +222,58 @@ class Context:
         f = lambda v: float(np.float32(v.value))
         return {"tau": f(tau), "beta": f(beta), "S": int(S.value), "tau_cur": f(tc), "beta_cur": f(bc)}
 
+    def update_from_losses(self, loss_plus, loss_minus, eps: float, lr: float):
+        """Device-side g = (F+ - F-) / (2 eps) and update; no host round trip."""
+        self._check(_lib.termezo_update_from_losses(self.handle, _ptr(loss_plus), _ptr(loss_minus),
+                                                    eps, lr), "update_from_losses")
+
     def mse_loss(self, y, target) -> float:
         out = _f32()
         self._check(_lib.termezo_mse_loss(self.handle, _ptr(y), _ptr(target), y.numel(),
                                           ctypes.byref(out)), "mse_loss")
         return float(np.float32(out.value))
+
+
+class Model:
+    """BitNet decoder bound to a Context whose layers are the 7 projections of
+    each block (q, k, v, o, gate, up, down); ``embedding`` is the frozen tied
+    token embedding [vocab, d_model] (device tensor in the activation dtype)."""
+
+    def __init__(self, ctx: Context, n_blocks: int, d_model: int, n_heads: int, n_kv_heads: int,
+                 d_ffn: int, vocab: int, embedding, rope_base: float = 10000.0,
+                 norm_eps: float = 1e-5):
+        self.ctx = ctx
+        self.embedding = embedding
+        cfg = ModelConfig(n_blocks, d_model, n_heads, n_kv_heads, d_ffn, vocab, rope_base,
+                          norm_eps, _dtype_code(embedding))
+        out = _P()
+        st = _lib.termezo_model_create(ctx.handle, ctypes.byref(cfg), _ptr(embedding),
+                                       ctypes.byref(out))
+        if st != OK:
+            raise TermezoError(st, "termezo_model_create failed")
+        self.handle = out.value
+        ctx._models.add(self)
+
+    def loss(self, tokens, loss_dev=None, row_loss_dev=None, host: bool = True) -> Optional[float]:
+        B, S = tokens.shape
+        out = _f32()
+        st = _lib.termezo_model_loss(self.handle, _ptr(tokens), B, S, _ptr(loss_dev),
+                                     _ptr(row_loss_dev), ctypes.byref(out) if host else None)
+        self.ctx._check(st, "model_loss")
+        return float(np.float32(out.value)) if host else None
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _lib.termezo_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        if sys.is_finalizing():
+            return
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def gauss(seed: int, gids, stream=None):

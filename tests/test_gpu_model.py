@@ -1,0 +1,127 @@
+"""GPU parity of the decoder step (the loss TerMeZO evaluates at w +/- eps z)
+against the decoder oracle, through the C ABI.
+
+Bar (losses): 1e-3 relative on the batch loss; per-position losses 5e-3
+relative (bf16 storage of activations and bf16 attention probabilities on the
+device, fp64 on the oracle).  Updated latents: bit-exact when both sides use
+the same projected gradient."""
+import numpy as np
+import pytest
+
+from paper_2609_33548_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _build(orc, dec, cfg, seed, B, S):
+    torch = _torch()
+    from paper_2609_33548_amd import termezo
+    shapes = cfg.layer_shapes()
+    w = synth.latents(seed, [o * i for o, i in shapes], bf16=cfg.bf16)
+    ref = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w, bf16=cfg.bf16)
+    dt = torch.bfloat16 if cfg.bf16 else torch.float32
+    tensors, off = [], 0
+    for o, i in shapes:
+        tensors.append(torch.from_numpy(w[off: off + o * i].reshape(o, i)).cuda().to(dt))
+        off += o * i
+    ctx = termezo.Context(tensors)
+    emb = synth.latents(seed + 1, [cfg.vocab * cfg.d_model], bf16=cfg.bf16).reshape(cfg.vocab, cfg.d_model)
+    E = torch.from_numpy(emb).cuda().to(dt)
+    model = termezo.Model(ctx, cfg.n_blocks, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.d_ffn,
+                          cfg.vocab, E)
+    tok = synth.tokens(seed + 2, B, S, cfg.vocab)
+    return ref, ctx, model, tensors, emb, E, tok, torch.from_numpy(tok).cuda()
+
+
+def _compare(dec, cfg, ref, emb, tok, rows_gpu, loss_gpu, codes, betas, rtol_rows):
+    rrows = dec.forward_row_losses(cfg, emb, tok, codes, betas)
+    rl = dec.mean_loss(rrows)
+    assert abs(loss_gpu - rl) <= 1e-3 * abs(rl), (loss_gpu, rl)
+    lab = rrows[:, :-1]
+    got = rows_gpu.reshape(rrows.shape)[:, :-1]
+    rel = np.abs(got - lab) / np.abs(lab)
+    assert rel.max() <= rtol_rows, f"max rel {rel.max()} at {np.unravel_index(rel.argmax(), rel.shape)}"
+    assert np.all(rows_gpu.reshape(rrows.shape)[:, -1] == 0.0)
+    return rl
+
+
+def test_tiny_decoder_fp32_steps(orc):
+    """2 blocks, d = 256, 4 heads, FFN 688 (SwiGLU), vocab 1024, seq 64,
+    batch 4, fp32 latents and activations, mask 1%, eps = 1e-3."""
+    torch = _torch()
+    from oracle import decoder_ref as dec
+    cfg = dec.DecoderConfig(n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4, d_ffn=688, vocab=1024)
+    B, S = 4, 64
+    ref, ctx, model, tensors, emb, E, tok, tokd = _build(orc, dec, cfg, 30, B, S)
+    assert ctx.build_mask(0.01) == ref.build_mask(0.01)
+    rows = torch.empty(B * S, device="cuda")
+    eps, lr = 1e-3, 1e-4
+    for t in range(3):
+        F = {}
+        for sign in (1, -1):
+            ctx.perturb(t, eps, sign)
+            F[sign] = model.loss(tokd, row_loss_dev=rows)
+            codes, _, betas = ref.perturb(t, eps, sign)
+            _compare(dec, cfg, ref, emb, tok, rows.cpu().numpy(), F[sign], codes, betas, 2e-3)
+        g = orc.projected_grad(F[1], F[-1], eps)     # the device's losses drive both updates
+        assert ctx.update(g, lr) == ref.update(g, lr)
+        got = np.concatenate([x.cpu().numpy().ravel() for x in tensors])
+        assert np.array_equal(got, ref.w)
+    model.close()
+    ctx.close()
+
+
+@pytest.mark.parametrize("d,H,Hkv,F,V,S,B", [
+    (256, 2, 1, 256, 300, 130, 2),     # head_dim 128, GQA 2:1, ragged seq and vocab tiles
+    (192, 2, 2, 192, 257, 64, 3),      # head_dim 96
+    (256, 4, 2, 512, 1000, 200, 1),    # head_dim 64
+])
+def test_bf16_decoder_loss(orc, d, H, Hkv, F, V, S, B):
+    torch = _torch()
+    from oracle import decoder_ref as dec
+    print(f"bf16 decoder d={d} H={H}/{Hkv} S={S} B={B} V={V}", flush=True)
+    cfg = dec.DecoderConfig(n_blocks=2, d_model=d, n_heads=H, n_kv_heads=Hkv, d_ffn=F, vocab=V,
+                            bf16=True)
+    ref, ctx, model, tensors, emb, E, tok, tokd = _build(orc, dec, cfg, 40, B, S)
+    ctx.build_mask(0.01)
+    ref.build_mask(0.01)
+    rows = torch.empty(B * S, device="cuda")
+    ctx.perturb(5, 1e-3, 1)
+    loss = model.loss(tokd, row_loss_dev=rows)
+    codes, _, betas = ref.perturb(5, 1e-3, 1)
+    _compare(dec, cfg, ref, emb, tok, rows.cpu().numpy(), loss, codes, betas, 5e-3)
+    model.close()
+    ctx.close()
+
+
+def test_device_side_update_matches_host_update(orc):
+    torch = _torch()
+    from oracle import decoder_ref as dec
+    cfg = dec.DecoderConfig(n_blocks=1, d_model=128, n_heads=1, n_kv_heads=1, d_ffn=256, vocab=200,
+                            bf16=True)
+    ref, ctx, model, tensors, emb, E, tok, tokd = _build(orc, dec, cfg, 50, 2, 64)
+    ctx.build_mask(0.02)
+    ref.build_mask(0.02)
+    Fd = torch.zeros(2, device="cuda")
+    eps, lr = 1e-3, 5e-2
+    for t in range(3):
+        ctx.perturb(t, eps, 1)
+        fp = model.loss(tokd, loss_dev=Fd[0:1])
+        ctx.perturb(t, eps, -1)
+        fm = model.loss(tokd, loss_dev=Fd[1:2])
+        ctx.update_from_losses(Fd[0:1], Fd[1:2], eps, lr)
+        ref.perturb(t, eps, 1)
+        g = orc.projected_grad(fp, fm, eps)
+        ref.update(g, lr)
+        assert ctx.active_count() == ref.k
+        got = np.concatenate([x.float().cpu().numpy().ravel() for x in tensors])
+        assert np.array_equal(got, ref.w), f"step {t}"
+    model.close()
+    ctx.close()
