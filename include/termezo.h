@@ -191,6 +191,18 @@ termezo_status termezo_model_loss(termezo_model* model, const int32_t* tokens, i
                                   int32_t seq, float* loss_dev, float* row_loss_dev,
                                   float* loss_host);
 
+/* Event timing of the model's matrix-core kernels, for measurement: with
+ * enable != 0 every following termezo_model_loss records a HIP event pair on
+ * the context's stream around each launch of class 0 (BitLinear int8 GEMM),
+ * 1 (attention) and 2 (LM head with cross-entropy partials); enabling or
+ * disabling clears the records.  termezo_model_timing waits for the stream and
+ * returns, for one class, the summed kernel time in ms, the number of launches
+ * and their algorithmic operation count (2 M K N per GEMM; 4 B H hd S(S+1)/2
+ * for causal attention; 2 M d V for the LM head). */
+termezo_status termezo_model_set_timing(termezo_model* model, int32_t enable);
+termezo_status termezo_model_timing(termezo_model* model, int32_t cls, double* ms,
+                                    int64_t* launches, double* ops);
+
 /* ---- inspection and support calls (not part of the four hot-path calls) ---- */
 
 /* Wait for the context's stream; reports a deferred NUMERIC error. */

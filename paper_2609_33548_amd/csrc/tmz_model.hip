@@ -549,6 +549,16 @@ struct termezo_model {
   float *rope_c = nullptr, *rope_s = nullptr;
   double* loss64 = nullptr;
   float* loss32 = nullptr;
+  // optional event timing of the matrix-core kernels (class 0: BitLinear
+  // GEMM, 1: attention, 2: LM head + cross-entropy partials)
+  struct Span {
+    hipEvent_t a, b;
+    int cls;
+    double ops;
+  };
+  bool timing = false;
+  std::vector<Span> spans;
+  size_t used = 0;
 };
 
 namespace {
@@ -556,6 +566,24 @@ namespace {
 void mfree(void*& p) {
   if (p) (void)hipFree(p);
   p = nullptr;
+}
+
+int span_begin(termezo_model* m, int cls, double ops, hipStream_t s) {
+  if (!m->timing) return -1;
+  if (m->used == m->spans.size()) {
+    termezo_model::Span sp{};
+    if (hipEventCreate(&sp.a) != hipSuccess || hipEventCreate(&sp.b) != hipSuccess) return -1;
+    m->spans.push_back(sp);
+  }
+  termezo_model::Span& sp = m->spans[m->used];
+  sp.cls = cls;
+  sp.ops = ops;
+  if (hipEventRecord(sp.a, s) != hipSuccess) return -1;
+  return (int)m->used++;
+}
+
+void span_end(termezo_model* m, int idx, hipStream_t s) {
+  if (idx >= 0) (void)hipEventRecord(m->spans[idx].b, s);
 }
 
 void model_free_buffers(termezo_model* m) {
@@ -696,9 +724,42 @@ termezo_status termezo_model_create(termezo_ctx* ctx, const termezo_model_config
   return TERMEZO_OK;
 }
 
+termezo_status termezo_model_set_timing(termezo_model* m, int32_t enable) {
+  if (!m) return TERMEZO_ERR_INVALID_ARG;
+  if (hipStreamSynchronize(m->stream) != hipSuccess) return TERMEZO_ERR_DEVICE;
+  m->timing = enable != 0;
+  m->used = 0;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_model_timing(termezo_model* m, int32_t cls, double* ms, int64_t* launches,
+                                    double* ops) {
+  if (!m || cls < 0 || cls > 2) return TERMEZO_ERR_INVALID_ARG;
+  if (hipStreamSynchronize(m->stream) != hipSuccess) return TERMEZO_ERR_DEVICE;
+  double t = 0.0, o = 0.0;
+  int64_t n = 0;
+  for (size_t i = 0; i < m->used; ++i) {
+    const termezo_model::Span& sp = m->spans[i];
+    if (sp.cls != cls) continue;
+    float e = 0.0f;
+    if (hipEventElapsedTime(&e, sp.a, sp.b) != hipSuccess) return TERMEZO_ERR_DEVICE;
+    t += e;
+    o += sp.ops;
+    ++n;
+  }
+  if (ms) *ms = t;
+  if (launches) *launches = n;
+  if (ops) *ops = o;
+  return TERMEZO_OK;
+}
+
 void termezo_model_destroy(termezo_model* m) {
   if (!m) return;
   (void)hipStreamSynchronize(m->stream);
+  for (auto& sp : m->spans) {
+    (void)hipEventDestroy(sp.a);
+    (void)hipEventDestroy(sp.b);
+  }
   model_free_buffers(m);
   delete m;
 }
@@ -756,8 +817,10 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o3.y[1] = m->k; o3.ld[1] = dkv; o3.beta[1] = c->d_beta_cur + l0 + 1;
     o3.y[2] = m->v; o3.ld[2] = dkv; o3.beta[2] = c->d_beta_cur + l0 + 2;
     o3.nstart[0] = 0; o3.nstart[1] = dq; o3.nstart[2] = dq + dkv; o3.nstart[3] = dq + 2 * dkv;
+    int sp = span_begin(m, 0, 2.0 * M * d * (dq + 2 * dkv), s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
                        kGemmStore, nullptr, s));
+    span_end(m, sp, s);
     const unsigned rg = (unsigned)std::min<int64_t>(8192, (M * cf.n_heads * (m->hd / 2) + 255) / 256);
     if (bf) {
       hipLaunchKernelGGL(k_rope<uint16_t>, dim3(rg), dim3(256), 0, s, (uint16_t*)m->q, M,
@@ -771,14 +834,18 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                          cf.n_kv_heads, m->hd, seq, m->rope_c, m->rope_s);
     }
     chk(hipGetLastError());
+    sp = span_begin(m, 1, 4.0 * batch * cf.n_heads * m->hd * (0.5 * seq * (seq + 1.0)), s);
     chk(run_attention(m, batch, seq, s));
+    span_end(m, sp, s);
     chk(launch_act_quant(m->attn, adt, M, dq, m->xq, m->xs, s));
     GemmOut oo = {};
     oo.nseg = 1;
     oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = c->d_beta_cur + l0 + 3;
     oo.nstart[0] = 0; oo.nstart[1] = d;
+    sp = span_begin(m, 0, 2.0 * M * dq * d, s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
                        nullptr, s));
+    span_end(m, sp, s);
     // MLP sub-block
     rmsq(m->xq, m->xs, nullptr);
     GemmOut o2 = {};
@@ -786,8 +853,10 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o2.y[0] = m->g; o2.ld[0] = F; o2.beta[0] = c->d_beta_cur + l0 + 4;
     o2.y[1] = m->u; o2.ld[1] = F; o2.beta[1] = c->d_beta_cur + l0 + 5;
     o2.nstart[0] = 0; o2.nstart[1] = F; o2.nstart[2] = 2 * F;
+    sp = span_begin(m, 0, 2.0 * M * d * 2 * F, s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt, kGemmStore,
                        nullptr, s));
+    span_end(m, sp, s);
     if (bf)
       hipLaunchKernelGGL(k_swiglu_quant<uint16_t>, dim3((unsigned)M), dim3(256), 0, s,
                          (const uint16_t*)m->g, (const uint16_t*)m->u, F, m->xq, m->xs);
@@ -799,10 +868,13 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     od.nseg = 1;
     od.y[0] = m->h; od.ld[0] = d; od.beta[0] = c->d_beta_cur + l0 + 6;
     od.nstart[0] = 0; od.nstart[1] = d;
+    sp = span_begin(m, 0, 2.0 * M * F * d, s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
                        nullptr, s));
+    span_end(m, sp, s);
   }
   rmsq(nullptr, nullptr, m->xf);
+  const int sp_lm = span_begin(m, 2, 2.0 * M * d * cf.vocab, s);
   if (bf)
     hipLaunchKernelGGL(k_lmhead_bf16, dim3((unsigned)nvt, (unsigned)((M + 127) / 128)), dim3(256), 0,
                        s, (const uint16_t*)m->xf, (const uint16_t*)m->emb, M, d,
@@ -812,6 +884,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                        (const float*)m->xf, (const float*)m->emb, M, d, (int64_t)cf.vocab,
                        m->labels, m->pmax, m->psum, m->lab, nvt);
   chk(hipGetLastError());
+  span_end(m, sp_lm, s);
   float* rows = row_loss_dev ? row_loss_dev : m->row;
   hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, m->pmax,
                      m->psum, m->lab, M, nvt, seq, rows);

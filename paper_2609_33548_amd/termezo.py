@@ -68,6 +68,9 @@ _SIGS = {
     "termezo_model_create": [_P, _P, _P, ctypes.POINTER(_P)],
     "termezo_model_destroy": [_P],
     "termezo_model_loss": [_P, _P, _i32, _i32, _P, _P, ctypes.POINTER(_f32)],
+    "termezo_model_set_timing": [_P, _i32],
+    "termezo_model_timing": [_P, _i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
+                             ctypes.POINTER(ctypes.c_double)],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -261,6 +264,19 @@ class Model:
                                      _ptr(row_loss_dev), ctypes.byref(out) if host else None)
         self.ctx._check(st, "model_loss")
         return float(np.float32(out.value)) if host else None
+
+    GEMM, ATTENTION, LM_HEAD = 0, 1, 2
+
+    def set_timing(self, enable: bool):
+        self.ctx._check(_lib.termezo_model_set_timing(self.handle, int(enable)), "set_timing")
+
+    def timing(self, cls: int):
+        """(kernel ms summed, launches, algorithmic ops) recorded for one class."""
+        ms, ops = ctypes.c_double(), ctypes.c_double()
+        n = _i64()
+        self.ctx._check(_lib.termezo_model_timing(self.handle, cls, ctypes.byref(ms), ctypes.byref(n),
+                                                  ctypes.byref(ops)), "timing")
+        return float(ms.value), int(n.value), float(ops.value)
 
     def close(self):
         if getattr(self, "handle", None):
