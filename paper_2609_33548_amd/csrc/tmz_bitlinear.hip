@@ -8,6 +8,7 @@ namespace tmz {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // Activation quantisation, one block per token row:
@@ -68,133 +69,209 @@ __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int6
 }
 
 // ---------------------------------------------------------------------------
-// Tiled int8 GEMM  acc = x_q c^T  with 2-bit codes unpacked into LDS.
-// Block tile 128 x 128 x 64, 4 waves in a 2 x 2 grid, each wave 64 x 64 made
-// of 2 x 2 tiles of v_mfma_i32_32x32x32_i8.  Within each 32-wide K step,
-// lane l supplies the 16 bytes at k = 16 (l / 32) .. +15 of row l % 32 for
-// both operands, so A and B agree on the K assignment.
+// Tiled int8 GEMM  acc = x_q c^T  with the 2-bit codes unpacked into LDS.
+//
+// Block tile BM x BN x 64; the waves form a (BM/WM) x (BN/WN) grid and each
+// owns a WM x WN sub-tile made of v_mfma_i32_32x32x32_i8 tiles (int32
+// accumulators in AGPRs).  LDS holds two stages (double buffer, one barrier per
+// K step); the global loads of step i+2 are issued while step i is computed.
+// Within each 32-wide K step lane l supplies the 16 bytes at k = 16 (l / 32)
+// of row l % 32 for both operands, so A and B agree on the K assignment.
 // Accumulator layout (32 x 32, 16 values per lane): column l % 32,
 // row 8 (r / 4) + 4 (l / 32) + (r % 4).
+// LDS rows are 64 data bytes + 16 pad (80 B stride: the 16-byte fragment reads of
+// consecutive rows fall in distinct banks).
 // ---------------------------------------------------------------------------
-constexpr int kBM = 128, kBN = 128, kBK = 64;
-constexpr int kLdsStride = 80;   // bytes per LDS row (64 data + 16 pad)
+// Block tile BM x BN with a K step of BK = 128; 8 waves in a 2 x 4 grid, each
+// owning a 128 x 64 sub-tile of v_mfma_i32_32x32x32_i8 tiles (int32
+// accumulators).  Two LDS stages (one barrier per K step); the global loads of
+// step k+2 are issued after step k's MFMAs and stored to LDS after step k+1's.
+// Within each 32-wide K sub-step, lane l supplies the 16 bytes at
+// k = 16 (l / 32) of row l % 32 for both operands, so A and B agree on the K
+// assignment.  Accumulator layout (32 x 32, 16 values per lane): column l % 32,
+// row 8 (r / 4) + 4 (l / 32) + (r % 4).  LDS rows are 128 data bytes + 16 pad
+// (144 B: 16-byte fragment reads of 16 consecutive rows hit distinct banks).
+// FULL = every tile is in bounds (M % BM = N % BN = K % BK = 0): no predication.
+// ---------------------------------------------------------------------------
+constexpr int kBK = 128;
+constexpr int kLdsStride = kBK + 16;
 
-__device__ __forceinline__ float load_act(const float* p) { return *p; }
-__device__ __forceinline__ float load_act(const uint16_t* p) { return bf16_to_f32(*p); }
-__device__ __forceinline__ void store_act(float* p, float v) { *p = v; }
-__device__ __forceinline__ void store_act(uint16_t* p, float v) { *p = f32_to_bf16_rne(v); }
-__device__ __forceinline__ float round_act(const float*, float v) { return v; }
-__device__ __forceinline__ float round_act(const uint16_t*, float v) {
-  return bf16_to_f32(f32_to_bf16_rne(v));
+// Block order: consecutive workgroups are dealt round-robin to the 8 XCDs
+// (each with its own L2).  The linear id is remapped so that each XCD gets a
+// contiguous range of tiles, walked in groups of kGroupM block-rows (N
+// fastest inside a group), so tiles resident on one XCD share A rows and code
+// columns in that XCD's L2.
+constexpr int kXcd = 8;
+constexpr int kGroupM = 4;
+
+__device__ __forceinline__ void tile_of_block(int64_t nb_m, int64_t nb_n, int64_t& tm, int64_t& tn) {
+  const int64_t total = nb_m * nb_n;
+  const int64_t b = blockIdx.x;
+  const int64_t xcd = b % kXcd, local = b / kXcd;
+  const int64_t full = total / kXcd, rem = total % kXcd;
+  const int64_t lb = xcd * full + min(xcd, rem) + local;
+  const int64_t span = (int64_t)kGroupM * nb_n;
+  const int64_t g = lb / span, in = lb % span;
+  const int64_t gm = min((int64_t)kGroupM, nb_m - g * kGroupM);
+  tm = g * kGroupM + in % gm;
+  tn = in / gm;
 }
 
-template <typename TY, int MODE>
-__global__ void __launch_bounds__(256) k_gemm_i8(const int8_t* __restrict__ xq,
-                                                 const float* __restrict__ s,
-                                                 const uint32_t* __restrict__ codes, int64_t M,
-                                                 int64_t K, int64_t N, GemmOut out,
-                                                 int32_t* __restrict__ acc_out) {
-  __shared__ __attribute__((aligned(16))) int8_t As[kBM * kLdsStride];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[kBN * kLdsStride];
-  __shared__ float rrow[kMaxSeg][kBM];
+__device__ __forceinline__ void store_act(float* p, float v) { *p = v; }
+__device__ __forceinline__ void store_act(uint16_t* p, float v) {
+  *reinterpret_cast<__bf16*>(p) = (__bf16)v;
+}
+__device__ __forceinline__ float load_act(const float* p) { return *p; }
+__device__ __forceinline__ float load_act(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ float round_act(const float*, float v) { return v; }
+__device__ __forceinline__ float round_act(const uint16_t*, float v) { return (float)(__bf16)v; }
+
+template <int BM, int BN, int WM, int WN, bool FULL, typename TY, int MODE>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+    k_gemm_i8(const int8_t* __restrict__ xq, const float* __restrict__ s,
+              const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+              int32_t* __restrict__ acc_out) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  constexpr int TM = WM / 32, TN = WN / 32;         // MFMA tiles per wave
+  constexpr int CPR = kBK / 16;                     // 16-byte chunks per row
+  constexpr int A_CH = BM * CPR / NT;               // A chunks per thread per stage
+  constexpr int WPR = kBK / 16;                     // code words per row per stage
+  constexpr int B_WORDS = BN * WPR / NT;            // code words per thread per stage
+  static_assert(A_CH >= 1 && B_WORDS >= 1 && B_WORDS <= 4 && WPR % B_WORDS == 0, "tiling");
+  constexpr int STAGE = (BM + BN) * kLdsStride;
+  __shared__ __attribute__((aligned(16))) int8_t smem[2 * STAGE];
+  __shared__ float rrow[kMaxSeg][BM];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * kBM, n0 = (int64_t)blockIdx.x * kBN;
-  const int64_t KW = K / 16;  // code words per row
+  const int wm = wid / (BN / WN), wn = wid % (BN / WN);
+  int64_t tm, tn;
+  tile_of_block((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t KW = K / 16;                        // code words per row
+  const int nk = (int)((K + kBK - 1) / kBK);
 
-  for (int i = tid; i < kMaxSeg * kBM; i += 256) {
-    const int sg = i / kBM, r = i % kBM;
+  for (int i = tid; i < kMaxSeg * BM; i += NT) {
+    const int sg = i / BM, r = i % BM;
     const int64_t m = m0 + r;
     rrow[sg][r] = (sg < out.nseg && m < M) ? __fdiv_rn(*out.beta[sg], s[m]) : 0.0f;
   }
 
-  v16i acc[2][2];
+  const int brow = (tid * B_WORDS) / WPR, bw0 = (tid * B_WORDS) % WPR;
+  const int8_t* abase = xq + m0 * K;
+  const uint32_t* bbase = codes + (n0 + brow) * KW + bw0;
+
+  v4u ra[A_CH];
+  uint32_t rb[B_WORDS];
+  auto gload = [&](int kt) __attribute__((always_inline)) {
+    const int64_t k0 = (int64_t)kt * kBK;
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+    for (int it = 0; it < A_CH; ++it) {
+      const int c = tid + NT * it;
+      const int row = c / CPR, col = c % CPR;
+      if (FULL || (m0 + row < M && k0 + 16 * col < K))
+        ra[it] = *reinterpret_cast<const v4u*>(abase + row * K + k0 + 16 * col);
+      else
+        ra[it] = v4u{0u, 0u, 0u, 0u};
+    }
+    const int64_t kw0 = k0 / 16;
+    if constexpr (FULL && B_WORDS == 4) {
+      const v4u v = *reinterpret_cast<const v4u*>(bbase + kw0);
+      rb[0] = v.x;
+      rb[1] = v.y;
+      rb[2] = v.z;
+      rb[3] = v.w;
+    } else if constexpr (FULL && B_WORDS == 2) {
+      const uint2 v = *reinterpret_cast<const uint2*>(bbase + kw0);
+      rb[0] = v.x;
+      rb[1] = v.y;
+    } else {
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+      for (int j = 0; j < B_WORDS; ++j)
+        rb[j] = (FULL || (n0 + brow < N && kw0 + bw0 + j < KW)) ? bbase[kw0 + j] : 0u;
+    }
+  };
+  auto lstore = [&](int buf) __attribute__((always_inline)) {
+    int8_t* As = smem + buf * STAGE;
+    int8_t* Bs = As + BM * kLdsStride;
+#pragma unroll
+    for (int it = 0; it < A_CH; ++it) {
+      const int c = tid + NT * it;
+      *reinterpret_cast<v4u*>(As + (c / CPR) * kLdsStride + 16 * (c % CPR)) = ra[it];
+    }
+#pragma unroll
+    for (int j = 0; j < B_WORDS; ++j) {
+      const v4u v = {unpack_group(rb[j], 0), unpack_group(rb[j], 1), unpack_group(rb[j], 2),
+                     unpack_group(rb[j], 3)};
+      *reinterpret_cast<v4u*>(Bs + brow * kLdsStride + 16 * (bw0 + j)) = v;
+    }
+  };
+
+  v16i acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
 
-  for (int64_t k0 = 0; k0 < K; k0 += kBK) {
-    // ---- stage A: 128 rows x 64 bytes ----
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int8_t* As = smem + (kt & 1) * STAGE;
+    const int8_t* Bs = As + BM * kLdsStride;
 #pragma unroll
-    for (int it = 0; it < 2; ++it) {
-      const int c = tid + 256 * it;
-      const int row = c >> 2, c16 = c & 3;
-      const int64_t m = m0 + row, k = k0 + 16 * c16;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (m < M && k < K) v = *reinterpret_cast<const uint4*>(xq + m * K + k);
-      *reinterpret_cast<uint4*>(As + row * kLdsStride + 16 * c16) = v;
-    }
-    // ---- stage B: 128 rows x 4 code words, unpacked to int8 ----
-#pragma unroll
-    for (int it = 0; it < 2; ++it) {
-      const int c = tid + 256 * it;
-      const int row = c >> 2, wi = c & 3;
-      const int64_t n = n0 + row, kw = k0 / 16 + wi;
-      uint32_t word = 0;
-      if (n < N && kw < KW) word = codes[n * KW + kw];
-      uint4 v;
-      v.x = unpack_group(word, 0);
-      v.y = unpack_group(word, 1);
-      v.z = unpack_group(word, 2);
-      v.w = unpack_group(word, 3);
-      *reinterpret_cast<uint4*>(Bs + row * kLdsStride + 16 * wi) = v;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < kBK / 32; ++ks) {
       const int kb = 32 * ks + 16 * (lane >> 5);
-      v4i af[2], bf[2];
+      v4i af[TM], bf[TN];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        const int row = wm * 64 + a * 32 + (lane & 31);
-        af[a] = *reinterpret_cast<const v4i*>(As + row * kLdsStride + kb);
-      }
+      for (int a = 0; a < TM; ++a)
+        af[a] = *reinterpret_cast<const v4i*>(As + (wm * WM + a * 32 + (lane & 31)) * kLdsStride + kb);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int row = wn * 64 + b * 32 + (lane & 31);
-        bf[b] = *reinterpret_cast<const v4i*>(Bs + row * kLdsStride + kb);
-      }
+      for (int b = 0; b < TN; ++b)
+        bf[b] = *reinterpret_cast<const v4i*>(Bs + (wn * WN + b * 32 + (lane & 31)) * kLdsStride + kb);
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < TN; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[a], bf[b], acc[a][b], 0, 0, 0);
+    }
+    if (kt + 1 < nk) {
+      lstore((kt + 1) & 1);
+      if (kt + 2 < nk) gload(kt + 2);
     }
     __syncthreads();
   }
 
   // ---- epilogue: y = float(acc) * (beta_seg / s_m); segments split N ----
+  const int rl = wm * WM + 4 * (lane >> 5);          // lane's first local row
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int64_t n = n0 + wn * 64 + b * 32 + (lane & 31);
-    if (n >= N) continue;
+  for (int b = 0; b < TN; ++b) {
+    const int64_t n = n0 + wn * WN + b * 32 + (lane & 31);
+    if (!FULL && n >= N) continue;
     int sg = 0;
     if (out.nseg > 1 && n >= out.nstart[1]) sg = 1;
     if (out.nseg > 2 && n >= out.nstart[2]) sg = 2;
-    TY* y = reinterpret_cast<TY*>(out.y[sg]);
     const int64_t ld = out.ld[sg];
-    const int64_t nl = n - out.nstart[sg];
+    TY* colp = reinterpret_cast<TY*>(out.y[sg]) + (n - out.nstart[sg]) + (m0 + rl) * ld;
+    const float* rr = &rrow[sg][rl];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < TM; ++a)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int li = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int64_t m = m0 + li;
-        if (m < M) {
+        const int ro = a * 32 + 8 * (r >> 2) + (r & 3);
+        if (FULL || m0 + rl + ro < M) {
           const int32_t v = acc[a][b][r];
-          const float yv = (float)v * rrow[sg][li];
-          TY* p = y + m * ld + nl;
+          const float yv = (float)v * rr[ro];
+          TY* p = colp + (int64_t)ro * ld;
           if (MODE == kGemmStore) {
             store_act(p, yv);
           } else {  // residual: h <- round(h + round(y))
             store_act(p, load_act(p) + round_act(p, yv));
           }
-          if (acc_out) acc_out[m * N + n] = v;
+          if (acc_out) acc_out[(m0 + rl + ro) * N + n] = v;
         }
       }
   }
@@ -211,26 +288,43 @@ hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WM, int WN, bool FULL>
+static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
+                              int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
+                              int32_t* acc, hipStream_t st) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  dim3 grid((unsigned)(((N + BN - 1) / BN) * ((M + BM - 1) / BM)));
+  if (ydt == TERMEZO_F32) {
+    if (mode == kGemmStore)
+      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, float, kGemmStore>), grid, dim3(NT), 0, st,
+                         xq, s, codes, M, K, N, out, acc);
+    else
+      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, float, kGemmResidual>), grid, dim3(NT), 0,
+                         st, xq, s, codes, M, K, N, out, acc);
+  } else {
+    if (mode == kGemmStore)
+      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, uint16_t, kGemmStore>), grid, dim3(NT), 0,
+                         st, xq, s, codes, M, K, N, out, acc);
+    else
+      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, uint16_t, kGemmResidual>), grid, dim3(NT),
+                         0, st, xq, s, codes, M, K, N, out, acc);
+  }
+  return hipGetLastError();
+}
+
+// Tile choice: 256 x 256 blocks of 8 waves (128 x 64 per wave, two waves per
+// SIMD) when the grid fills the chip, 128 x 128 blocks of 4 waves otherwise;
+// the unpredicated variant when every tile is in bounds.
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
                           int32_t* acc, hipStream_t st) {
-  dim3 grid((unsigned)((N + kBN - 1) / kBN), (unsigned)((M + kBM - 1) / kBM));
-  if (ydt == TERMEZO_F32) {
-    if (mode == kGemmStore)
-      hipLaunchKernelGGL((k_gemm_i8<float, kGemmStore>), grid, dim3(256), 0, st, xq, s, codes, M, K,
-                         N, out, acc);
-    else
-      hipLaunchKernelGGL((k_gemm_i8<float, kGemmResidual>), grid, dim3(256), 0, st, xq, s, codes, M,
-                         K, N, out, acc);
-  } else {
-    if (mode == kGemmStore)
-      hipLaunchKernelGGL((k_gemm_i8<uint16_t, kGemmStore>), grid, dim3(256), 0, st, xq, s, codes, M,
-                         K, N, out, acc);
-    else
-      hipLaunchKernelGGL((k_gemm_i8<uint16_t, kGemmResidual>), grid, dim3(256), 0, st, xq, s, codes,
-                         M, K, N, out, acc);
+  const int64_t big_blocks = ((M + 255) / 256) * ((N + 255) / 256);
+  if (big_blocks >= 256) {
+    if (M % 256 == 0 && N % 256 == 0 && K % kBK == 0)
+      return launch_tile<256, 256, 128, 64, true>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
+    return launch_tile<256, 256, 128, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
   }
-  return hipGetLastError();
+  return launch_tile<128, 128, 64, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
 }
 
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
