@@ -185,4 +185,25 @@ __device__ __forceinline__ uint32_t unpack_group(uint32_t word, int i) {
   return __builtin_amdgcn_perm(0u, 0xFFFF0100u, sel);
 }
 
+// Block order: consecutive workgroups are dealt round-robin to the 8 XCDs
+// (each with its own L2).  The linear id is remapped so that each XCD gets a
+// contiguous range of tiles, walked in groups of kGroupM block-rows (N
+// fastest inside a group), so tiles resident on one XCD share A rows and code
+// columns in that XCD's L2.
+constexpr int kXcd = 8;
+constexpr int kGroupM = 4;
+
+__device__ __forceinline__ void tile_of_block(int64_t nb_m, int64_t nb_n, int64_t& tm, int64_t& tn) {
+  const int64_t total = nb_m * nb_n;
+  const int64_t b = blockIdx.x;
+  const int64_t xcd = b % kXcd, local = b / kXcd;
+  const int64_t full = total / kXcd, rem = total % kXcd;
+  const int64_t lb = xcd * full + min(xcd, rem) + local;
+  const int64_t span = (int64_t)kGroupM * nb_n;
+  const int64_t g = lb / span, in = lb % span;
+  const int64_t gm = min((int64_t)kGroupM, nb_m - g * kGroupM);
+  tm = g * kGroupM + in % gm;
+  tn = in / gm;
+}
+
 }  // namespace tmz

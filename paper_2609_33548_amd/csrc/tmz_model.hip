@@ -390,114 +390,184 @@ __global__ void __launch_bounds__(256) k_lmhead_f32(const float* x, const float*
   }
 }
 
-// bf16 activations and embedding: 128 x 128 tile on v_mfma_f32_32x32x16_bf16,
-// logits staged in LDS for the row statistics.
-constexpr int kLStride = 80;   // bytes per staged row (32 bf16 + pad)
-__global__ void __launch_bounds__(256) k_lmhead_bf16(const uint16_t* __restrict__ x,
+// bf16 activations and embedding: 256 x 256 tiles of 8 waves (128 x 64 per
+// wave) of v_mfma_f32_32x32x16_bf16, K step 64 (128 bytes per row, 144-byte
+// LDS rows), double-buffered LDS, XCD-grouped tile order.  Epilogue: per row,
+// max and sum of exp over the tile's columns by lane shuffles (each row's 64
+// columns of a wave live in 32 lanes x 2 registers), then the 4 waves along N
+// are combined through LDS.
+constexpr int kLmBK = 64;                  // bf16 elements per K step
+constexpr int kLmStride = 2 * kLmBK + 16;  // bytes per LDS row
+constexpr int kLmTile = 256;               // rows and vocab columns per block
+
+template <bool FULL>
+__global__ void __launch_bounds__(512) k_lmhead_bf16(const uint16_t* __restrict__ x,
                                                      const uint16_t* __restrict__ E, int64_t M,
                                                      int64_t d, int64_t V,
                                                      const int32_t* __restrict__ labels,
                                                      float* pmax, float* psum, float* lab,
                                                      int64_t nvt) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[128 * 129 * 4];
-  uint8_t* As = smem;
-  uint8_t* Bs = smem + 128 * kLStride;
-  float* Ls = reinterpret_cast<float*>(smem);   // reused after the main loop: [128][129]
+  constexpr int BM = kLmTile, BN = kLmTile, WM = 128, WN = 64, NT = 512;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int CPR = 2 * kLmBK / 16;      // 16-byte chunks per row (8)
+  constexpr int CH = BM * CPR / NT;        // chunks per thread per operand (4)
+  constexpr int STAGE = (BM + BN) * kLmStride;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+  __shared__ int32_t lbl[BM];
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * 128, n0 = (int64_t)blockIdx.x * kVT;
-  v16f acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][bb][r] = 0.0f;
+  const int wm = wid / (BN / WN), wn = wid % (BN / WN);
+  int64_t tm, tn;
+  tile_of_block((M + BM - 1) / BM, nvt, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int nk = (int)((d + kLmBK - 1) / kLmBK);
+  for (int i = tid; i < BM; i += NT) lbl[i] = m0 + i < M ? labels[m0 + i] : -1;
 
-  for (int64_t k0 = 0; k0 < d; k0 += 32) {
+  typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+  v4u ra[CH], rb[CH];
+  const uint8_t* xa = reinterpret_cast<const uint8_t*>(x) + m0 * d * 2;
+  const uint8_t* eb = reinterpret_cast<const uint8_t*>(E) + n0 * d * 2;
+  auto gload = [&](int kt) __attribute__((always_inline)) {
+    const int64_t kb0 = (int64_t)kt * kLmBK * 2;   // byte offset in a row
 #pragma unroll
-    for (int it = 0; it < 2; ++it) {
-      const int cidx = tid + 256 * it;
-      const int row = cidx >> 2, c4 = cidx & 3;
-      const int64_t kk = k0 + 8 * c4;
-      uint4 av = make_uint4(0, 0, 0, 0), bv = make_uint4(0, 0, 0, 0);
-      if (m0 + row < M && kk < d) av = *reinterpret_cast<const uint4*>(x + (m0 + row) * d + kk);
-      if (n0 + row < V && kk < d) bv = *reinterpret_cast<const uint4*>(E + (n0 + row) * d + kk);
-      *reinterpret_cast<uint4*>(As + row * kLStride + 16 * c4) = av;
-      *reinterpret_cast<uint4*>(Bs + row * kLStride + 16 * c4) = bv;
+    for (int it = 0; it < CH; ++it) {
+      const int c = tid + NT * it;
+      const int row = c / CPR, col = c % CPR;
+      const int64_t kb = kb0 + 16 * col;
+      const bool kin = FULL || kb < d * 2;
+      ra[it] = (kin && (FULL || m0 + row < M))
+                   ? *reinterpret_cast<const v4u*>(xa + row * d * 2 + kb)
+                   : v4u{0u, 0u, 0u, 0u};
+      rb[it] = (kin && (FULL || n0 + row < V))
+                   ? *reinterpret_cast<const v4u*>(eb + row * d * 2 + kb)
+                   : v4u{0u, 0u, 0u, 0u};
     }
-    __syncthreads();
+  };
+  auto lstore = [&](int buf) __attribute__((always_inline)) {
+    uint8_t* As = smem + buf * STAGE;
+    uint8_t* Bs = As + BM * kLmStride;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int kb = 32 * ks + 16 * (lane >> 5);   // byte offset: 16 bf16 per step
-      v8bf af[2], bf[2];
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-        af[a] = __builtin_bit_cast(
-            v8bf, *reinterpret_cast<const uint4*>(As + (wm * 64 + a * 32 + (lane & 31)) * kLStride + kb));
-#pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
-        bf[bb] = __builtin_bit_cast(
-            v8bf, *reinterpret_cast<const uint4*>(Bs + (wn * 64 + bb * 32 + (lane & 31)) * kLStride + kb));
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int bb = 0; bb < 2; ++bb)
-          acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[bb], acc[a][bb], 0, 0, 0);
+    for (int it = 0; it < CH; ++it) {
+      const int c = tid + NT * it;
+      const int off = (c / CPR) * kLmStride + 16 * (c % CPR);
+      *reinterpret_cast<v4u*>(As + off) = ra[it];
+      *reinterpret_cast<v4u*>(Bs + off) = rb[it];
     }
-    __syncthreads();
-  }
-  // stage logits: Ls[row][col]
+  };
+
+  v16f acc[TM][TN];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < TM; ++a)
 #pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
+    for (int b = 0; b < TN; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int li = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int lj = wn * 64 + bb * 32 + (lane & 31);
-        Ls[li * 129 + lj] = acc[a][bb][r];
-      }
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
   __syncthreads();
-  // two threads per row, 64 columns each
-  const int row = tid >> 1, hf = tid & 1;
-  const int64_t m = m0 + row;
-  float mx = -INFINITY;
-  for (int j = 0; j < 64; ++j) {
-    const int64_t n = n0 + 64 * hf + j;
-    if (n < V) mx = fmaxf(mx, Ls[row * 129 + 64 * hf + j]);
-  }
-  mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
-  float se = 0.0f;
-  const int lbl = m < M ? labels[m] : -1;
-  for (int j = 0; j < 64; ++j) {
-    const int64_t n = n0 + 64 * hf + j;
-    if (n < V) {
-      const float lv = Ls[row * 129 + 64 * hf + j];
-      se += __builtin_amdgcn_exp2f((lv - mx) * 1.4426950408889634f);
-      if (n == lbl) lab[m] = lv;
+  for (int kt = 0; kt < nk; ++kt) {
+    const uint8_t* As = smem + (kt & 1) * STAGE;
+    const uint8_t* Bs = As + BM * kLmStride;
+#pragma unroll
+    for (int ks = 0; ks < 2 * kLmBK / 32; ++ks) {
+      const int kb = 32 * ks + 16 * (lane >> 5);
+      v8bf af[TM], bf[TN];
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+        af[a] = __builtin_bit_cast(
+            v8bf, *reinterpret_cast<const v4u*>(As + (wm * WM + a * 32 + (lane & 31)) * kLmStride + kb));
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        bf[b] = __builtin_bit_cast(
+            v8bf, *reinterpret_cast<const v4u*>(Bs + (wn * WN + b * 32 + (lane & 31)) * kLmStride + kb));
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[b], acc[a][b], 0, 0, 0);
     }
+    if (kt + 1 < nk) {
+      lstore((kt + 1) & 1);
+      if (kt + 2 < nk) gload(kt + 2);
+    }
+    __syncthreads();
   }
-  se += __shfl_xor(se, 1, 64);
-  if (hf == 0 && m < M) {
-    pmax[m * nvt + blockIdx.x] = mx;
-    psum[m * nvt + blockIdx.x] = se;
+
+  // ---- epilogue: row statistics of this tile ----
+  float* red = reinterpret_cast<float*>(smem);     // [4 waves along N][BM][2]
+  const float L2E = 1.4426950408889634f;
+  bool colok[TN];
+  int64_t col[TN];
+#pragma unroll
+  for (int b = 0; b < TN; ++b) {
+    col[b] = n0 + wn * WN + b * 32 + (lane & 31);
+    colok[b] = FULL || col[b] < V;
+  }
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int li = wm * WM + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        if (colok[b]) mx = fmaxf(mx, acc[a][b][r]);
+#pragma unroll
+      for (int off = 1; off < 32; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      float se = 0.0f;
+      const int lb = lbl[li];
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        if (colok[b]) {
+          se += __builtin_amdgcn_exp2f((acc[a][b][r] - mx) * L2E);
+          if (col[b] == lb) lab[m0 + li] = acc[a][b][r];
+        }
+#pragma unroll
+      for (int off = 1; off < 32; off <<= 1) se += __shfl_xor(se, off, 64);
+      if ((lane & 31) == 0) {
+        red[(wn * BM + li) * 2 + 0] = mx;
+        red[(wn * BM + li) * 2 + 1] = se;
+      }
+    }
+  __syncthreads();
+  if (tid < BM && (FULL || m0 + tid < M)) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < BN / WN; ++w) mx = fmaxf(mx, red[(w * BM + tid) * 2]);
+    float se = 0.0f;
+#pragma unroll
+    for (int w = 0; w < BN / WN; ++w) {
+      const float mw = red[(w * BM + tid) * 2];
+      if (mw != -INFINITY) se += red[(w * BM + tid) * 2 + 1] * __builtin_amdgcn_exp2f((mw - mx) * L2E);
+    }
+    pmax[(m0 + tid) * nvt + tn] = mx;
+    psum[(m0 + tid) * nvt + tn] = se;
   }
 }
 
 // Row loss = logsumexp - label logit; the last position of each sequence has
-// no label (0).  One thread per row.
-__global__ void k_ce_combine(const float* pmax, const float* psum, const float* lab, int64_t M,
-                             int64_t nvt, int S, float* row_loss) {
-  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// no label (0).  One wave per row over the vocabulary-tile partials.
+__global__ void __launch_bounds__(256) k_ce_combine(const float* pmax, const float* psum,
+                                                    const float* lab, int64_t M, int64_t nvt, int S,
+                                                    float* row_loss) {
+  const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (m >= M) return;
   float mx = -INFINITY;
-  for (int64_t t = 0; t < nvt; ++t) mx = fmaxf(mx, pmax[m * nvt + t]);
+  for (int64_t t = lane; t < nvt; t += 64) mx = fmaxf(mx, pmax[m * nvt + t]);
+  mx = wmax(mx);
   float s = 0.0f;
-  for (int64_t t = 0; t < nvt; ++t) s += psum[m * nvt + t] * expf(pmax[m * nvt + t] - mx);
-  const bool labelled = (m % S) != S - 1;
-  row_loss[m] = labelled ? (mx + logf(s)) - lab[m] : 0.0f;
+  for (int64_t t = lane; t < nvt; t += 64) {
+    const float pm = pmax[m * nvt + t];
+    if (pm != -INFINITY) s += psum[m * nvt + t] * expf(pm - mx);
+  }
+  s = wsum(s);
+  if (lane == 0) {
+    const bool labelled = (m % S) != S - 1;
+    row_loss[m] = labelled ? (mx + logf(s)) - lab[m] : 0.0f;
+  }
 }
 
 // Mean over the labelled positions, fp64 accumulation in a fixed order.
@@ -612,7 +682,8 @@ termezo_status model_reserve(termezo_model* m, int64_t M, int S) {
   const size_t es = c.act_dtype == TERMEZO_BF16 ? 2 : 4;
   const int64_t dq = (int64_t)c.n_heads * m->hd, dkv = (int64_t)c.n_kv_heads * m->hd;
   const int64_t kmax = std::max<int64_t>(std::max<int64_t>(c.d_model, dq), c.d_ffn);
-  const int64_t nvt = (c.vocab + kVT - 1) / kVT;
+  const int64_t nvt = c.act_dtype == TERMEZO_BF16 ? (c.vocab + kLmTile - 1) / kLmTile
+                                                  : (c.vocab + kVT - 1) / kVT;
   hipError_t e = hipSuccess;
   auto A = [&](void** p, size_t bytes) {
     if (e == hipSuccess) e = hipMalloc(p, bytes > 0 ? bytes : 1);
@@ -781,7 +852,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   const bool bf = cf.act_dtype == TERMEZO_BF16;
   const int64_t d = cf.d_model, F = cf.d_ffn, dq = (int64_t)cf.n_heads * m->hd,
                 dkv = (int64_t)cf.n_kv_heads * m->hd;
-  const int64_t nvt = (cf.vocab + kVT - 1) / kVT;
+  const int64_t nvt = bf ? (cf.vocab + kLmTile - 1) / kLmTile : (cf.vocab + kVT - 1) / kVT;
   hipError_t e = hipSuccess;
   auto chk = [&](hipError_t x) {
     if (e == hipSuccess) e = x;
@@ -875,10 +946,17 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   }
   rmsq(nullptr, nullptr, m->xf);
   const int sp_lm = span_begin(m, 2, 2.0 * M * d * cf.vocab, s);
-  if (bf)
-    hipLaunchKernelGGL(k_lmhead_bf16, dim3((unsigned)nvt, (unsigned)((M + 127) / 128)), dim3(256), 0,
-                       s, (const uint16_t*)m->xf, (const uint16_t*)m->emb, M, d,
-                       (int64_t)cf.vocab, m->labels, m->pmax, m->psum, m->lab, nvt);
+  if (bf) {
+    const unsigned nb = (unsigned)(nvt * ((M + kLmTile - 1) / kLmTile));
+    if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % kLmBK == 0)
+      hipLaunchKernelGGL(k_lmhead_bf16<true>, dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
+                         (const uint16_t*)m->emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
+                         m->psum, m->lab, nvt);
+    else
+      hipLaunchKernelGGL(k_lmhead_bf16<false>, dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
+                         (const uint16_t*)m->emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
+                         m->psum, m->lab, nvt);
+  }
   else
     hipLaunchKernelGGL(k_lmhead_f32, dim3((unsigned)nvt, (unsigned)((M + 1) / 2)), dim3(256), 0, s,
                        (const float*)m->xf, (const float*)m->emb, M, d, (int64_t)cf.vocab,
@@ -886,7 +964,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   chk(hipGetLastError());
   span_end(m, sp_lm, s);
   float* rows = row_loss_dev ? row_loss_dev : m->row;
-  hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, m->pmax,
+  hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, m->pmax,
                      m->psum, m->lab, M, nvt, seq, rows);
   hipLaunchKernelGGL(k_loss_mean, dim3(1), dim3(256), 0, s, rows, M,
                      (int64_t)batch * (seq - 1), loss_dev ? loss_dev : m->loss32, m->loss64);

@@ -79,6 +79,7 @@ for _name, _args in _SIGS.items():
         ctypes.c_char_p if _name == "termezo_last_error" else ctypes.c_int)
 
 lib = _lib
+_is_finalizing = sys.is_finalizing   # bound now: module globals may be gone at teardown
 
 # Contexts still open; closed (models first) before interpreter teardown, while
 # the HIP runtime is still alive.
@@ -163,9 +164,9 @@ class Context:
             self.handle = None
 
     def __del__(self):
-        if sys.is_finalizing():
-            return
         try:
+            if _is_finalizing():
+                return
             self.close()
         except Exception:
             pass
@@ -284,9 +285,9 @@ class Model:
             self.handle = None
 
     def __del__(self):
-        if sys.is_finalizing():
-            return
         try:
+            if _is_finalizing():
+                return
             self.close()
         except Exception:
             pass

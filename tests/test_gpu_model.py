@@ -82,6 +82,7 @@ def test_tiny_decoder_fp32_steps(orc):
     (256, 2, 1, 256, 300, 130, 2),     # head_dim 128, GQA 2:1, ragged seq and vocab tiles
     (192, 2, 2, 192, 257, 64, 3),      # head_dim 96
     (256, 4, 2, 512, 1000, 200, 1),    # head_dim 64
+    (256, 2, 1, 256, 512, 128, 2),     # M, vocab multiples of 256: full-tile LM head
 ])
 def test_bf16_decoder_loss(orc, d, H, Hkv, F, V, S, B):
     torch = _torch()
