@@ -204,18 +204,43 @@ __global__ void __launch_bounds__(256) k_attn_f32(const float* q, const float* k
 }
 
 // ---------------------------------------------------------------------------
+// V^T for attention: v [B*S][Hkv*hd] -> vt [B*Hkv][hd][S], through 64 x 64
+// LDS tiles (coalesced reads and writes).
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_transpose_v(const uint16_t* __restrict__ v,
+                                                     uint16_t* __restrict__ vt, int S, int Hkv,
+                                                     int hd) {
+  __shared__ uint16_t t[64][66];
+  const int s0 = blockIdx.x * 64, d0 = blockIdx.y * 64, bh = blockIdx.z;
+  const int b = bh / Hkv, h = bh % Hkv;
+  const int64_t rowv = (int64_t)Hkv * hd;
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int r = i / 64, c = i % 64;       // r: token, c: dim
+    uint16_t val = 0;
+    if (s0 + r < S && d0 + c < hd) val = v[((int64_t)b * S + s0 + r) * rowv + (int64_t)h * hd + d0 + c];
+    t[r][c] = val;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int r = i / 64, c = i % 64;       // r: dim, c: token
+    if (d0 + r < hd && s0 + c < S) vt[((int64_t)bh * hd + d0 + r) * S + s0 + c] = t[c][r];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Causal GQA flash attention on bf16 matrix cores (v_mfma_f32_16x16x32_bf16).
 // Block = 64 queries of one (batch, head); wave w owns 16 queries.  For each
 // 64-key tile: S^T = K Q^T (K from LDS as the A operand, Q^T from registers as
 // B), online softmax per query column (the query is the lane's column, so the
 // row statistics stay in the lane), then O^T += V^T P^T with P^T taken straight
 // from the S^T accumulators (K index of the 32-key step: group g, element j ->
-// key 16 (j / 4) + 4 g + j % 4) and V^T read from a transposed LDS copy.
+// key 16 (j / 4) + 4 g + j % 4) and V^T rows read from a pre-transposed copy
+// (vt [B*Hkv][hd][S]).  Only the diagonal tile needs the causal mask.
 // ---------------------------------------------------------------------------
 template <int HD>
 __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ k,
-                                                   const uint16_t* __restrict__ v,
+                                                   const uint16_t* __restrict__ vt,
                                                    uint16_t* __restrict__ o, int S, int Hq,
                                                    int Hkv, float scale_log2) {
   constexpr int KT = 64;               // keys per tile
@@ -230,6 +255,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   const int kh = h / (Hq / Hkv);
   const int64_t rowq = (int64_t)Hq * HD, rowkv = (int64_t)Hkv * HD;
   const int64_t base = (int64_t)b * S;
+  const uint16_t* vtb = vt + ((int64_t)b * Hkv + kh) * HD * S;
   const int qpos = qt * 64 + w * 16 + c;        // this lane's query position
 
   // Q^T fragments: lane holds Q[qpos][32 s + 8 g .. +7]
@@ -250,22 +276,24 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   const int last_tile = min(qt, (S - 1) / KT);
   for (int kt = 0; kt <= last_tile; ++kt) {
     const int k0 = kt * KT;
-    // ---- stage K [64][HD] and V^T [HD][64] ----
+    // ---- stage K [64][HD] and V^T [HD][64] (16-byte chunks) ----
     for (int e = tid; e < KT * HD / 8; e += 256) {
       const int kr = e / (HD / 8), dc = (e % (HD / 8)) * 8;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (k0 + kr < S) {
-        const int64_t off = (base + k0 + kr) * rowkv + (int64_t)kh * HD + dc;
-        kv = *reinterpret_cast<const uint4*>(k + off);
-        vv = *reinterpret_cast<const uint4*>(v + off);
-      }
+      uint4 kv = make_uint4(0, 0, 0, 0);
+      if (k0 + kr < S) kv = *reinterpret_cast<const uint4*>(k + (base + k0 + kr) * rowkv + (int64_t)kh * HD + dc);
       *reinterpret_cast<uint4*>(Ks + kr * KS + dc) = kv;
-      const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+      const int dr = e / (KT / 8), kc = (e % (KT / 8)) * 8;
+      uint4 vv = make_uint4(0, 0, 0, 0);
+      if ((S & 7) == 0 && k0 + kc + 8 <= S) {     // 16-byte aligned rows
+        vv = *reinterpret_cast<const uint4*>(vtb + (int64_t)dr * S + k0 + kc);
+      } else {
+        uint16_t tmp[8];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        Vt[(dc + 2 * j) * VS + kr] = (uint16_t)(vw[j] & 0xFFFFu);
-        Vt[(dc + 2 * j + 1) * VS + kr] = (uint16_t)(vw[j] >> 16);
+        for (int j = 0; j < 8; ++j) tmp[j] = (k0 + kc + j < S) ? vtb[(int64_t)dr * S + k0 + kc + j] : 0;
+        vv = make_uint4(tmp[0] | ((uint32_t)tmp[1] << 16), tmp[2] | ((uint32_t)tmp[3] << 16),
+                        tmp[4] | ((uint32_t)tmp[5] << 16), tmp[6] | ((uint32_t)tmp[7] << 16));
       }
+      *reinterpret_cast<uint4*>(Vt + dr * VS + kc) = vv;
     }
     __syncthreads();
 
@@ -282,14 +310,17 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
       }
     }
     // st[t][i] = score(query c of this wave, key k0 + 16 t + 4 g + i)
+    const bool diag = kt == last_tile;          // only tile that can hold keys > query or >= S
     float mx = mrun;
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = k0 + 16 * t + 4 * g + i;
         float sv = st[t][i] * scale_log2;
-        if (key > qpos || key >= S) sv = -INFINITY;
+        if (diag) {
+          const int key = k0 + 16 * t + 4 * g + i;
+          if (key > qpos || key >= S) sv = -INFINITY;
+        }
         st[t][i] = sv;
         mx = fmaxf(mx, sv);
       }
@@ -307,14 +338,12 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
       for (int jj = 0; jj < 4; ++jj) {
         // elements j = 2 jj, 2 jj + 1 -> sub-tile 2 hh + j / 4, register j % 4
         const int j0 = 2 * jj, j1 = 2 * jj + 1;
-        const float p0 = st[2 * hh + j0 / 4][j0 % 4] == -INFINITY
-                             ? 0.0f
-                             : __builtin_amdgcn_exp2f(st[2 * hh + j0 / 4][j0 % 4] - mnew);
-        const float p1 = st[2 * hh + j1 / 4][j1 % 4] == -INFINITY
-                             ? 0.0f
-                             : __builtin_amdgcn_exp2f(st[2 * hh + j1 / 4][j1 % 4] - mnew);
+        const float p0 = __builtin_amdgcn_exp2f(st[2 * hh + j0 / 4][j0 % 4] - mnew);
+        const float p1 = __builtin_amdgcn_exp2f(st[2 * hh + j1 / 4][j1 % 4] - mnew);
         psum += p0 + p1;
-        pk[jj] = (uint32_t)f32_to_bf16_rne(p0) | ((uint32_t)f32_to_bf16_rne(p1) << 16);
+        const __bf16 b0 = (__bf16)p0, b1 = (__bf16)p1;
+        pk[jj] = (uint32_t)__builtin_bit_cast(uint16_t, b0) |
+                 ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
       }
       pf[hh] = __builtin_bit_cast(v8bf, make_uint4(pk[0], pk[1], pk[2], pk[3]));
     }
@@ -342,10 +371,12 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
     uint16_t* orow = o + (base + qpos) * rowq + (int64_t)h * HD;
 #pragma unroll
     for (int t = 0; t < HD / 16; ++t) {
-      const uint32_t w0 = (uint32_t)f32_to_bf16_rne(ot[t][0] * inv) |
-                          ((uint32_t)f32_to_bf16_rne(ot[t][1] * inv) << 16);
-      const uint32_t w1 = (uint32_t)f32_to_bf16_rne(ot[t][2] * inv) |
-                          ((uint32_t)f32_to_bf16_rne(ot[t][3] * inv) << 16);
+      const __bf16 e0 = (__bf16)(ot[t][0] * inv), e1 = (__bf16)(ot[t][1] * inv);
+      const __bf16 e2 = (__bf16)(ot[t][2] * inv), e3 = (__bf16)(ot[t][3] * inv);
+      const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, e0) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, e1) << 16);
+      const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, e2) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, e3) << 16);
       *reinterpret_cast<uint2*>(orow + 16 * t + 4 * g) = make_uint2(w0, w1);
     }
   }
@@ -610,8 +641,8 @@ struct termezo_model {
   int hd = 0;
   int64_t cap_M = 0;
   int cap_S = 0;
-  void *h = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *attn = nullptr, *g = nullptr,
-       *u = nullptr, *xf = nullptr;
+  void *h = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *vt = nullptr, *attn = nullptr,
+       *g = nullptr, *u = nullptr, *xf = nullptr;
   int8_t* xq = nullptr;
   float* xs = nullptr;
   float *pmax = nullptr, *psum = nullptr, *lab = nullptr, *row = nullptr;
@@ -657,7 +688,8 @@ void span_end(termezo_model* m, int idx, hipStream_t s) {
 }
 
 void model_free_buffers(termezo_model* m) {
-  mfree(m->h); mfree(m->q); mfree(m->k); mfree(m->v); mfree(m->attn); mfree(m->g); mfree(m->u);
+  mfree(m->h); mfree(m->q); mfree(m->k); mfree(m->v); mfree(m->vt); mfree(m->attn); mfree(m->g);
+  mfree(m->u);
   mfree(m->xf);
   void* p;
   p = m->xq; mfree(p); m->xq = nullptr;
@@ -692,6 +724,7 @@ termezo_status model_reserve(termezo_model* m, int64_t M, int S) {
   A(&m->q, M * dq * es);
   A(&m->k, M * dkv * es);
   A(&m->v, M * dkv * es);
+  A(&m->vt, M * dkv * es);
   A(&m->attn, M * dq * es);
   A(&m->g, M * c.d_ffn * es);
   A(&m->u, M * c.d_ffn * es);
@@ -741,10 +774,14 @@ hipError_t run_attention(termezo_model* m, int B, int S, hipStream_t st) {
     return hipGetLastError();
   }
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)m->hd));
+  hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((S + 63) / 64), (unsigned)((m->hd + 63) / 64),
+                                         (unsigned)(B * c.n_kv_heads)),
+                     dim3(256), 0, st, (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads,
+                     m->hd);
   dim3 grid((unsigned)((S + 63) / 64), c.n_heads, B);
 #define TMZ_ATTN(HDV)                                                                        \
   hipLaunchKernelGGL(k_attn_bf16<HDV>, grid, dim3(256), 0, st, (const uint16_t*)m->q,          \
-                     (const uint16_t*)m->k, (const uint16_t*)m->v, (uint16_t*)m->attn, S,      \
+                     (const uint16_t*)m->k, (const uint16_t*)m->vt, (uint16_t*)m->attn, S,     \
                      c.n_heads, c.n_kv_heads, sl2)
   switch (m->hd) {
     case 64: TMZ_ATTN(64); break;
