@@ -55,7 +55,6 @@ __device__ __forceinline__ int8_t q8(float x, float s) {
   return (int8_t)fminf(fmaxf(__builtin_rintf(x * s), -128.0f), 127.0f);
 }
 
-constexpr int kRowMax = 32;  // per-thread register budget: rows up to 256 * 32 elements
 
 // ---------------------------------------------------------------------------
 // h[m] = E[tok[m]]
@@ -68,75 +67,121 @@ __global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, i
 }
 
 // ---------------------------------------------------------------------------
-// RMSNorm (unit weight) fused with the 8-bit activation quantiser:
-// x = h / sqrt(mean(h^2) + eps) in fp32, then x_q, s as in BitLinear.
-// With xf != nullptr the normalised row is stored instead (final norm).
+// Row kernels, one wave per token row, 8 elements (one 16-byte bf16 load, or
+// two 16-byte fp32 loads) per lane per chunk, the row kept in registers:
+//   kRowNormQuant  x = h / sqrt(mean(h^2) + eps) (unit-weight RMSNorm), then
+//                  the 8-bit quantiser: s = 127 / max(max|x|, 1e-5),
+//                  x_q = clamp(rne(x s), -128, 127)
+//   kRowNormStore  the RMSNorm output stored in the activation dtype
+//   kRowSwiGLU     a = silu(g) * u, then the quantiser
+//   kRowQuant      the quantiser alone
+// Rows up to 64 * 8 * kRowChunks elements.
 // ---------------------------------------------------------------------------
-template <typename T>
-__global__ void __launch_bounds__(256) k_rmsnorm_quant(const T* h, int64_t d, float eps,
-                                                       int8_t* xq, float* xs, T* xf) {
-  __shared__ float red[4];
-  const int64_t m = blockIdx.x;
-  float v[kRowMax];
-  float ss = 0.0f;
+constexpr int kRowNormQuant = 0, kRowNormStore = 1, kRowSwiGLU = 2, kRowQuant = 3;
+constexpr int kRowChunks = 16;
+
+__device__ __forceinline__ void load8(const uint16_t* p, float v[8]) {
+  const uint4 r = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
-  for (int j = 0; j < kRowMax; ++j) {
-    const int64_t i = threadIdx.x + 256 * j;
-    v[j] = i < d ? ld_act(h, m * d + i) : 0.0f;
-    ss = fmaf(v[j], v[j], ss);
-  }
-  ss = bsum(ss, red);
-  const float r = __fdiv_rn(1.0f, sqrt_rn(ss / (float)d + eps));
-  float a = 0.0f;
-#pragma unroll
-  for (int j = 0; j < kRowMax; ++j) {
-    v[j] = v[j] * r;
-    a = fmaxf(a, fabsf(v[j]));
-  }
-  if (xf) {
-#pragma unroll
-    for (int j = 0; j < kRowMax; ++j) {
-      const int64_t i = threadIdx.x + 256 * j;
-      if (i < d) st_act(xf, m * d + i, v[j]);
-    }
-    return;
-  }
-  a = bmax(a, red);
-  const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
-  if (threadIdx.x == 0) xs[m] = sc;
-#pragma unroll
-  for (int j = 0; j < kRowMax; ++j) {
-    const int64_t i = threadIdx.x + 256 * j;
-    if (i < d) xq[m * d + i] = q8(v[j], sc);
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = __uint_as_float(w[j] << 16);
+    v[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
   }
 }
-
-// SwiGLU fused with the activation quantiser: a = silu(g) * u (fp32).
-template <typename T>
-__global__ void __launch_bounds__(256) k_swiglu_quant(const T* g, const T* u, int64_t F,
-                                                      int8_t* xq, float* xs) {
-  __shared__ float red[4];
-  const int64_t m = blockIdx.x;
-  float v[kRowMax];
-  float a = 0.0f;
+__device__ __forceinline__ void load8(const float* p, float v[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void store8(uint16_t* p, const float v[8]) {
+  uint32_t w[4];
 #pragma unroll
-  for (int j = 0; j < kRowMax; ++j) {
-    const int64_t i = threadIdx.x + 256 * j;
-    float x = 0.0f;
-    if (i < F) {
-      const float gv = ld_act(g, m * F + i);
-      x = gv / (1.0f + expf(-gv)) * ld_act(u, m * F + i);
-    }
-    v[j] = x;
-    a = fmaxf(a, fabsf(x));
+  for (int j = 0; j < 4; ++j) {
+    const __bf16 a = (__bf16)v[2 * j], b = (__bf16)v[2 * j + 1];
+    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
   }
-  a = bmax(a, red);
-  const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
-  if (threadIdx.x == 0) xs[m] = sc;
+  *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ void store8(float* p, const float v[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+template <int MODE, typename T>
+__global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* __restrict__ u,
+                                             int64_t M, int64_t K, float eps, int8_t* xq,
+                                             float* xs, T* xf) {
+  const int lane = threadIdx.x & 63;
+  const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;                       // whole wave
+  const int nch = (int)(K / 8);
+  float v[kRowChunks][8];
+  float acc = 0.0f;
 #pragma unroll
-  for (int j = 0; j < kRowMax; ++j) {
-    const int64_t i = threadIdx.x + 256 * j;
-    if (i < F) xq[m * F + i] = q8(v[j], sc);
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int idx = c * 64 + lane;
+    if (idx < nch) {
+      load8(x + m * K + idx * 8, v[c]);
+      if (MODE == kRowSwiGLU) {
+        float uu[8];
+        load8(u + m * K + idx * 8, uu);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float gv = v[c][j];
+          const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(gv * -1.4426950408889634f));
+          v[c][j] = gv * sg * uu[j];
+          acc = fmaxf(acc, fabsf(v[c][j]));
+        }
+      } else if (MODE == kRowQuant) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = fmaxf(acc, fabsf(v[c][j]));
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = fmaf(v[c][j], v[c][j], acc);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[c][j] = 0.0f;
+    }
+  }
+  float amax;
+  if (MODE == kRowSwiGLU || MODE == kRowQuant) {
+    amax = wmax(acc);
+  } else {
+    const float ss = wsum(acc);
+    const float r = __fdiv_rn(1.0f, sqrt_rn(ss / (float)K + eps));
+    float a = 0.0f;
+#pragma unroll
+    for (int c = 0; c < kRowChunks; ++c)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[c][j] = v[c][j] * r;
+        a = fmaxf(a, fabsf(v[c][j]));
+      }
+    if (MODE == kRowNormStore) {
+#pragma unroll
+      for (int c = 0; c < kRowChunks; ++c) {
+        const int idx = c * 64 + lane;
+        if (idx < nch) store8(xf + m * K + idx * 8, v[c]);
+      }
+      return;
+    }
+    amax = wmax(a);
+  }
+  const float sc = __fdiv_rn(127.0f, fmaxf(amax, 1e-5f));
+  if (lane == 0) xs[m] = sc;
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int idx = c * 64 + lane;
+    if (idx < nch) {
+      uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        w0 |= ((uint32_t)(uint8_t)q8(v[c][j], sc)) << (8 * j);
+        w1 |= ((uint32_t)(uint8_t)q8(v[c][4 + j], sc)) << (8 * j);
+      }
+      *reinterpret_cast<uint2*>(xq + m * K + idx * 8) = make_uint2(w0, w1);
+    }
   }
 }
 
@@ -204,50 +249,96 @@ __global__ void __launch_bounds__(256) k_attn_f32(const float* q, const float* k
 }
 
 // ---------------------------------------------------------------------------
-// V^T for attention: v [B*S][Hkv*hd] -> vt [B*Hkv][hd][S], through 64 x 64
-// LDS tiles (coalesced reads and writes).
+// Per-layer preparation of K and V for attention (one block per 64 tokens of
+// one KV head): K is rotated in place (RoPE, as in k_rope), V is transposed to
+// vt [B*Hkv][hd][S] through an LDS tile (coalesced reads and writes).
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) k_transpose_v(const uint16_t* __restrict__ v,
-                                                     uint16_t* __restrict__ vt, int S, int Hkv,
-                                                     int hd) {
-  __shared__ uint16_t t[64][66];
-  const int s0 = blockIdx.x * 64, d0 = blockIdx.y * 64, bh = blockIdx.z;
+// Rotary embedding of one 8-dim chunk at dims d0..d0+7 given its partner
+// chunk (d0 -/+ hd/2), as in k_rope: low half a c - b s, high half a s + b c
+// (a = low-half value, b = high-half value), rounded to bf16.
+__device__ __forceinline__ uint4 rope_chunk(uint4 own, uint4 par, bool low, const float* cs,
+                                            const float* sn) {
+  float o8[8], p8[8];
+  load8(reinterpret_cast<const uint16_t*>(&own), o8);
+  load8(reinterpret_cast<const uint16_t*>(&par), p8);
+  float r[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float c = cs[j], sv = sn[j];
+    r[j] = low ? o8[j] * c - p8[j] * sv : p8[j] * sv + o8[j] * c;
+  }
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const __bf16 a = (__bf16)r[2 * j], b = (__bf16)r[2 * j + 1];
+    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+template <int HD>
+__global__ void __launch_bounds__(256) k_kv_prep(uint16_t* __restrict__ k,
+                                                 const uint16_t* __restrict__ v,
+                                                 uint16_t* __restrict__ vt, int S, int Hkv,
+                                                 const float* __restrict__ rope_c,
+                                                 const float* __restrict__ rope_s) {
+  constexpr int HALF = HD / 2;
+  __shared__ uint16_t t[64][HD + 2];
+  const int s0 = blockIdx.x * 64, bh = blockIdx.y;
   const int b = bh / Hkv, h = bh % Hkv;
-  const int64_t rowv = (int64_t)Hkv * hd;
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int r = i / 64, c = i % 64;       // r: token, c: dim
-    uint16_t val = 0;
-    if (s0 + r < S && d0 + c < hd) val = v[((int64_t)b * S + s0 + r) * rowv + (int64_t)h * hd + d0 + c];
-    t[r][c] = val;
+  const int64_t rowkv = (int64_t)Hkv * HD;
+  // K: rotary chunk pairs, in place
+  for (int e = threadIdx.x; e < 64 * HALF / 8; e += 256) {
+    const int r = e / (HALF / 8), dc = (e % (HALF / 8)) * 8;
+    if (s0 + r >= S) continue;
+    uint16_t* kp = k + ((int64_t)b * S + s0 + r) * rowkv + (int64_t)h * HD;
+    const uint4 lo = *reinterpret_cast<const uint4*>(kp + dc);
+    const uint4 hi = *reinterpret_cast<const uint4*>(kp + dc + HALF);
+    const int ti = (s0 + r) * HALF + dc;
+    *reinterpret_cast<uint4*>(kp + dc) = rope_chunk(lo, hi, true, rope_c + ti, rope_s + ti);
+    *reinterpret_cast<uint4*>(kp + dc + HALF) = rope_chunk(hi, lo, false, rope_c + ti, rope_s + ti);
+  }
+  // V^T
+  for (int i = threadIdx.x; i < 64 * HD; i += 256) {
+    const int r = i / HD, c = i % HD;       // r: token, c: dim
+    t[r][c] = (s0 + r < S) ? v[((int64_t)b * S + s0 + r) * rowkv + (int64_t)h * HD + c] : 0;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+  for (int i = threadIdx.x; i < 64 * HD; i += 256) {
     const int r = i / 64, c = i % 64;       // r: dim, c: token
-    if (d0 + r < hd && s0 + c < S) vt[((int64_t)bh * hd + d0 + r) * S + s0 + c] = t[c][r];
+    if (s0 + c < S) vt[((int64_t)bh * HD + r) * S + s0 + c] = t[c][r];
   }
 }
 
 // ---------------------------------------------------------------------------
 // Causal GQA flash attention on bf16 matrix cores (v_mfma_f32_16x16x32_bf16).
-// Block = 64 queries of one (batch, head); wave w owns 16 queries.  For each
-// 64-key tile: S^T = K Q^T (K from LDS as the A operand, Q^T from registers as
-// B), online softmax per query column (the query is the lane's column, so the
-// row statistics stay in the lane), then O^T += V^T P^T with P^T taken straight
-// from the S^T accumulators (K index of the 32-key step: group g, element j ->
-// key 16 (j / 4) + 4 g + j % 4) and V^T rows read from a pre-transposed copy
-// (vt [B*Hkv][hd][S]).  Only the diagonal tile needs the causal mask.
+// Block = 128 queries of one (batch, head), 8 waves of 16 queries.  For each
+// 64-key tile: S^T = K Q^T (K from LDS as the A operand, rope(Q)^T from
+// registers as B), online softmax per query column (the query is the lane's
+// column, so row statistics stay in the lane), then O^T += V^T P^T with P^T
+// taken straight from the S^T accumulators (K index of the 32-key step: group
+// g, element j -> key 16 (j / 4) + 4 g + j % 4) and V^T rows from vt.  K/V
+// tiles are double-buffered in LDS with the next tile's global loads in
+// flight during the current tile's MFMAs; a wave skips tiles entirely in its
+// causal future, and only the diagonal tile is masked.
 // ---------------------------------------------------------------------------
 template <int HD>
-__global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ q,
+__global__ void __launch_bounds__(512) k_attn_bf16(const uint16_t* __restrict__ q,
                                                    const uint16_t* __restrict__ k,
                                                    const uint16_t* __restrict__ vt,
                                                    uint16_t* __restrict__ o, int S, int Hq,
-                                                   int Hkv, float scale_log2) {
+                                                   int Hkv, float scale_log2,
+                                                   const float* __restrict__ rope_c,
+                                                   const float* __restrict__ rope_s) {
+  constexpr int HALF = HD / 2;
+  constexpr int QB = 128;              // queries per block
   constexpr int KT = 64;               // keys per tile
   constexpr int KS = HD + 8;           // K tile row stride (bf16)
   constexpr int VS = KT + 8;           // V^T tile row stride (bf16)
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * VS];
+  constexpr int KCH = KT * HD / 8;     // 16-byte chunks per K tile (= per V^T tile)
+  constexpr int CPT = (KCH + 511) / 512;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][HD * VS];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c = lane & 15, g = lane >> 4;
@@ -255,115 +346,154 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const uint16_t* __restrict__ 
   const int kh = h / (Hq / Hkv);
   const int64_t rowq = (int64_t)Hq * HD, rowkv = (int64_t)Hkv * HD;
   const int64_t base = (int64_t)b * S;
+  const uint16_t* kb = k + base * rowkv + (int64_t)kh * HD;
   const uint16_t* vtb = vt + ((int64_t)b * Hkv + kh) * HD * S;
-  const int qpos = qt * 64 + w * 16 + c;        // this lane's query position
+  const int qw0 = qt * QB + w * 16;             // first query of this wave
+  const int qpos = qw0 + c;                     // this lane's query
+  const bool vec_v = (S & 7) == 0;
 
-  // Q^T fragments: lane holds Q[qpos][32 s + 8 g .. +7]
+  // rope(Q)^T fragments: lane holds rope(Q)[qpos][32 s + 8 g .. +7]
   v8bf qf[HD / 32];
 #pragma unroll
   for (int s = 0; s < HD / 32; ++s) {
     uint4 raw = make_uint4(0, 0, 0, 0);
-    if (qpos < S)
-      raw = *reinterpret_cast<const uint4*>(q + (base + qpos) * rowq + (int64_t)h * HD + 32 * s + 8 * g);
+    if (qpos < S) {
+      const int d0 = 32 * s + 8 * g;
+      const bool low = d0 < HALF;
+      const uint16_t* qr = q + (base + qpos) * rowq + (int64_t)h * HD;
+      const uint4 own = *reinterpret_cast<const uint4*>(qr + d0);
+      const uint4 par = *reinterpret_cast<const uint4*>(qr + (low ? d0 + HALF : d0 - HALF));
+      const int ti = qpos * HALF + (low ? d0 : d0 - HALF);
+      raw = rope_chunk(own, par, low, rope_c + ti, rope_s + ti);
+    }
     qf[s] = __builtin_bit_cast(v8bf, raw);
   }
+
+  uint4 rk[CPT], rv[CPT];
+  auto gload = [&](int kt) __attribute__((always_inline)) {
+    const int k0 = kt * KT;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = tid + 512 * i;
+      rk[i] = make_uint4(0, 0, 0, 0);
+      rv[i] = make_uint4(0, 0, 0, 0);
+      if (e < KCH) {
+        const int kr = e / (HD / 8), dc = (e % (HD / 8)) * 8;
+        if (k0 + kr < S) rk[i] = *reinterpret_cast<const uint4*>(kb + (int64_t)(k0 + kr) * rowkv + dc);
+        const int dr = e / (KT / 8), kc = (e % (KT / 8)) * 8;
+        const uint16_t* vp = vtb + (int64_t)dr * S + k0 + kc;
+        if (vec_v && k0 + kc + 8 <= S) {
+          rv[i] = *reinterpret_cast<const uint4*>(vp);
+        } else {
+          uint32_t t4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t lo16 = (k0 + kc + 2 * j < S) ? vp[2 * j] : 0u;
+            const uint32_t hi16 = (k0 + kc + 2 * j + 1 < S) ? vp[2 * j + 1] : 0u;
+            t4[j] = lo16 | (hi16 << 16);
+          }
+          rv[i] = make_uint4(t4[0], t4[1], t4[2], t4[3]);
+        }
+      }
+    }
+  };
+  auto lstore = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = tid + 512 * i;
+      if (e < KCH) {
+        const int kr = e / (HD / 8), dc = (e % (HD / 8)) * 8;
+        *reinterpret_cast<uint4*>(&Ks[buf][kr * KS + dc]) = rk[i];
+        const int dr = e / (KT / 8), kc = (e % (KT / 8)) * 8;
+        *reinterpret_cast<uint4*>(&Vs[buf][dr * VS + kc]) = rv[i];
+      }
+    }
+  };
 
   v4f ot[HD / 16];
 #pragma unroll
   for (int t = 0; t < HD / 16; ++t) ot[t] = v4f{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.0f;
 
-  const int last_tile = min(qt, (S - 1) / KT);
-  for (int kt = 0; kt <= last_tile; ++kt) {
+  const int q_last = min(qt * QB + QB, S) - 1;             // block's last query
+  const int ntile = q_last / KT + 1;
+  gload(0);
+  lstore(0);
+  if (ntile > 1) gload(1);
+  __syncthreads();
+  for (int kt = 0; kt < ntile; ++kt) {
     const int k0 = kt * KT;
-    // ---- stage K [64][HD] and V^T [HD][64] (16-byte chunks) ----
-    for (int e = tid; e < KT * HD / 8; e += 256) {
-      const int kr = e / (HD / 8), dc = (e % (HD / 8)) * 8;
-      uint4 kv = make_uint4(0, 0, 0, 0);
-      if (k0 + kr < S) kv = *reinterpret_cast<const uint4*>(k + (base + k0 + kr) * rowkv + (int64_t)kh * HD + dc);
-      *reinterpret_cast<uint4*>(Ks + kr * KS + dc) = kv;
-      const int dr = e / (KT / 8), kc = (e % (KT / 8)) * 8;
-      uint4 vv = make_uint4(0, 0, 0, 0);
-      if ((S & 7) == 0 && k0 + kc + 8 <= S) {     // 16-byte aligned rows
-        vv = *reinterpret_cast<const uint4*>(vtb + (int64_t)dr * S + k0 + kc);
-      } else {
-        uint16_t tmp[8];
+    const uint16_t* Kb = Ks[kt & 1];
+    const uint16_t* Vb = Vs[kt & 1];
+    if (k0 <= qw0 + 15 && qw0 < S) {            // wave-uniform: tile not entirely in the future
+      v4f st[4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) tmp[j] = (k0 + kc + j < S) ? vtb[(int64_t)dr * S + k0 + kc + j] : 0;
-        vv = make_uint4(tmp[0] | ((uint32_t)tmp[1] << 16), tmp[2] | ((uint32_t)tmp[3] << 16),
-                        tmp[4] | ((uint32_t)tmp[5] << 16), tmp[6] | ((uint32_t)tmp[7] << 16));
-      }
-      *reinterpret_cast<uint4*>(Vt + dr * VS + kc) = vv;
-    }
-    __syncthreads();
-
-    // ---- S^T for the 4 key sub-tiles ----
-    v4f st[4];
+      for (int t = 0; t < 4; ++t) {
+        st[t] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      st[t] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < HD / 32; ++s) {
-        const uint4 raw = *reinterpret_cast<const uint4*>(Ks + (16 * t + c) * KS + 32 * s + 8 * g);
-        st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, raw), qf[s], st[t],
-                                                        0, 0, 0);
-      }
-    }
-    // st[t][i] = score(query c of this wave, key k0 + 16 t + 4 g + i)
-    const bool diag = kt == last_tile;          // only tile that can hold keys > query or >= S
-    float mx = mrun;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float sv = st[t][i] * scale_log2;
-        if (diag) {
-          const int key = k0 + 16 * t + 4 * g + i;
-          if (key > qpos || key >= S) sv = -INFINITY;
+        for (int s = 0; s < HD / 32; ++s) {
+          const uint4 raw = *reinterpret_cast<const uint4*>(Kb + (16 * t + c) * KS + 32 * s + 8 * g);
+          st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, raw), qf[s],
+                                                          st[t], 0, 0, 0);
         }
-        st[t][i] = sv;
-        mx = fmaxf(mx, sv);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mnew = mx;
-    const float alpha = (mrun == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mrun - mnew);
-    mrun = mnew;
-    float psum = 0.0f;
-    v8bf pf[2];
+      // st[t][i] = score(query qpos, key k0 + 16 t + 4 g + i)
+      const bool diag = k0 + KT - 1 > qw0;      // some key may exceed some query of the wave
+      float mx = mrun;
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      uint32_t pk[4];
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        // elements j = 2 jj, 2 jj + 1 -> sub-tile 2 hh + j / 4, register j % 4
-        const int j0 = 2 * jj, j1 = 2 * jj + 1;
-        const float p0 = __builtin_amdgcn_exp2f(st[2 * hh + j0 / 4][j0 % 4] - mnew);
-        const float p1 = __builtin_amdgcn_exp2f(st[2 * hh + j1 / 4][j1 % 4] - mnew);
-        psum += p0 + p1;
-        const __bf16 b0 = (__bf16)p0, b1 = (__bf16)p1;
-        pk[jj] = (uint32_t)__builtin_bit_cast(uint16_t, b0) |
-                 ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
-      }
-      pf[hh] = __builtin_bit_cast(v8bf, make_uint4(pk[0], pk[1], pk[2], pk[3]));
-    }
-    lrun = lrun * alpha + psum;
-#pragma unroll
-    for (int t = 0; t < HD / 16; ++t) {
-      ot[t] *= alpha;
+        for (int i = 0; i < 4; ++i) {
+          float sv = st[t][i] * scale_log2;
+          if (diag) {
+            const int key = k0 + 16 * t + 4 * g + i;
+            if (key > qpos || key >= S) sv = -INFINITY;
+          }
+          st[t][i] = sv;
+          mx = fmaxf(mx, sv);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = mx;
+      const float alpha = (mrun == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mrun - mnew);
+      mrun = mnew;
+      float psum = 0.0f;
+      v8bf pf[2];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        // A = V^T rows d = 16 t + c, keys 32 hh + {4g..4g+3} and 32 hh + 16 + {4g..4g+3}
-        const uint16_t* vr = Vt + (16 * t + c) * VS + 32 * hh + 4 * g;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-        const v8bf af = __builtin_bit_cast(v8bf, make_uint4(lo.x, lo.y, hi.x, hi.y));
-        ot[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, pf[hh], ot[t], 0, 0, 0);
+        uint32_t pk[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int j0 = 2 * jj, j1 = 2 * jj + 1;
+          const float p0 = __builtin_amdgcn_exp2f(st[2 * hh + j0 / 4][j0 % 4] - mnew);
+          const float p1 = __builtin_amdgcn_exp2f(st[2 * hh + j1 / 4][j1 % 4] - mnew);
+          psum += p0 + p1;
+          const __bf16 b0 = (__bf16)p0, b1 = (__bf16)p1;
+          pk[jj] = (uint32_t)__builtin_bit_cast(uint16_t, b0) |
+                   ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
+        }
+        pf[hh] = __builtin_bit_cast(v8bf, make_uint4(pk[0], pk[1], pk[2], pk[3]));
       }
+      lrun = lrun * alpha + psum;
+#pragma unroll
+      for (int t = 0; t < HD / 16; ++t) {
+        ot[t] *= alpha;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const uint16_t* vr = Vb + (16 * t + c) * VS + 32 * hh + 4 * g;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+          const v8bf af = __builtin_bit_cast(v8bf, make_uint4(lo.x, lo.y, hi.x, hi.y));
+          ot[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, pf[hh], ot[t], 0, 0, 0);
+        }
+      }
+    }
+    if (kt + 1 < ntile) {
+      lstore((kt + 1) & 1);
+      if (kt + 2 < ntile) gload(kt + 2);
     }
     __syncthreads();
   }
-  // the partial sums of the 4 lanes sharing a query
   lrun += __shfl_xor(lrun, 16, 64);
   lrun += __shfl_xor(lrun, 32, 64);
   if (qpos < S) {
@@ -774,15 +904,15 @@ hipError_t run_attention(termezo_model* m, int B, int S, hipStream_t st) {
     return hipGetLastError();
   }
   const float sl2 = (float)(1.4426950408889634 / std::sqrt((double)m->hd));
-  hipLaunchKernelGGL(k_transpose_v, dim3((unsigned)((S + 63) / 64), (unsigned)((m->hd + 63) / 64),
-                                         (unsigned)(B * c.n_kv_heads)),
-                     dim3(256), 0, st, (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads,
-                     m->hd);
-  dim3 grid((unsigned)((S + 63) / 64), c.n_heads, B);
+  dim3 pgrid((unsigned)((S + 63) / 64), (unsigned)(B * c.n_kv_heads));
+  dim3 grid((unsigned)((S + 127) / 128), c.n_heads, B);
 #define TMZ_ATTN(HDV)                                                                        \
-  hipLaunchKernelGGL(k_attn_bf16<HDV>, grid, dim3(256), 0, st, (const uint16_t*)m->q,          \
+  hipLaunchKernelGGL(k_kv_prep<HDV>, pgrid, dim3(256), 0, st, (uint16_t*)m->k,                  \
+                     (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads, m->rope_c,      \
+                     m->rope_s);                                                              \
+  hipLaunchKernelGGL(k_attn_bf16<HDV>, grid, dim3(512), 0, st, (const uint16_t*)m->q,          \
                      (const uint16_t*)m->k, (const uint16_t*)m->vt, (uint16_t*)m->attn, S,     \
-                     c.n_heads, c.n_kv_heads, sl2)
+                     c.n_heads, c.n_kv_heads, sl2, m->rope_c, m->rope_s)
   switch (m->hd) {
     case 64: TMZ_ATTN(64); break;
     case 96: TMZ_ATTN(96); break;
@@ -812,7 +942,8 @@ termezo_status termezo_model_create(termezo_ctx* ctx, const termezo_model_config
   if (hd % 2 != 0 || c.d_model % 16 != 0 || c.d_ffn % 16 != 0) return TERMEZO_ERR_INVALID_ARG;
   if (c.act_dtype == TERMEZO_BF16 && hd != 64 && hd != 96 && hd != 128)
     return TERMEZO_ERR_INVALID_ARG;
-  if (std::max(c.d_model, c.d_ffn) > 256 * kRowMax) return TERMEZO_ERR_INVALID_ARG;
+  if (std::max(c.d_model, c.d_ffn) > 64 * 8 * kRowChunks || (c.d_model / c.n_heads) % 16 != 0)
+    return TERMEZO_ERR_INVALID_ARG;
   if ((reinterpret_cast<uintptr_t>(embedding) & 15u) != 0) return TERMEZO_ERR_INVALID_ARG;
   if (ctx->L != 7 * c.n_blocks) return TERMEZO_ERR_INVALID_ARG;
   const int64_t dq = (int64_t)c.n_heads * hd, dkv = (int64_t)c.n_kv_heads * hd;
@@ -905,13 +1036,27 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   chk(hipGetLastError());
   hipLaunchKernelGGL(k_labels, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, tokens, M, seq,
                      m->labels);
+  const unsigned rowg = (unsigned)((M + 3) / 4);
   auto rmsq = [&](int8_t* xq, float* xs, void* xf) {
-    if (bf)
-      hipLaunchKernelGGL(k_rmsnorm_quant<uint16_t>, dim3((unsigned)M), dim3(256), 0, s,
-                         (const uint16_t*)m->h, d, cf.norm_eps, xq, xs, (uint16_t*)xf);
-    else
-      hipLaunchKernelGGL(k_rmsnorm_quant<float>, dim3((unsigned)M), dim3(256), 0, s,
-                         (const float*)m->h, d, cf.norm_eps, xq, xs, (float*)xf);
+    if (bf) {
+      if (xf)
+        hipLaunchKernelGGL((k_row<kRowNormStore, uint16_t>), dim3(rowg), dim3(256), 0, s,
+                           (const uint16_t*)m->h, (const uint16_t*)nullptr, M, d, cf.norm_eps, xq,
+                           xs, (uint16_t*)xf);
+      else
+        hipLaunchKernelGGL((k_row<kRowNormQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
+                           (const uint16_t*)m->h, (const uint16_t*)nullptr, M, d, cf.norm_eps, xq,
+                           xs, (uint16_t*)nullptr);
+    } else {
+      if (xf)
+        hipLaunchKernelGGL((k_row<kRowNormStore, float>), dim3(rowg), dim3(256), 0, s,
+                           (const float*)m->h, (const float*)nullptr, M, d, cf.norm_eps, xq, xs,
+                           (float*)xf);
+      else
+        hipLaunchKernelGGL((k_row<kRowNormQuant, float>), dim3(rowg), dim3(256), 0, s,
+                           (const float*)m->h, (const float*)nullptr, M, d, cf.norm_eps, xq, xs,
+                           (float*)nullptr);
+    }
     chk(hipGetLastError());
   };
   for (int blk = 0; blk < cf.n_blocks; ++blk) {
@@ -929,23 +1074,27 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
                        kGemmStore, nullptr, s));
     span_end(m, sp, s);
-    const unsigned rg = (unsigned)std::min<int64_t>(8192, (M * cf.n_heads * (m->hd / 2) + 255) / 256);
-    if (bf) {
-      hipLaunchKernelGGL(k_rope<uint16_t>, dim3(rg), dim3(256), 0, s, (uint16_t*)m->q, M,
-                         cf.n_heads, m->hd, seq, m->rope_c, m->rope_s);
-      hipLaunchKernelGGL(k_rope<uint16_t>, dim3(rg), dim3(256), 0, s, (uint16_t*)m->k, M,
-                         cf.n_kv_heads, m->hd, seq, m->rope_c, m->rope_s);
-    } else {
+    if (!bf) {   // bf16: the rotation is applied inside the attention kernel
+      const unsigned rg =
+          (unsigned)std::min<int64_t>(8192, (M * cf.n_heads * (m->hd / 2) + 255) / 256);
       hipLaunchKernelGGL(k_rope<float>, dim3(rg), dim3(256), 0, s, (float*)m->q, M, cf.n_heads,
                          m->hd, seq, m->rope_c, m->rope_s);
       hipLaunchKernelGGL(k_rope<float>, dim3(rg), dim3(256), 0, s, (float*)m->k, M,
                          cf.n_kv_heads, m->hd, seq, m->rope_c, m->rope_s);
+      chk(hipGetLastError());
     }
-    chk(hipGetLastError());
     sp = span_begin(m, 1, 4.0 * batch * cf.n_heads * m->hd * (0.5 * seq * (seq + 1.0)), s);
     chk(run_attention(m, batch, seq, s));
     span_end(m, sp, s);
-    chk(launch_act_quant(m->attn, adt, M, dq, m->xq, m->xs, s));
+    if (bf)
+      hipLaunchKernelGGL((k_row<kRowQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
+                         (const uint16_t*)m->attn, (const uint16_t*)nullptr, M, dq, 0.0f, m->xq,
+                         m->xs, (uint16_t*)nullptr);
+    else
+      hipLaunchKernelGGL((k_row<kRowQuant, float>), dim3(rowg), dim3(256), 0, s,
+                         (const float*)m->attn, (const float*)nullptr, M, dq, 0.0f, m->xq, m->xs,
+                         (float*)nullptr);
+    chk(hipGetLastError());
     GemmOut oo = {};
     oo.nseg = 1;
     oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = c->d_beta_cur + l0 + 3;
@@ -966,11 +1115,13 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                        nullptr, s));
     span_end(m, sp, s);
     if (bf)
-      hipLaunchKernelGGL(k_swiglu_quant<uint16_t>, dim3((unsigned)M), dim3(256), 0, s,
-                         (const uint16_t*)m->g, (const uint16_t*)m->u, F, m->xq, m->xs);
+      hipLaunchKernelGGL((k_row<kRowSwiGLU, uint16_t>), dim3(rowg), dim3(256), 0, s,
+                         (const uint16_t*)m->g, (const uint16_t*)m->u, M, F, 0.0f, m->xq, m->xs,
+                         (uint16_t*)nullptr);
     else
-      hipLaunchKernelGGL(k_swiglu_quant<float>, dim3((unsigned)M), dim3(256), 0, s,
-                         (const float*)m->g, (const float*)m->u, F, m->xq, m->xs);
+      hipLaunchKernelGGL((k_row<kRowSwiGLU, float>), dim3(rowg), dim3(256), 0, s,
+                         (const float*)m->g, (const float*)m->u, M, F, 0.0f, m->xq, m->xs,
+                         (float*)nullptr);
     chk(hipGetLastError());
     GemmOut od = {};
     od.nseg = 1;
