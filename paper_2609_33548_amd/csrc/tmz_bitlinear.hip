@@ -105,6 +105,28 @@ __device__ __forceinline__ float load_act(const uint16_t* p) { return bf16_to_f3
 __device__ __forceinline__ float round_act(const float*, float v) { return v; }
 __device__ __forceinline__ float round_act(const uint16_t*, float v) { return (float)(__bf16)v; }
 
+// Four consecutive activations: one 8-byte (bf16) or 16-byte (fp32) access.
+__device__ __forceinline__ void store4(float* p, const float v[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store4(uint16_t* p, const float v[4]) {
+  const __bf16 a = (__bf16)v[0], b = (__bf16)v[1], c = (__bf16)v[2], d = (__bf16)v[3];
+  const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, c) | ((uint32_t)__builtin_bit_cast(uint16_t, d) << 16);
+  *reinterpret_cast<uint2*>(p) = make_uint2(w0, w1);
+}
+__device__ __forceinline__ void load4v(const float* p, float v[4]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+}
+__device__ __forceinline__ void load4v(const uint16_t* p, float v[4]) {
+  const uint2 a = *reinterpret_cast<const uint2*>(p);
+  v[0] = __uint_as_float(a.x << 16);
+  v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(a.y << 16);
+  v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+}
+
 template <int BM, int BN, int WM, int WN, bool FULL, typename TY, int MODE>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
     k_gemm_i8(const int8_t* __restrict__ xq, const float* __restrict__ s,
@@ -256,6 +278,196 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
   }
 }
 
+// ---------------------------------------------------------------------------
+// Full-tile variant with direct global -> LDS loads (global_load_lds_dwordx4:
+// lane i of a wave writes its 16 bytes at the wave's LDS base + 16 i, no VGPRs)
+// and a 3-stage LDS ring, so step k+2 is in flight while step k is computed.
+//   A stage: 256 rows x 128 bytes, 16-byte chunk c of row r stored at chunk
+//            c ^ ((r >> 1) & 7) (the fragment reads of 16 consecutive rows
+//            then hit distinct banks).
+//   B stage: 256 rows x 32 bytes of packed 2-bit codes; each fragment read
+//            takes one 32-bit word (16 codes) and unpacks it in registers.
+// 8 waves as 2 x 4, 128 x 64 per wave, v_mfma_i32_32x32x32_i8.
+// Requires M % 256 == 0, N % 256 == 0, K % 128 == 0.
+// ---------------------------------------------------------------------------
+// One 16-byte-per-lane direct global -> LDS load; lds_base is the wave's
+// destination (LDS byte offset, wave-uniform).  Issued as inline assembly so
+// that its completion is tracked only by the explicit vmcnt waits below.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(gptr), "s"(lds_base)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+__device__ __forceinline__ void wait_vmcnt_le5() {
+  // s_waitcnt vmcnt(5): vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt left at their maxima
+  __builtin_amdgcn_s_waitcnt((5 & 0xF) | (0x7 << 4) | (0xF << 8));
+}
+
+template <typename TY, int MODE>
+__global__ void __launch_bounds__(512)
+    k_gemm_i8_dma(const int8_t* __restrict__ xq, const float* __restrict__ s,
+                  const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+                  int32_t* __restrict__ acc_out) {
+  constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int AROW = 128;                       // bytes per A row per stage (no pad)
+  constexpr int BROW = 32;                        // bytes of packed codes per B row per stage
+  constexpr int ASTAGE = BM * AROW, BSTAGE = BN * BROW;
+  __shared__ __attribute__((aligned(1024))) int8_t lds[3 * (ASTAGE + BSTAGE)];
+  __shared__ float rrow[kMaxSeg][BM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wid = tid >> 6;
+  const int wm = wid / (BN / WN), wn = wid % (BN / WN);
+  int64_t tm, tn;
+  tile_of_block(M / BM, N / BN, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t KW = K / 16;
+  const int nk = (int)(K / kBK);
+
+  for (int i = tid; i < kMaxSeg * BM; i += NT) {
+    const int sg = i / BM, r = i % BM;
+    rrow[sg][r] = sg < out.nseg ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
+  }
+
+  // Per-lane global sources.  A: wave w fills 1 KB chunks 4w..4w+3 (8 rows
+  // each); lane i -> row 8 j + i / 8, physical chunk i % 8.  B: wave w fills
+  // rows 32 w .. 32 w + 31, two lanes per row.
+  const int8_t* asrc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = 8 * (4 * wid + j) + (lane >> 3);
+    const int chunk = (lane & 7) ^ ((row >> 1) & 7);
+    asrc[j] = xq + (m0 + row) * K + 16 * chunk;
+  }
+  const uint32_t* bsrc = codes + (n0 + 32 * wid + (lane >> 1)) * KW + 4 * (lane & 1);
+
+  const uint32_t wbase = __builtin_amdgcn_readfirstlane(wid);   // wave-uniform
+  auto issue = [&](int kt, int8_t* Ad, uint32_t* Bd) __attribute__((always_inline)) {
+    const int64_t koff = (int64_t)kt * kBK;
+    const uint32_t abase = lds_offset(Ad) + 4096u * wbase;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma16(asrc[j] + koff, abase + 1024u * j);
+    dma16(bsrc + koff / 16, lds_offset(Bd) + 1024u * wbase);
+  };
+
+  v16i acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
+
+  const int arow0 = wm * WM + (lane & 31);        // A fragment row of this lane (a = 0)
+  const int brow0 = wn * WN + (lane & 31);
+  // One K step: four 32-wide sub-steps; the fragments of sub-step ks+1 are
+  // read from LDS before the MFMAs of sub-step ks are issued (register double
+  // buffer), so LDS latency hides behind the matrix-core work.
+  auto compute = [&](const int8_t* As, const uint32_t* Bs) __attribute__((always_inline)) {
+    v4i af[2][TM];
+    uint32_t bw[2][TN];
+    auto frag = [&](int ks, int slot) __attribute__((always_inline)) {
+      const int c = 2 * ks + (lane >> 5);            // logical 16-byte chunk
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int row = arow0 + 32 * a;
+        af[slot][a] = *reinterpret_cast<const v4i*>(As + row * AROW + 16 * (c ^ ((row >> 1) & 7)));
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) bw[slot][b] = Bs[(brow0 + 32 * b) * (BROW / 4) + c];
+    };
+    frag(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < kBK / 32) frag(ks + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+      v4i bf[TN];
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+        bf[b] = v4i{(int)unpack_group(bw[cur][b], 0), (int)unpack_group(bw[cur][b], 1),
+                    (int)unpack_group(bw[cur][b], 2), (int)unpack_group(bw[cur][b], 3)};
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)   // codes as the A operand: acc holds Y^T
+          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[b], af[cur][a], acc[a][b], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  auto Ast = [&](int st) { return lds + st * ASTAGE; };
+  auto Bst = [&](int st) { return reinterpret_cast<uint32_t*>(lds + 3 * ASTAGE + st * BSTAGE); };
+  // prologue: stages 0 and 1 in flight, stage 0 complete before the loop
+  issue(0, Ast(0), Bst(0));
+  if (nk > 1) issue(1, Ast(1), Bst(1));
+  if (nk > 1) wait_vmcnt_le5(); else __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int cur = 0;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int nxt2 = cur == 0 ? 2 : cur - 1;     // (kt + 2) % 3
+    if (kt + 2 < nk) issue(kt + 2, Ast(nxt2), Bst(nxt2));
+    compute(Ast(cur), Bst(cur));
+    if (kt + 2 < nk) wait_vmcnt_le5(); else __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    cur = cur == 2 ? 0 : cur + 1;
+  }
+
+  // ---- epilogue (every tile is in bounds).  acc[a][b] is the transposed
+  // 32 x 32 tile: lane column = token m (one scale beta'/s_m per lane),
+  // register r = output feature 8 (r / 4) + 4 (l / 32) + (r % 4), so each group
+  // of 4 registers is 4 consecutive features: one 8-byte (bf16) store.
+  // Segment boundaries are multiples of 32, so a 32-feature tile lies in one
+  // segment.
+  const int ml = wm * WM + (lane & 31);             // local token of tile a = 0
+#pragma unroll
+  for (int b = 0; b < TN; ++b) {
+    const int64_t nb = n0 + wn * WN + b * 32;        // first feature of the tile
+    int sg = 0;
+    if (out.nseg > 1 && nb >= out.nstart[1]) sg = 1;
+    if (out.nseg > 2 && nb >= out.nstart[2]) sg = 2;
+    const int64_t ld = out.ld[sg];
+    TY* base = reinterpret_cast<TY*>(out.y[sg]) + (nb - out.nstart[sg]) + 4 * (lane >> 5);
+#pragma unroll
+    for (int a = 0; a < TM; ++a) {
+      const int mloc = ml + 32 * a;
+      const float rr = rrow[sg][mloc];
+      TY* rowp = base + (m0 + mloc) * ld;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v4[j] = (float)acc[a][b][4 * q + j] * rr;
+        TY* p = rowp + 8 * q;
+        if (MODE == kGemmStore) {
+          store4(p, v4);
+        } else {   // residual: h <- round(h + round(y))
+          float h4[4];
+          load4v(p, h4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v4[j] = h4[j] + round_act(p, v4[j]);
+          store4(p, v4);
+        }
+        if (acc_out) {
+          const int64_t n = nb + 8 * q + 4 * (lane >> 5);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc_out[(m0 + mloc) * N + n + j] = acc[a][b][4 * q + j];
+        }
+      }
+    }
+  }
+}
+
 // ===========================================================================
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, hipStream_t st) {
@@ -299,8 +511,30 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
                           int32_t* acc, hipStream_t st) {
   const int64_t big_blocks = ((M + 255) / 256) * ((N + 255) / 256);
   if (big_blocks >= 256) {
-    if (M % 256 == 0 && N % 256 == 0 && K % kBK == 0)
-      return launch_tile<256, 256, 128, 64, true>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
+    bool seg32 = true;
+    for (int i = 1; i < out.nseg; ++i) seg32 = seg32 && out.nstart[i] % 32 == 0;
+    const uintptr_t vec = ydt == TERMEZO_F32 ? 16 : 8;   // 4-element store width
+    for (int i = 0; i < out.nseg; ++i)
+      seg32 = seg32 && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
+    if (M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32) {
+      dim3 grid((unsigned)((N / 256) * (M / 256)));
+      if (ydt == TERMEZO_F32) {
+        if (mode == kGemmStore)
+          hipLaunchKernelGGL((k_gemm_i8_dma<float, kGemmStore>), grid, dim3(512), 0, st, xq, s, codes,
+                             M, K, N, out, acc);
+        else
+          hipLaunchKernelGGL((k_gemm_i8_dma<float, kGemmResidual>), grid, dim3(512), 0, st, xq, s,
+                             codes, M, K, N, out, acc);
+      } else {
+        if (mode == kGemmStore)
+          hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmStore>), grid, dim3(512), 0, st, xq, s,
+                             codes, M, K, N, out, acc);
+        else
+          hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmResidual>), grid, dim3(512), 0, st, xq, s,
+                             codes, M, K, N, out, acc);
+      }
+      return hipGetLastError();
+    }
     return launch_tile<256, 256, 128, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
   }
   return launch_tile<128, 128, 64, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
