@@ -278,18 +278,6 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
   }
 }
 
-// ---------------------------------------------------------------------------
-// Full-tile variant with direct global -> LDS loads (global_load_lds_dwordx4:
-// lane i of a wave writes its 16 bytes at the wave's LDS base + 16 i, no VGPRs)
-// and a 3-stage LDS ring, so step k+2 is in flight while step k is computed.
-//   A stage: 256 rows x 128 bytes, 16-byte chunk c of row r stored at chunk
-//            c ^ ((r >> 1) & 7) (the fragment reads of 16 consecutive rows
-//            then hit distinct banks).
-//   B stage: 256 rows x 32 bytes of packed 2-bit codes; each fragment read
-//            takes one 32-bit word (16 codes) and unpacks it in registers.
-// 8 waves as 2 x 4, 128 x 64 per wave, v_mfma_i32_32x32x32_i8.
-// Requires M % 256 == 0, N % 256 == 0, K % 128 == 0.
-// ---------------------------------------------------------------------------
 // One 16-byte-per-lane direct global -> LDS load; lds_base is the wave's
 // destination (LDS byte offset, wave-uniform).  Issued as inline assembly so
 // that its completion is tracked only by the explicit vmcnt waits below.
@@ -307,57 +295,89 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-__device__ __forceinline__ void wait_vmcnt_le5() {
-  // s_waitcnt vmcnt(5): vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt left at their maxima
-  __builtin_amdgcn_s_waitcnt((5 & 0xF) | (0x7 << 4) | (0xF << 8));
+// ---------------------------------------------------------------------------
+// Full-tile GEMM with direct global -> LDS loads (global_load_lds_dwordx4:
+// lane i of a wave writes its 16 bytes at the wave's LDS base + 16 i, no VGPRs)
+// and a 3-stage LDS ring, so step k+2 is in flight while step k is computed.
+//   A stage: BM rows x 128 bytes, 16-byte chunk c of row r stored at chunk
+//            c ^ ((r >> 1) & 7).
+//   B stage: BN rows x 32 bytes of packed 2-bit codes, 16-byte half h of
+//            row r stored at half h ^ bit2(r) ^ bit3(r).
+// The swizzles keep the 16-byte fragment reads of 8 or 16 consecutive rows on
+// distinct banks.  8 waves as 2 x 4, WM x WN per wave,
+// v_mfma_i32_32x32x32_i8 with the codes as the first operand, so the
+// accumulator tile is Y^T (lane column = token).
+// K assignment: in sub-step ks (32 wide) of a K step, lane l supplies the 16
+// values at k = 16 (4 (l / 32) + ks) for both operands, so one 16-byte read
+// gives a lane the codes of all four sub-steps.  The codes of sub-step ks+1
+// are unpacked between the MFMAs of sub-step ks.
+//
+// Tiles are 256 x 256 (128 x 64 per wave).  When the last round of tiles
+// would fill at most half of the compute units, its tiles are instead cut
+// into four 128 x 128 tiles (64 x 32 per wave), so the tail takes about a
+// quarter of a round instead of a whole one.
+// Requires M % 256 == 0, N % 256 == 0, K % 128 == 0.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int bswz(int row) { return ((row >> 2) ^ (row >> 3)) & 1; }
+
+__device__ __forceinline__ v4i unpack16(uint32_t w) {
+  return v4i{(int)unpack_group(w, 0), (int)unpack_group(w, 1), (int)unpack_group(w, 2),
+             (int)unpack_group(w, 3)};
 }
 
-template <typename TY, int MODE>
-__global__ void __launch_bounds__(512)
-    k_gemm_i8_dma(const int8_t* __restrict__ xq, const float* __restrict__ s,
-                  const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
-                  int32_t* __restrict__ acc_out) {
-  constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512;
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_le() {
+  // s_waitcnt vmcnt(N): vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt left at their maxima
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8));
+}
+
+constexpr int kDmaBM = 256, kDmaBN = 256;
+constexpr int kDmaLds = 3 * (kDmaBM * 128 + kDmaBN * 32);
+
+template <int BM, int BN, int WM, int WN, typename TY, int MODE>
+__device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
+                                              const uint32_t* __restrict__ codes, int64_t K,
+                                              int64_t N, const GemmOut& out, int32_t* acc_out,
+                                              int64_t m0, int64_t n0, int8_t* lds,
+                                              const float (*rrow)[kDmaBM]) {
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int AROW = 128;                       // bytes per A row per stage (no pad)
   constexpr int BROW = 32;                        // bytes of packed codes per B row per stage
   constexpr int ASTAGE = BM * AROW, BSTAGE = BN * BROW;
-  __shared__ __attribute__((aligned(1024))) int8_t lds[3 * (ASTAGE + BSTAGE)];
-  __shared__ float rrow[kMaxSeg][BM];
-
+  constexpr int KS = kBK / 32;                    // MFMA sub-steps per K step
+  constexpr int AJ = BM / 64;                     // A loads per wave per stage
+  constexpr int BW = BN / 32;                     // waves holding distinct B rows
+  static_assert((BM / WM) * (BN / WN) == 8 && BW <= 8 && 3 * (ASTAGE + BSTAGE) <= kDmaLds, "tile");
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
-  int64_t tm, tn;
-  tile_of_block(M / BM, N / BN, tm, tn);
-  const int64_t m0 = tm * BM, n0 = tn * BN;
   const int64_t KW = K / 16;
   const int nk = (int)(K / kBK);
 
-  for (int i = tid; i < kMaxSeg * BM; i += NT) {
-    const int sg = i / BM, r = i % BM;
-    rrow[sg][r] = sg < out.nseg ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
-  }
-
-  // Per-lane global sources.  A: wave w fills 1 KB chunks 4w..4w+3 (8 rows
-  // each); lane i -> row 8 j + i / 8, physical chunk i % 8.  B: wave w fills
-  // rows 32 w .. 32 w + 31, two lanes per row.
-  const int8_t* asrc[4];
+  // Per-lane global sources.  A: wave w fills 1 KB chunks AJ w .. AJ w + AJ-1
+  // (8 rows each); lane i -> row 8 j + i / 8, physical chunk i % 8.  B: wave
+  // w fills rows 32 (w % BW) .. + 31, two lanes (physical halves) per row
+  // (with BW < 8 two waves write the same bytes).
+  const int8_t* asrc[AJ];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = 8 * (4 * wid + j) + (lane >> 3);
+  for (int j = 0; j < AJ; ++j) {
+    const int row = 8 * (AJ * wid + j) + (lane >> 3);
     const int chunk = (lane & 7) ^ ((row >> 1) & 7);
     asrc[j] = xq + (m0 + row) * K + 16 * chunk;
   }
-  const uint32_t* bsrc = codes + (n0 + 32 * wid + (lane >> 1)) * KW + 4 * (lane & 1);
+  const int bw = wid % BW;
+  const int brow_l = 32 * bw + (lane >> 1);
+  const uint32_t* bsrc = codes + (n0 + brow_l) * KW + 4 * ((lane & 1) ^ bswz(brow_l));
 
-  const uint32_t wbase = __builtin_amdgcn_readfirstlane(wid);   // wave-uniform
+  const uint32_t wa = __builtin_amdgcn_readfirstlane(wid);   // wave-uniform
+  const uint32_t wb = __builtin_amdgcn_readfirstlane(bw);
   auto issue = [&](int kt, int8_t* Ad, uint32_t* Bd) __attribute__((always_inline)) {
     const int64_t koff = (int64_t)kt * kBK;
-    const uint32_t abase = lds_offset(Ad) + 4096u * wbase;
+    const uint32_t abase = lds_offset(Ad) + 1024u * AJ * wa;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) dma16(asrc[j] + koff, abase + 1024u * j);
-    dma16(bsrc + koff / 16, lds_offset(Bd) + 1024u * wbase);
+    for (int j = 0; j < AJ; ++j) dma16(asrc[j] + koff, abase + 1024u * j);
+    dma16(bsrc + koff / 16, lds_offset(Bd) + 1024u * wb);
   };
 
   v16i acc[TM][TN];
@@ -368,41 +388,52 @@ __global__ void __launch_bounds__(512)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
 
+  const int h = lane >> 5;
   const int arow0 = wm * WM + (lane & 31);        // A fragment row of this lane (a = 0)
   const int brow0 = wn * WN + (lane & 31);
-  // One K step: four 32-wide sub-steps; the fragments of sub-step ks+1 are
-  // read from LDS before the MFMAs of sub-step ks are issued (register double
-  // buffer), so LDS latency hides behind the matrix-core work.
   auto compute = [&](const int8_t* As, const uint32_t* Bs) __attribute__((always_inline)) {
     v4i af[2][TM];
-    uint32_t bw[2][TN];
-    auto frag = [&](int ks, int slot) __attribute__((always_inline)) {
-      const int c = 2 * ks + (lane >> 5);            // logical 16-byte chunk
+    v4i bq[TN], bfc[TN], bfn[TN];
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+      const int row = brow0 + 32 * b;
+      bq[b] = *reinterpret_cast<const v4i*>(Bs + row * (BROW / 4) + 4 * (h ^ bswz(row)));
+    }
+    auto afrag = [&](int ks, int slot) __attribute__((always_inline)) {
+      const int c = 4 * h + ks;                      // logical 16-byte chunk
 #pragma unroll
       for (int a = 0; a < TM; ++a) {
         const int row = arow0 + 32 * a;
         af[slot][a] = *reinterpret_cast<const v4i*>(As + row * AROW + 16 * (c ^ ((row >> 1) & 7)));
       }
-#pragma unroll
-      for (int b = 0; b < TN; ++b) bw[slot][b] = Bs[(brow0 + 32 * b) * (BROW / 4) + c];
     };
-    frag(0, 0);
+    afrag(0, 0);
 #pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
+    for (int b = 0; b < TN; ++b) bfc[b] = unpack16((uint32_t)bq[b][0]);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1;
-      if (ks + 1 < kBK / 32) frag(ks + 1, cur ^ 1);
-      __builtin_amdgcn_sched_barrier(0);
-      v4i bf[TN];
+      if (ks + 1 < KS) {
+        afrag(ks + 1, cur ^ 1);
 #pragma unroll
-      for (int b = 0; b < TN; ++b)
-        bf[b] = v4i{(int)unpack_group(bw[cur][b], 0), (int)unpack_group(bw[cur][b], 1),
-                    (int)unpack_group(bw[cur][b], 2), (int)unpack_group(bw[cur][b], 3)};
+        for (int b = 0; b < TN; ++b) bfn[b] = unpack16((uint32_t)bq[b][ks + 1]);
+      }
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
         for (int b = 0; b < TN; ++b)   // codes as the A operand: acc holds Y^T
-          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf[b], af[cur][a], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bfc[b], af[cur][a], acc[a][b], 0, 0, 0);
+      if (ks + 1 < KS) {
+        __builtin_amdgcn_sched_group_barrier(0x100, TM, 0);      // next A fragments (LDS reads)
+#pragma unroll
+        for (int i = 0; i < TM * TN; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);     // then unpack work (VALU)
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int b = 0; b < TN; ++b) bfc[b] = bfn[b];
     }
   };
 
@@ -411,14 +442,14 @@ __global__ void __launch_bounds__(512)
   // prologue: stages 0 and 1 in flight, stage 0 complete before the loop
   issue(0, Ast(0), Bst(0));
   if (nk > 1) issue(1, Ast(1), Bst(1));
-  if (nk > 1) wait_vmcnt_le5(); else __builtin_amdgcn_s_waitcnt(0);
+  if (nk > 1) wait_vmcnt_le<AJ + 1>(); else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int cur = 0;
   for (int kt = 0; kt < nk; ++kt) {
     const int nxt2 = cur == 0 ? 2 : cur - 1;     // (kt + 2) % 3
     if (kt + 2 < nk) issue(kt + 2, Ast(nxt2), Bst(nxt2));
     compute(Ast(cur), Bst(cur));
-    if (kt + 2 < nk) wait_vmcnt_le5(); else __builtin_amdgcn_s_waitcnt(0);
+    if (kt + 2 < nk) wait_vmcnt_le<AJ + 1>(); else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     cur = cur == 2 ? 0 : cur + 1;
   }
@@ -468,6 +499,41 @@ __global__ void __launch_bounds__(512)
   }
 }
 
+// Blocks [0, full) take 256 x 256 tiles [0, full) of the grouped order (XCD
+// aware); the following blocks take the four 128 x 128 quarters of each tile
+// in [full, T).
+template <typename TY, int MODE>
+__global__ void __launch_bounds__(512)
+    k_gemm_i8_dma(const int8_t* __restrict__ xq, const float* __restrict__ s,
+                  const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+                  int64_t full, int32_t* __restrict__ acc_out) {
+  __shared__ __attribute__((aligned(1024))) int8_t lds[kDmaLds];
+  __shared__ float rrow[kMaxSeg][kDmaBM];
+  const int64_t nb_m = M / kDmaBM, nb_n = N / kDmaBN;
+  const bool quarter = (int64_t)blockIdx.x >= full;
+  int64_t t, tm, tn;
+  int q = 0;
+  if (!quarter) {
+    t = xcd_linear(blockIdx.x, full);
+  } else {
+    const int64_t i = (int64_t)blockIdx.x - full;
+    t = full + i / 4;
+    q = (int)(i % 4);
+  }
+  tile_of_linear(t, nb_m, nb_n, tm, tn);
+  const int64_t m0 = tm * kDmaBM + (quarter ? 128 * (q >> 1) : 0);
+  const int64_t n0 = tn * kDmaBN + (quarter ? 128 * (q & 1) : 0);
+  const int rows = quarter ? 128 : kDmaBM;
+  for (int i = threadIdx.x; i < kMaxSeg * kDmaBM; i += 512) {
+    const int sg = i / kDmaBM, r = i % kDmaBM;
+    rrow[sg][r] = (sg < out.nseg && r < rows) ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
+  }
+  if (!quarter)
+    gemm_tile_dma<256, 256, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, rrow);
+  else
+    gemm_tile_dma<128, 128, 64, 32, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, rrow);
+}
+
 // ===========================================================================
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, hipStream_t st) {
@@ -505,10 +571,12 @@ static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* 
 
 // Tile choice: 256 x 256 blocks of 8 waves (128 x 64 per wave, two waves per
 // SIMD) when the grid fills the chip, 128 x 128 blocks of 4 waves otherwise;
-// the unpredicated variant when every tile is in bounds.
+// the direct-to-LDS variant when every tile is in bounds and the outputs allow
+// 4-wide stores, with its last round cut into 128 x 128 quarter tiles when it
+// would fill at most half of the n_cu compute units (n_cu = 0: never).
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
-                          int32_t* acc, hipStream_t st) {
+                          int32_t* acc, int n_cu, hipStream_t st) {
   const int64_t big_blocks = ((M + 255) / 256) * ((N + 255) / 256);
   if (big_blocks >= 256) {
     bool seg32 = true;
@@ -517,21 +585,27 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
     for (int i = 0; i < out.nseg; ++i)
       seg32 = seg32 && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
     if (M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32) {
-      dim3 grid((unsigned)((N / 256) * (M / 256)));
+      const int64_t T = big_blocks;
+      int64_t full = T;
+      if (n_cu > 0 && T > n_cu) {
+        const int64_t rem = T % n_cu;
+        if (rem > 0 && 2 * rem <= n_cu) full = T - rem;
+      }
+      dim3 grid((unsigned)(full + 4 * (T - full)));
       if (ydt == TERMEZO_F32) {
         if (mode == kGemmStore)
           hipLaunchKernelGGL((k_gemm_i8_dma<float, kGemmStore>), grid, dim3(512), 0, st, xq, s, codes,
-                             M, K, N, out, acc);
+                             M, K, N, out, full, acc);
         else
           hipLaunchKernelGGL((k_gemm_i8_dma<float, kGemmResidual>), grid, dim3(512), 0, st, xq, s,
-                             codes, M, K, N, out, acc);
+                             codes, M, K, N, out, full, acc);
       } else {
         if (mode == kGemmStore)
           hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmStore>), grid, dim3(512), 0, st, xq, s,
-                             codes, M, K, N, out, acc);
+                             codes, M, K, N, out, full, acc);
         else
           hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmResidual>), grid, dim3(512), 0, st, xq, s,
-                             codes, M, K, N, out, acc);
+                             codes, M, K, N, out, full, acc);
       }
       return hipGetLastError();
     }
@@ -542,7 +616,7 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
 
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
                                  const float* beta_dev, int64_t M, int64_t K, int64_t N, void* y,
-                                 termezo_dtype ydt, int32_t* acc, hipStream_t st) {
+                                 termezo_dtype ydt, int32_t* acc, int n_cu, hipStream_t st) {
   GemmOut out = {};
   out.nseg = 1;
   out.y[0] = y;
@@ -550,7 +624,7 @@ hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_
   out.beta[0] = beta_dev;
   out.nstart[0] = 0;
   out.nstart[1] = N;
-  return launch_gemm_i8(xq, s, codes, M, K, N, out, ydt, kGemmStore, acc, st);
+  return launch_gemm_i8(xq, s, codes, M, K, N, out, ydt, kGemmStore, acc, n_cu, st);
 }
 
 }  // namespace tmz

@@ -193,17 +193,23 @@ __device__ __forceinline__ uint32_t unpack_group(uint32_t word, int i) {
 constexpr int kXcd = 8;
 constexpr int kGroupM = 4;
 
-__device__ __forceinline__ void tile_of_block(int64_t nb_m, int64_t nb_n, int64_t& tm, int64_t& tn) {
-  const int64_t total = nb_m * nb_n;
-  const int64_t b = blockIdx.x;
+__device__ __forceinline__ int64_t xcd_linear(int64_t b, int64_t total) {
   const int64_t xcd = b % kXcd, local = b / kXcd;
   const int64_t full = total / kXcd, rem = total % kXcd;
-  const int64_t lb = xcd * full + min(xcd, rem) + local;
+  return xcd * full + min(xcd, rem) + local;
+}
+
+__device__ __forceinline__ void tile_of_linear(int64_t lb, int64_t nb_m, int64_t nb_n, int64_t& tm,
+                                               int64_t& tn) {
   const int64_t span = (int64_t)kGroupM * nb_n;
   const int64_t g = lb / span, in = lb % span;
   const int64_t gm = min((int64_t)kGroupM, nb_m - g * kGroupM);
   tm = g * kGroupM + in % gm;
   tn = in / gm;
+}
+
+__device__ __forceinline__ void tile_of_block(int64_t nb_m, int64_t nb_n, int64_t& tm, int64_t& tn) {
+  tile_of_linear(xcd_linear(blockIdx.x, nb_m * nb_n), nb_m, nb_n, tm, tn);
 }
 
 }  // namespace tmz

@@ -110,6 +110,7 @@ struct termezo_ctx {
   int64_t blk_cap = 0;
   double* d_loss = nullptr;                  // loss accumulators
   float* d_scal = nullptr;                   // [0] update coefficient a, [1] g
+  int n_cu = 0;                              // compute units of the device
   int8_t* d_xq = nullptr;                    // activation-quantisation scratch
   int64_t xq_cap = 0;
   float* d_xs = nullptr;
@@ -179,9 +180,10 @@ hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t
                             float* s, hipStream_t st);
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
-                          int32_t* acc, hipStream_t st);
+                          int32_t* acc, int n_cu, hipStream_t st);
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
                                  const float* beta_dev, int64_t M, int64_t K, int64_t N,
-                                 void* y, termezo_dtype ydt, int32_t* acc, hipStream_t st);
+                                 void* y, termezo_dtype ydt, int32_t* acc, int n_cu,
+                                 hipStream_t st);
 
 }  // namespace tmz

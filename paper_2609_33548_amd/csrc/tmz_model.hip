@@ -1072,7 +1072,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o3.nstart[0] = 0; o3.nstart[1] = dq; o3.nstart[2] = dq + dkv; o3.nstart[3] = dq + 2 * dkv;
     int sp = span_begin(m, 0, 2.0 * M * d * (dq + 2 * dkv), s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
-                       kGemmStore, nullptr, s));
+                       kGemmStore, nullptr, c->n_cu, s));
     span_end(m, sp, s);
     if (!bf) {   // bf16: the rotation is applied inside the attention kernel
       const unsigned rg =
@@ -1101,7 +1101,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     oo.nstart[0] = 0; oo.nstart[1] = d;
     sp = span_begin(m, 0, 2.0 * M * dq * d, s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
-                       nullptr, s));
+                       nullptr, c->n_cu, s));
     span_end(m, sp, s);
     // MLP sub-block
     rmsq(m->xq, m->xs, nullptr);
@@ -1112,7 +1112,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o2.nstart[0] = 0; o2.nstart[1] = F; o2.nstart[2] = 2 * F;
     sp = span_begin(m, 0, 2.0 * M * d * 2 * F, s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt, kGemmStore,
-                       nullptr, s));
+                       nullptr, c->n_cu, s));
     span_end(m, sp, s);
     if (bf)
       hipLaunchKernelGGL((k_row<kRowSwiGLU, uint16_t>), dim3(rowg), dim3(256), 0, s,
@@ -1129,7 +1129,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     od.nstart[0] = 0; od.nstart[1] = d;
     sp = span_begin(m, 0, 2.0 * M * F * d, s);
     chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
-                       nullptr, s));
+                       nullptr, c->n_cu, s));
     span_end(m, sp, s);
   }
   rmsq(nullptr, nullptr, m->xf);

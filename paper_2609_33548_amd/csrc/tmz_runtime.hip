@@ -217,6 +217,8 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_tile_eqb, (size_t)c->T), "alloc");
   chk(dalloc(&c->d_loss, 4), "alloc");
   chk(dalloc(&c->d_scal, 4), "alloc");
+  chk(hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device),
+      "device attribute");
   if (st == TERMEZO_OK) {
     chk(hipMemcpy(c->d_wptr, wptr.data(), n_layers * sizeof(void*), hipMemcpyHostToDevice), "copy");
     chk(hipMemcpy(c->d_n, n.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice), "copy");
@@ -353,7 +355,7 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
   }
   TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->stream));
   TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
-                                   L.d_in, L.d_out, y, y_dtype, acc_out, c->stream));
+                                   L.d_in, L.d_out, y, y_dtype, acc_out, c->n_cu, c->stream));
   return TERMEZO_OK;
 }
 

@@ -140,13 +140,17 @@ def test_bitlinear_matches_oracle(orc, M, K, N, xdt, ydt):
     assert np.array_equal(y.float().cpu().numpy(), ry)
 
 
-@pytest.mark.parametrize("M,K,N", [(8192, 2560, 2560),   # 256x256 tiles, every tile full
+@pytest.mark.parametrize("M,K,N", [(8192, 2560, 2560),   # 320 tiles: last 64 cut in quarters
+                                   (8192, 1024, 2816),   # 352 tiles: last 96 cut in quarters
+                                   (8192, 2560, 3840),   # 480 tiles: whole tiles only
                                    (8232, 2560, 2560),   # ragged M on the large-tile path
                                    (8192, 688, 8192),    # K not a multiple of the K step
-                                   (4096, 6912, 4352)])  # K = 6912, N = 17 x 256
+                                   (4096, 6912, 4352)])  # 272 tiles: last 16 cut in quarters
 def test_bitlinear_large_grid_sampled_rows(orc, M, K, N):
-    """Launch sizes that select the large-tile kernels; the oracle evaluates a
-    sample of rows (rows are independent), including the first and last."""
+    """Launch sizes that select the large-tile kernels (with and without the
+    quarter-tile tail); the oracle evaluates a sample of rows (rows are
+    independent), including the first and last and a band of the last quarter
+    of rows, where the tail tiles lie.  Two calls in a row with new inputs."""
     torch = _torch()
     print(f"bitlinear large M={M} K={K} N={N}", flush=True)
     ref, ctx, _ = _setup(orc, [(N, K)], bf16=True, seed=8)
@@ -154,22 +158,24 @@ def test_bitlinear_large_grid_sampled_rows(orc, M, K, N):
     ref.build_mask(0.001)
     ctx.perturb(21, 1e-3, -1)
     codes, _, betas = ref.perturb(21, 1e-3, -1)
-    xd = synth.torch_normal(9, (M, K), torch.bfloat16, "cuda")
     y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
     acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
     xq = torch.empty((M, K), dtype=torch.int8, device="cuda")
     s = torch.empty(M, dtype=torch.float32, device="cuda")
-    ctx.bitlinear_forward(0, xd, y, xq, s, acc)
-    torch.cuda.synchronize()
-    rows = np.unique(np.concatenate([[0, 1, 255, 256, M - 1],
-                                     np.random.default_rng(0).integers(0, M, 40)]))
-    x = xd[torch.from_numpy(rows).cuda()].float().cpu().numpy()
-    rxq, rs = orc.act_quant(x)
-    racc, ry = orc.bitlinear(rxq, rs, codes[0], betas[0])
-    assert np.array_equal(xq.cpu().numpy()[rows], rxq)
-    assert np.array_equal(s.cpu().numpy()[rows], rs)
-    assert np.array_equal(acc.cpu().numpy()[rows], racc)
-    assert np.array_equal(y.float().cpu().numpy()[rows], orc.bf16_round(ry))
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, M - 256, M - 1],
+                                     np.random.default_rng(0).integers(0, M, 40),
+                                     np.random.default_rng(1).integers(M - M // 4, M, 16)]))
+    for xseed in (9, 10):
+        xd = synth.torch_normal(xseed, (M, K), torch.bfloat16, "cuda")
+        ctx.bitlinear_forward(0, xd, y, xq, s, acc)
+        torch.cuda.synchronize()
+        x = xd[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+        rxq, rs = orc.act_quant(x)
+        racc, ry = orc.bitlinear(rxq, rs, codes[0], betas[0])
+        assert np.array_equal(xq.cpu().numpy()[rows], rxq)
+        assert np.array_equal(s.cpu().numpy()[rows], rs)
+        assert np.array_equal(acc.cpu().numpy()[rows], racc)
+        assert np.array_equal(y.float().cpu().numpy()[rows], orc.bf16_round(ry))
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
