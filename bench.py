@@ -129,6 +129,173 @@ def cpu_baseline(c, rho, seed=0):
         "extrapolated_step_s": t_step,
     }
 
+# ---------------------------------------------------------------------------
+# Kernel sweeps (--sweep): the perturb/requant and update kernels over a
+# 2.4e9-latent tensor at several mask ratios, and the BitLinear forward over
+# small and large token counts.  Each point prints one JSON line.
+# ---------------------------------------------------------------------------
+HBM_PEAK_GBS = 8000.0
+SWEEP_LAYER = (6912, 2560)           # 136 layers of this shape: 2,406,481,920 latents
+SWEEP_LAYERS = 136
+SWEEP_RATIOS = (1e-4, 1e-3, 1e-2, 1.0)
+SWEEP_GEMM_KN = ((2560, 2560), (2560, 6912), (6912, 2560))
+SWEEP_GEMM_M = (1, 16, 128, 2048, 8192)
+
+
+def _emit(rec):
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_latent_sweep(ratio, seed=0):
+    """Oracle perturb(+)/update(+shrink) on one sweep layer; seconds per call."""
+    from oracle import termezo_ref as orc
+    from paper_2609_33548_amd import synth
+    o, i = SWEEP_LAYER
+    w = synth.latents(seed, [o * i], bf16=True)
+    st = orc.TerMeZOOracle([orc.Layer(o, i)], w, bf16=True)
+    st.build_mask(ratio)
+    t0 = time.perf_counter()
+    st.perturb(1, 1e-3, 1)
+    t_p = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    st.update(1.0, 1e-5)
+    t_u = time.perf_counter() - t0
+    return t_p, t_u
+
+
+def sweep_latent(torch, termezo, synth, dev, cpu):
+    o, i = SWEEP_LAYER
+    D = SWEEP_LAYERS * o * i
+    lat = synth.torch_latents(4321, D, torch.bfloat16, dev)
+    layers = [lat[l * o * i:(l + 1) * o * i].view(o, i) for l in range(SWEEP_LAYERS)]
+    torch.cuda.synchronize()
+    ctx = termezo.Context(layers)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 10
+    for r in SWEEP_RATIOS:
+        k0, _ = ctx.build_mask(r)
+        ctx.perturb(0, 1e-3, 1)
+        ctx.update(1.0, 1e-5, want_k=False)
+        ctx.perturb(1, 1e-3, 1)          # warm
+        k = ctx.active_count()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for t in range(reps):
+            ctx.perturb(100 + t, 1e-3, 1 if t % 2 == 0 else -1)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        t_p = ev0.elapsed_time(ev1) / reps * 1e-3
+        up = 0.0
+        for t in range(reps):
+            ctx.perturb(200 + t, 1e-3, 1)
+            ev0.record(stream)
+            ctx.update(1.0, 1e-5, want_k=False)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            up += ev0.elapsed_time(ev1) * 1e-3
+        t_u = up / reps
+        k_after = ctx.active_count()
+        b_p = D * (2 + 0.25) + k * (4 + 2)
+        b_u = 16 * k
+        cp = cu = None
+        if cpu:
+            c_p, c_u = cpu_latent_sweep(r)
+            cp = {"value": (o * i * 2.25 + (k / SWEEP_LAYERS) * 6) / c_p / 1e9, "unit": "GB/s",
+                  "kind": "oracle", "sample": f"one {o}x{i} layer, perturb(+), same ratio"}
+            cu = {"value": c_u * SWEEP_LAYERS * 1e6, "unit": "us (scaled x136)", "kind": "oracle",
+                  "sample": f"one {o}x{i} layer, update+shrink, same ratio"}
+        _emit({"sweep": "perturb_requant", "latents": D, "ratio": r, "k": k, "ms": t_p * 1e3,
+               "algorithmic_bytes": b_p, "GB/s": b_p / t_p / 1e9,
+               "frac_hbm": b_p / t_p / 1e9 / HBM_PEAK_GBS, "cpu_baseline": cp})
+        _emit({"sweep": "update", "latents": D, "ratio": r, "k": k, "k_after": k_after,
+               "us": t_u * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_u / 1e9,
+               "frac_hbm": b_u / t_u / 1e9 / HBM_PEAK_GBS, "cpu_baseline": cu})
+    ctx.close()
+    del lat, layers
+    torch.cuda.empty_cache()
+
+
+def cpu_bitlinear(M, K, N, seed=0):
+    """Oracle BitLinear (activation quantisation + exact integer product) on at
+    most 16 rows; seconds for the full M by row scaling."""
+    import numpy as np
+    from oracle import termezo_ref as orc
+    from paper_2609_33548_amd import synth
+    m = min(M, 16)
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(-1, 2, size=(N, K)).astype(np.int8)
+    x = synth.activations(seed, m, K, bf16=True)
+    t0 = time.perf_counter()
+    xq, s = orc.act_quant(x)
+    orc.bitlinear(xq, s, codes, 0.016)
+    return (time.perf_counter() - t0) * M / m
+
+
+def sweep_bitlinear(torch, termezo, synth, dev, cpu):
+    for K, N in SWEEP_GEMM_KN:
+        code_bytes = N * K // 4
+        L = max(64, -(-(512 << 20) // code_bytes))       # >= 512 MB of codes: beyond the caches
+        lat = synth.torch_latents(77, L * N * K, torch.bfloat16, dev)
+        layers = [lat[l * N * K:(l + 1) * N * K].view(N, K) for l in range(L)]
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            ctx = termezo.Context(layers, stream=stream)
+            ctx.build_mask(1e-3)
+            ctx.perturb(1, 1e-3, 1)
+        for M in SWEEP_GEMM_M:
+            x = synth.torch_normal(5, (M, K), torch.float32, dev).to(torch.bfloat16)
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            torch.cuda.synchronize()
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(stream):
+                ctx.bitlinear_forward(0, x, y)          # sizes the scratch before any capture
+                stream.synchronize()
+                if M <= 128:
+                    # one graph cycling over all L code buffers (cold caches), replayed 3 times
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=stream):
+                        for l in range(L):
+                            ctx.bitlinear_forward(l, x, y)
+                    g.replay()
+                    stream.synchronize()
+                    ev0.record(stream)
+                    for _ in range(3):
+                        g.replay()
+                    ev1.record(stream)
+                    stream.synchronize()
+                    calls = 3 * L
+                    del g
+                else:
+                    for _ in range(2):
+                        ctx.bitlinear_forward(0, x, y)
+                    ev0.record(stream)
+                    calls = 10
+                    for _ in range(calls):
+                        ctx.bitlinear_forward(0, x, y)
+                    ev1.record(stream)
+                    stream.synchronize()
+            t = ev0.elapsed_time(ev1) * 1e-3 / calls
+            ops = 2.0 * M * K * N
+            byts = K * N / 4 + M * K + 4 * M + 2 * M * N
+            c = None
+            if cpu:
+                tc = cpu_bitlinear(M, K, N)
+                c = {"value": ops / tc / 1e12, "unit": "TOP/s", "kind": "oracle",
+                     "sample": f"{min(M, 16)} rows scaled to {M}"}
+            _emit({"sweep": "bitlinear_forward", "M": M, "K": K, "N": N, "us": t * 1e6,
+                   "TOP/s": ops / t / 1e12, "frac_int8_peak": ops / t / 1e12 / PEAK_INT8_TOPS,
+                   "algorithmic_bytes": byts, "GB/s": byts / t / 1e9,
+                   "frac_hbm": byts / t / 1e9 / HBM_PEAK_GBS,
+                   "protocol": (f"graph over {L} code buffers ({L * code_bytes >> 20} MiB), "
+                                "activation quantisation included") if M <= 128 else
+                               "10 back-to-back calls, activation quantisation included",
+                   "cpu_baseline": c})
+        ctx.close()
+        del lat, layers
+        torch.cuda.empty_cache()
+
+
 
 def main():
     ap = argparse.ArgumentParser()
@@ -140,6 +307,8 @@ def main():
     ap.add_argument("--eps", type=float, default=1e-3)
     ap.add_argument("--lr", type=float, default=1e-5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", choices=["latent", "bitlinear", "all"],
+                    help="run the kernel sweeps instead of the step benchmark")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the measurement, copy 1 GiB device to device (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
@@ -152,9 +321,15 @@ def main():
     import torch
     from paper_2609_33548_amd import synth, termezo
 
-    c = CONFIGS[args.config]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.sweep:
+        if args.sweep in ("latent", "all"):
+            sweep_latent(torch, termezo, synth, dev, not args.no_cpu_baseline)
+        if args.sweep in ("bitlinear", "all"):
+            sweep_bitlinear(torch, termezo, synth, dev, not args.no_cpu_baseline)
+        return
+    c = CONFIGS[args.config]
     shapes = layer_shapes(c)
     D = sum(o * i for o, i in shapes)
     print(f"[bench] config {args.config}: {len(shapes)} ternary projections, {D} latents", flush=True)

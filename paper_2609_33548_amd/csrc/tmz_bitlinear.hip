@@ -38,17 +38,37 @@ __device__ __forceinline__ int32_t quant_byte(float x, float s) {
   return (int32_t)q;
 }
 
+// Rows of up to kActRegs * 4 * 256 values are held in registers (one read of
+// x); longer rows are read twice.
+constexpr int kActRegs = 8;
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int64_t K,
                                                    int8_t* __restrict__ xq, float* __restrict__ s) {
   __shared__ float red[4];
   const int64_t m = blockIdx.x;
   const T* row = x + m * K;
+  uint32_t* out = reinterpret_cast<uint32_t*>(xq + m * K);
+  const bool held = K <= (int64_t)kActRegs * 4 * 256;
+  float v[kActRegs][4];
   float a = 0.0f;
-  for (int64_t k = (int64_t)threadIdx.x * 4; k < K; k += 256 * 4) {
-    float v[4];
-    load4(row + k, v);
-    a = fmaxf(a, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+  if (held) {
+#pragma unroll
+    for (int i = 0; i < kActRegs; ++i) {
+      const int64_t k = ((int64_t)i * 256 + threadIdx.x) * 4;
+      if (k < K) {
+        load4(row + k, v[i]);
+      } else {
+        v[i][0] = v[i][1] = v[i][2] = v[i][3] = 0.0f;
+      }
+      a = fmaxf(a, fmaxf(fmaxf(fabsf(v[i][0]), fabsf(v[i][1])), fmaxf(fabsf(v[i][2]), fabsf(v[i][3]))));
+    }
+  } else {
+    for (int64_t k = (int64_t)threadIdx.x * 4; k < K; k += 256 * 4) {
+      float w[4];
+      load4(row + k, w);
+      a = fmaxf(a, fmaxf(fmaxf(fabsf(w[0]), fabsf(w[1])), fmaxf(fabsf(w[2]), fabsf(w[3]))));
+    }
   }
   a = wave_max(a);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
@@ -56,15 +76,25 @@ __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int6
   a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
   if (threadIdx.x == 0) s[m] = sc;
-  uint32_t* out = reinterpret_cast<uint32_t*>(xq + m * K);
-  for (int64_t k = (int64_t)threadIdx.x * 4; k < K; k += 256 * 4) {
-    float v[4];
-    load4(row + k, v);
-    const uint32_t b0 = (uint32_t)quant_byte(v[0], sc) & 0xFFu;
-    const uint32_t b1 = (uint32_t)quant_byte(v[1], sc) & 0xFFu;
-    const uint32_t b2 = (uint32_t)quant_byte(v[2], sc) & 0xFFu;
-    const uint32_t b3 = (uint32_t)quant_byte(v[3], sc) & 0xFFu;
-    out[k / 4] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+  auto pack = [&](const float* w) __attribute__((always_inline)) {
+    const uint32_t b0 = (uint32_t)quant_byte(w[0], sc) & 0xFFu;
+    const uint32_t b1 = (uint32_t)quant_byte(w[1], sc) & 0xFFu;
+    const uint32_t b2 = (uint32_t)quant_byte(w[2], sc) & 0xFFu;
+    const uint32_t b3 = (uint32_t)quant_byte(w[3], sc) & 0xFFu;
+    return b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+  };
+  if (held) {
+#pragma unroll
+    for (int i = 0; i < kActRegs; ++i) {
+      const int64_t k = ((int64_t)i * 256 + threadIdx.x) * 4;
+      if (k < K) out[k / 4] = pack(v[i]);
+    }
+  } else {
+    for (int64_t k = (int64_t)threadIdx.x * 4; k < K; k += 256 * 4) {
+      float w[4];
+      load4(row + k, w);
+      out[k / 4] = pack(w);
+    }
   }
 }
 
@@ -534,6 +564,153 @@ __global__ void __launch_bounds__(512)
     gemm_tile_dma<128, 128, 64, 32, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, rrow);
 }
 
+// ---------------------------------------------------------------------------
+// Small-M BitLinear (M <= kGemvMaxM): one block of 8 waves per 16 output
+// features, so even M = 1 spreads the code stream over N / 16 blocks.
+// v_mfma_i32_16x16x64_i8 with the codes as the first operand (16 features x
+// 64 k) and a group of 16 tokens as the second.  K is cut in chunks of 256
+// (16 code words per feature); in a chunk, lane l loads the 4 words
+// 4 (l / 16) .. 4 (l / 16) + 3 of feature l % 16 (one 16-byte load) and MFMA j
+// takes word j, i.e. k = 16 (4 (l / 16) + j) .. + 15, with the 16 int8
+// activations of token l % 16 at the same k.  Chunks are dealt round-robin to
+// the 8 waves; their int32 partial sums meet in LDS.
+// Accumulator (16 x 16, 4 values per lane): token l % 16, features
+// 4 (l / 16) .. 4 (l / 16) + 3.  Segment boundaries are multiples of 16.
+// ---------------------------------------------------------------------------
+constexpr int kGemvMaxM = 128;
+
+template <typename TY, int MODE, bool CVEC>
+__global__ void __launch_bounds__(512)
+    k_gemv_i8(const int8_t* __restrict__ xq, const float* __restrict__ s,
+              const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+              int yvec, int32_t* __restrict__ acc_out) {
+  constexpr int NW = 8, G = kGemvMaxM / 16;
+  __shared__ int32_t red[NW][G][4][64];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t n0 = (int64_t)blockIdx.x * 16;
+  const int64_t KW = K / 16;
+  const int nchunk = (int)((KW + 15) / 16);
+  const int ng = (int)((M + 15) / 16);
+  const int fr = lane & 15, g = lane >> 4;
+  const bool row_ok = n0 + fr < N;
+  const uint32_t* crow = codes + (row_ok ? n0 + fr : 0) * KW;
+  // Every load below is unconditional, from a clamped in-bounds address, and
+  // out-of-range values are zeroed afterwards: no load sits in a branch, so
+  // all of them are in flight together.
+  v4i acc[G];
+#pragma unroll
+  for (int tg = 0; tg < G; ++tg) acc[tg] = v4i{0, 0, 0, 0};
+  // code words of chunk c (zero outside the matrix)
+  auto cload = [&](int c, uint32_t* cw) __attribute__((always_inline)) {
+    const int64_t w0 = (int64_t)c * 16 + 4 * g;        // first code word of this lane
+    if (CVEC) {                                        // KW % 4 == 0: 4 words or none
+      const v4u v = *reinterpret_cast<const v4u*>(crow + (w0 < KW ? w0 : 0));
+      const bool ok = row_ok && w0 < KW;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cw[j] = ok ? v[j] : 0u;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t v = crow[w0 + j < KW ? w0 + j : 0];
+        cw[j] = (row_ok && w0 + j < KW) ? v : 0u;
+      }
+    }
+  };
+  // activations of token group tg at this lane's 4 k chunks of chunk c (zero outside)
+  auto xload = [&](int c, int tg, v4i* b) __attribute__((always_inline)) {
+    const int64_t kb = ((int64_t)c * 16 + 4 * g) * 16;
+    const int64_t m = 16 * tg + fr;
+    const int8_t* xr = xq + (m < M ? m : 0) * K;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t k = kb + 16 * j;
+      b[j] = *reinterpret_cast<const v4i*>(xr + (k < K ? k : 0));
+      if (!(m < M && k < K)) b[j] = v4i{0, 0, 0, 0};
+    }
+  };
+  auto mfma4 = [&](const v4i* a, const v4i* b, v4i& acc_) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc_ = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[j], b[j], acc_, 0, 0, 0);
+  };
+  // Two chunks per pass (c and c + NW; the second may lie beyond the matrix
+  // and then contributes zero): both chunks' loads are in flight together.
+  for (int c = wid; c < nchunk; c += 2 * NW) {
+    uint32_t cw0[4], cw1[4];
+    v4i b0[4], b1[4];
+    cload(c, cw0);
+    cload(c + NW, cw1);
+    xload(c, 0, b0);
+    xload(c + NW, 0, b1);
+    v4i a0[4], a1[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) a0[j] = unpack16(cw0[j]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) a1[j] = unpack16(cw1[j]);
+    mfma4(a0, b0, acc[0]);
+    mfma4(a1, b1, acc[0]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int tg = 1; tg < G; ++tg) {
+      if (tg < ng) {
+        xload(c, tg, b0);
+        xload(c + NW, tg, b1);
+        mfma4(a0, b0, acc[tg]);
+        mfma4(a1, b1, acc[tg]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int tg = 0; tg < G; ++tg)
+    if (tg < ng)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wid][tg][i][lane] = acc[tg][i];
+  __syncthreads();
+
+  for (int tg = wid; tg < ng; tg += NW) {             // one wave per token group
+    const int64_t m = 16 * tg + fr;
+    if (m >= M) continue;
+    int32_t v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int32_t t = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) t += red[w][tg][i][lane];
+      v[i] = t;
+    }
+    const int64_t n = n0 + 4 * g;
+    if (n >= N) continue;
+    int sg = 0;
+    if (out.nseg > 1 && n >= out.nstart[1]) sg = 1;
+    if (out.nseg > 2 && n >= out.nstart[2]) sg = 2;
+    const float rr = __fdiv_rn(*out.beta[sg], s[m]);
+    TY* p = reinterpret_cast<TY*>(out.y[sg]) + m * out.ld[sg] + (n - out.nstart[sg]);
+    float y4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y4[i] = (float)v[i] * rr;
+    if (yvec && n + 3 < N) {
+      if (MODE == kGemmStore) {
+        store4(p, y4);
+      } else {
+        float h4[4];
+        load4v(p, h4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) y4[i] = h4[i] + round_act(p, y4[i]);
+        store4(p, y4);
+      }
+    } else {
+      for (int i = 0; i < 4 && n + i < N; ++i) {
+        if (MODE == kGemmStore)
+          store_act(p + i, y4[i]);
+        else
+          store_act(p + i, load_act(p + i) + round_act(p + i, y4[i]));
+      }
+    }
+    if (acc_out)
+      for (int i = 0; i < 4 && n + i < N; ++i) acc_out[m * N + n + i] = v[i];
+  }
+}
+
 // ===========================================================================
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, hipStream_t st) {
@@ -569,7 +746,7 @@ static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* 
   return hipGetLastError();
 }
 
-// Tile choice: 256 x 256 blocks of 8 waves (128 x 64 per wave, two waves per
+// Tile choice: the small-M kernel up to kGemvMaxM tokens; 256 x 256 blocks of 8 waves (128 x 64 per wave, two waves per
 // SIMD) when the grid fills the chip, 128 x 128 blocks of 4 waves otherwise;
 // the direct-to-LDS variant when every tile is in bounds and the outputs allow
 // 4-wide stores, with its last round cut into 128 x 128 quarter tiles when it
@@ -577,6 +754,31 @@ static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* 
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
                           int32_t* acc, int n_cu, hipStream_t st) {
+  if (M <= kGemvMaxM) {
+    bool seg16 = true;
+    for (int i = 1; i < out.nseg; ++i) seg16 = seg16 && out.nstart[i] % 16 == 0;
+    if (seg16) {
+      const int cvec = (K / 16) % 4 == 0 && reinterpret_cast<uintptr_t>(codes) % 16 == 0;
+      const uintptr_t vec = ydt == TERMEZO_F32 ? 16 : 8;   // 4-element store width
+      int yvec = 1;
+      for (int i = 0; i < out.nseg; ++i)
+        yvec = yvec && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
+      dim3 grid((unsigned)((N + 15) / 16));
+#define TMZ_GEMV(TY, MD, CV)                                                                    \
+  hipLaunchKernelGGL((k_gemv_i8<TY, MD, CV>), grid, dim3(512), 0, st, xq, s, codes, M, K, N, out, \
+                     yvec, acc)
+      const bool f32 = ydt == TERMEZO_F32, store = mode == kGemmStore;
+      if (cvec) {
+        if (f32) { if (store) TMZ_GEMV(float, kGemmStore, true); else TMZ_GEMV(float, kGemmResidual, true); }
+        else { if (store) TMZ_GEMV(uint16_t, kGemmStore, true); else TMZ_GEMV(uint16_t, kGemmResidual, true); }
+      } else {
+        if (f32) { if (store) TMZ_GEMV(float, kGemmStore, false); else TMZ_GEMV(float, kGemmResidual, false); }
+        else { if (store) TMZ_GEMV(uint16_t, kGemmStore, false); else TMZ_GEMV(uint16_t, kGemmResidual, false); }
+      }
+#undef TMZ_GEMV
+      return hipGetLastError();
+    }
+  }
   const int64_t big_blocks = ((M + 255) / 256) * ((N + 255) / 256);
   if (big_blocks >= 256) {
     bool seg32 = true;

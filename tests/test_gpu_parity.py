@@ -76,7 +76,8 @@ def test_gauss_is_bit_identical_to_oracle(orc):
 
 @pytest.mark.parametrize("shapes", [[(256, 256)], C2_LAYERS], ids=["c1", "c2"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-@pytest.mark.parametrize("rho0,inclusive", [(0.01, False), (0.001, False), (0.01, True)])
+@pytest.mark.parametrize("rho0,inclusive", [(0.01, False), (0.001, False), (0.01, True),
+                                           (1.0, False)])
 def test_build_mask_matches_oracle(orc, shapes, bf16, rho0, inclusive):
     print(f"mask shapes={len(shapes)} bf16={bf16} rho0={rho0} incl={inclusive}", flush=True)
     ref, ctx, _ = _setup(orc, shapes, bf16, seed=1)
@@ -91,11 +92,12 @@ def test_build_mask_matches_oracle(orc, shapes, bf16, rho0, inclusive):
 
 @pytest.mark.parametrize("shapes", [[(256, 256)], C2_LAYERS], ids=["c1", "c2"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-def test_perturb_codes_match_oracle(orc, shapes, bf16):
-    print(f"perturb shapes={len(shapes)} bf16={bf16}", flush=True)
+@pytest.mark.parametrize("rho0", [0.05, 1.0])
+def test_perturb_codes_match_oracle(orc, shapes, bf16, rho0):
+    print(f"perturb shapes={len(shapes)} bf16={bf16} rho0={rho0}", flush=True)
     ref, ctx, tensors = _setup(orc, shapes, bf16, seed=2)
-    ctx.build_mask(0.05)
-    ref.build_mask(0.05)
+    ctx.build_mask(rho0)
+    ref.build_mask(rho0)
     before = [t.clone() for t in tensors]
     for seed, eps, sign in [(7, 1e-3, 1), (7, 1e-3, -1), (123456789, 5e-3, 1), (7, 1e-3, 0)]:
         ctx.perturb(seed, eps, sign)
@@ -111,7 +113,11 @@ def test_perturb_codes_match_oracle(orc, shapes, bf16):
 
 @pytest.mark.parametrize("M,K,N", [(1, 256, 256), (8, 256, 256), (16, 2560, 2560),
                                    (130, 688, 256), (257, 256, 688), (64, 6912, 2560),
-                                   (300, 2560, 640)])
+                                   (300, 2560, 640),
+                                   # small-M kernel: ragged features, K not a multiple of 64,
+                                   # a partial token group, the largest token count, K = 16
+                                   (1, 2560, 6912), (17, 688, 100), (128, 6912, 2560),
+                                   (3, 16, 48), (100, 256, 200)])
 @pytest.mark.parametrize("xdt,ydt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
 def test_bitlinear_matches_oracle(orc, M, K, N, xdt, ydt):
     torch = _torch()
@@ -179,11 +185,12 @@ def test_bitlinear_large_grid_sampled_rows(orc, M, K, N):
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-def test_update_and_shrink_match_oracle(orc, bf16):
-    print(f"update bf16={bf16}", flush=True)
+@pytest.mark.parametrize("rho0", [0.01, 1.0])
+def test_update_and_shrink_match_oracle(orc, bf16, rho0):
+    print(f"update bf16={bf16} rho0={rho0}", flush=True)
     ref, ctx, tensors = _setup(orc, C2_LAYERS, bf16, seed=5)
-    ctx.build_mask(0.01)
-    ref.build_mask(0.01)
+    ctx.build_mask(rho0)
+    ref.build_mask(rho0)
     gs = [40.0, -25.0, 60.0, -80.0, 10.0, 120.0]
     for t, g in enumerate(gs):
         seed = t
