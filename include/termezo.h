@@ -72,7 +72,8 @@ typedef struct termezo_ctx termezo_ctx;
  * BF16) and allocate the library-owned state: packed 2-bit ternary codes
  * (d_out * d_in / 4 bytes per layer), per-layer thresholds and fixed-point
  * sums, and mask storage.  hip_stream: a hipStream_t (NULL = default stream).
- * Errors: INVALID_ARG (null pointers, n_layers <= 0, d_in % 16 != 0,
+ * At most 2048 layers per context; each layer at most 2^25 weights.
+ * Errors: INVALID_ARG (null pointers, n_layers <= 0 or > 2048, d_in % 16 != 0,
  * misaligned latent, layer too large, bad dtype), DEVICE, OOM. */
 termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
                               termezo_dtype latent_dtype, void* hip_stream,

@@ -130,6 +130,29 @@ __device__ __forceinline__ float gauss_at(uint64_t seed, uint64_t gid) {
   return (lane & 1u) ? zs : zc;
 }
 
+// z for a run of global ids: ids of one quad share their Philox call and ids
+// of one pair share their Box-Muller evaluation (the same operations as
+// gauss_at, so the values are identical).
+struct GaussCache {
+  uint64_t quad = ~0ull, pair = ~0ull;
+  U4 x = {0u, 0u, 0u, 0u};
+  float zc = 0.0f, zs = 0.0f;
+  __device__ __forceinline__ float get(uint64_t seed, uint64_t gid) {
+    const uint64_t p = gid >> 1;
+    if (p != pair) {
+      const uint64_t q = gid >> 2;
+      if (q != quad) {
+        x = philox10((uint32_t)q, (uint32_t)(q >> 32), 0u, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
+        quad = q;
+      }
+      const bool hi = (gid & 2u) != 0;
+      box_muller(hi ? x.c : x.a, hi ? x.d : x.b, zc, zs);
+      pair = p;
+    }
+    return (gid & 1u) ? zs : zc;
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Fixed-point |w|: floor(|w| * 2^36) taken from the fp32 bit pattern.
 // Valid for |w| < 4 (then the result is below 2^38).

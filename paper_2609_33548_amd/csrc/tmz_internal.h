@@ -13,6 +13,7 @@ namespace tmz {
 constexpr int kTile = 8192;          // elements per streaming tile (never straddles layers)
 constexpr int kBlock = 256;          // threads per block for streaming kernels
 constexpr int kHistBins = 2048;      // radix-select histogram width (11 bits)
+constexpr int kMaxLayers = 2048;     // layers per context (active-list offsets fit in LDS)
 
 struct LayerHost {
   void* w;
@@ -29,6 +30,8 @@ struct DevState {
   const int64_t* code_off;           // [L]
   const int32_t* tile_layer;         // [T]
   const int64_t* tile_start;         // [T] layer-local start element
+  const int64_t* tile0;              // [L] first tile of each layer
+  int64_t* tile_act;                 // [T+1] first active-list position at or after tile t
   uint32_t* codes;                   // packed codes, all layers
   int64_t* S_clean;                  // [L] fixed-point sum of |w|
   int64_t* S_cur;                    // [L] fixed-point sum of |w'| of the current codes
@@ -81,6 +84,8 @@ struct termezo_ctx {
   int64_t* d_code_off = nullptr;
   int32_t* d_tile_layer = nullptr;
   int64_t* d_tile_start = nullptr;
+  int64_t* d_tile0 = nullptr;
+  int64_t* d_tile_act = nullptr;             // T + 1
   uint32_t* d_codes = nullptr;
   int64_t* d_S_clean = nullptr;
   int64_t* d_S_cur = nullptr;
@@ -138,6 +143,8 @@ struct termezo_ctx {
     s.code_off = d_code_off;
     s.tile_layer = d_tile_layer;
     s.tile_start = d_tile_start;
+    s.tile0 = d_tile0;
+    s.tile_act = d_tile_act;
     s.codes = d_codes;
     s.S_clean = d_S_clean;
     s.S_cur = d_S_cur;
@@ -163,14 +170,17 @@ hipError_t launch_copy_i64(int64_t* dst, const int64_t* src, int64_t n, hipStrea
 hipError_t launch_select(termezo_ctx* c, int64_t k0);     // three radix passes -> d_sel
 hipError_t launch_mask_compact_counts(termezo_ctx* c, int inclusive);  // -> act_off
 hipError_t launch_mask_compact_write(termezo_ctx* c, int inclusive);   // -> act
-hipError_t launch_requant_dense(termezo_ctx* c);          // codes of w with tau_cur
+hipError_t launch_tile_ranges(termezo_ctx* c);            // d_act, d_act_off -> d_tile_act
+// codes of w with tau_cur; with patch, the actives' codes from their perturbed values d_wp
+hipError_t launch_requant(termezo_ctx* c, int patch);
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se);
-hipError_t launch_patch_codes(termezo_ctx* c, int64_t k);
 hipError_t launch_set_coeff(termezo_ctx* c, float a);
 hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float* fm, float eps,
                                     float lr);
-hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed);   // a from d_scal[0]
-hipError_t launch_shrink(termezo_ctx* c, int64_t k);      // d_act -> d_act_tmp, offsets -> tmp
+// a from d_scal[0]; the updated values of the actives go to d_wp (list order)
+hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed);
+// from d_wp (the updated values): d_act -> d_act_tmp, offsets -> tmp
+hipError_t launch_shrink(termezo_ctx* c, int64_t k);
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);
 hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z, hipStream_t s);
 hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hipStream_t s);

@@ -75,7 +75,7 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   TMZ_HIP(c, dalloc(&c->d_act, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_act_tmp, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_wp, (size_t)cap));
-  c->blk_cap = cap / 4096 + 2;
+  c->blk_cap = cap / 1024 + 2;   // shrink blocks hold at least 1024 entries (4 per thread)
   TMZ_HIP(c, dalloc(&c->d_blk_cnt, (size_t)c->blk_cap));
   c->act_cap = cap;
   return TERMEZO_OK;
@@ -105,6 +105,8 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_code_off);
   dfree(c->d_tile_layer);
   dfree(c->d_tile_start);
+  dfree(c->d_tile0);
+  dfree(c->d_tile_act);
   dfree(c->d_codes);
   dfree(c->d_S_clean);
   dfree(c->d_S_cur);
@@ -140,7 +142,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
                               termezo_dtype latent_dtype, void* hip_stream, termezo_ctx** out) {
   if (!out) return TERMEZO_ERR_INVALID_ARG;
   *out = nullptr;
-  if (!layers || n_layers <= 0) return TERMEZO_ERR_INVALID_ARG;
+  if (!layers || n_layers <= 0 || n_layers > kMaxLayers) return TERMEZO_ERR_INVALID_ARG;
   if (latent_dtype != TERMEZO_F32 && latent_dtype != TERMEZO_BF16) return TERMEZO_ERR_INVALID_ARG;
   for (int32_t l = 0; l < n_layers; ++l) {
     const termezo_layer& L = layers[l];
@@ -162,7 +164,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   c->L = n_layers;
 
   std::vector<void*> wptr(n_layers);
-  std::vector<int64_t> n(n_layers), gid0(n_layers), code_off(n_layers);
+  std::vector<int64_t> n(n_layers), gid0(n_layers), code_off(n_layers), tile0(n_layers);
   std::vector<int32_t> tile_layer;
   int64_t D = 0, words = 0;
   for (int32_t l = 0; l < n_layers; ++l) {
@@ -184,6 +186,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
     n[l] = h.n;
     gid0[l] = h.gid0;
     code_off[l] = h.code_off;
+    tile0[l] = h.tile0;
     D += h.n;
     words += h.n / 16;
   }
@@ -200,6 +203,8 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_code_off, n_layers), "alloc");
   chk(dalloc(&c->d_tile_layer, (size_t)c->T), "alloc");
   chk(dalloc(&c->d_tile_start, (size_t)c->T), "alloc");
+  chk(dalloc(&c->d_tile0, n_layers), "alloc");
+  chk(dalloc(&c->d_tile_act, (size_t)c->T + 1), "alloc");
   chk(dalloc(&c->d_codes, (size_t)words), "alloc codes");
   chk(dalloc(&c->d_S_clean, n_layers), "alloc");
   chk(dalloc(&c->d_S_cur, n_layers), "alloc");
@@ -224,6 +229,8 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
     chk(hipMemcpy(c->d_n, n.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice), "copy");
     chk(hipMemcpy(c->d_gid0, gid0.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice), "copy");
     chk(hipMemcpy(c->d_code_off, code_off.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice),
+        "copy");
+    chk(hipMemcpy(c->d_tile0, tile0.data(), n_layers * sizeof(int64_t), hipMemcpyHostToDevice),
         "copy");
     chk(hipMemcpy(c->d_tile_layer, tile_layer.data(), c->T * sizeof(int32_t), hipMemcpyHostToDevice),
         "copy");
@@ -288,11 +295,12 @@ termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32
   st = ensure_active_capacity(c, total);
   if (st != TERMEZO_OK) return st;
   TMZ_HIP(c, launch_mask_compact_write(c, inclusive));
+  TMZ_HIP(c, launch_tile_ranges(c));
 
   // clean codes: current = clean
   TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
-  TMZ_HIP(c, launch_requant_dense(c));
+  TMZ_HIP(c, launch_requant(c, 0));
 
   SelectState sel;
   TMZ_HIP(c, hipMemcpyAsync(&sel, c->d_sel, sizeof(sel), hipMemcpyDeviceToHost, c->stream));
@@ -320,8 +328,7 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
   TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
-  TMZ_HIP(c, launch_requant_dense(c));
-  TMZ_HIP(c, launch_patch_codes(c, c->k_bound));
+  TMZ_HIP(c, launch_requant(c, 1));
   c->codes_valid = true;
   c->pending_perturb = true;
   c->last_seed = seed;
@@ -368,6 +375,7 @@ termezo_status finish_update(termezo_ctx* c, int64_t* k_out) {
   TMZ_HIP(c, launch_shrink(c, c->k_bound));
   std::swap(c->d_act, c->d_act_tmp);
   std::swap(c->d_act_off, c->d_act_off_tmp);
+  TMZ_HIP(c, launch_tile_ranges(c));
   c->codes_valid = false;
   c->pending_perturb = false;
   if (k_out) {

@@ -10,6 +10,8 @@
 
 namespace tmz {
 
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
 // ---------------------------------------------------------------------------
 // Latent loads: 16 consecutive elements (64 B fp32 or 32 B bf16) as fp32.
 // ---------------------------------------------------------------------------
@@ -102,6 +104,12 @@ __device__ __forceinline__ int layer_of(const int64_t* act_off, int L, int64_t j
     if (act_off[mid] <= j) lo = mid; else hi = mid - 1;
   }
   return lo;
+}
+
+// The L+1 active-list offsets in LDS (L <= kMaxLayers); all threads call.
+__device__ __forceinline__ void load_offsets(int64_t* aoff, const int64_t* act_off, int L) {
+  for (int i = threadIdx.x; i <= L; i += blockDim.x) aoff[i] = act_off[i];
+  __syncthreads();
 }
 
 // Flush a per-lane (layer, delta) partial into S[layer]: one atomic per wave
@@ -373,27 +381,181 @@ __global__ void __launch_bounds__(256) k_mask_write(DevState st, const SelectSta
 }
 
 // ---------------------------------------------------------------------------
-// Dense requantisation of every layer with its current threshold.
+// Per-tile active ranges: tile_act[t] = first position of the active list
+// whose element lies in tile t or a later tile; tile_act[T] = k.  One thread
+// per tile, binary search in its layer's part of the list.
 // ---------------------------------------------------------------------------
-template <typename T>
-__global__ void __launch_bounds__(256) k_requant(DevState st, int64_t tpb) {
-  const int64_t t0 = (int64_t)blockIdx.x * tpb;
-  const int64_t t1 = min(st.T, t0 + tpb);
-  for (int64_t t = t0; t < t1; ++t) {
-    const int l = st.tile_layer[t];
-    const float tau = st.tau_cur[l];
-    const int64_t start = st.tile_start[t];
-    const int64_t cnt = min((int64_t)kTile, st.n[l] - start);
-    const T* w = reinterpret_cast<const T*>(st.w[l]) + start;
-    uint32_t* out = st.codes + st.code_off[l] + start / 16;
-    for (int64_t e = (int64_t)threadIdx.x * 16; e < cnt; e += 256 * 16) {
-      float v[16];
-      load16(w + e, v);
-      uint32_t word = 0;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) word |= ternary_code(v[j], tau) << code_shift(j);
-      out[e / 16] = word;
+__global__ void __launch_bounds__(256) k_tile_ranges(DevState st, const uint32_t* act,
+                                                     const int64_t* act_off) {
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  load_offsets(aoff, act_off, st.L);
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t <= st.T;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    if (t == st.T) {
+      st.tile_act[t] = aoff[st.L];
+      continue;
     }
+    const int l = st.tile_layer[t];
+    const uint32_t key = (uint32_t)st.tile_start[t];
+    int64_t lo = aoff[l], hi = aoff[l + 1];
+    while (lo < hi) {
+      const int64_t mid = lo + ((hi - lo) >> 1);
+      if (act[mid] < key) lo = mid + 1; else hi = mid;
+    }
+    st.tile_act[t] = lo;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Dense requantisation of every layer with its current threshold; with
+// PATCH the codes of the actives come from their perturbed values wp (the
+// latents themselves are never written).  One block of 128 threads per tile;
+// a thread streams 64 consecutive latents (non-temporal 16-byte loads: they
+// are read once) and writes their 4 code words (one 16-byte non-temporal
+// store where aligned).  A tile's actives are tile_act[t] .. tile_act[t+1]-1:
+// with none, LDS is not touched; with some, the words meet in LDS and the
+// actives are patched with LDS atomics; with every element active, the codes
+// come from wp directly.
+// ---------------------------------------------------------------------------
+// Global-address-space views (the pointers are computed from device tables,
+// so the compiler would otherwise emit FLAT accesses).
+typedef const __attribute__((address_space(1))) v4u gv4u_c;
+typedef __attribute__((address_space(1))) v4u gv4u;
+typedef __attribute__((address_space(1))) uint32_t gu32;
+
+__device__ __forceinline__ void vec_values(const v4u* b, int nvec, float* out, const float*) {
+  for (int v = 0; v < nvec; ++v)
+    for (int i = 0; i < 4; ++i) out[4 * v + i] = __uint_as_float(b[v][i]);
+}
+__device__ __forceinline__ void vec_values(const v4u* b, int nvec, float* out, const uint16_t*) {
+  for (int v = 0; v < nvec; ++v)
+    for (int i = 0; i < 4; ++i) {
+      out[8 * v + 2 * i] = __uint_as_float(b[v][i] << 16);
+      out[8 * v + 2 * i + 1] = __uint_as_float(b[v][i] & 0xFFFF0000u);
+    }
+}
+
+__device__ __forceinline__ uint32_t code_word(const float* v, float tau) {
+  uint32_t word = 0;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) word |= ternary_code(v[q], tau) << code_shift(q);
+  return word;
+}
+
+constexpr int kRqThreads = 128;
+
+// Code bits of the 16 / CPW consecutive elements v[] that start at element
+// (part * 16 / CPW) of a code word.
+template <int N>
+__device__ __forceinline__ uint32_t partial_word(const float* v, int part, float tau) {
+  uint32_t word = 0;
+#pragma unroll
+  for (int q = 0; q < N; ++q) word |= ternary_code(v[q], tau) << code_shift(part * N + q);
+  return word;
+}
+
+// OR of a code word's parts held by CPW adjacent lanes (all of them get it).
+template <int CPW>
+__device__ __forceinline__ uint32_t join_word(uint32_t w) {
+#pragma unroll
+  for (int m = 1; m < CPW; m <<= 1) w |= (uint32_t)__shfl_xor((int)w, m, 64);
+  return w;
+}
+
+// Loads are coalesced: 16-byte chunk c of the tile goes to lane c % 128, so
+// one load instruction covers 1 KB of consecutive bytes; a code word's chunks
+// (2 for bf16, 4 for fp32) sit in adjacent lanes and are joined by shuffles.
+template <typename T, bool PATCH>
+__global__ void __launch_bounds__(kRqThreads) k_requant_tile(DevState st, const uint32_t* act,
+                                                            const float* wp) {
+  constexpr int EPC = 16 / (int)sizeof(T);       // elements per 16-byte chunk
+  constexpr int CPW = 16 / EPC;                  // chunks per code word
+  constexpr int CPT = kTile / EPC / kRqThreads;  // chunks per thread
+  __shared__ uint32_t words[kTile / 16];
+  const int tid = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  const int l = st.tile_layer[t];
+  const int64_t start = st.tile_start[t];
+  const int cnt = (int)min((int64_t)kTile, st.n[l] - start);
+  const float tau = st.tau_cur[l];
+  const T* w = reinterpret_cast<const T*>(st.w[l]) + start;
+  gu32* out = (gu32*)(st.codes + st.code_off[l] + start / 16);
+  const bool owner = (tid % CPW) == 0;            // stores the word of its lane group
+  int64_t a0 = 0, a1 = 0;
+  uint32_t aw = 0;
+  float pw = 0.0f;
+  if (PATCH) {
+    a0 = st.tile_act[t];
+    a1 = st.tile_act[t + 1];
+    const int64_t jj = a0 + tid;
+    const int64_t jc = jj < a1 ? jj : (a0 < a1 ? a0 : 0);   // the list holds at least one slot
+    aw = act[jc];
+    pw = wp[jc];
+  }
+  const int64_t na = a1 - a0;
+  if (PATCH && na == cnt) {
+    // every element active: the codes come from wp (fp32, 4 per chunk)
+    constexpr int FC = kTile / 4 / kRqThreads;   // 16 chunks per thread
+    const float* src = wp + a0;
+    const bool vec = (a0 & 3) == 0;
+#pragma unroll
+    for (int v = 0; v < FC; ++v) {
+      const int c = v * kRqThreads + tid;
+      const int e = c * 4;
+      float x[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (e < cnt) {
+        if (vec) {
+          const v4u b = __builtin_nontemporal_load((gv4u_c*)(src + e));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] = __uint_as_float(b[r]);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] = src[e + r];
+        }
+      }
+      const uint32_t wd = join_word<4>(partial_word<4>(x, c & 3, tau));
+      if ((tid & 3) == 0 && e < cnt) out[c / 4] = wd;
+    }
+    return;
+  }
+  v4u buf[CPT];
+#pragma unroll
+  for (int v = 0; v < CPT; ++v) {
+    const int e = (v * kRqThreads + tid) * EPC;
+    buf[v] = __builtin_nontemporal_load((gv4u_c*)(w + (e < cnt ? e : 0)));   // clamped
+  }
+  uint32_t wd[CPT];
+#pragma unroll
+  for (int v = 0; v < CPT; ++v) {
+    const int c = v * kRqThreads + tid;
+    float x[EPC];
+    vec_values(&buf[v], 1, x, (const T*)nullptr);
+    wd[v] = join_word<CPW>(partial_word<EPC>(x, c % CPW, tau));
+  }
+  if (PATCH && na > 0) {
+#pragma unroll
+    for (int v = 0; v < CPT; ++v)
+      if (owner) words[(v * kRqThreads + tid) / CPW] = wd[v];
+    __syncthreads();
+    auto patch_one = [&](uint32_t i, float x) __attribute__((always_inline)) {
+      const uint32_t li = i - (uint32_t)start;
+      const uint32_t code = ternary_code(x, tau);
+      const int sh = code_shift((int)(li & 15u));
+      atomicAnd(&words[li >> 4], ~(3u << sh));
+      if (code) atomicOr(&words[li >> 4], code << sh);
+    };
+    if (tid < na) patch_one(aw, pw);
+    for (int64_t jj = a0 + kRqThreads + tid; jj - tid < a1; jj += kRqThreads)
+      if (jj < a1) patch_one(act[jj], wp[jj]);
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < CPT; ++v)
+      if (owner) wd[v] = words[(v * kRqThreads + tid) / CPW];
+  }
+#pragma unroll
+  for (int v = 0; v < CPT; ++v) {
+    const int c = v * kRqThreads + tid;
+    if (owner && c * EPC < cnt) out[c / CPW] = wd[v];
   }
 }
 
@@ -404,48 +566,119 @@ __global__ void __launch_bounds__(256) k_requant(DevState st, int64_t tpb) {
 // ---------------------------------------------------------------------------
 constexpr int kRun = 4;
 
+// The kRun = 4 active-list entries j0 .. j0+3 of a run (j0 % 4 == 0): one
+// 16-byte load when the run is whole; n = entries of the run below je.
+__device__ __forceinline__ int run_entries(const uint32_t* act, int64_t j0, int64_t je,
+                                           uint32_t i[4]) {
+  if (j0 + 3 < je) {
+    const v4u v = *reinterpret_cast<const v4u*>(act + j0);
+    i[0] = v[0]; i[1] = v[1]; i[2] = v[2]; i[3] = v[3];
+    return 4;
+  }
+  int n = 0;
+  for (int r = 0; r < 4; ++r) {
+    i[r] = j0 + r < je ? act[j0 + r] : 0u;
+    n += j0 + r < je;
+  }
+  return n;
+}
+
+// Latents at four local indices: one load when they are the consecutive,
+// 4-aligned i0 .. i0+3 (dense runs), four gathers otherwise.
+__device__ __forceinline__ void gather4(const float* w, const uint32_t i[4], int n, float v[4]) {
+  if (n == 4 && i[3] == i[0] + 3 && (i[0] & 3u) == 0) {
+    const float4 a = *reinterpret_cast<const float4*>(w + i[0]);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  } else {
+    for (int r = 0; r < 4; ++r) v[r] = r < n ? w[i[r]] : 0.0f;
+  }
+}
+__device__ __forceinline__ void gather4(const uint16_t* w, const uint32_t i[4], int n, float v[4]) {
+  if (n == 4 && i[3] == i[0] + 3 && (i[0] & 3u) == 0) {
+    const uint2 a = *reinterpret_cast<const uint2*>(w + i[0]);
+    v[0] = __uint_as_float(a.x << 16);
+    v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(a.y << 16);
+    v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+  } else {
+    for (int r = 0; r < 4; ++r) v[r] = r < n ? bf16_to_f32(w[i[r]]) : 0.0f;
+  }
+}
+__device__ __forceinline__ void scatter4(float* w, const uint32_t i[4], int n, const float v[4]) {
+  if (n == 4 && i[3] == i[0] + 3 && (i[0] & 3u) == 0) {
+    *reinterpret_cast<float4*>(w + i[0]) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    for (int r = 0; r < 4; ++r)
+      if (r < n) w[i[r]] = v[r];
+  }
+}
+__device__ __forceinline__ void scatter4(uint16_t* w, const uint32_t i[4], int n, const float v[4]) {
+  if (n == 4 && i[3] == i[0] + 3 && (i[0] & 3u) == 0) {
+    const uint32_t lo = (uint32_t)f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+    const uint32_t hi = (uint32_t)f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+    *reinterpret_cast<uint2*>(w + i[0]) = make_uint2(lo, hi);
+  } else {
+    for (int r = 0; r < 4; ++r)
+      if (r < n) w[i[r]] = f32_to_bf16_rne(v[r]);
+  }
+}
+// Four values to wp[j0 ..]: one 16-byte store for a whole run.
+__device__ __forceinline__ void put4(float* wp, int64_t j0, int n, const float v[4]) {
+  if (n == 4) {
+    *reinterpret_cast<float4*>(wp + j0) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    for (int r = 0; r < n; ++r) wp[j0 + r] = v[r];
+  }
+}
+
 template <typename T>
-__global__ void __launch_bounds__(256) k_perturb_delta(DevState st, const uint32_t* act,
+__global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
+                                                       const uint32_t* __restrict__ act,
                                                        const int64_t* act_off, uint64_t seed,
-                                                       float se, float* wp) {
-  const int64_t k = act_off[st.L];
-  const int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kRun;
-  int l = j0 < k ? layer_of(act_off, st.L, j0) : 0;
-  long long acc = 0;
+                                                       float se, float* __restrict__ wp) {
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  load_offsets(aoff, act_off, st.L);
+  const int64_t k = aoff[st.L];
+  // Block b owns the contiguous entries [jb, je): a thread's layer changes
+  // rarely, so its partial sum goes out with one atomic per layer change and
+  // one wave-level atomic at the end.
+  const int64_t per = (k + gridDim.x - 1) / gridDim.x;
+  const int64_t chunk = (per + 256 * kRun - 1) / (256 * kRun) * (256 * kRun);
+  const int64_t jb = (int64_t)blockIdx.x * chunk, je = min(k, jb + chunk);
   bool bad = false, any = false;
-  for (int r = 0; r < kRun; ++r) {
-    const int64_t j = j0 + r;
-    if (j >= k) break;
-    if (act_off[l + 1] <= j) {              // the run crosses into a later layer
-      if (any) atomicAdd((unsigned long long*)&st.S_cur[l], (unsigned long long)acc);
-      acc = 0;
-      while (act_off[l + 1] <= j) ++l;
+  int l = -1;
+  long long acc = 0;
+  GaussCache zc;
+  for (int64_t base = jb; base < je; base += 256 * kRun) {
+    const int64_t j0 = base + (int64_t)threadIdx.x * kRun;
+    if (j0 >= je) continue;
+    uint32_t i[4];
+    const int n = run_entries(act, j0, je, i);
+    // the run lies in one layer, or it is handled entry by entry
+    const int lr = layer_of(aoff, st.L, j0);
+    const bool one = aoff[lr + 1] >= j0 + n;
+    float wv[4], v[4];
+    if (one) gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
+    for (int r = 0; r < n; ++r) {
+      const int64_t j = j0 + r;
+      if (l < 0) {
+        l = layer_of(aoff, st.L, j);
+      } else if (aoff[l + 1] <= j) {        // into a later layer
+        if (any) atomicAdd((unsigned long long*)&st.S_cur[l], (unsigned long long)acc);
+        acc = 0;
+        any = false;
+        while (aoff[l + 1] <= j) ++l;
+      }
+      if (!one) wv[r] = load1(reinterpret_cast<const T*>(st.w[l]), i[r]);
+      v[r] = se != 0.0f ? fmaf(se, zc.get(seed, (uint64_t)(st.gid0[l] + i[r])), wv[r]) : wv[r];
+      bad |= !in_fix_range(v[r]);
+      acc += (long long)fix_abs(v[r]) - (long long)fix_abs(wv[r]);
+      any = true;
     }
-    const uint32_t i = act[j];
-    const float wv = load1(reinterpret_cast<const T*>(st.w[l]), i);
-    const float v = se != 0.0f ? fmaf(se, gauss_at(seed, (uint64_t)(st.gid0[l] + i)), wv) : wv;
-    wp[j] = v;
-    bad |= !in_fix_range(v);
-    acc += (long long)fix_abs(v) - (long long)fix_abs(wv);
-    any = true;
+    put4(wp, j0, n, v);
   }
   flush_delta((long long*)st.S_cur, l, acc, any);
   if (bad) atomicOr(st.err, 1);
-}
-
-// Sparse code patch at the actives with the current threshold.
-__global__ void __launch_bounds__(256) k_patch_codes(DevState st, const uint32_t* act,
-                                                     const int64_t* act_off, const float* wp) {
-  const int64_t k = act_off[st.L];
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= k) return;
-  const int l = layer_of(act_off, st.L, j);
-  const uint32_t i = act[j];
-  uint32_t* word = st.codes + st.code_off[l] + i / 16;
-  const int sh = code_shift((int)(i & 15u));
-  const uint32_t code = ternary_code(wp[j], st.tau_cur[l]);
-  atomicAnd(word, ~(3u << sh));
-  if (code) atomicOr(word, code << sh);
 }
 
 // ---------------------------------------------------------------------------
@@ -467,33 +700,57 @@ __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps,
   if (!isfinite(a)) atomicOr(err, 2);
 }
 
+// The new values also go, in list order, to wn (read by the shrink).  With a
+// non-finite coefficient (reported by the coefficient kernel) the latents are
+// left untouched and wn holds their current values.
 template <typename T>
-__global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* act,
+__global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __restrict__ act,
                                                 const int64_t* act_off, uint64_t seed,
-                                                const float* scal) {
+                                                const float* scal, float* __restrict__ wn) {
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  load_offsets(aoff, act_off, st.L);
   const float a = scal[0];
-  if (!isfinite(a)) return;   // reported by the coefficient kernel; latents untouched
-  const int64_t k = act_off[st.L];
-  const int64_t j0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kRun;
-  int l = j0 < k ? layer_of(act_off, st.L, j0) : 0;
-  long long acc = 0;
+  const bool a_ok = isfinite(a);
+  const int64_t k = aoff[st.L];
+  const int64_t per = (k + gridDim.x - 1) / gridDim.x;
+  const int64_t chunk = (per + 256 * kRun - 1) / (256 * kRun) * (256 * kRun);
+  const int64_t jb = (int64_t)blockIdx.x * chunk, je = min(k, jb + chunk);
   bool bad = false, any = false;
-  for (int r = 0; r < kRun; ++r) {
-    const int64_t j = j0 + r;
-    if (j >= k) break;
-    if (act_off[l + 1] <= j) {
-      if (any) atomicAdd((unsigned long long*)&st.S_clean[l], (unsigned long long)acc);
-      acc = 0;
-      while (act_off[l + 1] <= j) ++l;
+  int l = -1;
+  long long acc = 0;
+  GaussCache zc;
+  for (int64_t base = jb; base < je; base += 256 * kRun) {
+    const int64_t j0 = base + (int64_t)threadIdx.x * kRun;
+    if (j0 >= je) continue;
+    uint32_t i[4];
+    const int n = run_entries(act, j0, je, i);
+    const int lr = layer_of(aoff, st.L, j0);
+    const bool one = aoff[lr + 1] >= j0 + n;
+    float wv[4], nv[4];
+    if (one) gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
+    for (int r = 0; r < n; ++r) {
+      const int64_t j = j0 + r;
+      if (l < 0) {
+        l = layer_of(aoff, st.L, j);
+      } else if (aoff[l + 1] <= j) {
+        if (any) atomicAdd((unsigned long long*)&st.S_clean[l], (unsigned long long)acc);
+        acc = 0;
+        any = false;
+        while (aoff[l + 1] <= j) ++l;
+      }
+      T* w = reinterpret_cast<T*>(const_cast<void*>(st.w[l]));
+      if (!one) wv[r] = load1(w, i[r]);
+      nv[r] = wv[r];
+      if (a_ok) {
+        nv[r] = storage_round(w, fmaf(a, zc.get(seed, (uint64_t)(st.gid0[l] + i[r])), wv[r]));
+        if (!one) store1(w, i[r], nv[r]);
+      }
+      bad |= !in_fix_range(nv[r]);
+      acc += (long long)fix_abs(nv[r]) - (long long)fix_abs(wv[r]);
+      any = true;
     }
-    const uint32_t i = act[j];
-    T* w = reinterpret_cast<T*>(const_cast<void*>(st.w[l]));
-    const float wv = load1(w, i);
-    const float nv = storage_round(w, fmaf(a, gauss_at(seed, (uint64_t)(st.gid0[l] + i)), wv));
-    store1(w, i, nv);
-    bad |= !in_fix_range(nv);
-    acc += (long long)fix_abs(nv) - (long long)fix_abs(wv);
-    any = true;
+    if (one && a_ok) scatter4(reinterpret_cast<T*>(const_cast<void*>(st.w[lr])), i, n, nv);
+    put4(wn, j0, n, nv);
   }
   flush_delta((long long*)st.S_clean, l, acc, any);
   if (bad) atomicOr(st.err, 1);
@@ -501,76 +758,135 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* act
 
 // ---------------------------------------------------------------------------
 // Shrink-only set update: keep the actives with ||w| - tau| <= xi0.
-// Block b handles entries [b * kShrinkBlk, (b+1) * kShrinkBlk).
+// Block b handles entries [b * 256 per, (b+1) * 256 per); thread t takes
+// entries b * 256 per + 256 r + t (r < per <= kShrinkPer), so reads and writes
+// of a wave are contiguous; per grows with the list so that small lists still
+// spread over many blocks.  The updated values come from wn (list order).
 // ---------------------------------------------------------------------------
-constexpr int kShrinkPer = 16;
-constexpr int kShrinkBlk = 256 * kShrinkPer;
+constexpr int kShrinkPer = 64;                // entries per thread at most (block: 256 * per)
 
-template <typename T>
-__device__ __forceinline__ uint32_t shrink_flags(const DevState& st, const uint32_t* act,
-                                                 const int64_t* act_off, int64_t k, int64_t j0,
-                                                 float xi0) {
-  uint32_t m = 0;
+// Offsets and clean thresholds of every layer in LDS; all threads call.
+__device__ __forceinline__ void load_layer_lds(int64_t* aoff, float* tau, const int64_t* act_off,
+                                               const float* tau_g, int L) {
+  for (int i = threadIdx.x; i <= L; i += blockDim.x) {
+    aoff[i] = act_off[i];
+    if (i < L) tau[i] = tau_g[i];
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ uint64_t shrink_flags(const int64_t* aoff, const float* tau, int L,
+                                                 const float* __restrict__ wn, int64_t k,
+                                                 int64_t base, int per, float xi0) {
+  uint64_t m = 0;
+  const int64_t j0 = base + threadIdx.x;
   if (j0 >= k) return 0;
-  int l = layer_of(act_off, st.L, j0);
-  for (int r = 0; r < kShrinkPer; ++r) {
-    const int64_t j = j0 + r;
+  int l = layer_of(aoff, L, j0);
+  for (int r = 0; r < per; ++r) {
+    const int64_t j = j0 + 256 * r;
     if (j >= k) break;
-    while (act_off[l + 1] <= j) ++l;
-    const uint32_t i = act[j];
-    const float wv = load1(reinterpret_cast<const T*>(st.w[l]), i);
-    if (fabsf(fabsf(wv) - st.tau[l]) <= xi0) m |= 1u << r;
+    while (aoff[l + 1] <= j) ++l;
+    if (fabsf(fabsf(wn[j]) - tau[l]) <= xi0) m |= 1ull << r;
   }
   return m;
 }
 
-template <typename T>
-__global__ void __launch_bounds__(256) k_shrink_count(DevState st, const uint32_t* act,
-                                                      const int64_t* act_off, float xi0,
-                                                      int64_t* blk_cnt) {
+__global__ void __launch_bounds__(256) k_shrink_count(DevState st, const int64_t* act_off,
+                                                      const float* __restrict__ wn, float xi0,
+                                                      int per, int64_t* blk_cnt) {
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  __shared__ float tau[kMaxLayers];
   __shared__ unsigned long long red[4];
-  const int64_t k = act_off[st.L];
-  const int64_t j0 = (int64_t)blockIdx.x * kShrinkBlk + (int64_t)threadIdx.x * kShrinkPer;
-  const uint32_t m = shrink_flags<T>(st, act, act_off, k, j0, xi0);
-  const unsigned long long s = block_sum_u64(__popc(m), red);
+  load_layer_lds(aoff, tau, act_off, st.tau, st.L);
+  const int64_t k = aoff[st.L];
+  const uint64_t m = shrink_flags(aoff, tau, st.L, wn, k, (int64_t)blockIdx.x * 256 * per, per, xi0);
+  const unsigned long long s = block_sum_u64(__popcll(m), red);
   if (threadIdx.x == 0) blk_cnt[blockIdx.x] = (int64_t)s;
 }
 
-__global__ void __launch_bounds__(256) k_blocks_scan(int64_t* blk_cnt, int64_t nb, int64_t* total) {
-  __shared__ long long lds[256];
-  const int64_t per = (nb + 255) / 256;
-  const int64_t a = min(nb, (int64_t)threadIdx.x * per), b = min(nb, a + per);
-  long long s = 0;
-  for (int64_t i = a; i < b; ++i) s += blk_cnt[i];
-  long long tot;
-  long long off = block_excl_scan_i64(s, lds, &tot);
-  for (int64_t i = a; i < b; ++i) {
-    const long long c = blk_cnt[i];
-    blk_cnt[i] = off;
-    off += c;
+// Exclusive scan of the per-block counts in place (one block of 1024 threads,
+// 1024 counts per round, the next round's counts loaded ahead); *total = sum.
+__device__ __forceinline__ long long wave_incl_scan_i64(long long v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t lo = __shfl_up((uint32_t)v, off, 64);
+    const uint32_t hi = __shfl_up((uint32_t)((unsigned long long)v >> 32), off, 64);
+    const long long u = (long long)(((unsigned long long)hi << 32) | lo);
+    if (lane >= off) v += u;
   }
-  if (threadIdx.x == 0) *total = tot;
+  return v;
 }
 
-template <typename T>
-__global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_t* act,
-                                                      const int64_t* act_off, float xi0,
-                                                      const int64_t* blk_off, uint32_t* act_new,
+__global__ void __launch_bounds__(1024) k_blocks_scan(int64_t* blk_cnt, int64_t nb, int64_t* total) {
+  __shared__ long long wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  long long carry = 0;
+  long long v = tid < nb ? blk_cnt[tid] : 0;
+  for (int64_t base = 0; base < nb; base += 1024) {
+    const int64_t i = base + tid;
+    const int64_t in = i + 1024;
+    const long long vn = in < nb ? blk_cnt[in] : 0;       // next round, in flight
+    const long long inc = wave_incl_scan_i64(v);
+    if (lane == 63) wsum[wid] = inc;
+    __syncthreads();
+    long long before = 0, round = 0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      const long long t = wsum[w];
+      before += w < wid ? t : 0;
+      round += t;
+    }
+    if (i < nb) blk_cnt[i] = carry + before + inc - v;
+    carry += round;
+    v = vn;
+    __syncthreads();
+  }
+  if (tid == 0) *total = carry;
+}
+
+__global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_t* __restrict__ act,
+                                                      const int64_t* act_off,
+                                                      const float* __restrict__ wn, float xi0,
+                                                      int per, const int64_t* blk_off,
+                                                      uint32_t* __restrict__ act_new,
                                                       int64_t* act_off_new) {
-  __shared__ long long lds[256];
-  const int64_t k = act_off[st.L];
-  const int64_t j0 = (int64_t)blockIdx.x * kShrinkBlk + (int64_t)threadIdx.x * kShrinkPer;
-  const uint32_t m = shrink_flags<T>(st, act, act_off, k, j0, xi0);
-  long long tot;
-  long long pos = blk_off[blockIdx.x] + block_excl_scan_i64(__popc(m), lds, &tot);
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  __shared__ float tau[kMaxLayers];
+  __shared__ int32_t cnt[kShrinkPer * 4];   // kept entries per (r, wave), then their offsets
+  load_layer_lds(aoff, tau, act_off, st.tau, st.L);
+  const int64_t k = aoff[st.L];
+  const int64_t base = (int64_t)blockIdx.x * 256 * per;
+  const uint64_t m = shrink_flags(aoff, tau, st.L, wn, k, base, per, xi0);
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int r = 0; r < per; ++r) {
+    const unsigned long long b = __ballot((m >> r) & 1ull);
+    if (lane == 0) cnt[4 * r + wid] = __popcll(b);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {                    // entries are ordered r, then wave, then lane
+    int32_t run = 0;
+    for (int i = 0; i < per * 4; ++i) {
+      const int32_t c = cnt[i];
+      cnt[i] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  const int64_t j0 = base + threadIdx.x;
   if (j0 >= k) return;
-  int l = layer_of(act_off, st.L, j0);
-  for (int r = 0; r < kShrinkPer; ++r) {
-    const int64_t j = j0 + r;
+  const int64_t boff = blk_off[blockIdx.x];
+  int l = layer_of(aoff, st.L, j0);
+  for (int r = 0; r < per; ++r) {
+    const int64_t j = j0 + 256 * r;
+    const bool keep = (m >> r) & 1ull;
+    const unsigned long long b = __ballot(keep);
     if (j >= k) break;
-    while (act_off[l + 1] <= j) ++l;
-    if (j == act_off[l]) act_off_new[l] = pos;   // first entry of layer l
-    if (m & (1u << r)) act_new[pos++] = act[j];
+    const int64_t pos = boff + cnt[4 * r + wid] + __popcll(b & below);
+    while (aoff[l + 1] <= j) ++l;
+    if (j == aoff[l]) act_off_new[l] = pos;   // first entry of layer l
+    if (keep) act_new[pos] = act[j];
   }
 }
 
@@ -709,33 +1025,44 @@ hipError_t launch_mask_compact_write(termezo_ctx* c, int inclusive) {
   return hipGetLastError();
 }
 
-hipError_t launch_requant_dense(termezo_ctx* c) {
-  int64_t tpb;
-  const int64_t g = grid_for(c->T, 8192, &tpb);
-  if (c->dtype == TERMEZO_F32)
-    hipLaunchKernelGGL(k_requant<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), tpb);
-  else
-    hipLaunchKernelGGL(k_requant<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), tpb);
+hipError_t launch_requant(termezo_ctx* c, int patch) {
+  const dim3 g((unsigned)c->T), b(kRqThreads);
+  if (c->dtype == TERMEZO_F32) {
+    if (patch)
+      hipLaunchKernelGGL((k_requant_tile<float, true>), g, b, 0, c->stream, c->dev(), c->d_act, c->d_wp);
+    else
+      hipLaunchKernelGGL((k_requant_tile<float, false>), g, b, 0, c->stream, c->dev(), c->d_act, c->d_wp);
+  } else {
+    if (patch)
+      hipLaunchKernelGGL((k_requant_tile<uint16_t, true>), g, b, 0, c->stream, c->dev(), c->d_act,
+                         c->d_wp);
+    else
+      hipLaunchKernelGGL((k_requant_tile<uint16_t, false>), g, b, 0, c->stream, c->dev(), c->d_act,
+                         c->d_wp);
+  }
   return hipGetLastError();
+}
+
+hipError_t launch_tile_ranges(termezo_ctx* c) {
+  const int64_t g = max((int64_t)1, min((int64_t)2048, (c->T + 1 + 255) / 256));
+  hipLaunchKernelGGL(k_tile_ranges, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
+                     c->d_act_off);
+  return hipGetLastError();
+}
+
+static inline int64_t sparse_grid(int64_t k) {
+  return max((int64_t)1, min((int64_t)8192, (k + 256 * kRun - 1) / (256 * kRun)));
 }
 
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se) {
   if (k <= 0) return hipSuccess;
-  const int64_t threads = (k + kRun - 1) / kRun;
-  const int64_t g = (threads + 255) / 256;
+  const int64_t g = sparse_grid(k);
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_perturb_delta<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
                        c->d_act_off, seed, se, c->d_wp);
   else
     hipLaunchKernelGGL(k_perturb_delta<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(),
                        c->d_act, c->d_act_off, seed, se, c->d_wp);
-  return hipGetLastError();
-}
-
-hipError_t launch_patch_codes(termezo_ctx* c, int64_t k) {
-  if (k <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_patch_codes, dim3((k + 255) / 256), dim3(256), 0, c->stream, c->dev(),
-                     c->d_act, c->d_act_off, c->d_wp);
   return hipGetLastError();
 }
 
@@ -753,36 +1080,29 @@ hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float
 
 hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed) {
   if (k <= 0) return hipSuccess;
-  const int64_t threads = (k + kRun - 1) / kRun;
-  const int64_t g = (threads + 255) / 256;
+  const int64_t g = sparse_grid(k);
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, (const float*)c->d_scal);
+                       c->d_act_off, seed, (const float*)c->d_scal, c->d_wp);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, (const float*)c->d_scal);
+                       c->d_act_off, seed, (const float*)c->d_scal, c->d_wp);
   return hipGetLastError();
 }
 
 hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
-  const int64_t nb = max((int64_t)1, (k + kShrinkBlk - 1) / kShrinkBlk);
+  // entries per thread: 4 .. kShrinkPer, about 2048 blocks for large lists
+  int per = 4;
+  while (per < kShrinkPer && k > (int64_t)2048 * 256 * per) per *= 2;
+  const int64_t nb = max((int64_t)1, (k + 256 * per - 1) / (256 * per));
   int64_t* total = c->d_blk_cnt + nb;  // blk_cap >= nb + 1
-  if (c->dtype == TERMEZO_F32)
-    hipLaunchKernelGGL(k_shrink_count<float>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
-                       c->d_act, c->d_act_off, c->xi0, c->d_blk_cnt);
-  else
-    hipLaunchKernelGGL(k_shrink_count<uint16_t>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
-                       c->d_act, c->d_act_off, c->xi0, c->d_blk_cnt);
-  hipLaunchKernelGGL(k_blocks_scan, dim3(1), dim3(256), 0, c->stream, c->d_blk_cnt, nb, total);
+  hipLaunchKernelGGL(k_shrink_count, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act_off,
+                     c->d_wp, c->xi0, per, c->d_blk_cnt);
+  hipLaunchKernelGGL(k_blocks_scan, dim3(1), dim3(1024), 0, c->stream, c->d_blk_cnt, nb, total);
   // offsets of layers without any entry are fixed afterwards
-  if (c->dtype == TERMEZO_F32)
-    hipLaunchKernelGGL(k_shrink_write<float>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
-                       c->d_act, c->d_act_off, c->xi0, c->d_blk_cnt, c->d_act_tmp,
-                       c->d_act_off_tmp);
-  else
-    hipLaunchKernelGGL(k_shrink_write<uint16_t>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
-                       c->d_act, c->d_act_off, c->xi0, c->d_blk_cnt, c->d_act_tmp,
-                       c->d_act_off_tmp);
+  hipLaunchKernelGGL(k_shrink_write, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act,
+                     c->d_act_off, c->d_wp, c->xi0, per, c->d_blk_cnt, c->d_act_tmp,
+                     c->d_act_off_tmp);
   hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(1), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
   return hipGetLastError();

@@ -92,7 +92,7 @@ def test_build_mask_matches_oracle(orc, shapes, bf16, rho0, inclusive):
 
 @pytest.mark.parametrize("shapes", [[(256, 256)], C2_LAYERS], ids=["c1", "c2"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-@pytest.mark.parametrize("rho0", [0.05, 1.0])
+@pytest.mark.parametrize("rho0", [0.05, 0.9999, 1.0])   # 0.9999: fully active tiles after ragged ones
 def test_perturb_codes_match_oracle(orc, shapes, bf16, rho0):
     print(f"perturb shapes={len(shapes)} bf16={bf16} rho0={rho0}", flush=True)
     ref, ctx, tensors = _setup(orc, shapes, bf16, seed=2)
@@ -185,7 +185,7 @@ def test_bitlinear_large_grid_sampled_rows(orc, M, K, N):
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-@pytest.mark.parametrize("rho0", [0.01, 1.0])
+@pytest.mark.parametrize("rho0", [0.01, 0.9999, 1.0])
 def test_update_and_shrink_match_oracle(orc, bf16, rho0):
     print(f"update bf16={bf16} rho0={rho0}", flush=True)
     ref, ctx, tensors = _setup(orc, C2_LAYERS, bf16, seed=5)
