@@ -308,23 +308,6 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
   }
 }
 
-// One 16-byte-per-lane direct global -> LDS load; lds_base is the wave's
-// destination (LDS byte offset, wave-uniform).  Issued as inline assembly so
-// that its completion is tracked only by the explicit vmcnt waits below.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
-  asm volatile(
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
-      :
-      : "v"(gptr), "s"(lds_base)
-      : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_offset(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
 // ---------------------------------------------------------------------------
 // Full-tile GEMM with direct global -> LDS loads (global_load_lds_dwordx4:
 // lane i of a wave writes its 16 bytes at the wave's LDS base + 16 i, no VGPRs)
@@ -353,13 +336,6 @@ __device__ __forceinline__ int bswz(int row) { return ((row >> 2) ^ (row >> 3)) 
 __device__ __forceinline__ v4i unpack16(uint32_t w) {
   return v4i{(int)unpack_group(w, 0), (int)unpack_group(w, 1), (int)unpack_group(w, 2),
              (int)unpack_group(w, 3)};
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt_le() {
-  // s_waitcnt vmcnt(N): vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt left at their maxima
-  static_assert(N >= 0 && N < 16, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8));
 }
 
 constexpr int kDmaBM = 256, kDmaBN = 256;

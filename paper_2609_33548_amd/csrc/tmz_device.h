@@ -235,4 +235,32 @@ __device__ __forceinline__ void tile_of_block(int64_t nb_m, int64_t nb_n, int64_
   tile_of_linear(xcd_linear(blockIdx.x, nb_m * nb_n), nb_m, nb_n, tm, tn);
 }
 
+// ---------------------------------------------------------------------------
+// Direct global -> LDS loads (gfx950 global_load_lds_dwordx4).
+// ---------------------------------------------------------------------------
+// One 16-byte-per-lane direct global -> LDS load; lds_base is the wave's
+// destination (LDS byte offset, wave-uniform).  Issued as inline assembly so
+// that its completion is tracked only by the caller's explicit vmcnt waits
+// (the compiler would otherwise wait conservatively).
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(gptr), "s"(lds_base)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_le() {
+  // s_waitcnt vmcnt(N): vmcnt in bits [3:0] and [15:14]; expcnt, lgkmcnt left at their maxima
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8));
+}
+
 }  // namespace tmz

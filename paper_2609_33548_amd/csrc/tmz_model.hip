@@ -708,6 +708,170 @@ __global__ void __launch_bounds__(512) k_lmhead_bf16(const uint16_t* __restrict_
   }
 }
 
+// LM head + cross-entropy partials on full tiles with direct global -> LDS
+// loads: 256 tokens x 256 vocabulary columns per block, 8 waves as 2 x 4
+// (128 tokens x 64 columns per wave), v_mfma_f32_32x32x16_bf16 with the
+// embedding rows as the first operand, so the accumulator is the transpose
+// of the logits: a lane owns one token and 16 of its columns per 32 x 32
+// tile, and a token's max and sum of exp over the block's columns reduce in
+// registers, across the two lane halves and, through LDS, across the 4 waves
+// along the vocabulary.  Operands stream through STAGES stages of BK bf16
+// columns (a stage row is 2 BK bytes); 16-byte chunk c of row r sits at
+// chunk c ^ sw(r), so the fragment reads of 16 consecutive rows hit distinct
+// banks.  K assignment: in sub-step ks, lane half h supplies chunk
+// h * (2 BK / 32) + ks of its row for both operands.
+// Requires M % 256 == 0, V % 256 == 0, d % BK == 0.
+template <int STAGES, int BK>
+__global__ void __launch_bounds__(512) k_lmhead_dma(const uint16_t* __restrict__ x,
+                                                    const uint16_t* __restrict__ E, int64_t M,
+                                                    int64_t d, int64_t V,
+                                                    const int32_t* __restrict__ labels,
+                                                    float* pmax, float* psum, float* lab,
+                                                    int64_t nvt) {
+  constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int ROWB = 2 * BK, CPR = ROWB / 16;   // bytes and 16-byte chunks per stage row
+  constexpr int OPB = BM * ROWB;                  // bytes per operand per stage
+  constexpr int KS = CPR / 2;                     // MFMA sub-steps per stage
+  constexpr int IPW = CPR / 2;                    // loads per operand per wave per stage
+  static_assert(CPR == 8 || CPR == 4, "stage width");
+  static_assert(STAGES >= 2 && STAGES * 2 * OPB <= 152 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES * 2 * OPB];
+  __shared__ int32_t lbl[BM];
+  auto sw = [](int row) __attribute__((always_inline)) {
+    return CPR == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid / (BN / WN), wn = wid % (BN / WN);
+  int64_t tm, tn;
+  tile_of_block(M / BM, nvt, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int nk = (int)(d / BK);
+  for (int i = tid; i < BM; i += NT) lbl[i] = labels[m0 + i];
+
+  // load j of wave w fills the 64 LDS chunks (w * IPW + j) * 64 .. + 63 of an operand
+  const uint8_t* asrc[IPW];
+  const uint8_t* bsrc[IPW];
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int q = (wid * IPW + j) * 64 + lane;
+    const int row = q / CPR, lc = (q % CPR) ^ sw(row);
+    asrc[j] = reinterpret_cast<const uint8_t*>(x) + (m0 + row) * d * 2 + 16 * lc;
+    bsrc[j] = reinterpret_cast<const uint8_t*>(E) + (n0 + row) * d * 2 + 16 * lc;
+  }
+  const uint32_t wbase = __builtin_amdgcn_readfirstlane(wid) * IPW * 1024u;
+  auto Ast = [&](int st) { return lds + st * 2 * OPB; };
+  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+    const int64_t koff = (int64_t)kt * ROWB;
+    const uint32_t ab = lds_offset(Ast(st)) + wbase, bb = ab + OPB;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      dma16(asrc[j] + koff, ab + 1024u * j);
+      dma16(bsrc[j] + koff, bb + 1024u * j);
+    }
+  };
+
+  v16f acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+
+  typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+  const int h = lane >> 5;
+  const int arow0 = wm * WM + (lane & 31), brow0 = wn * WN + (lane & 31);
+  auto compute = [&](const uint8_t* As, const uint8_t* Bs) __attribute__((always_inline)) {
+    v8bf af[2][TM], bfr[2][TN];
+    auto frag = [&](int ks, int slot) __attribute__((always_inline)) {
+      const int c = h * KS + ks;
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int row = arow0 + 32 * a;
+        af[slot][a] = __builtin_bit_cast(
+            v8bf, *reinterpret_cast<const v4u*>(As + row * ROWB + 16 * (c ^ sw(row))));
+      }
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int row = brow0 + 32 * b;
+        bfr[slot][b] = __builtin_bit_cast(
+            v8bf, *reinterpret_cast<const v4u*>(Bs + row * ROWB + 16 * (c ^ sw(row))));
+      }
+    };
+    frag(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < KS) frag(ks + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b)   // embedding rows first: acc holds logits^T
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][b], af[cur][a], acc[a][b], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // prologue: STAGES - 1 stages in flight, stage 0 complete
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) issue(st, st);
+  if (nk >= STAGES - 1) wait_vmcnt_le<(STAGES - 2) * 2 * IPW>(); else __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt % STAGES;
+    const bool more = kt + STAGES - 1 < nk;
+    if (more) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);   // the stage freed at kt-1
+    compute(Ast(st), Ast(st) + OPB);
+    if (more) wait_vmcnt_le<(STAGES - 2) * 2 * IPW>(); else __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+
+  // ---- epilogue: per token, max and sum of exp over the block's 256 columns ----
+  float* red = reinterpret_cast<float*>(lds);     // [4 waves along N][BM][2]
+  const float L2E = 1.4426950408889634f;
+#pragma unroll
+  for (int a = 0; a < TM; ++a) {
+    const int li = wm * WM + 32 * a + (lane & 31);
+    const int lb = lbl[li];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[a][b][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float se = 0.0f;
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        se += __builtin_amdgcn_exp2f((acc[a][b][r] - mx) * L2E);
+        const int64_t col = n0 + wn * WN + 32 * b + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (col == lb) lab[m0 + li] = acc[a][b][r];
+      }
+    se += __shfl_xor(se, 32, 64);
+    if (h == 0) {
+      red[(wn * BM + li) * 2 + 0] = mx;
+      red[(wn * BM + li) * 2 + 1] = se;
+    }
+  }
+  __syncthreads();
+  if (tid < BM) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < BN / WN; ++w) mx = fmaxf(mx, red[(w * BM + tid) * 2]);
+    float se = 0.0f;
+#pragma unroll
+    for (int w = 0; w < BN / WN; ++w)
+      se += red[(w * BM + tid) * 2 + 1] * __builtin_amdgcn_exp2f((red[(w * BM + tid) * 2] - mx) * L2E);
+    pmax[(m0 + tid) * nvt + tn] = mx;
+    psum[(m0 + tid) * nvt + tn] = se;
+  }
+}
+
 // Row loss = logsumexp - label logit; the last position of each sequence has
 // no label (0).  One wave per row over the vocabulary-tile partials.
 __global__ void __launch_bounds__(256) k_ce_combine(const float* pmax, const float* psum,
@@ -1136,8 +1300,8 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   const int sp_lm = span_begin(m, 2, 2.0 * M * d * cf.vocab, s);
   if (bf) {
     const unsigned nb = (unsigned)(nvt * ((M + kLmTile - 1) / kLmTile));
-    if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % kLmBK == 0)
-      hipLaunchKernelGGL(k_lmhead_bf16<true>, dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
+    if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % 64 == 0)
+      hipLaunchKernelGGL((k_lmhead_dma<2, 64>), dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
                          (const uint16_t*)m->emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
                          m->psum, m->lab, nvt);
     else
