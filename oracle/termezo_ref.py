@@ -184,6 +184,39 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
+# Layer-level steps of Algorithm 1 for callers that hold one layer at a time
+# (global ids start at gid0); the same routines TerMeZOOracle applies.
+# --------------------------------------------------------------------------
+def perturbed_layer_values(w: np.ndarray, act, gid0: int, seed: int, eps: float,
+                           sign: int) -> np.ndarray:
+    """w + sign eps z(seed) at the active local indices act, w elsewhere."""
+    w = _f32(w).ravel()
+    act = _i64(act)
+    out = np.empty_like(w)
+    lib().orc_perturbed_layer(_p(w), w.size, _p(act), act.size, int(gid0),
+                              seed & (2**64 - 1), float(eps), int(sign), _p(out))
+    return out
+
+
+def updated_layer_values(w: np.ndarray, act, gid0: int, seed: int, lr: float, g: float,
+                         bf16: bool) -> np.ndarray:
+    """A copy of w after w_i <- rnd(fma(-(lr g), z_i, w_i)) at the actives."""
+    w = _f32(w).ravel().copy()
+    act = _i64(act)
+    lib().orc_update_layer(_p(w), _p(act), act.size, int(gid0), seed & (2**64 - 1), float(lr),
+                           float(g), int(bool(bf16)))
+    return w
+
+
+def shrink_layer(w: np.ndarray, act, tau: float, xi0: float) -> np.ndarray:
+    """The actives kept by eq. selection_ (distance to tau at most xi0), in order."""
+    w = _f32(w).ravel()
+    act = _i64(act).copy()
+    n = lib().orc_shrink_layer(_p(w), _p(act), act.size, float(tau), float(xi0))
+    return act[:n].copy()
+
+
+# --------------------------------------------------------------------------
 # BitLinear (8-bit activations x ternary weights)
 # --------------------------------------------------------------------------
 def act_quant(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:

@@ -453,3 +453,24 @@ def test_mse_and_projected_grad(orc):
     ref = float(np.mean((y.astype(np.float64) - t.astype(np.float64)) ** 2))
     assert abs(orc.mse(y, t) - ref) <= 1e-6 * ref
     assert orc.projected_grad(1.5, 1.25, 1e-3) == pytest.approx(125.0, rel=1e-6)
+
+
+def test_layer_level_wrappers_match_the_state_object(orc):
+    """The one-layer entry points (used where the oracle cannot hold every
+    layer) give what TerMeZOOracle gives for the same layer and global ids."""
+    shapes = [(64, 32), (48, 64), (32, 32)]
+    w = synth.latents(11, [o * i for o, i in shapes], bf16=True)
+    ref = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w.copy(), bf16=True)
+    ref.build_mask(0.05)
+    l = 1
+    lw = ref.layer_w(l).copy()
+    act = ref.active[l].copy()
+    gid0 = int(ref.offsets[l])
+    assert np.array_equal(orc.perturbed_layer_values(lw, act, gid0, 9, 1e-3, -1),
+                          ref.perturbed_layer(l, 9, 1e-3, -1))
+    ref.perturb(9, 1e-3, 1)
+    upd = orc.updated_layer_values(lw, act, gid0, 9, 1e-4, 25.0, True)
+    ref.update(25.0, 1e-4)
+    assert np.array_equal(upd, ref.layer_w(l))
+    tau, _ = orc.threshold(orc.layer_abs_sum(upd), upd.size, 1e-5)
+    assert np.array_equal(orc.shrink_layer(upd, act, tau, ref.xi0), ref.active[l])
