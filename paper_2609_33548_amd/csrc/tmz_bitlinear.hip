@@ -352,9 +352,11 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   constexpr int BROW = 32;                        // bytes of packed codes per B row per stage
   constexpr int ASTAGE = BM * AROW, BSTAGE = BN * BROW;
   constexpr int KS = kBK / 32;                    // MFMA sub-steps per K step
-  constexpr int AJ = BM / 64;                     // A loads per wave per stage
-  constexpr int BW = BN / 32;                     // waves holding distinct B rows
-  static_assert((BM / WM) * (BN / WN) == 8 && BW <= 8 && 3 * (ASTAGE + BSTAGE) <= kDmaLds, "tile");
+  constexpr int NW = (BM / WM) * (BN / WN);       // waves per block
+  constexpr int AJ = BM / (8 * NW);               // A loads per wave per stage
+  constexpr int BW = BN / 32 < NW ? BN / 32 : NW; // waves holding distinct B rows
+  static_assert(AJ >= 1 && BM % (8 * NW) == 0 && BN / 32 <= NW && 3 * (ASTAGE + BSTAGE) <= kDmaLds,
+                "tile");
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
@@ -364,7 +366,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   // Per-lane global sources.  A: wave w fills 1 KB chunks AJ w .. AJ w + AJ-1
   // (8 rows each); lane i -> row 8 j + i / 8, physical chunk i % 8.  B: wave
   // w fills rows 32 (w % BW) .. + 31, two lanes (physical halves) per row
-  // (with BW < 8 two waves write the same bytes).
+  // (with BW < NW several waves write the same bytes).
   const int8_t* asrc[AJ];
 #pragma unroll
   for (int j = 0; j < AJ; ++j) {

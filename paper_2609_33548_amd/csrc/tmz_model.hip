@@ -8,6 +8,7 @@
 #include <cmath>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "tmz_device.h"
@@ -18,6 +19,13 @@ namespace tmz {
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// Two floats to a packed pair of bf16 (RNE), low half = a: one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
+}
 
 __device__ __forceinline__ float ld_act(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld_act(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
@@ -267,13 +275,8 @@ __device__ __forceinline__ uint4 rope_chunk(uint4 own, uint4 par, bool low, cons
     const float c = cs[j], sv = sn[j];
     r[j] = low ? o8[j] * c - p8[j] * sv : p8[j] * sv + o8[j] * c;
   }
-  uint32_t w[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const __bf16 a = (__bf16)r[2 * j], b = (__bf16)r[2 * j + 1];
-    w[j] = (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
-  }
-  return make_uint4(w[0], w[1], w[2], w[3]);
+  return make_uint4(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]), pack_bf16x2(r[4], r[5]),
+                    pack_bf16x2(r[6], r[7]));
 }
 
 template <int HD>
@@ -508,6 +511,270 @@ __global__ void __launch_bounds__(512) k_attn_bf16(const uint16_t* __restrict__ 
       const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, e2) |
                           ((uint32_t)__builtin_bit_cast(uint16_t, e3) << 16);
       *reinterpret_cast<uint2*>(orow + 16 * t + 4 * g) = make_uint2(w0, w1);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Causal GQA flash attention for a whole query group (v_mfma_f32_32x32x16_bf16).
+// Block = QT = 256 / G queries of one (sequence, KV head) for all G query
+// heads that share the KV head, 8 waves of 32 (query, head) rows, so every K
+// and V^T tile brought into LDS feeds all G heads.
+//  * Q: the block's rows are read coalesced (item = one query and one pair of
+//    rotary-partner 16-byte chunks, for all G heads, so the cos/sin entries
+//    are read once per query), rotated, and staged in LDS; each wave then
+//    takes its rope(Q)^T fragments into registers.  The normalised output
+//    goes back through the same staging rows and leaves as whole rows.
+//  * Per 64-key tile a wave computes S^T = K rope(Q)^T (K rows from LDS as
+//    the first operand), an online softmax per query (the query is the lane's
+//    accumulator column, so its statistics stay in the lane pair l, l ^ 32)
+//    and O^T += V^T P^T with P^T taken straight from the S^T accumulators.
+//    For that the K rows of a 32-key block are read in the order pi (bits 2
+//    and 3 of the row swapped): accumulator element j of lane half h then
+//    holds key 16 (j / 8) + 8 h + j % 8, i.e. in every 16-key step a lane owns
+//    8 consecutive keys, the B-operand layout, and the matching V^T fragment
+//    is one 16-byte chunk of a V^T row.  The row sum is taken from the bf16
+//    probabilities that enter the product (v_dot2 with ones).
+//  * K and V^T tiles stream through 2 LDS stages with direct global -> LDS
+//    loads; 16-byte chunk c of a K row r sits at c ^ (r & 15) (128-dim rows)
+//    or c ^ ((r >> 1) & 7) (64-dim rows), of a V^T row at c ^ ((r >> 1) & 7),
+//    so the fragment reads of 16 lanes hit distinct banks; staging rows put
+//    chunk c at c ^ (r & (CPR - 1)).
+//  * 32-key blocks entirely in a wave's causal future are skipped and only
+//    the diagonal block is masked.  The running maximum is raised only when a
+//    tile's maximum exceeds it by more than 2^8 (in exp2 units); the
+//    normalised result does not depend on that choice.  Query tiles are
+//    dispatched heaviest first.
+// Requires S % 64 == 0 and S % QT == 0.
+// ---------------------------------------------------------------------------
+template <int HD, int G>
+__global__ void __launch_bounds__(512) k_attn_gqa(const uint16_t* __restrict__ q,
+                                                  const uint16_t* __restrict__ k,
+                                                  const uint16_t* __restrict__ vt,
+                                                  uint16_t* __restrict__ o, int S, int Hkv,
+                                                  int nbh, int nqt, float scale_log2,
+                                                  const float* __restrict__ rope_c,
+                                                  const float* __restrict__ rope_s) {
+  constexpr int HALF = HD / 2;
+  constexpr int QT = 256 / G;                 // queries per block
+  constexpr int KT = 64;                      // keys per stage
+  constexpr int KROWB = 2 * HD, CPR = HD / 8; // bytes and 16-byte chunks per K / Q row
+  constexpr int TB = KT * KROWB;              // bytes per K tile (= per V^T tile)
+  constexpr int QB = 256 * KROWB;             // Q / O staging: 256 (query, head) rows
+  constexpr int LPW = TB / 1024 / 8;          // 1 KB loads per wave per operand per stage
+  constexpr int NS = HD / 16;                 // 16-dim K steps of S^T
+  constexpr int ND = HD / 32;                 // 32-dim blocks of O^T
+  static_assert(HD == 64 || HD == 128, "head dim");
+  static_assert(G == 1 || G == 2 || G == 4 || G == 8, "group");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * TB + QB];
+  uint8_t* stg = lds + 4 * TB;                // Q / O staging rows (query r, head g) -> r G + g
+  auto swk = [](int r) __attribute__((always_inline)) {
+    return CPR == 16 ? (r & 15) : ((r >> 1) & 7);
+  };
+  auto swv = [](int r) __attribute__((always_inline)) { return (r >> 1) & 7; };
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 31, h = lane >> 5;
+  const int lb = blockIdx.x;
+  const int qt = nqt - 1 - lb / nbh, bh = lb % nbh;
+  const int b = bh / Hkv, kvh = bh % Hkv;
+  const int Hq = Hkv * G;
+  const int64_t rowq = (int64_t)Hq * HD, rowkv = (int64_t)Hkv * HD;
+  const int64_t base = (int64_t)b * S;
+  const int q0 = qt * QT;
+  const int hq0 = kvh * G;                    // first query head of the group
+  const int rq = 32 * (wid / G) + n;          // this lane's query within the block
+  const int qw0 = q0 + 32 * (wid / G);        // first query of this wave
+  const int qpos = q0 + rq;                   // this lane's query
+  const int srow = rq * G + wid % G;          // this lane's staging row
+
+  // direct-load sources: load j of wave w fills LDS chunks (w LPW + j) 64 + lane
+  const uint8_t* ksrc[LPW];
+  const uint8_t* vsrc[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int c = (wid * LPW + j) * 64 + lane;
+    const int kr = c / CPR, kc = (c % CPR) ^ swk(kr);
+    ksrc[j] = reinterpret_cast<const uint8_t*>(k + (base + kr) * rowkv + (int64_t)kvh * HD) + 16 * kc;
+    const int vr = c / 8, vc = (c % 8) ^ swv(vr);
+    vsrc[j] = reinterpret_cast<const uint8_t*>(vt + (((int64_t)b * Hkv + kvh) * HD + vr) * S) + 16 * vc;
+  }
+  const uint32_t wbase = wid * LPW * 1024u;
+  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+    const uint32_t kb = lds_offset(lds + st * 2 * TB) + wbase, vb = kb + TB;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      dma16(ksrc[j] + (int64_t)kt * KT * rowkv * 2, kb + 1024u * j);
+      dma16(vsrc[j] + (int64_t)kt * KT * 2, vb + 1024u * j);
+    }
+  };
+
+  const int ntile = (q0 + QT - 1) / KT + 1;
+  issue(0, 0);
+
+  // rope(Q) into the staging rows
+  for (int it = tid; it < QT * (CPR / 2); it += 512) {
+    const int r = it / (CPR / 2), cg = it % (CPR / 2);
+    const int pos = q0 + r;
+    const uint16_t* qr = q + (base + pos) * rowq + (int64_t)hq0 * HD + 8 * cg;
+    uint4 lo[G], hi[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      lo[g] = *reinterpret_cast<const uint4*>(qr + g * HD);
+      hi[g] = *reinterpret_cast<const uint4*>(qr + g * HD + HALF);
+    }
+    const int ti = pos * HALF + 8 * cg;
+    const int sw = r & (CPR - 1);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      uint8_t* row = stg + (r * G + g) * KROWB;
+      *reinterpret_cast<uint4*>(row + 16 * (cg ^ sw)) = rope_chunk(lo[g], hi[g], true, rope_c + ti, rope_s + ti);
+      *reinterpret_cast<uint4*>(row + 16 * ((cg + CPR / 2) ^ sw)) =
+          rope_chunk(hi[g], lo[g], false, rope_c + ti, rope_s + ti);
+    }
+  }
+  __syncthreads();
+  // rope(Q)^T fragments: for K step s the lane holds dims 16 s + 8 h .. + 7 of its query
+  v8bf qf[NS];
+  {
+    const uint8_t* row = stg + srow * KROWB;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qf[s] = __builtin_bit_cast(v8bf, *reinterpret_cast<const uint4*>(row + 16 * ((2 * s + h) ^ (rq & (CPR - 1)))));
+  }
+
+  v16f ot[ND];
+#pragma unroll
+  for (int d = 0; d < ND; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ot[d][r] = 0.0f;
+  float mrun = -INFINITY, lrun = 0.0f;
+
+  typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+  // K row read by lane n of a 32-key block: pi(n) swaps bits 2 and 3
+  const int krow = (n & ~12) | ((n & 4) << 1) | ((n & 8) >> 1);
+  // lane parts of the fragment addresses (stage, key block and dim block parts are constants)
+  uint32_t kad[NS], vad[4];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) kad[s] = krow * KROWB + 16 * ((2 * s + h) ^ swk(krow));
+#pragma unroll
+  for (int s = 0; s < 4; ++s) vad[s] = n * 128 + 16 * ((2 * s + h) ^ swv(n));
+  const v2bf ones2 = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // one 64-key tile of keys k0.. in stage ST with NKB 32-key blocks; diag: mask the last one
+  auto tile = [&](auto st_c, int k0, auto nkb_c, bool diag) __attribute__((always_inline)) {
+    constexpr int NKB = decltype(nkb_c)::value;
+    constexpr int ST = decltype(st_c)::value;
+    const uint8_t* Ks = lds + ST * 2 * TB;
+    const uint8_t* Vs = Ks + TB;
+    v16f sc[NKB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[kb][r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const v8bf kf = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(Ks + kad[s] + 32 * kb * KROWB));
+        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sc[kb], 0, 0, 0);
+      }
+    }
+    if (diag) {   // key offset within the last block vs this lane's query offset
+      const int lim = qpos - (k0 + 32 * (NKB - 1));
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (16 * (r >> 3) + 8 * h + (r & 7) > lim) sc[NKB - 1][r] = -INFINITY;
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
+    {   // combine the two lane halves (same query, other keys)
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    const float ms = mx * scale_log2;
+    const bool raise = ms > mrun + 8.0f;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+      const float mnew = raise ? ms : mrun;
+      const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
+      lrun *= alpha;
+#pragma unroll
+      for (int d = 0; d < ND; ++d) ot[d] *= alpha;
+      mrun = mnew;
+    }
+    v8bf pf[2 * NKB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        uint32_t pk[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[kb][8 * t + 2 * i], scale_log2, -mrun));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[kb][8 * t + 2 * i + 1], scale_log2, -mrun));
+          pk[i] = pack_bf16x2(p0, p1);
+          lrun = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(v2bf, pk[i]), ones2, lrun, false);
+        }
+        pf[2 * kb + t] = __builtin_bit_cast(v8bf, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+      }
+#pragma unroll
+    for (int s = 0; s < 2 * NKB; ++s)
+#pragma unroll
+      for (int d = 0; d < ND; ++d) {
+        const v8bf vf = __builtin_bit_cast(v8bf, *reinterpret_cast<const v4u*>(Vs + vad[s] + 32 * d * 128));
+        ot[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[s], ot[d], 0, 0, 0);
+      }
+  };
+
+  // tile kt in stage kt & 1; the next tile's loads are in flight during the current one
+  auto body = [&](int kt, auto st_c) __attribute__((always_inline)) {
+    constexpr int ST = decltype(st_c)::value;
+    if (kt + 1 < ntile) issue(kt + 1, ST ^ 1);
+    const int k0 = kt * KT;
+    if (k0 + 32 < qw0) {
+      tile(st_c, k0, std::integral_constant<int, 2>{}, false);
+    } else if (k0 + 32 == qw0) {
+      tile(st_c, k0, std::integral_constant<int, 2>{}, true);
+    } else if (k0 == qw0) {
+      tile(st_c, k0, std::integral_constant<int, 1>{}, true);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+  for (int kt = 0; kt < ntile; kt += 2) {
+    body(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 < ntile) body(kt + 1, std::integral_constant<int, 1>{});
+  }
+
+  {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(lrun), __float_as_uint(lrun), false, false);
+    lrun = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  }
+  const float inv = 1.0f / lrun;
+  {
+    uint8_t* row = stg + srow * KROWB;
+#pragma unroll
+    for (int d = 0; d < ND; ++d)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const uint32_t w0 = pack_bf16x2(ot[d][4 * g] * inv, ot[d][4 * g + 1] * inv);
+        const uint32_t w1 = pack_bf16x2(ot[d][4 * g + 2] * inv, ot[d][4 * g + 3] * inv);
+        *reinterpret_cast<uint2*>(row + 16 * ((4 * d + g) ^ (rq & (CPR - 1))) + 8 * h) = make_uint2(w0, w1);
+      }
+  }
+  __syncthreads();
+  for (int it = tid; it < QT * (CPR / 2); it += 512) {
+    const int r = it / (CPR / 2), cg = it % (CPR / 2);
+    const int sw = r & (CPR - 1);
+    uint16_t* orow = o + (base + q0 + r) * rowq + (int64_t)hq0 * HD + 8 * cg;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint8_t* row = stg + (r * G + g) * KROWB;
+      *reinterpret_cast<uint4*>(orow + g * HD) = *reinterpret_cast<const uint4*>(row + 16 * (cg ^ sw));
+      *reinterpret_cast<uint4*>(orow + g * HD + HALF) =
+          *reinterpret_cast<const uint4*>(row + 16 * ((cg + CPR / 2) ^ sw));
     }
   }
 }
@@ -1077,6 +1344,37 @@ hipError_t run_attention(termezo_model* m, int B, int S, hipStream_t st) {
   hipLaunchKernelGGL(k_attn_bf16<HDV>, grid, dim3(512), 0, st, (const uint16_t*)m->q,          \
                      (const uint16_t*)m->k, (const uint16_t*)m->vt, (uint16_t*)m->attn, S,     \
                      c.n_heads, c.n_kv_heads, sl2, m->rope_c, m->rope_s)
+  const int G = c.n_heads / c.n_kv_heads;
+  const bool gqa = (m->hd == 64 || m->hd == 128) && (G == 1 || G == 2 || G == 4 || G == 8) &&
+                   S % 64 == 0 && S % (256 / G) == 0;
+  if (gqa) {
+    const int nbh = B * c.n_kv_heads, nqt = S / (256 / G);
+    if (m->hd == 128)
+      hipLaunchKernelGGL(k_kv_prep<128>, pgrid, dim3(256), 0, st, (uint16_t*)m->k,
+                         (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads, m->rope_c,
+                         m->rope_s);
+    else
+      hipLaunchKernelGGL(k_kv_prep<64>, pgrid, dim3(256), 0, st, (uint16_t*)m->k,
+                         (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads, m->rope_c,
+                         m->rope_s);
+#define TMZ_GQA(HDV, GV)                                                                      \
+  hipLaunchKernelGGL((k_attn_gqa<HDV, GV>), dim3((unsigned)(nqt * nbh)), dim3(512), 0, st,      \
+                     (const uint16_t*)m->q, (const uint16_t*)m->k, (const uint16_t*)m->vt,     \
+                     (uint16_t*)m->attn, S, c.n_kv_heads, nbh, nqt, sl2, m->rope_c, m->rope_s)
+    switch (m->hd * 16 + G) {
+      case 128 * 16 + 1: TMZ_GQA(128, 1); break;
+      case 128 * 16 + 2: TMZ_GQA(128, 2); break;
+      case 128 * 16 + 4: TMZ_GQA(128, 4); break;
+      case 128 * 16 + 8: TMZ_GQA(128, 8); break;
+      case 64 * 16 + 1: TMZ_GQA(64, 1); break;
+      case 64 * 16 + 2: TMZ_GQA(64, 2); break;
+      case 64 * 16 + 4: TMZ_GQA(64, 4); break;
+      case 64 * 16 + 8: TMZ_GQA(64, 8); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef TMZ_GQA
+    return hipGetLastError();
+  }
   switch (m->hd) {
     case 64: TMZ_ATTN(64); break;
     case 96: TMZ_ATTN(96); break;

@@ -83,6 +83,10 @@ def test_tiny_decoder_fp32_steps(orc):
     (192, 2, 2, 192, 257, 64, 3),      # head_dim 96
     (256, 4, 2, 512, 1000, 200, 1),    # head_dim 64
     (256, 2, 1, 256, 512, 128, 2),     # M, vocab multiples of 256: full-tile LM head
+    (512, 4, 1, 512, 300, 128, 2),     # GQA 4:1, head_dim 128 (grouped-query kernel, 64-query tiles)
+    (512, 8, 1, 256, 300, 64, 2),      # GQA 8:1, head_dim 64 (32-query tiles)
+    (256, 2, 2, 256, 300, 256, 1),     # MHA, head_dim 128 (256-query tiles)
+    (256, 4, 2, 256, 300, 128, 2),     # GQA 2:1, head_dim 64
 ])
 def test_bf16_decoder_loss(orc, d, H, Hkv, F, V, S, B):
     torch = _torch()
