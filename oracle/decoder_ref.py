@@ -143,7 +143,7 @@ def forward_row_losses(cfg: DecoderConfig, emb: np.ndarray, tokens: np.ndarray,
         x = rmsnorm(h, cfg.norm_eps)
         g = store(bitlinear_fp32_in(x, c[4], be[4]), bf)
         u = store(bitlinear_fp32_in(x, c[5], be[5]), bf)
-        m = silu_mul(g, u)
+        m = store(silu_mul(g, u), bf)
         dn = store(bitlinear_fp32_in(m, c[6], be[6]), bf)
         h = store(h.astype(np.float64) + dn, bf)
     xf = store(rmsnorm(h, cfg.norm_eps), bf)

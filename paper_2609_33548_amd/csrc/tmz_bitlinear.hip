@@ -376,7 +376,14 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   }
   const int bw = wid % BW;
   const int brow_l = 32 * bw + (lane >> 1);
-  const uint32_t* bsrc = codes + (n0 + brow_l) * KW + 4 * ((lane & 1) ^ bswz(brow_l));
+  int64_t crow = n0 + brow_l;                     // code row of tile row brow_l
+  if constexpr (MODE == kGemmSwiGLU) {
+    // column 32 p + c holds gate row 16 p + c (c < 16) or up row F + 16 p + c - 16, so a
+    // lane's accumulator registers r and r + 8 are the gate and up value of one feature
+    const int64_t p = crow >> 5, c = crow & 31;
+    crow = c < 16 ? 16 * p + c : (N >> 1) + 16 * p + (c - 16);
+  }
+  const uint32_t* bsrc = codes + crow * KW + 4 * ((lane & 1) ^ bswz(brow_l));
 
   const uint32_t wa = __builtin_amdgcn_readfirstlane(wid);   // wave-uniform
   const uint32_t wb = __builtin_amdgcn_readfirstlane(bw);
@@ -460,6 +467,36 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     if (kt + 2 < nk) wait_vmcnt_le<AJ + 1>(); else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     cur = cur == 2 ? 0 : cur + 1;
+  }
+
+  if constexpr (MODE == kGemmSwiGLU) {
+    // registers 0..7 of a 32-column block p are gate features 16 p + 8 (r / 4) + 4 h + r % 4,
+    // registers 8..15 the up values of the same features
+    const int64_t ld = out.ld[0];
+    const int ml = wm * WM + (lane & 31);
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+      const int64_t f0 = (n0 + wn * WN + b * 32) >> 1;
+      TY* base = reinterpret_cast<TY*>(out.y[0]) + f0 + 4 * (lane >> 5);
+#pragma unroll
+      for (int a = 0; a < TM; ++a) {
+        const int mloc = ml + 32 * a;
+        const float rg = rrow[0][mloc], ru = rrow[1][mloc];
+        TY* rowp = base + (m0 + mloc) * ld;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          float v4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float g = round_act(rowp, (float)acc[a][b][4 * q + j] * rg);
+            const float u = round_act(rowp, (float)acc[a][b][4 * q + 8 + j] * ru);
+            v4[j] = silu_mul(g, u);
+          }
+          store4(rowp + 8 * q, v4);
+        }
+      }
+    }
+    return;
   }
 
   // ---- epilogue (every tile is in bounds).  acc[a][b] is the transposed
@@ -729,9 +766,34 @@ static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* 
 // the direct-to-LDS variant when every tile is in bounds and the outputs allow
 // 4-wide stores, with its last round cut into 128 x 128 quarter tiles when it
 // would fill at most half of the n_cu compute units (n_cu = 0: never).
+bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt) {
+  return ydt == TERMEZO_BF16 && M % kDmaBM == 0 && N % kDmaBN == 0 && K % kBK == 0 && M > 0 &&
+         K > 0;
+}
+
+// Launch plan of the full-tile path: blocks [0, full) take 256 x 256 tiles, the rest take
+// quarters of the remaining ones.
+static int64_t dma_full_tiles(int64_t T, int n_cu) {
+  int64_t full = T;
+  if (n_cu > 0 && T > n_cu) {
+    const int64_t rem = T % n_cu;
+    if (rem > 0 && 2 * rem <= n_cu) full = T - rem;
+  }
+  return full;
+}
+
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
                           int32_t* acc, int n_cu, hipStream_t st) {
+  if (mode == kGemmSwiGLU) {
+    if (!gemm_swiglu_ok(M, K, N, ydt) || out.nseg != 2 || out.nstart[1] * 2 != N || acc ||
+        out.ld[0] % 4 != 0 || reinterpret_cast<uintptr_t>(out.y[0]) % 8 != 0)
+      return hipErrorInvalidValue;
+    const int64_t T = (M / kDmaBM) * (N / kDmaBN), full = dma_full_tiles(T, n_cu);
+    hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU>), dim3((unsigned)(full + 4 * (T - full))),
+                       dim3(512), 0, st, xq, s, codes, M, K, N, out, full, acc);
+    return hipGetLastError();
+  }
   if (M <= kGemvMaxM) {
     bool seg16 = true;
     for (int i = 1; i < out.nseg; ++i) seg16 = seg16 && out.nstart[i] % 16 == 0;
@@ -765,12 +827,7 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
     for (int i = 0; i < out.nseg; ++i)
       seg32 = seg32 && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
     if (M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32) {
-      const int64_t T = big_blocks;
-      int64_t full = T;
-      if (n_cu > 0 && T > n_cu) {
-        const int64_t rem = T % n_cu;
-        if (rem > 0 && 2 * rem <= n_cu) full = T - rem;
-      }
+      const int64_t T = big_blocks, full = dma_full_tiles(T, n_cu);
       dim3 grid((unsigned)(full + 4 * (T - full)));
       if (ydt == TERMEZO_F32) {
         if (mode == kGemmStore)

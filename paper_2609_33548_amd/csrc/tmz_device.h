@@ -235,6 +235,13 @@ __device__ __forceinline__ void tile_of_block(int64_t nb_m, int64_t nb_n, int64_
   tile_of_linear(xcd_linear(blockIdx.x, nb_m * nb_n), nb_m, nb_n, tm, tn);
 }
 
+// silu(g) * u as the decoder evaluates it (hardware exp2 and reciprocal), shared by the
+// SwiGLU row kernel and the SwiGLU GEMM epilogue so the two give identical results.
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g * -1.4426950408889634f));
+  return g * sg * u;
+}
+
 // ---------------------------------------------------------------------------
 // Direct global -> LDS loads (gfx950 global_load_lds_dwordx4).
 // ---------------------------------------------------------------------------

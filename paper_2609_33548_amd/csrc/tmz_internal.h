@@ -50,6 +50,9 @@ struct DevState {
 constexpr int kMaxSeg = 3;
 constexpr int kGemmStore = 0;      // y = round(acc * beta / s)
 constexpr int kGemmResidual = 1;   // y <- round(y + round(acc * beta / s))
+// SwiGLU of a gate|up pair: N = 2F code rows (gate rows 0..F-1, up rows F..2F-1), output
+// y[m][f] = round(silu(g) u) with g, u the rounded gate and up projections (bf16 only)
+constexpr int kGemmSwiGLU = 2;
 struct GemmOut {
   void* y[kMaxSeg];
   int64_t ld[kMaxSeg];
@@ -191,6 +194,8 @@ hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
                           int32_t* acc, int n_cu, hipStream_t st);
+// Whether kGemmSwiGLU (full-tile path only) supports an M x K x N gate|up pair.
+bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt);
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
                                  const float* beta_dev, int64_t M, int64_t K, int64_t N,
                                  void* y, termezo_dtype ydt, int32_t* acc, int n_cu,

@@ -27,6 +27,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
 }
 
+__device__ __forceinline__ float round_to(const float*, float v) { return v; }
+__device__ __forceinline__ float round_to(const uint16_t*, float v) { return (float)(__bf16)v; }
 __device__ __forceinline__ float ld_act(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld_act(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
 __device__ __forceinline__ void st_act(float* p, int64_t i, float v) { p[i] = v; }
@@ -81,7 +83,7 @@ __global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, i
 //                  the 8-bit quantiser: s = 127 / max(max|x|, 1e-5),
 //                  x_q = clamp(rne(x s), -128, 127)
 //   kRowNormStore  the RMSNorm output stored in the activation dtype
-//   kRowSwiGLU     a = silu(g) * u, then the quantiser
+//   kRowSwiGLU     a = silu(g) * u rounded to the activation dtype, then the quantiser
 //   kRowQuant      the quantiser alone
 // Rows up to 64 * 8 * kRowChunks elements.
 // ---------------------------------------------------------------------------
@@ -135,9 +137,7 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
         load8(u + m * K + idx * 8, uu);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float gv = v[c][j];
-          const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(gv * -1.4426950408889634f));
-          v[c][j] = gv * sg * uu[j];
+          v[c][j] = round_to(x, silu_mul(v[c][j], uu[j]));   // the product is an activation
           acc = fmaxf(acc, fabsf(v[c][j]));
         }
       } else if (MODE == kRowQuant) {
@@ -1572,11 +1572,18 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o2.y[0] = m->g; o2.ld[0] = F; o2.beta[0] = c->d_beta_cur + l0 + 4;
     o2.y[1] = m->u; o2.ld[1] = F; o2.beta[1] = c->d_beta_cur + l0 + 5;
     o2.nstart[0] = 0; o2.nstart[1] = F; o2.nstart[2] = 2 * F;
+    // gate|up with the SwiGLU in the epilogue where the full-tile path applies (the
+    // product lands in g), else the two projections and the SwiGLU row kernel
+    const bool fused = gemm_swiglu_ok(M, d, 2 * F, adt);
     sp = span_begin(m, 0, 2.0 * M * d * 2 * F, s);
-    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt, kGemmStore,
-                       nullptr, c->n_cu, s));
+    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt,
+                       fused ? kGemmSwiGLU : kGemmStore, nullptr, c->n_cu, s));
     span_end(m, sp, s);
-    if (bf)
+    if (fused)
+      hipLaunchKernelGGL((k_row<kRowQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
+                         (const uint16_t*)m->g, (const uint16_t*)nullptr, M, F, 0.0f, m->xq, m->xs,
+                         (uint16_t*)nullptr);
+    else if (bf)
       hipLaunchKernelGGL((k_row<kRowSwiGLU, uint16_t>), dim3(rowg), dim3(256), 0, s,
                          (const uint16_t*)m->g, (const uint16_t*)m->u, M, F, 0.0f, m->xq, m->xs,
                          (uint16_t*)nullptr);
