@@ -259,7 +259,7 @@ __global__ void __launch_bounds__(256) k_attn_f32(const float* q, const float* k
 // ---------------------------------------------------------------------------
 // Per-layer preparation of K and V for attention (one block per 64 tokens of
 // one KV head): K is rotated in place (RoPE, as in k_rope), V is transposed to
-// vt [B*Hkv][hd][S] through an LDS tile (coalesced reads and writes).
+// vt [B*Hkv][hd][S] through an LDS tile (16-byte reads and writes).
 // ---------------------------------------------------------------------------
 // Rotary embedding of one 8-dim chunk at dims d0..d0+7 given its partner
 // chunk (d0 -/+ hd/2), as in k_rope: low half a c - b s, high half a s + b c
@@ -286,7 +286,7 @@ __global__ void __launch_bounds__(256) k_kv_prep(uint16_t* __restrict__ k,
                                                  const float* __restrict__ rope_c,
                                                  const float* __restrict__ rope_s) {
   constexpr int HALF = HD / 2;
-  __shared__ uint16_t t[64][HD + 2];
+  __shared__ __attribute__((aligned(16))) uint16_t t[64][HD + 8];
   const int s0 = blockIdx.x * 64, bh = blockIdx.y;
   const int b = bh / Hkv, h = bh % Hkv;
   const int64_t rowkv = (int64_t)Hkv * HD;
@@ -301,15 +301,27 @@ __global__ void __launch_bounds__(256) k_kv_prep(uint16_t* __restrict__ k,
     *reinterpret_cast<uint4*>(kp + dc) = rope_chunk(lo, hi, true, rope_c + ti, rope_s + ti);
     *reinterpret_cast<uint4*>(kp + dc + HALF) = rope_chunk(hi, lo, false, rope_c + ti, rope_s + ti);
   }
-  // V^T
-  for (int i = threadIdx.x; i < 64 * HD; i += 256) {
-    const int r = i / HD, c = i % HD;       // r: token, c: dim
-    t[r][c] = (s0 + r < S) ? v[((int64_t)b * S + s0 + r) * rowkv + (int64_t)h * HD + c] : 0;
+  // V^T: 64 token rows in 16-byte chunks into LDS, then 8 tokens of one dim per 16-byte store
+  for (int i = threadIdx.x; i < 64 * HD / 8; i += 256) {
+    const int r = i / (HD / 8), c8 = (i % (HD / 8)) * 8;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (s0 + r < S) val = *reinterpret_cast<const uint4*>(v + ((int64_t)b * S + s0 + r) * rowkv + (int64_t)h * HD + c8);
+    *reinterpret_cast<uint4*>(&t[r][c8]) = val;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 64 * HD; i += 256) {
-    const int r = i / 64, c = i % 64;       // r: dim, c: token
-    if (s0 + c < S) vt[((int64_t)bh * HD + r) * S + s0 + c] = t[c][r];
+  for (int i = threadIdx.x; i < HD * 8; i += 256) {
+    const int r = i / 8, c8 = (i % 8) * 8;   // r: dim, c8: first of 8 tokens
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = (uint32_t)t[c8 + 2 * j][r] | ((uint32_t)t[c8 + 2 * j + 1][r] << 16);
+    uint16_t* dst = vt + ((int64_t)bh * HD + r) * S + s0 + c8;
+    if ((S & 7) == 0 && s0 + c8 + 8 <= S) {
+      *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (s0 + c8 + j < S) dst[j] = t[c8 + j][r];
+    }
   }
 }
 
