@@ -26,11 +26,18 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 CONFIGS = {
+    # config 4 (headline): BitNet b1.58 2B shape, bf16 latents and activations
     "2b": dict(n_blocks=30, d_model=2560, n_heads=20, n_kv_heads=5, d_ffn=6912, vocab=128256,
-               seq=512, batch=16),
+               seq=512, batch=16, rho=1e-3, lr=1e-5),
+    # config 3: 700M-class shape, 16 heads of 96 (MHA), bf16
     "700m": dict(n_blocks=24, d_model=1536, n_heads=16, n_kv_heads=16, d_ffn=4096, vocab=32000,
-                 seq=512, batch=8),
+                 seq=512, batch=8, rho=1e-3, lr=1e-5),
+    # config 2: tiny decoder, fp32 latents and activations
+    "tiny": dict(n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4, d_ffn=688, vocab=1024,
+                 seq=64, batch=4, rho=1e-2, lr=1e-4, fp32=True),
 }
+# config 1: one 256 x 256 BitLinear (fp32 latents), 8 token rows, MSE to a target
+C1 = dict(d_out=256, d_in=256, tokens=8, rho=1e-2, eps=1e-3, lr=1e-4)
 PEAK_INT8_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 # HBM traffic of the GEMM launches measured with rocprofv3 counters (FETCH_SIZE,
 # WRITE_SIZE), valid only for the kernel source it was measured on.
@@ -54,8 +61,9 @@ def gemm_algorithmic_bytes(c):
     hd = c["d_model"] // c["n_heads"]
     d, F = c["d_model"], c["d_ffn"]
     dq, dkv = c["n_heads"] * hd, c["n_kv_heads"] * hd
-    launches = [(d, dq + 2 * dkv, 1), (dq, d, 2), (d, 2 * F, 1), (F, d, 2)]  # (K, N, output passes)
-    total = sum(M * K + N * K // 4 + passes * 2 * M * N for K, N, passes in launches)
+    # (K, N code rows, output columns, output passes); gate|up writes only the SwiGLU product
+    launches = [(d, dq + 2 * dkv, dq + 2 * dkv, 1), (dq, d, d, 2), (d, 2 * F, F, 1), (F, d, d, 2)]
+    total = sum(M * K + N * K // 4 + passes * 2 * M * No for K, N, No, passes in launches)
     return total / len(launches)
 
 
@@ -128,6 +136,105 @@ def cpu_baseline(c, rho, seed=0):
                    f"positions scaled x{ntok // n_pos}; two forwards per step; sample wall {wall:.1f}s"),
         "extrapolated_step_s": t_step,
     }
+
+def cpu_baseline_c1(n_steps=200, seed=0):
+    """The oracle's full config-1 step (perturb +/-, BitLinear, MSE, update), timed."""
+    import numpy as np
+    from oracle import termezo_ref as orc
+    from paper_2609_33548_amd import synth
+    w = synth.latents(seed, [C1["d_out"] * C1["d_in"]])
+    st = orc.TerMeZOOracle([orc.Layer(C1["d_out"], C1["d_in"])], w)
+    x = synth.activations(100, C1["tokens"], C1["d_in"])
+    tgt = synth.activations(101, C1["tokens"], C1["d_out"])
+    st.build_mask(C1["rho"])
+    xq, s = orc.act_quant(x)
+    t0 = time.perf_counter()
+    for t in range(n_steps):
+        f = {}
+        for sign in (1, -1):
+            codes, _, betas = st.perturb(t, C1["eps"], sign)
+            _, y = orc.bitlinear(xq, s, codes[0], betas[0], want_acc=False)
+            f[sign] = orc.mse(y, tgt)
+        st.update(orc.projected_grad(f[1], f[-1], C1["eps"]), C1["lr"])
+    dt = (time.perf_counter() - t0) / n_steps
+    return {"value": 1.0 / dt, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n_steps} full oracle steps of the same workload (single thread, C + numpy)"}
+
+
+def cpu_baseline_full(c, rho, n_steps=8, seed=0):
+    """The oracle's full decoder step (perturb +/-, two forwards, update) on the same
+    workload, for configurations small enough to run whole."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import decoder_ref as dec
+    from oracle import termezo_ref as orc
+    from paper_2609_33548_amd import synth
+    bf = not c.get("fp32", False)
+    cfg = dec.DecoderConfig(n_blocks=c["n_blocks"], d_model=c["d_model"], n_heads=c["n_heads"],
+                            n_kv_heads=c["n_kv_heads"], d_ffn=c["d_ffn"], vocab=c["vocab"], bf16=bf)
+    shapes = cfg.layer_shapes()
+    w = synth.latents(seed, [o * i for o, i in shapes], bf16=bf)
+    st = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w, bf16=bf)
+    emb = synth.latents(seed + 1, [c["vocab"] * c["d_model"]], bf16=bf).reshape(c["vocab"], c["d_model"])
+    tok = synth.tokens(seed + 2, c["batch"], c["seq"], c["vocab"])
+    st.build_mask(rho)
+    t0 = time.perf_counter()
+    for t in range(n_steps):
+        f = {}
+        for sign in (1, -1):
+            codes, _, betas = st.perturb(t, 1e-3, sign)
+            f[sign] = dec.mean_loss(dec.forward_row_losses(cfg, emb, tok, codes, betas))
+        st.update(orc.projected_grad(f[1], f[-1], 1e-3), c["lr"])
+    dt = (time.perf_counter() - t0) / n_steps
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": 1.0 / dt, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_steps} full oracle steps of the same workload"}
+
+
+def run_c1(args, torch, termezo, synth, dev):
+    """Config 1: one BitLinear 256 x 256 with fp32 latents, 8 token rows, MSE to a
+    N(0, 1) target, mask ratio 1e-2; a step is perturb +/-, two forwards with the MSE
+    read back, g on the host and the masked update."""
+    import numpy as np
+    w = synth.torch_latents(0, C1["d_out"] * C1["d_in"], torch.float32, dev).view(C1["d_out"], C1["d_in"])
+    x = torch.from_numpy(synth.activations(100, C1["tokens"], C1["d_in"])).to(dev)
+    tgt = torch.from_numpy(synth.activations(101, C1["tokens"], C1["d_out"])).to(dev)
+    y = torch.empty((C1["tokens"], C1["d_out"]), device=dev)
+    ctx = termezo.Context([w])
+    k0, _ = ctx.build_mask(C1["rho"])
+    eps32, two = np.float32(C1["eps"]), np.float32(2.0)
+
+    def step(t):
+        f = {}
+        for sign in (1, -1):
+            ctx.perturb(t, C1["eps"], sign)
+            ctx.bitlinear_forward(0, x, y)
+            f[sign] = np.float32(ctx.mse_loss(y, tgt))
+        g = np.float32((f[1] - f[-1]) / (two * eps32))      # projected gradient, fp32
+        ctx.update(float(g), C1["lr"], want_k=False)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.warmup, args.warmup + args.steps):
+        step(t)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    cpu = None if args.no_cpu_baseline else cpu_baseline_c1()
+    out = {"metric": "ZO steps/sec, single BitLinear with MSE loss", "value": 1000.0 / ms,
+           "unit": "steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "int8xternary+f32", "data": "synthetic",
+           "config": {"workload": "termezo_zo_step_bitlinear_256x256_mse", **C1, "k0": k0,
+                      "parallelism": "single_gpu"},
+           "roofline": None,
+           "note": "launch-latency bound (two host read-backs of the loss per step); "
+                   "wall-clock over the timed steps",
+           "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
 
 # ---------------------------------------------------------------------------
 # Kernel sweeps (--sweep): the perturb/requant and update kernels over a
@@ -302,10 +409,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="2b", choices=sorted(CONFIGS))
-    ap.add_argument("--rho", type=float, default=1e-3)
+    ap.add_argument("--config", default="2b", choices=sorted(CONFIGS) + ["c1"],
+                    help="2b (default, config 4), 700m (config 3), tiny (config 2), c1 (config 1)")
+    ap.add_argument("--rho", type=float, default=None, help="mask ratio (default: the config's)")
     ap.add_argument("--eps", type=float, default=1e-3)
-    ap.add_argument("--lr", type=float, default=1e-5)
+    ap.add_argument("--lr", type=float, default=None, help="learning rate (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", choices=["latent", "bitlinear", "all"],
                     help="run the kernel sweeps instead of the step benchmark")
@@ -329,17 +437,26 @@ def main():
         if args.sweep in ("bitlinear", "all"):
             sweep_bitlinear(torch, termezo, synth, dev, not args.no_cpu_baseline)
         return
+    if args.config == "c1":
+        run_c1(args, torch, termezo, synth, dev)
+        return
     c = CONFIGS[args.config]
+    if args.rho is None:
+        args.rho = c["rho"]
+    if args.lr is None:
+        args.lr = c["lr"]
+    fp32 = c.get("fp32", False)
+    adt = torch.float32 if fp32 else torch.bfloat16
     shapes = layer_shapes(c)
     D = sum(o * i for o, i in shapes)
     print(f"[bench] config {args.config}: {len(shapes)} ternary projections, {D} latents", flush=True)
-    lat = synth.torch_latents(1234, D, torch.bfloat16, dev)
+    lat = synth.torch_latents(1234, D, adt, dev)
     layers, off = [], 0
     for o, i in shapes:
         layers.append(lat[off: off + o * i].view(o, i))
         off += o * i
     E = synth.torch_normal(1235, (c["vocab"], c["d_model"]), torch.float32, dev)
-    E = (E * synth.LATENT_STD).to(torch.bfloat16)
+    E = (E * synth.LATENT_STD).to(adt)
     tok = synth.torch_tokens(1236, c["batch"], c["seq"], c["vocab"], dev)
     torch.cuda.synchronize()
 
@@ -405,11 +522,14 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
-        cpu = cpu_baseline(c, args.rho)
+        cpu = cpu_baseline_full(c, args.rho) if args.config == "tiny" else cpu_baseline(c, args.rho)
         print(f"[bench] cpu baseline sample took {time.perf_counter() - t0:.1f} s", flush=True)
 
+    metric = METRIC if args.config == "2b" else {
+        "700m": "ZO steps/sec at the 700M-class decoder shape (24 blocks, d 1536, 16 heads of 96)",
+        "tiny": "ZO steps/sec, tiny decoder (2 blocks, d 256, fp32)"}[args.config]
     out = {
-        "metric": METRIC,
+        "metric": metric,
         "value": 1000.0 / ms_per_step,
         "unit": "steps/s",
         "n_gpus": 1,
@@ -419,9 +539,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int8xternary+bf16",
+        "dtype": "int8xternary+f32" if fp32 else "int8xternary+bf16",
         "data": "synthetic",
-        "config": {"workload": f"termezo_zo_step_bitnet_{args.config}", **c,
+        "config": {"workload": (f"termezo_zo_step_tiny_decoder" if args.config == "tiny"
+                                else f"termezo_zo_step_bitnet_{args.config}"),
+                   **{k: v for k, v in c.items() if k not in ("rho", "lr", "fp32")},
                    "tokens_per_forward": c["batch"] * c["seq"], "latents": D,
                    "mask_ratio": args.rho, "k0": k0, "k_final": k_final, "eps": args.eps,
                    "lr": args.lr, "parallelism": "single_gpu"},
@@ -441,6 +563,8 @@ def main():
         "mask_build_ms": mask_ms,
         "cpu_baseline": cpu,
     }
+    if args.config == "tiny":
+        out["note"] = "launch-latency bound; the roofline figures are those of its tiny GEMMs"
     print(json.dumps(out), flush=True)
     model.close()
     ctx.close()
