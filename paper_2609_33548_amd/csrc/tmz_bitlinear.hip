@@ -232,8 +232,9 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
     }
 #pragma unroll
     for (int j = 0; j < B_WORDS; ++j) {
-      const v4u v = {unpack_group(rb[j], 0), unpack_group(rb[j], 1), unpack_group(rb[j], 2),
-                     unpack_group(rb[j], 3)};
+      uint32_t o[4];
+      unpack_word(rb[j], o);
+      const v4u v = {o[0], o[1], o[2], o[3]};
       *reinterpret_cast<v4u*>(Bs + brow * kLdsStride + 16 * (bw0 + j)) = v;
     }
   };
@@ -334,8 +335,9 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __device__ __forceinline__ int bswz(int row) { return ((row >> 2) ^ (row >> 3)) & 1; }
 
 __device__ __forceinline__ v4i unpack16(uint32_t w) {
-  return v4i{(int)unpack_group(w, 0), (int)unpack_group(w, 1), (int)unpack_group(w, 2),
-             (int)unpack_group(w, 3)};
+  uint32_t o[4];
+  unpack_word(w, o);
+  return v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
 }
 
 constexpr int kDmaBM = 256, kDmaBN = 256;

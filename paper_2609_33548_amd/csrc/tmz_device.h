@@ -190,13 +190,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float v) {
 
 // ---------------------------------------------------------------------------
 // Ternary code and its 2-bit packing.
-// Code values: 0 -> 0b00, +1 -> 0b01, -1 -> 0b11 (two's complement).
+// Code values: 0 -> 0b00, +1 -> 0b01, -1 -> 0b10.
 // A 32-bit word holds 16 codes of one row along d_in; the code at offset
 // j = 4 i + b (i, b in 0..3) sits at bits [8 b + 2 i, 8 b + 2 i + 1], so that
 // (word >> 2i) & 0x03030303 puts codes 4i..4i+3 in the low bits of bytes 0..3.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t ternary_code(float w, float tau) {
-  return w > tau ? 1u : (w < -tau ? 3u : 0u);
+  return w > tau ? 1u : (w < -tau ? 2u : 0u);
 }
 
 __device__ __forceinline__ int code_shift(int j) { return 8 * (j & 3) + 2 * (j >> 2); }
@@ -204,8 +204,21 @@ __device__ __forceinline__ int code_shift(int j) { return 8 * (j & 3) + 2 * (j >
 // Expand the four codes of group i (offsets 4i..4i+3) to four int8 lanes.
 __device__ __forceinline__ uint32_t unpack_group(uint32_t word, int i) {
   const uint32_t sel = (word >> (2 * i)) & 0x03030303u;
-  // byte selector 0 -> 0x00, 1 -> 0x01, 2 -> 0xFF, 3 -> 0xFF
+  // byte selector 0 -> 0x00, 1 -> 0x01, 2 -> 0xFF
   return __builtin_amdgcn_perm(0u, 0xFFFF0100u, sel);
+}
+
+// All 16 codes of a word as four int8 lanes of four (offsets 0..15) with one
+// shift: groups 0 and 2 (bits 0-1 of each byte of w and w >> 4) are byte
+// selectors 0, 1, 2 into 0x00, 0x01, 0xFF; groups 1 and 3 (bits 2-3), masked in
+// place, are selectors 0, 4, 8: byte 0 of the low table (0x00), byte 0 of the
+// high table (0x01) and the sign of the low table's byte 1 (0xFF).
+__device__ __forceinline__ void unpack_word(uint32_t w, uint32_t out[4]) {
+  const uint32_t y = w >> 4;
+  out[0] = __builtin_amdgcn_perm(0u, 0x00FF0100u, w & 0x03030303u);
+  out[1] = __builtin_amdgcn_perm(0x01u, 0x00008000u, w & 0x0C0C0C0Cu);
+  out[2] = __builtin_amdgcn_perm(0u, 0x00FF0100u, y & 0x03030303u);
+  out[3] = __builtin_amdgcn_perm(0x01u, 0x00008000u, y & 0x0C0C0C0Cu);
 }
 
 // Block order: consecutive workgroups are dealt round-robin to the 8 XCDs

@@ -907,7 +907,7 @@ __global__ void k_unpack(const uint32_t* codes, int64_t n, int8_t* out) {
        i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t word = codes[i / 16];
     const uint32_t c = (word >> code_shift((int)(i & 15))) & 3u;
-    out[i] = c == 1u ? 1 : (c == 3u ? -1 : 0);
+    out[i] = c == 1u ? 1 : (c == 2u ? -1 : 0);
   }
 }
 
