@@ -822,14 +822,16 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
     }
   }
   const int64_t big_blocks = ((M + 255) / 256) * ((N + 255) / 256);
-  if (big_blocks >= 256) {
-    bool seg32 = true;
-    for (int i = 1; i < out.nseg; ++i) seg32 = seg32 && out.nstart[i] % 32 == 0;
-    const uintptr_t vec = ydt == TERMEZO_F32 ? 16 : 8;   // 4-element store width
-    for (int i = 0; i < out.nseg; ++i)
-      seg32 = seg32 && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
-    if (M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32) {
-      const int64_t T = big_blocks, full = dma_full_tiles(T, n_cu);
+  bool seg32 = true;
+  for (int i = 1; i < out.nseg; ++i) seg32 = seg32 && out.nstart[i] % 32 == 0;
+  const uintptr_t vec = ydt == TERMEZO_F32 ? 16 : 8;   // 4-element store width
+  for (int i = 0; i < out.nseg; ++i)
+    seg32 = seg32 && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
+  const bool dma = M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32;
+  if (big_blocks >= 256 || (dma && n_cu > 0)) {
+    if (dma) {
+      // fewer full tiles than compute units: every tile as four 128 x 128 quarters
+      const int64_t T = big_blocks, full = T < n_cu ? 0 : dma_full_tiles(T, n_cu);
       dim3 grid((unsigned)(full + 4 * (T - full)));
       if (ydt == TERMEZO_F32) {
         if (mode == kGemmStore)
