@@ -145,6 +145,23 @@ __device__ __forceinline__ void store4(uint16_t* p, const float v[4]) {
   const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, c) | ((uint32_t)__builtin_bit_cast(uint16_t, d) << 16);
   *reinterpret_cast<uint2*>(p) = make_uint2(w0, w1);
 }
+// h + y for a 16-byte unit of outputs, rounded to the output type.
+__device__ __forceinline__ v4u add_units(v4u h, v4u y, const float*) {
+  v4u r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r[i] = __float_as_uint(__uint_as_float(h[i]) + __uint_as_float(y[i]));
+  return r;
+}
+__device__ __forceinline__ v4u add_units(v4u h, v4u y, const uint16_t*) {
+  v4u r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const __bf16 lo = (__bf16)(__uint_as_float(h[i] << 16) + __uint_as_float(y[i] << 16));
+    const __bf16 hi = (__bf16)(__uint_as_float(h[i] & 0xFFFF0000u) + __uint_as_float(y[i] & 0xFFFF0000u));
+    r[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+  }
+  return r;
+}
 __device__ __forceinline__ void load4v(const float* p, float v[4]) {
   const float4 a = *reinterpret_cast<const float4*>(p);
   v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
@@ -348,7 +365,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
                                               const uint32_t* __restrict__ codes, int64_t K,
                                               int64_t N, const GemmOut& out, int32_t* acc_out,
                                               int64_t m0, int64_t n0, int8_t* lds,
-                                              const float (*rrow)[kDmaBM]) {
+                                              const float* __restrict__ s, int rows,
+                                              float (*rrow)[kDmaBM]) {
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int AROW = 128;                       // bytes per A row per stage (no pad)
   constexpr int BROW = 32;                        // bytes of packed codes per B row per stage
@@ -459,6 +477,12 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   // prologue: stages 0 and 1 in flight, stage 0 complete before the loop
   issue(0, Ast(0), Bst(0));
   if (nk > 1) issue(1, Ast(1), Bst(1));
+  // per-token output scales beta'/s_m while the first stages load (published to
+  // all waves by the loop's barriers)
+  for (int i = tid; i < kMaxSeg * kDmaBM; i += NW * 64) {
+    const int sg = i / kDmaBM, r = i % kDmaBM;
+    rrow[sg][r] = (sg < out.nseg && r < rows) ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
+  }
   if (nk > 1) wait_vmcnt_le<AJ + 1>(); else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int cur = 0;
@@ -471,76 +495,88 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     cur = cur == 2 ? 0 : cur + 1;
   }
 
-  if constexpr (MODE == kGemmSwiGLU) {
-    // registers 0..7 of a 32-column block p are gate features 16 p + 8 (r / 4) + 4 h + r % 4,
-    // registers 8..15 the up values of the same features
-    const int64_t ld = out.ld[0];
-    const int ml = wm * WM + (lane & 31);
+  // ---- epilogue.  Each wave stages one 32-token slice (MFMA row tile a) of its
+  // outputs row-major in a private LDS region (the ring is free after the last
+  // barrier), then writes whole 16-byte units, so a store instruction covers
+  // 64 / UPR tokens of UPR * 16 contiguous bytes each instead of 32 tokens of 8
+  // bytes.  Unit u of staged row r sits at unit u ^ (r % UPR).  The LDS writes
+  // and reads of one wave need no barrier: a wave's LDS operations are ordered.
+  const int ml = lane & 31;                          // token of the lane (h: register half)
+  constexpr int OW = MODE == kGemmSwiGLU ? WN / 2 : WN;   // outputs per staged row
+  constexpr int UB = 16 / (int)sizeof(TY);                // outputs per 16-byte unit
+  constexpr int UPR = OW / UB;                            // units per staged row
+  constexpr int RB = OW * (int)sizeof(TY);                // bytes per staged row
+  constexpr int RPL = 32 * UPR / 64;                      // units read per lane
+  static_assert(NW * 32 * RB <= 3 * (ASTAGE + BSTAGE) && RPL >= 1 && UPR <= 16, "epilogue staging");
+  int8_t* wl = lds + wid * 32 * RB;
+  auto stage4 = [&](int f, const float v[4]) __attribute__((always_inline)) {
+    // four consecutive outputs f..f+3 of staged row ml
+    const int u = f / UB, off = (f % UB) * (int)sizeof(TY);
+    store4(reinterpret_cast<TY*>(wl + ml * RB + 16 * (u ^ (ml % UPR)) + off), v);
+  };
+  const int64_t fbase = MODE == kGemmSwiGLU ? (n0 + wn * WN) / 2 : n0 + wn * WN;
 #pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      const int64_t f0 = (n0 + wn * WN + b * 32) >> 1;
-      TY* base = reinterpret_cast<TY*>(out.y[0]) + f0 + 4 * (lane >> 5);
+  for (int a = 0; a < TM; ++a) {
+    const int mloc = wm * WM + 32 * a + ml;
+    if constexpr (MODE == kGemmSwiGLU) {
+      // registers 0..7 of a 32-column block p are gate features 16 p + 8 (r / 4) + 4 h + r % 4,
+      // registers 8..15 the up values of the same features
+      const float rg = rrow[0][mloc], ru = rrow[1][mloc];
 #pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        const int mloc = ml + 32 * a;
-        const float rg = rrow[0][mloc], ru = rrow[1][mloc];
-        TY* rowp = base + (m0 + mloc) * ld;
+      for (int b = 0; b < TN; ++b)
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           float v4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const float g = round_act(rowp, (float)acc[a][b][4 * q + j] * rg);
-            const float u = round_act(rowp, (float)acc[a][b][4 * q + 8 + j] * ru);
+            const float g = round_act((TY*)nullptr, (float)acc[a][b][4 * q + j] * rg);
+            const float u = round_act((TY*)nullptr, (float)acc[a][b][4 * q + 8 + j] * ru);
             v4[j] = silu_mul(g, u);
           }
-          store4(rowp + 8 * q, v4);
+          stage4(16 * b + 8 * q + 4 * h, v4);
+        }
+    } else {
+      // acc[a][b] is the transposed 32 x 32 tile: lane column = token, register r =
+      // output 8 (r / 4) + 4 h + (r % 4) of the 32-column block b
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int64_t nb = n0 + wn * WN + b * 32;
+        const int sg = (out.nseg > 2 && nb >= out.nstart[2]) ? 2 : (out.nseg > 1 && nb >= out.nstart[1]) ? 1 : 0;
+        const float rr = rrow[sg][mloc];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v4[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v4[j] = round_act((TY*)nullptr, (float)acc[a][b][4 * q + j] * rr);
+          stage4(32 * b + 8 * q + 4 * h, v4);
+        }
+        if (acc_out) {   // int32 accumulators (parity only), straight from the registers
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              acc_out[(m0 + mloc) * N + nb + 8 * q + 4 * h + j] = acc[a][b][4 * q + j];
         }
       }
     }
-    return;
-  }
-
-  // ---- epilogue (every tile is in bounds).  acc[a][b] is the transposed
-  // 32 x 32 tile: lane column = token m (one scale beta'/s_m per lane),
-  // register r = output feature 8 (r / 4) + 4 (l / 32) + (r % 4), so each group
-  // of 4 registers is 4 consecutive features: one 8-byte (bf16) store.
-  // Segment boundaries are multiples of 32, so a 32-feature tile lies in one
-  // segment.
-  const int ml = wm * WM + (lane & 31);             // local token of tile a = 0
+    // read back whole units and write them to the outputs
 #pragma unroll
-  for (int b = 0; b < TN; ++b) {
-    const int64_t nb = n0 + wn * WN + b * 32;        // first feature of the tile
-    int sg = 0;
-    if (out.nseg > 1 && nb >= out.nstart[1]) sg = 1;
-    if (out.nseg > 2 && nb >= out.nstart[2]) sg = 2;
-    const int64_t ld = out.ld[sg];
-    TY* base = reinterpret_cast<TY*>(out.y[sg]) + (nb - out.nstart[sg]) + 4 * (lane >> 5);
-#pragma unroll
-    for (int a = 0; a < TM; ++a) {
-      const int mloc = ml + 32 * a;
-      const float rr = rrow[sg][mloc];
-      TY* rowp = base + (m0 + mloc) * ld;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v4[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v4[j] = (float)acc[a][b][4 * q + j] * rr;
-        TY* p = rowp + 8 * q;
-        if (MODE == kGemmStore) {
-          store4(p, v4);
-        } else {   // residual: h <- round(h + round(y))
-          float h4[4];
-          load4v(p, h4);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v4[j] = h4[j] + round_act(p, v4[j]);
-          store4(p, v4);
-        }
-        if (acc_out) {
-          const int64_t n = nb + 8 * q + 4 * (lane >> 5);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc_out[(m0 + mloc) * N + n + j] = acc[a][b][4 * q + j];
-        }
+    for (int i = 0; i < RPL; ++i) {
+      const int c = 64 * i + lane, row = c / UPR, u = c % UPR;
+      const v4u v = *reinterpret_cast<const v4u*>(wl + row * RB + 16 * (u ^ (row % UPR)));
+      const int64_t tok = m0 + wm * WM + 32 * a + row;
+      const int64_t f = fbase + (int64_t)u * UB;
+      int sg = 0;
+      if constexpr (MODE != kGemmSwiGLU) {
+        if (out.nseg > 1 && f >= out.nstart[1]) sg = 1;
+        if (out.nseg > 2 && f >= out.nstart[2]) sg = 2;
+      }
+      TY* p = reinterpret_cast<TY*>(out.y[sg]) + tok * out.ld[sg] + (f - out.nstart[sg]);
+      if (MODE == kGemmResidual) {   // h <- round(h + y), y already rounded
+        const v4u hv = *reinterpret_cast<const v4u*>(p);
+        *reinterpret_cast<v4u*>(p) = add_units(hv, v, (TY*)nullptr);
+      } else {
+        *reinterpret_cast<v4u*>(p) = v;
       }
     }
   }
@@ -570,15 +606,10 @@ __global__ void __launch_bounds__(512)
   tile_of_linear(t, nb_m, nb_n, tm, tn);
   const int64_t m0 = tm * kDmaBM + (quarter ? 128 * (q >> 1) : 0);
   const int64_t n0 = tn * kDmaBN + (quarter ? 128 * (q & 1) : 0);
-  const int rows = quarter ? 128 : kDmaBM;
-  for (int i = threadIdx.x; i < kMaxSeg * kDmaBM; i += 512) {
-    const int sg = i / kDmaBM, r = i % kDmaBM;
-    rrow[sg][r] = (sg < out.nseg && r < rows) ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
-  }
   if (!quarter)
-    gemm_tile_dma<256, 256, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, rrow);
+    gemm_tile_dma<256, 256, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, s, 256, rrow);
   else
-    gemm_tile_dma<128, 128, 64, 32, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, rrow);
+    gemm_tile_dma<128, 128, 64, 32, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, s, 128, rrow);
 }
 
 // ---------------------------------------------------------------------------
@@ -789,7 +820,7 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
                           int32_t* acc, int n_cu, hipStream_t st) {
   if (mode == kGemmSwiGLU) {
     if (!gemm_swiglu_ok(M, K, N, ydt) || out.nseg != 2 || out.nstart[1] * 2 != N || acc ||
-        out.ld[0] % 4 != 0 || reinterpret_cast<uintptr_t>(out.y[0]) % 8 != 0)
+        out.ld[0] % 8 != 0 || reinterpret_cast<uintptr_t>(out.y[0]) % 16 != 0)
       return hipErrorInvalidValue;
     const int64_t T = (M / kDmaBM) * (N / kDmaBN), full = dma_full_tiles(T, n_cu);
     hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU>), dim3((unsigned)(full + 4 * (T - full))),
@@ -824,9 +855,9 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
   const int64_t big_blocks = ((M + 255) / 256) * ((N + 255) / 256);
   bool seg32 = true;
   for (int i = 1; i < out.nseg; ++i) seg32 = seg32 && out.nstart[i] % 32 == 0;
-  const uintptr_t vec = ydt == TERMEZO_F32 ? 16 : 8;   // 4-element store width
+  const int64_t ue = ydt == TERMEZO_F32 ? 4 : 8;       // outputs per 16-byte unit
   for (int i = 0; i < out.nseg; ++i)
-    seg32 = seg32 && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
+    seg32 = seg32 && out.ld[i] % ue == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % 16 == 0;
   const bool dma = M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32;
   if (big_blocks >= 256 || (dma && n_cu > 0)) {
     if (dma) {

@@ -146,25 +146,27 @@ def test_bitlinear_matches_oracle(orc, M, K, N, xdt, ydt):
     assert np.array_equal(y.float().cpu().numpy(), ry)
 
 
-@pytest.mark.parametrize("M,K,N", [(8192, 2560, 2560),   # 320 tiles: last 64 cut in quarters
-                                   (8192, 1024, 2816),   # 352 tiles: last 96 cut in quarters
-                                   (8192, 2560, 3840),   # 480 tiles: whole tiles only
-                                   (8232, 2560, 2560),   # ragged M on the large-tile path
-                                   (8192, 688, 8192),    # K not a multiple of the K step
-                                   (4096, 6912, 4352)])  # 272 tiles: last 16 cut in quarters
-def test_bitlinear_large_grid_sampled_rows(orc, M, K, N):
+@pytest.mark.parametrize("M,K,N,ydt", [(8192, 2560, 2560, "bf16"),   # 320 tiles: last 64 cut in quarters
+                                       (8192, 1024, 2816, "bf16"),   # 352 tiles: last 96 cut in quarters
+                                       (8192, 2560, 3840, "bf16"),   # 480 tiles: whole tiles only
+                                       (8232, 2560, 2560, "bf16"),   # ragged M on the large-tile path
+                                       (8192, 688, 8192, "bf16"),    # K not a multiple of the K step
+                                       (4096, 6912, 4352, "bf16"),   # 272 tiles: last 16 cut in quarters
+                                       (8192, 2560, 2560, "f32"),    # fp32 outputs, whole and quarter tiles
+                                       (512, 256, 512, "f32")])      # 4 tiles: quarters only
+def test_bitlinear_large_grid_sampled_rows(orc, M, K, N, ydt):
     """Launch sizes that select the large-tile kernels (with and without the
     quarter-tile tail); the oracle evaluates a sample of rows (rows are
     independent), including the first and last and a band of the last quarter
     of rows, where the tail tiles lie.  Two calls in a row with new inputs."""
     torch = _torch()
-    print(f"bitlinear large M={M} K={K} N={N}", flush=True)
+    print(f"bitlinear large M={M} K={K} N={N} y={ydt}", flush=True)
     ref, ctx, _ = _setup(orc, [(N, K)], bf16=True, seed=8)
     ctx.build_mask(0.001)
     ref.build_mask(0.001)
     ctx.perturb(21, 1e-3, -1)
     codes, _, betas = ref.perturb(21, 1e-3, -1)
-    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    y = torch.empty((M, N), dtype=torch.bfloat16 if ydt == "bf16" else torch.float32, device="cuda")
     acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
     xq = torch.empty((M, K), dtype=torch.int8, device="cuda")
     s = torch.empty(M, dtype=torch.float32, device="cuda")
@@ -181,7 +183,7 @@ def test_bitlinear_large_grid_sampled_rows(orc, M, K, N):
         assert np.array_equal(xq.cpu().numpy()[rows], rxq)
         assert np.array_equal(s.cpu().numpy()[rows], rs)
         assert np.array_equal(acc.cpu().numpy()[rows], racc)
-        assert np.array_equal(y.float().cpu().numpy()[rows], orc.bf16_round(ry))
+        assert np.array_equal(y.float().cpu().numpy()[rows], orc.bf16_round(ry) if ydt == "bf16" else ry)
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
