@@ -375,8 +375,10 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   constexpr int NW = (BM / WM) * (BN / WN);       // waves per block
   constexpr int AJ = BM / (8 * NW);               // A loads per wave per stage
   constexpr int BW = BN / 32 < NW ? BN / 32 : NW; // waves holding distinct B rows
-  static_assert(AJ >= 1 && BM % (8 * NW) == 0 && BN / 32 <= NW && 3 * (ASTAGE + BSTAGE) <= kDmaLds,
-                "tile");
+  constexpr int BJ = BN / 32 > NW ? BN / (32 * NW) : 1;   // B loads per wave per stage
+  constexpr int DJ = AJ + BJ;                     // direct loads per wave per stage
+  static_assert(AJ >= 1 && BM % (8 * NW) == 0 && (BN / 32 <= NW || BN % (32 * NW) == 0) &&
+                    DJ < 16, "tile");
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
@@ -385,8 +387,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
 
   // Per-lane global sources.  A: wave w fills 1 KB chunks AJ w .. AJ w + AJ-1
   // (8 rows each); lane i -> row 8 j + i / 8, physical chunk i % 8.  B: wave
-  // w fills rows 32 (w % BW) .. + 31, two lanes (physical halves) per row
-  // (with BW < NW several waves write the same bytes).
+  // w fills the 32-row blocks BJ (w % BW) .. + BJ-1, two lanes (physical halves)
+  // per row (with BW < NW several waves write the same bytes).
   const int8_t* asrc[AJ];
 #pragma unroll
   for (int j = 0; j < AJ; ++j) {
@@ -395,15 +397,19 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     asrc[j] = xq + (m0 + row) * K + 16 * chunk;
   }
   const int bw = wid % BW;
-  const int brow_l = 32 * bw + (lane >> 1);
-  int64_t crow = n0 + brow_l;                     // code row of tile row brow_l
-  if constexpr (MODE == kGemmSwiGLU) {
-    // column 32 p + c holds gate row 16 p + c (c < 16) or up row F + 16 p + c - 16, so a
-    // lane's accumulator registers r and r + 8 are the gate and up value of one feature
-    const int64_t p = crow >> 5, c = crow & 31;
-    crow = c < 16 ? 16 * p + c : (N >> 1) + 16 * p + (c - 16);
+  const uint32_t* bsrc[BJ];
+#pragma unroll
+  for (int j = 0; j < BJ; ++j) {
+    const int brow_l = 32 * (BJ * bw + j) + (lane >> 1);
+    int64_t crow = n0 + brow_l;                   // code row of tile row brow_l
+    if constexpr (MODE == kGemmSwiGLU) {
+      // column 32 p + c holds gate row 16 p + c (c < 16) or up row F + 16 p + c - 16, so a
+      // lane's accumulator registers r and r + 8 are the gate and up value of one feature
+      const int64_t p = crow >> 5, c = crow & 31;
+      crow = c < 16 ? 16 * p + c : (N >> 1) + 16 * p + (c - 16);
+    }
+    bsrc[j] = codes + crow * KW + 4 * ((lane & 1) ^ bswz(brow_l));
   }
-  const uint32_t* bsrc = codes + crow * KW + 4 * ((lane & 1) ^ bswz(brow_l));
 
   const uint32_t wa = __builtin_amdgcn_readfirstlane(wid);   // wave-uniform
   const uint32_t wb = __builtin_amdgcn_readfirstlane(bw);
@@ -412,7 +418,9 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     const uint32_t abase = lds_offset(Ad) + 1024u * AJ * wa;
 #pragma unroll
     for (int j = 0; j < AJ; ++j) dma16(asrc[j] + koff, abase + 1024u * j);
-    dma16(bsrc + koff / 16, lds_offset(Bd) + 1024u * wb);
+    const uint32_t bbase = lds_offset(Bd) + 1024u * BJ * wb;
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) dma16(bsrc[j] + koff / 16, bbase + 1024u * j);
   };
 
   v16i acc[TM][TN];
@@ -483,14 +491,14 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     const int sg = i / kDmaBM, r = i % kDmaBM;
     rrow[sg][r] = (sg < out.nseg && r < rows) ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
   }
-  if (nk > 1) wait_vmcnt_le<AJ + 1>(); else __builtin_amdgcn_s_waitcnt(0);
+  if (nk > 1) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int cur = 0;
   for (int kt = 0; kt < nk; ++kt) {
     const int nxt2 = cur == 0 ? 2 : cur - 1;     // (kt + 2) % 3
     if (kt + 2 < nk) issue(kt + 2, Ast(nxt2), Bst(nxt2));
     compute(Ast(cur), Bst(cur));
-    if (kt + 2 < nk) wait_vmcnt_le<AJ + 1>(); else __builtin_amdgcn_s_waitcnt(0);
+    if (kt + 2 < nk) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     cur = cur == 2 ? 0 : cur + 1;
   }
@@ -515,9 +523,36 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     store4(reinterpret_cast<TY*>(wl + ml * RB + 16 * (u ^ (ml % UPR)) + off), v);
   };
   const int64_t fbase = MODE == kGemmSwiGLU ? (n0 + wn * WN) / 2 : n0 + wn * WN;
+  // output unit i (of RPL) of slice a of this lane
+  auto unit_ptr = [&](int a, int i) __attribute__((always_inline)) {
+    const int c = 64 * i + lane, row = c / UPR, u = c % UPR;
+    const int64_t tok = m0 + wm * WM + 32 * a + row;
+    const int64_t f = fbase + (int64_t)u * UB;
+    int sg = 0;
+    if constexpr (MODE != kGemmSwiGLU) {
+      if (out.nseg > 1 && f >= out.nstart[1]) sg = 1;
+      if (out.nseg > 2 && f >= out.nstart[2]) sg = 2;
+    }
+    return reinterpret_cast<v4u*>(reinterpret_cast<TY*>(out.y[sg]) + tok * out.ld[sg] +
+                                  (f - out.nstart[sg]));
+  };
+  // residual inputs: all of a lane's units loaded up front (at most 16 units, else
+  // one slice at a time) so their latency overlaps the staging
+  constexpr int HPRE = MODE == kGemmResidual ? (TM * RPL <= 16 ? TM : 1) : 0;
+  v4u hin[HPRE > 0 ? HPRE : 1][RPL];
+  if constexpr (HPRE == TM) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int i = 0; i < RPL; ++i) hin[a][i] = *unit_ptr(a, i);
+  }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
     const int mloc = wm * WM + 32 * a + ml;
+    if constexpr (HPRE == 1) {
+#pragma unroll
+      for (int i = 0; i < RPL; ++i) hin[0][i] = *unit_ptr(a, i);
+    }
     if constexpr (MODE == kGemmSwiGLU) {
       // registers 0..7 of a 32-column block p are gate features 16 p + 8 (r / 4) + 4 h + r % 4,
       // registers 8..15 the up values of the same features
@@ -564,20 +599,11 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     for (int i = 0; i < RPL; ++i) {
       const int c = 64 * i + lane, row = c / UPR, u = c % UPR;
       const v4u v = *reinterpret_cast<const v4u*>(wl + row * RB + 16 * (u ^ (row % UPR)));
-      const int64_t tok = m0 + wm * WM + 32 * a + row;
-      const int64_t f = fbase + (int64_t)u * UB;
-      int sg = 0;
-      if constexpr (MODE != kGemmSwiGLU) {
-        if (out.nseg > 1 && f >= out.nstart[1]) sg = 1;
-        if (out.nseg > 2 && f >= out.nstart[2]) sg = 2;
-      }
-      TY* p = reinterpret_cast<TY*>(out.y[sg]) + tok * out.ld[sg] + (f - out.nstart[sg]);
-      if (MODE == kGemmResidual) {   // h <- round(h + y), y already rounded
-        const v4u hv = *reinterpret_cast<const v4u*>(p);
-        *reinterpret_cast<v4u*>(p) = add_units(hv, v, (TY*)nullptr);
-      } else {
-        *reinterpret_cast<v4u*>(p) = v;
-      }
+      v4u* p = unit_ptr(a, i);
+      if constexpr (MODE == kGemmResidual)   // h <- round(h + y), y already rounded
+        *p = add_units(hin[HPRE == TM ? a : 0][i], v, (TY*)nullptr);
+      else
+        *p = v;
     }
   }
 }
@@ -610,6 +636,26 @@ __global__ void __launch_bounds__(512)
     gemm_tile_dma<256, 256, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, s, 256, rrow);
   else
     gemm_tile_dma<128, 128, 64, 32, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, s, 128, rrow);
+}
+
+// Two blocks per compute unit: 128 x 256 tiles of 4 waves (128 x 64 per wave, the
+// same per-wave work as the 256 x 256 tile) with a 72 KB ring, so that one
+// block's barriers, prologue and epilogue overlap the other block's MFMAs and a
+// block left alone on a compute unit at the end of the grid runs at its full rate.
+constexpr int kHalfBM = 128, kHalfBN = 256;
+constexpr int kHalfLds = 3 * (kHalfBM * 128 + kHalfBN * 32);
+
+template <typename TY, int MODE>
+__global__ void __launch_bounds__(256, 2)
+    k_gemm_i8_dma_h(const int8_t* __restrict__ xq, const float* __restrict__ s,
+                    const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+                    int32_t* __restrict__ acc_out) {
+  __shared__ __attribute__((aligned(1024))) int8_t lds[kHalfLds];
+  __shared__ float rrow[kMaxSeg][kDmaBM];
+  int64_t tm, tn;
+  tile_of_block(M / kHalfBM, N / kHalfBN, tm, tn);
+  gemm_tile_dma<kHalfBM, kHalfBN, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, tm * kHalfBM,
+                                                     tn * kHalfBN, lds, s, kHalfBM, rrow);
 }
 
 // ---------------------------------------------------------------------------
@@ -804,6 +850,14 @@ bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt) {
          K > 0;
 }
 
+// Two blocks per compute unit (128 x 256 tiles) measured faster than the 256 x 256
+// grid with a quarter-tile tail when the 256 x 256 grid is below one round of compute
+// units (M = 2048: 1.2-1.4x) or spans at least three rounds (gate|up at the 2B shape:
+// 1.04-1.07x), and slower in between (1.25 and 1.9 rounds: 0.9x).
+static bool use_half_tiles(int64_t M, int64_t T, int n_cu) {
+  return n_cu > 0 && M % kHalfBM == 0 && (T < n_cu || T >= 3 * (int64_t)n_cu);
+}
+
 // Launch plan of the full-tile path: blocks [0, full) take 256 x 256 tiles, the rest take
 // quarters of the remaining ones.
 static int64_t dma_full_tiles(int64_t T, int n_cu) {
@@ -823,8 +877,12 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
         out.ld[0] % 8 != 0 || reinterpret_cast<uintptr_t>(out.y[0]) % 16 != 0)
       return hipErrorInvalidValue;
     const int64_t T = (M / kDmaBM) * (N / kDmaBN), full = dma_full_tiles(T, n_cu);
-    hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU>), dim3((unsigned)(full + 4 * (T - full))),
-                       dim3(512), 0, st, xq, s, codes, M, K, N, out, full, acc);
+    if (use_half_tiles(M, T, n_cu))
+      hipLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)(2 * T)), dim3(256),
+                         0, st, xq, s, codes, M, K, N, out, acc);
+    else
+      hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU>), dim3((unsigned)(full + 4 * (T - full))),
+                         dim3(512), 0, st, xq, s, codes, M, K, N, out, full, acc);
     return hipGetLastError();
   }
   if (M <= kGemvMaxM) {
@@ -861,8 +919,21 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
   const bool dma = M % 256 == 0 && N % 256 == 0 && K % kBK == 0 && seg32;
   if (big_blocks >= 256 || (dma && n_cu > 0)) {
     if (dma) {
+      const int64_t T = big_blocks;
+      if (use_half_tiles(M, T, n_cu)) {
+        dim3 gh((unsigned)(2 * T));
+#define TMZ_HALF(TY, MD) \
+  hipLaunchKernelGGL((k_gemm_i8_dma_h<TY, MD>), gh, dim3(256), 0, st, xq, s, codes, M, K, N, out, acc)
+        if (ydt == TERMEZO_F32) {
+          if (mode == kGemmStore) TMZ_HALF(float, kGemmStore); else TMZ_HALF(float, kGemmResidual);
+        } else {
+          if (mode == kGemmStore) TMZ_HALF(uint16_t, kGemmStore); else TMZ_HALF(uint16_t, kGemmResidual);
+        }
+#undef TMZ_HALF
+        return hipGetLastError();
+      }
       // fewer full tiles than compute units: every tile as four 128 x 128 quarters
-      const int64_t T = big_blocks, full = T < n_cu ? 0 : dma_full_tiles(T, n_cu);
+      const int64_t full = T < n_cu ? 0 : dma_full_tiles(T, n_cu);
       dim3 grid((unsigned)(full + 4 * (T - full)));
       if (ydt == TERMEZO_F32) {
         if (mode == kGemmStore)

@@ -153,7 +153,9 @@ def test_bitlinear_matches_oracle(orc, M, K, N, xdt, ydt):
                                        (8192, 688, 8192, "bf16"),    # K not a multiple of the K step
                                        (4096, 6912, 4352, "bf16"),   # 272 tiles: last 16 cut in quarters
                                        (8192, 2560, 2560, "f32"),    # fp32 outputs, whole and quarter tiles
-                                       (512, 256, 512, "f32")])      # 4 tiles: quarters only
+                                       (512, 256, 512, "f32"),       # 4 tiles: two 128 x 256 blocks per CU
+                                       (2048, 2560, 6912, "bf16"),   # 216 tiles: two blocks per CU
+                                       (8192, 2560, 6912, "bf16")])  # 864 tiles: two blocks per CU
 def test_bitlinear_large_grid_sampled_rows(orc, M, K, N, ydt):
     """Launch sizes that select the large-tile kernels (with and without the
     quarter-tile tail); the oracle evaluates a sample of rows (rows are
