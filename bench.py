@@ -339,6 +339,32 @@ def cpu_bitlinear(M, K, N, seed=0):
     return (time.perf_counter() - t0) * M / m
 
 
+def vendor_int8_gemm(torch, dev, M, K, N):
+    """Context only, not part of the path: the vendor library's dense int8 GEMM
+    (hipBLASLt through torch._int_mm) on int8 operands of the same shape, the
+    weights as a dense int8 ternary matrix (one byte per weight, no unpacking),
+    timed the same way (10 back-to-back calls after 2 untimed ones)."""
+    try:
+        g = torch.Generator(device=dev)
+        g.manual_seed(7)
+        a = torch.randint(-127, 128, (M, K), dtype=torch.int8, device=dev, generator=g)
+        w = torch.randint(-1, 2, (N, K), dtype=torch.int8, device=dev, generator=g)
+        b = w.t()                              # [K, N] view of the row-major weights
+        for _ in range(2):
+            torch._int_mm(a, b)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            torch._int_mm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) * 1e-3 / 10
+    except RuntimeError as ex:                 # library call unavailable for this shape
+        return {"library": "hipBLASLt via torch._int_mm", "error": str(ex)[:120]}
+    return {"library": "hipBLASLt via torch._int_mm", "operands": "int8 x int8, no quantisation",
+            "us": t * 1e6, "TOP/s": 2.0 * M * K * N / t / 1e12}
+
+
 def sweep_bitlinear(torch, termezo, synth, dev, cpu):
     for K, N in SWEEP_GEMM_KN:
         code_bytes = N * K // 4
@@ -385,6 +411,7 @@ def sweep_bitlinear(torch, termezo, synth, dev, cpu):
             t = ev0.elapsed_time(ev1) * 1e-3 / calls
             ops = 2.0 * M * K * N
             byts = K * N / 4 + M * K + 4 * M + 2 * M * N
+            vendor = vendor_int8_gemm(torch, dev, M, K, N) if M > 128 else None
             c = None
             if cpu:
                 tc = cpu_bitlinear(M, K, N)
@@ -397,7 +424,7 @@ def sweep_bitlinear(torch, termezo, synth, dev, cpu):
                    "protocol": (f"graph over {L} code buffers ({L * code_bytes >> 20} MiB), "
                                 "activation quantisation included") if M <= 128 else
                                "10 back-to-back calls, activation quantisation included",
-                   "cpu_baseline": c})
+                   "vendor_int8_gemm": vendor, "cpu_baseline": c})
         ctx.close()
         del lat, layers
         torch.cuda.empty_cache()
@@ -548,8 +575,8 @@ def main():
                    "mask_ratio": args.rho, "k0": k0, "k_final": k_final, "eps": args.eps,
                    "lr": args.lr, "parallelism": "single_gpu"},
         "roofline": {"bound": "mfma",
-                     "kernel": "k_gemm_i8_dma (BitLinear int8 x ternary GEMM, all four "
-                               "projections of a block)",
+                     "kernel": "k_gemm_i8_dma + k_gemm_i8_dma_h (BitLinear int8 x ternary "
+                               "GEMM, all four projections of a block)",
                      "achieved": gemm_tops, "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                      "frac": gemm_tops / PEAK_INT8_TOPS, "traffic": measured_traffic(),
                      "traffic_unit": "HBM bytes per launch",
