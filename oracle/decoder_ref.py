@@ -3,12 +3,15 @@
 The paper fixes the BitNet structure only in outline (Sec. 3): every linear
 projection of a transformer block (q, k, v, o and the MLP linears) is a ternary
 BitLinear with 8-bit activations, while the embeddings, the normalisation
-layers and the LM head stay in full precision (theta, frozen here).  The
+layers and the LM head stay in full precision (theta: frozen, or perturbed and
+updated by the caller, which passes the values to evaluate).  The
 objective is the batch mean of the per-sample loss (eq. objective_est); for
 supervised fine-tuning that is next-token cross-entropy.  The remaining details
 are readings (the paper is silent on them):
 
-  * pre-norm blocks with RMSNorm (eps 1e-5, unit weights);
+  * pre-norm blocks with RMSNorm (eps 1e-5; weights one unless given: row
+    2 b scales the attention input of block b, row 2 b + 1 the MLP input, the
+    last row the LM-head input);
   * rotary position embedding, base 10000, on (i, i + head_dim/2) pairs;
   * causal grouped-query attention with softmax scale 1/sqrt(head_dim);
   * SwiGLU MLP: down( silu(gate x) * up x );
@@ -63,11 +66,14 @@ def store(x: np.ndarray, bf16: bool) -> np.ndarray:
     return orc.bf16_round(x) if bf16 else x
 
 
-def rmsnorm(h: np.ndarray, eps: float) -> np.ndarray:
-    """h / sqrt(mean(h^2) + eps), unit weights; fp32 result."""
+def rmsnorm(h: np.ndarray, eps: float, weight: Optional[np.ndarray] = None) -> np.ndarray:
+    """weight * h / sqrt(mean(h^2) + eps) (weight one when None); fp32 result."""
     h64 = h.astype(np.float64)
     r = 1.0 / np.sqrt(np.mean(h64 * h64, axis=-1, keepdims=True) + eps)
-    return (h64 * r).astype(np.float32)
+    y = h64 * r
+    if weight is not None:
+        y = y * weight.astype(np.float64)
+    return y.astype(np.float32)
 
 
 def rope(x: np.ndarray, pos: np.ndarray, n_heads: int, head_dim: int, base: float) -> np.ndarray:
@@ -117,11 +123,14 @@ def bitlinear_fp32_in(x32: np.ndarray, codes: np.ndarray, beta: float) -> np.nda
 
 
 def forward_row_losses(cfg: DecoderConfig, emb: np.ndarray, tokens: np.ndarray,
-                       codes: Sequence[np.ndarray], betas: Sequence[float]) -> np.ndarray:
+                       codes: Sequence[np.ndarray], betas: Sequence[float],
+                       norm_w: Optional[np.ndarray] = None) -> np.ndarray:
     """Per-position cross-entropy [B, S] (position S-1 has no label: 0).
 
     emb: [V, d] fp32 values (bf16 values when cfg.bf16); tokens: [B, S];
-    codes/betas: ternary codes and scales of the 7 * n_blocks projections."""
+    codes/betas: ternary codes and scales of the 7 * n_blocks projections;
+    norm_w: RMSNorm weights [2 n_blocks + 1, d] (None: one)."""
+    nw = (lambda i: None) if norm_w is None else (lambda i: norm_w.reshape(-1, cfg.d_model)[i])
     B, S = tokens.shape
     d, Hq, Hkv, hd = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
     bf = cfg.bf16
@@ -131,7 +140,7 @@ def forward_row_losses(cfg: DecoderConfig, emb: np.ndarray, tokens: np.ndarray,
     for blk in range(cfg.n_blocks):
         c = codes[7 * blk: 7 * blk + 7]
         be = betas[7 * blk: 7 * blk + 7]
-        x = rmsnorm(h, cfg.norm_eps)
+        x = rmsnorm(h, cfg.norm_eps, nw(2 * blk))
         q = store(bitlinear_fp32_in(x, c[0], be[0]), bf)
         k = store(bitlinear_fp32_in(x, c[1], be[1]), bf)
         v = store(bitlinear_fp32_in(x, c[2], be[2]), bf)
@@ -140,13 +149,13 @@ def forward_row_losses(cfg: DecoderConfig, emb: np.ndarray, tokens: np.ndarray,
         a = store(attention(q, k, v, B, S, Hq, Hkv, hd), bf)
         o = store(bitlinear_fp32_in(a, c[3], be[3]), bf)
         h = store(h.astype(np.float64) + o, bf)
-        x = rmsnorm(h, cfg.norm_eps)
+        x = rmsnorm(h, cfg.norm_eps, nw(2 * blk + 1))
         g = store(bitlinear_fp32_in(x, c[4], be[4]), bf)
         u = store(bitlinear_fp32_in(x, c[5], be[5]), bf)
         m = store(silu_mul(g, u), bf)
         dn = store(bitlinear_fp32_in(m, c[6], be[6]), bf)
         h = store(h.astype(np.float64) + dn, bf)
-    xf = store(rmsnorm(h, cfg.norm_eps), bf)
+    xf = store(rmsnorm(h, cfg.norm_eps, nw(2 * cfg.n_blocks)), bf)
     logits = xf.astype(np.float64) @ emb.astype(np.float64).T          # [M, V]
     lab = np.zeros((B, S), np.int64)
     lab[:, :-1] = tokens[:, 1:]

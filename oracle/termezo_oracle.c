@@ -2,8 +2,9 @@
  * TerMeZO CPU oracle -- TEST INFRASTRUCTURE ONLY.
  *
  * A plain, slow, obviously-correct CPU statement of what the TerMeZO sparse
- * zeroth-order step computes (Algorithm 1 of the paper, K = 1, full-precision
- * parameters frozen).  Only the test-suite, the smoke check and the bench's
+ * zeroth-order step computes (Algorithm 1 of the paper, K = 1; the
+ * full-precision parameters theta either frozen or perturbed and updated with
+ * the latents).  Only the test-suite, the smoke check and the bench's
  * CPU baseline may load this library; the product path never does.  It shares
  * no code, header, table or helper with the HIP library.
  *
@@ -406,4 +407,34 @@ int64_t orc_shrink_layer(const float* w, int64_t* act, int64_t k, float tau, flo
     if (d <= xi0) act[n++] = i;
   }
   return n;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Full-precision parameters theta (Sec. 3: embeddings, norms, LM head),     */
+/* perturbed and updated densely with the latents (Algorithm 1): from the    */
+/* same seed, z_theta is drawn on Philox stream 1 at theta ids tid0 + i      */
+/* (tensors enumerated in registration order).  The perturbed values are     */
+/* materialised in the storage type for the forward pass:                    */
+/*   theta'_i = rnd(fma(sign * eps, z_i, theta_i));                          */
+/* the update is theta_i <- rnd(fma(-(lr g), z_i, theta_i)), with rnd the    */
+/* round-to-nearest-even bf16 conversion for bf16 storage, else identity.    */
+/* ------------------------------------------------------------------------ */
+void orc_theta_perturbed(const float* theta, int64_t n, int64_t tid0, uint64_t seed,
+                         float eps, int sign, int bf16_storage, float* out) {
+  float se = (float)sign * eps;
+  for (int64_t i = 0; i < n; ++i) {
+    float z = orc_gauss_one(seed, 1u, (uint64_t)(tid0 + i));
+    float v = fmaf(se, z, theta[i]);
+    out[i] = bf16_storage ? orc_round_bf16(v) : v;
+  }
+}
+
+void orc_theta_update(float* theta, int64_t n, int64_t tid0, uint64_t seed, float lr, float g,
+                      int bf16_storage) {
+  float a = -(lr * g);
+  for (int64_t i = 0; i < n; ++i) {
+    float z = orc_gauss_one(seed, 1u, (uint64_t)(tid0 + i));
+    float v = fmaf(a, z, theta[i]);
+    theta[i] = bf16_storage ? orc_round_bf16(v) : v;
+  }
 }

@@ -1,7 +1,8 @@
 """TerMeZO CPU oracle -- TEST INFRASTRUCTURE ONLY.
 
 Plain, slow, obviously-correct statement of the TerMeZO sparse zeroth-order
-step (Algorithm 1 with K = 1 and the full-precision parameters theta frozen),
+step (Algorithm 1 with K = 1; the full-precision parameters theta frozen or,
+when given, perturbed and updated densely with the masked latents),
 composed from the C primitives in ``termezo_oracle.c``.  Only ``tests/``,
 ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
 this module.  It shares no code with the HIP library.
@@ -14,7 +15,10 @@ Step by step (paper section in brackets):
   * perturbed evaluation at w +/- eps m (.) z, with z regenerated from
     the seed, requantised with the perturbed layer's own threshold    [Algorithm 1]
   * BitLinear: per-token absmax int8 activations x ternary codes     [Sec. 1, Sec. 3]
-  * g = (F+ - F-) / (2 eps); w <- w - lr g m (.) z                   [eq. spsa, Algorithm 1]
+  * theta' = rnd(theta + sign eps z_theta), z_theta from the same seed
+    (Philox stream 1, theta ids in registration order)               [Algorithm 1]
+  * g = (F+ - F-) / (2 eps); w <- w - lr g m (.) z;
+    theta <- rnd(theta - lr g z_theta)                                [eq. spsa, Algorithm 1]
   * S_{t+1} = {i in S_t : d_i(w_{t+1}) <= xi_0}                      [eq. selection_]
 """
 from __future__ import annotations
@@ -66,6 +70,8 @@ def lib():
         "orc_bf16_round_array": (None, [P, i64, P]),
         "orc_update_layer": (None, [P, P, i64, i64, u64, f32, f32, i32]),
         "orc_shrink_layer": (i64, [P, P, i64, f32, f32]),
+        "orc_theta_perturbed": (None, [P, i64, i64, u64, f32, i32, i32, P]),
+        "orc_theta_update": (None, [P, i64, i64, u64, f32, f32, i32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -208,6 +214,25 @@ def updated_layer_values(w: np.ndarray, act, gid0: int, seed: int, lr: float, g:
     return w
 
 
+def theta_perturbed(theta: np.ndarray, tid0: int, seed: int, eps: float, sign: int,
+                    bf16: bool) -> np.ndarray:
+    """theta'_i = rnd(fma(sign eps, z_i, theta_i)) with z on Philox stream 1 at ids tid0 + i."""
+    theta = _f32(theta).ravel()
+    out = np.empty_like(theta)
+    lib().orc_theta_perturbed(_p(theta), theta.size, int(tid0), seed & (2**64 - 1), float(eps),
+                              int(sign), int(bool(bf16)), _p(out))
+    return out
+
+
+def theta_updated(theta: np.ndarray, tid0: int, seed: int, lr: float, g: float,
+                  bf16: bool) -> np.ndarray:
+    """A copy of theta after theta_i <- rnd(fma(-(lr g), z_i, theta_i)) (stream 1)."""
+    theta = _f32(theta).ravel().copy()
+    lib().orc_theta_update(_p(theta), theta.size, int(tid0), seed & (2**64 - 1), float(lr),
+                           float(g), int(bool(bf16)))
+    return theta
+
+
 def shrink_layer(w: np.ndarray, act, tau: float, xi0: float) -> np.ndarray:
     """The actives kept by eq. selection_ (distance to tau at most xi0), in order."""
     w = _f32(w).ravel()
@@ -303,8 +328,19 @@ class TerMeZOOracle:
     k0: int = 0
     last_seed: Optional[int] = None
     last_eps: Optional[float] = None
+    # full-precision parameters theta (all registered tensors concatenated in
+    # registration order, held as fp32; bf16 storage rounds perturbed and
+    # updated values back to bf16).  None: theta frozen.
+    theta: Optional[np.ndarray] = None
+    theta_bf16: bool = False
+    theta_cur: Optional[np.ndarray] = field(init=False, default=None)
 
     def __post_init__(self):
+        if self.theta is not None:
+            self.theta = _f32(self.theta).ravel().copy()
+            if self.theta_bf16:
+                assert np.array_equal(bf16_round(self.theta), self.theta), "bf16 theta must be bf16 values"
+            self.theta_cur = self.theta.copy()
         self.w = _f32(self.w).ravel().copy()
         sizes = [l.n for l in self.layers]
         self.offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
@@ -376,6 +412,9 @@ class TerMeZOOracle:
             codes.append(quantize(wp, tau).reshape(L.d_out, L.d_in))
             taus.append(tau)
             betas.append(beta)
+        if self.theta is not None:
+            self.theta_cur = (theta_perturbed(self.theta, 0, seed, eps, sign, self.theta_bf16)
+                              if sign != 0 else self.theta.copy())
         self.last_seed, self.last_eps = seed, eps
         return codes, taus, betas
 
@@ -388,6 +427,9 @@ class TerMeZOOracle:
             lib().orc_update_layer(_p(w), _p(act), act.size, int(self.offsets[l]),
                                    self.last_seed & (2**64 - 1), float(lr), float(g),
                                    int(self.bf16))
+        if self.theta is not None:
+            self.theta = theta_updated(self.theta, 0, self.last_seed, lr, g, self.theta_bf16)
+            self.theta_cur = self.theta.copy()
         self._refresh_thresholds()
         for l in range(len(self.layers)):
             act = _i64(self.active[l]).copy()

@@ -19,6 +19,16 @@ def test_rmsnorm_matches_torch():
     assert np.allclose(dec.rmsnorm(h, 1e-5), ref, rtol=1e-6, atol=1e-7)
 
 
+def test_weighted_rmsnorm_matches_torch_and_unit_weight():
+    rng = np.random.default_rng(1)
+    h = rng.standard_normal((5, 48)).astype(np.float32)
+    w = (1.0 + 0.1 * rng.standard_normal(48)).astype(np.float32)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(h).double(), (48,),
+                                       torch.from_numpy(w).double(), eps=1e-5).numpy()
+    assert np.allclose(dec.rmsnorm(h, 1e-5, w), ref, rtol=1e-6, atol=1e-7)
+    assert np.array_equal(dec.rmsnorm(h, 1e-5, np.ones(48, np.float32)), dec.rmsnorm(h, 1e-5))
+
+
 def test_rope_is_complex_rotation_and_relative():
     M, H, hd = 6, 3, 16
     x = synth.activations(2, M, H * hd).astype(np.float64)

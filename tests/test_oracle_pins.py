@@ -312,6 +312,77 @@ def test_two_point_estimator_is_unbiased_for_smoothed_gradient(orc):
     assert np.all(np.abs(mean - grad) < 5 * se + 1e-3)
 
 
+def test_joint_spsa_with_theta_on_quadratic(orc):
+    """Algorithm 1 perturbs the full-precision parameters theta densely with the
+    masked latents, from the same seed (quantiser bypassed, fp32 theta).  For
+    F(v) = v'Av/2 + b'v over v = (w, theta) the two-point difference equals
+    u'(Av + b) with u = (m (.) z_w, z_theta); theta moves by +-eps z_theta at
+    every coordinate, z_theta is the stream-1 draw (uncorrelated with the
+    stream-0 draw at the same ids), and the update moves every theta coordinate
+    by -lr g z_theta and the latents only on the mask."""
+    Dw, Dt = 64, 48
+    A, b = _quadratic_problem(Dw + Dt, 3)
+    w0 = synth.latents(4, [Dw])
+    t0 = synth.latents(5, [Dt])
+    st = orc.TerMeZOOracle([orc.Layer(4, 16)], w0, theta=t0)
+    st.build_mask(0.25)
+    act = st.active[0]
+    eps, lr, seed = 1e-3, 1e-2, 1234
+    F = lambda v: 0.5 * v @ A @ v + b @ v
+    st.perturb(seed, eps, +1)
+    wp, tp = st.perturbed_layer(0, seed, eps, +1), st.theta_cur.copy()
+    st.perturb(seed, eps, -1)
+    wm, tm = st.perturbed_layer(0, seed, eps, -1), st.theta_cur.copy()
+    zw = orc.gauss(seed, act)
+    zt = orc.gauss_range(seed, 0, Dt, stream=1)
+    assert np.allclose(tp - t0, eps * zt, atol=1e-9) and np.allclose(t0 - tm, eps * zt, atol=1e-9)
+    # perturbed values are the fp32 roundings of t0 +- eps z: within half an ulp
+    for sgn, tv in ((1, tp), (-1, tm)):
+        exact = [Fraction(float(a)) + sgn * Fraction(float(np.float32(eps))) * Fraction(float(z))
+                 for a, z in zip(t0, zt)]
+        err = np.array([abs(float(Fraction(float(v)) - e)) for v, e in zip(tv, exact)])
+        assert np.all(err <= 0.5 * _ulp32(tv))
+    assert abs(np.corrcoef(orc.gauss_range(seed, 0, 4096, stream=1),
+                           orc.gauss_range(seed, 0, 4096, stream=0))[0, 1]) < 0.06
+    u = np.zeros(Dw + Dt)
+    u[act] = zw
+    u[Dw:] = zt
+    v0 = np.concatenate([w0, t0]).astype(np.float64)
+    g = (F(np.concatenate([wp, tp]).astype(np.float64)) -
+         F(np.concatenate([wm, tm]).astype(np.float64))) / (2 * eps)
+    gref = u @ (A @ v0 + b)
+    assert abs(g - gref) < 1e-3 * (1 + abs(gref))
+    st.perturb(seed, eps, +1)
+    st.update(np.float32(g), lr)
+    dt = st.theta.astype(np.float64) - t0
+    assert np.allclose(dt, -lr * np.float32(g) * zt, rtol=1e-5, atol=1e-9)
+    off = np.setdiff1d(np.arange(Dw), act)
+    assert np.array_equal(st.layer_w(0)[off], w0[off])
+    assert np.array_equal(st.theta_cur, st.theta)
+
+
+def test_theta_bf16_storage_rounds_to_nearest_even(orc):
+    """bf16 theta: the perturbed and updated values are bf16 numbers, and each is
+    the bf16 value nearest to the fp32 result (ties to even), checked with exact
+    rationals against its two bf16 neighbours."""
+    t0 = orc.bf16_round(synth.latents(6, [4096]))
+    zt = orc.gauss_range(77, 0, t0.size, stream=1)
+    tp = orc.theta_perturbed(t0, 0, 77, 1e-3, 1, bf16=True)
+    assert np.array_equal(orc.bf16_round(tp), tp)
+    f32 = (t0.astype(np.float64) + np.float64(np.float32(1e-3)) * zt.astype(np.float64))
+    # the fp32 value theta + eps z (an fp32 fma), then its nearest bf16 neighbour
+    for i in range(0, t0.size, 37):
+        r = Fraction(float(np.float32(f32[i])))
+        v = Fraction(float(tp[i]))
+        bits = np.float32(tp[i]).view(np.uint32)
+        lo = Fraction(float(np.uint32(bits - 0x10000).view(np.float32))) if bits & 0x7FFF0000 else v
+        hi = Fraction(float(np.uint32(bits + 0x10000).view(np.float32)))
+        assert abs(v - r) <= abs(lo - r) and abs(v - r) <= abs(hi - r)
+    tu = orc.theta_updated(t0, 0, 77, 1e-2, 3.0, bf16=True)
+    assert np.array_equal(orc.bf16_round(tu), tu)
+    assert np.max(np.abs(tu - (t0 - np.float32(1e-2 * 3.0) * zt))) <= np.max(_ulp32(t0)) * 2**16
+
+
 def test_smoothed_gradient_of_ternary_objective(orc):
     """F(w) = c'Q(w) with tau held fixed: the Gaussian-smoothed gradient has the
     closed form (c_i/eps)(phi((w_i-tau)/eps) + phi((w_i+tau)/eps)), and the
