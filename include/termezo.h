@@ -150,13 +150,57 @@ termezo_status termezo_update(termezo_ctx* ctx, float proj_grad, float lr,
 termezo_status termezo_update_from_losses(termezo_ctx* ctx, const float* loss_plus,
                                           const float* loss_minus, float eps, float lr);
 
+/* ---- full-precision parameters theta (Sec. 3; Algorithm 1) ---------------------
+ * Algorithm 1 perturbs and updates the full-precision parameters (embeddings,
+ * normalisation weights, LM head) densely, together with the masked latents,
+ * with directions drawn from the same seed.  Registering theta switches this on;
+ * without registration theta is frozen.
+ *   - theta ids: the registered tensors are enumerated in registration order,
+ *     each flat; id = (sum of the sizes of the earlier tensors) + index.
+ *     z_theta(id) is drawn like z (Philox4x32-10 + Box-Muller, same seed) on
+ *     counter stream 1: counter = (id >> 2, stream 1).
+ *   - termezo_perturb(seed, eps, sign != 0) makes the forward read
+ *     theta' = round(fma(sign * eps, z_theta, theta)) (round = to nearest-even
+ *     bf16 for BF16 tensors, identity for F32), held in library-owned copies;
+ *     theta itself is not modified.  Both signs of a (seed, eps) pair are
+ *     produced by the first of the two calls; sign = 0 reads theta itself.
+ *   - termezo_update / termezo_update_from_losses apply, after the latent
+ *     update, theta <- round(fma(-(lr * g), z_theta, theta)) in place (a
+ *     non-finite g leaves theta untouched), and the forward reads theta again.
+ * The tensors are BORROWED (caller-owned device memory that must outlive the
+ * context); the caller must not write them while a perturbation is pending. */
+typedef struct {
+  void* data;              /* device pointer, 16-byte aligned                 */
+  int64_t n;               /* number of elements                              */
+  termezo_dtype dtype;     /* F32 or BF16                                     */
+} termezo_theta;
+
+/* Register n tensors as theta (once per context).  Allocates two copies of each
+ * (the +eps and -eps values).  Errors: INVALID_ARG (null or misaligned data,
+ * n <= 0, bad dtype), STATE (already registered), OOM. */
+termezo_status termezo_theta_register(termezo_ctx* ctx, const termezo_theta* params,
+                                      int32_t n);
+
+/* *values receives the device pointer the forward pass must read for tensor i
+ * now: the perturbed copy after termezo_perturb with sign +1 or -1, else the
+ * caller's tensor.  Errors: INVALID_ARG (i out of range, null values). */
+termezo_status termezo_theta_current(termezo_ctx* ctx, int32_t i, void** values);
+
+/* Copy (device to device, ordered on the context's stream, no wait) the values
+ * termezo_theta_current points to for tensor i into the caller's device buffer
+ * dst (n elements of the tensor's dtype).  Inspection support.
+ * Errors: INVALID_ARG (i out of range, null dst), DEVICE. */
+termezo_status termezo_theta_copy(termezo_ctx* ctx, int32_t i, void* dst);
+
 /* ---- BitNet decoder around the registered projections (Sec. 3) ----------------
  * The context's layers must be the ternary projections of n_blocks decoder
  * blocks in the order q, k, v, o, gate, up, down (shapes [n_heads*hd][d],
  * [n_kv_heads*hd][d] twice, [d][n_heads*hd], [d_ffn][d] twice, [d][d_ffn],
- * hd = d_model / n_heads).  The full-precision parameters are frozen: the
- * token embedding (tied to the LM head) is the caller's device matrix
- * [vocab][d_model] in act_dtype; RMSNorm weights are one.  Blocks are pre-norm:
+ * hd = d_model / n_heads).  The full-precision parameters are the token
+ * embedding (tied to the LM head), the caller's device matrix [vocab][d_model]
+ * in act_dtype, and the RMSNorm weights (one unless set with
+ * termezo_model_set_norm_weights).  Either may be a registered theta tensor;
+ * the forward then reads its current values.  Blocks are pre-norm:
  * h += o(attn(rope(q(x)), rope(k(x)), v(x))), x = rmsnorm(h); then
  * h += down(silu(gate(x)) * up(x)).  Attention is causal grouped-query with
  * scale 1/sqrt(hd); rotary pairs are (i, i + hd/2) with angle
@@ -177,6 +221,12 @@ typedef struct termezo_model termezo_model;
  * d_ffn above 8192, bad dtype). */
 termezo_status termezo_model_create(termezo_ctx* ctx, const termezo_model_config* cfg,
                                     const void* embedding, termezo_model** out);
+/* RMSNorm weights of the model: norm_weights is a device [2 n_blocks + 1][d_model]
+ * array in act_dtype, 16-byte aligned, borrowed (row 2 b scales the attention
+ * input of block b, row 2 b + 1 its MLP input, the last row the LM-head input);
+ * NULL restores weights one.  Errors: INVALID_ARG (misaligned pointer). */
+termezo_status termezo_model_set_norm_weights(termezo_model* model, const void* norm_weights);
+
 /* Free the model's activation buffers (it does not touch the context, which
  * may already have been destroyed).  NULL is a no-op. */
 void termezo_model_destroy(termezo_model* model);

@@ -61,6 +61,16 @@ struct GemmOut {
   int nseg;
 };
 
+// One registered full-precision parameter tensor (theta).
+struct ThetaHost {
+  void* data;                        // caller's tensor (clean values, updated in place)
+  int64_t n;                         // elements
+  int64_t tid0;                      // first theta id (Philox stream 1)
+  termezo_dtype dtype;               // F32 or BF16
+  void* plus;                        // library copies theta +- eps z (same dtype and size)
+  void* minus;
+};
+
 struct SelectState {                 // radix-select bookkeeping (device)
   unsigned long long k0;             // budget
   unsigned long long less;           // keys strictly below the current prefix bucket
@@ -124,6 +134,14 @@ struct termezo_ctx {
   float* d_xs = nullptr;
   int64_t xs_cap = 0;
 
+  // full-precision parameters theta (dense perturbation and update)
+  std::vector<tmz::ThetaHost> theta;
+  int64_t theta_P = 0;               // total theta elements
+  int theta_sign = 0;                // which values the forward reads: 0 clean, +1 / -1 copies
+  bool theta_pair_valid = false;     // copies hold theta +- eps z(seed) for the recorded pair
+  uint64_t theta_pair_seed = 0;
+  float theta_pair_eps = 0.f;
+
   // state
   bool has_mask = false;
   bool codes_valid = false;
@@ -185,6 +203,9 @@ hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed);
 // from d_wp (the updated values): d_act -> d_act_tmp, offsets -> tmp
 hipError_t launch_shrink(termezo_ctx* c, int64_t k);
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);
+// theta: both perturbed copies in one pass; in-place update with the coefficient in d_scal[0]
+hipError_t launch_theta_pair(termezo_ctx* c, const ThetaHost& t, uint64_t seed, float eps);
+hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, uint64_t seed);
 hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z, hipStream_t s);
 hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hipStream_t s);
 

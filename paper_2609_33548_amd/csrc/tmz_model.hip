@@ -79,7 +79,8 @@ __global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, i
 // ---------------------------------------------------------------------------
 // Row kernels, one wave per token row, 8 elements (one 16-byte bf16 load, or
 // two 16-byte fp32 loads) per lane per chunk, the row kept in registers:
-//   kRowNormQuant  x = h / sqrt(mean(h^2) + eps) (unit-weight RMSNorm), then
+//   kRowNormQuant  x = (h / sqrt(mean(h^2) + eps)) * weight (RMSNorm; the weight
+//                  row is the u argument, one when null), then
 //                  the 8-bit quantiser: s = 127 / max(max|x|, 1e-5),
 //                  x_q = clamp(rne(x s), -128, 127)
 //   kRowNormStore  the RMSNorm output stored in the activation dtype
@@ -160,12 +161,16 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
     const float r = __fdiv_rn(1.0f, sqrt_rn(ss / (float)K + eps));
     float a = 0.0f;
 #pragma unroll
-    for (int c = 0; c < kRowChunks; ++c)
+    for (int c = 0; c < kRowChunks; ++c) {
+      float wt[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+      const int idx = c * 64 + lane;
+      if (u && idx < nch) load8(u + idx * 8, wt);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        v[c][j] = v[c][j] * r;
+        v[c][j] = v[c][j] * r * wt[j];
         a = fmaxf(a, fabsf(v[c][j]));
       }
+    }
     if (MODE == kRowNormStore) {
 #pragma unroll
       for (int c = 0; c < kRowChunks; ++c) {
@@ -1211,6 +1216,7 @@ struct termezo_model {
   hipStream_t stream = nullptr;   // copy of the context's stream (destroy never reads ctx)
   termezo_model_config cfg{};
   const void* emb = nullptr;
+  const void* normw = nullptr;    // RMSNorm weights [2 n_blocks + 1][d] (null: one)
   int hd = 0;
   int64_t cap_M = 0;
   int cap_S = 0;
@@ -1466,6 +1472,16 @@ termezo_status termezo_model_timing(termezo_model* m, int32_t cls, double* ms, i
   return TERMEZO_OK;
 }
 
+termezo_status termezo_model_set_norm_weights(termezo_model* m, const void* norm_weights) {
+  if (!m) return TERMEZO_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(norm_weights) & 15u) != 0) {
+    m->ctx->last_error = "model_set_norm_weights: pointer must be 16-byte aligned";
+    return TERMEZO_ERR_INVALID_ARG;
+  }
+  m->normw = norm_weights;
+  return TERMEZO_OK;
+}
+
 void termezo_model_destroy(termezo_model* m) {
   if (!m) return;
   (void)hipStreamSynchronize(m->stream);
@@ -1492,6 +1508,16 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   if (st != TERMEZO_OK) return st;
   hipStream_t s = c->stream;
   const bool bf = cf.act_dtype == TERMEZO_BF16;
+  // full-precision parameters: a registered theta tensor is read at its current
+  // (possibly perturbed) values
+  auto current = [&](const void* p) -> const void* {
+    if (!p || c->theta_sign == 0) return p;
+    for (const ThetaHost& t : c->theta)
+      if (t.data == p) return c->theta_sign > 0 ? t.plus : t.minus;
+    return p;
+  };
+  const void* emb = current(m->emb);
+  const void* nrm = current(m->normw);
   const int64_t d = cf.d_model, F = cf.d_ffn, dq = (int64_t)cf.n_heads * m->hd,
                 dkv = (int64_t)cf.n_kv_heads * m->hd;
   const int64_t nvt = bf ? (cf.vocab + kLmTile - 1) / kLmTile : (cf.vocab + kVT - 1) / kVT;
@@ -1503,33 +1529,33 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
 
   if (bf)
     hipLaunchKernelGGL(k_embed<uint16_t>, dim3((unsigned)M), dim3(256), 0, s, tokens,
-                       (const uint16_t*)m->emb, d, (uint16_t*)m->h);
+                       (const uint16_t*)emb, d, (uint16_t*)m->h);
   else
     hipLaunchKernelGGL(k_embed<float>, dim3((unsigned)M), dim3(256), 0, s, tokens,
-                       (const float*)m->emb, d, (float*)m->h);
+                       (const float*)emb, d, (float*)m->h);
   chk(hipGetLastError());
   hipLaunchKernelGGL(k_labels, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, tokens, M, seq,
                      m->labels);
   const unsigned rowg = (unsigned)((M + 3) / 4);
-  auto rmsq = [&](int8_t* xq, float* xs, void* xf) {
+  // RMSNorm (weight row wr of the norm weights, one when there are none), then
+  // the quantiser, or stored (the LM-head input)
+  auto rmsq = [&](int8_t* xq, float* xs, void* xf, int wr) {
     if (bf) {
+      const uint16_t* w = nrm ? (const uint16_t*)nrm + (int64_t)wr * d : nullptr;
       if (xf)
         hipLaunchKernelGGL((k_row<kRowNormStore, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                           (const uint16_t*)m->h, (const uint16_t*)nullptr, M, d, cf.norm_eps, xq,
-                           xs, (uint16_t*)xf);
+                           (const uint16_t*)m->h, w, M, d, cf.norm_eps, xq, xs, (uint16_t*)xf);
       else
         hipLaunchKernelGGL((k_row<kRowNormQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                           (const uint16_t*)m->h, (const uint16_t*)nullptr, M, d, cf.norm_eps, xq,
-                           xs, (uint16_t*)nullptr);
+                           (const uint16_t*)m->h, w, M, d, cf.norm_eps, xq, xs, (uint16_t*)nullptr);
     } else {
+      const float* w = nrm ? (const float*)nrm + (int64_t)wr * d : nullptr;
       if (xf)
         hipLaunchKernelGGL((k_row<kRowNormStore, float>), dim3(rowg), dim3(256), 0, s,
-                           (const float*)m->h, (const float*)nullptr, M, d, cf.norm_eps, xq, xs,
-                           (float*)xf);
+                           (const float*)m->h, w, M, d, cf.norm_eps, xq, xs, (float*)xf);
       else
         hipLaunchKernelGGL((k_row<kRowNormQuant, float>), dim3(rowg), dim3(256), 0, s,
-                           (const float*)m->h, (const float*)nullptr, M, d, cf.norm_eps, xq, xs,
-                           (float*)nullptr);
+                           (const float*)m->h, w, M, d, cf.norm_eps, xq, xs, (float*)nullptr);
     }
     chk(hipGetLastError());
   };
@@ -1537,7 +1563,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     const int l0 = 7 * blk;
     const LayerHost* Ls = &c->layers[l0];
     // attention sub-block
-    rmsq(m->xq, m->xs, nullptr);
+    rmsq(m->xq, m->xs, nullptr, 2 * blk);
     GemmOut o3 = {};
     o3.nseg = 3;
     o3.y[0] = m->q; o3.ld[0] = dq; o3.beta[0] = c->d_beta_cur + l0;
@@ -1578,7 +1604,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                        nullptr, c->n_cu, s));
     span_end(m, sp, s);
     // MLP sub-block
-    rmsq(m->xq, m->xs, nullptr);
+    rmsq(m->xq, m->xs, nullptr, 2 * blk + 1);
     GemmOut o2 = {};
     o2.nseg = 2;
     o2.y[0] = m->g; o2.ld[0] = F; o2.beta[0] = c->d_beta_cur + l0 + 4;
@@ -1613,22 +1639,22 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                        nullptr, c->n_cu, s));
     span_end(m, sp, s);
   }
-  rmsq(nullptr, nullptr, m->xf);
+  rmsq(nullptr, nullptr, m->xf, 2 * cf.n_blocks);
   const int sp_lm = span_begin(m, 2, 2.0 * M * d * cf.vocab, s);
   if (bf) {
     const unsigned nb = (unsigned)(nvt * ((M + kLmTile - 1) / kLmTile));
     if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % 64 == 0)
       hipLaunchKernelGGL((k_lmhead_dma<2, 64>), dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
-                         (const uint16_t*)m->emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
+                         (const uint16_t*)emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
                          m->psum, m->lab, nvt);
     else
       hipLaunchKernelGGL(k_lmhead_bf16<false>, dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
-                         (const uint16_t*)m->emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
+                         (const uint16_t*)emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
                          m->psum, m->lab, nvt);
   }
   else
     hipLaunchKernelGGL(k_lmhead_f32, dim3((unsigned)nvt, (unsigned)((M + 1) / 2)), dim3(256), 0, s,
-                       (const float*)m->xf, (const float*)m->emb, M, d, (int64_t)cf.vocab,
+                       (const float*)m->xf, (const float*)emb, M, d, (int64_t)cf.vocab,
                        m->labels, m->pmax, m->psum, m->lab, nvt);
   chk(hipGetLastError());
   span_end(m, sp_lm, s);

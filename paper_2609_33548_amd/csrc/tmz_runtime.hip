@@ -130,6 +130,11 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_scal);
   dfree(c->d_xq);
   dfree(c->d_xs);
+  for (ThetaHost& t : c->theta) {
+    if (t.plus) (void)hipFree(t.plus);
+    if (t.minus) (void)hipFree(t.minus);
+  }
+  c->theta.clear();
 }
 
 bool finite(float v) { return std::isfinite(v); }
@@ -329,6 +334,17 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
   TMZ_HIP(c, launch_requant(c, 1));
+  // theta: both signs of the pair come from one pass, so the second evaluation
+  // of a pair (same seed and eps) only switches to the other copy
+  if (!c->theta.empty() && sign != 0 &&
+      !(c->theta_pair_valid && c->theta_pair_seed == seed && c->theta_pair_eps == eps)) {
+    c->theta_pair_valid = false;
+    for (const ThetaHost& t : c->theta) TMZ_HIP(c, launch_theta_pair(c, t, seed, eps));
+    c->theta_pair_valid = true;
+    c->theta_pair_seed = seed;
+    c->theta_pair_eps = eps;
+  }
+  c->theta_sign = sign;
   c->codes_valid = true;
   c->pending_perturb = true;
   c->last_seed = seed;
@@ -371,6 +387,9 @@ namespace {
 // thresholds and the shrink; the compacted list replaces the old one.
 termezo_status finish_update(termezo_ctx* c, int64_t* k_out) {
   TMZ_HIP(c, launch_update(c, c->k_bound, c->last_seed));
+  c->theta_pair_valid = false;
+  c->theta_sign = 0;
+  for (const ThetaHost& t : c->theta) TMZ_HIP(c, launch_theta_update(c, t, c->last_seed));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_clean, c->d_tau, c->d_beta));
   TMZ_HIP(c, launch_shrink(c, c->k_bound));
   std::swap(c->d_act, c->d_act_tmp);
@@ -410,6 +429,68 @@ termezo_status termezo_update_from_losses(termezo_ctx* c, const float* loss_plus
   if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
   TMZ_HIP(c, launch_coeff_from_losses(c, loss_plus, loss_minus, eps, lr));
   return finish_update(c, nullptr);
+}
+
+termezo_status termezo_theta_register(termezo_ctx* c, const termezo_theta* params, int32_t n) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!params || n <= 0) return fail(c, TERMEZO_ERR_INVALID_ARG, "no theta tensors");
+  if (!c->theta.empty()) return fail(c, TERMEZO_ERR_STATE, "theta is already registered");
+  for (int32_t i = 0; i < n; ++i) {
+    const termezo_theta& p = params[i];
+    if (!p.data || p.n <= 0 || (p.dtype != TERMEZO_F32 && p.dtype != TERMEZO_BF16))
+      return fail(c, TERMEZO_ERR_INVALID_ARG, "theta tensor: null data, n <= 0 or bad dtype");
+    if ((reinterpret_cast<uintptr_t>(p.data) & 15u) != 0)
+      return fail(c, TERMEZO_ERR_INVALID_ARG, "theta tensors must be 16-byte aligned");
+  }
+  std::vector<ThetaHost> th;
+  int64_t tid = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    ThetaHost t;
+    t.data = params[i].data;
+    t.n = params[i].n;
+    t.dtype = params[i].dtype;
+    t.tid0 = tid;
+    t.plus = t.minus = nullptr;
+    const size_t bytes = (size_t)t.n * dtype_size(t.dtype);
+    hipError_t e = hipMalloc(&t.plus, bytes);
+    if (e == hipSuccess) e = hipMalloc(&t.minus, bytes);
+    if (e != hipSuccess) {
+      if (t.plus) (void)hipFree(t.plus);
+      for (ThetaHost& u : th) {
+        (void)hipFree(u.plus);
+        (void)hipFree(u.minus);
+      }
+      return hip_fail(c, e, "alloc theta copies");
+    }
+    th.push_back(t);
+    tid += t.n;
+  }
+  c->theta = std::move(th);
+  c->theta_P = tid;
+  c->theta_sign = 0;
+  c->theta_pair_valid = false;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_theta_current(termezo_ctx* c, int32_t i, void** values) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!values || i < 0 || i >= (int32_t)c->theta.size())
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "theta index out of range or null output");
+  const ThetaHost& t = c->theta[i];
+  *values = c->theta_sign == 0 ? t.data : (c->theta_sign > 0 ? t.plus : t.minus);
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_theta_copy(termezo_ctx* c, int32_t i, void* dst) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  void* src = nullptr;
+  termezo_status st = termezo_theta_current(c, i, &src);
+  if (st != TERMEZO_OK) return st;
+  if (!dst) return fail(c, TERMEZO_ERR_INVALID_ARG, "null destination");
+  const ThetaHost& t = c->theta[i];
+  TMZ_HIP(c, hipMemcpyAsync(dst, src, (size_t)t.n * dtype_size(t.dtype), hipMemcpyDeviceToDevice,
+                            c->stream));
+  return TERMEZO_OK;
 }
 
 termezo_status termezo_gauss(void* hip_stream, uint64_t seed, const uint64_t* gids, int64_t n,

@@ -682,6 +682,114 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
 }
 
 // ---------------------------------------------------------------------------
+// Full-precision parameters theta (Algorithm 1 perturbs and updates them
+// densely, together with the masked latents): z at theta id t is the draw of
+// the step's seed on Philox stream 1.  One Philox call per id quad and one
+// Box-Muller pair per two ids -- the operations of gauss_at, so the values are
+// the same.  Both perturbed copies theta +- eps z (rounded to the storage
+// type) come from one pass; the update is in place.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void gauss_quad(uint64_t seed, uint64_t q, uint32_t stream, float z[4]) {
+  const U4 x = philox10((uint32_t)q, (uint32_t)(q >> 32), stream, 0u, (uint32_t)seed,
+                        (uint32_t)(seed >> 32));
+  box_muller(x.a, x.b, z[0], z[1]);     // ids 4q, 4q+1: cos, sin of the pair (x0, x1)
+  box_muller(x.c, x.d, z[2], z[3]);     // ids 4q+2, 4q+3: cos, sin of the pair (x2, x3)
+}
+
+__device__ __forceinline__ float th_load(const float* p) { return *p; }
+__device__ __forceinline__ float th_load(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ void th_store(float* p, float v) { *p = v; }
+__device__ __forceinline__ void th_store(uint16_t* p, float v) { *p = f32_to_bf16_rne(v); }
+
+// Quads q of the theta id space covering [tid0, tid0 + n); the four elements of a
+// quad are local indices 4q - tid0 .. + 3.  With tid0 % 4 == 0 (and 16-byte
+// aligned tensors) inner quads are one 16-byte (fp32) or 8-byte (bf16) access.
+template <typename F>
+__device__ __forceinline__ void theta_quads(int64_t n, int64_t tid0, F&& f) {
+  const int64_t q0 = tid0 >> 2, q1 = (tid0 + n + 3) >> 2;
+  for (int64_t q = q0 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < q1;
+       q += (int64_t)gridDim.x * blockDim.x)
+    f(q, 4 * q - tid0);
+}
+
+__device__ __forceinline__ void gather_quad(const float* p, float v[4]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+}
+__device__ __forceinline__ void gather_quad(const uint16_t* p, float v[4]) {
+  const uint2 a = *reinterpret_cast<const uint2*>(p);
+  v[0] = __uint_as_float(a.x << 16);
+  v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(a.y << 16);
+  v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+}
+__device__ __forceinline__ void scatter_quad(float* p, const float v[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void scatter_quad(uint16_t* p, const float v[4]) {
+  const uint32_t lo = (uint32_t)f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+  const uint32_t hi = (uint32_t)f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+  *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+}
+template <typename T>
+__device__ __forceinline__ void load_quad(const T* p, int64_t e0, int64_t n, bool vec, float v[4]) {
+  if (vec && e0 >= 0 && e0 + 3 < n) {
+    gather_quad(p + e0, v);
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = (e0 + r >= 0 && e0 + r < n) ? th_load(p + e0 + r) : 0.0f;
+  }
+}
+template <typename T>
+__device__ __forceinline__ void store_quad(T* p, int64_t e0, int64_t n, bool vec, const float v[4]) {
+  if (vec && e0 >= 0 && e0 + 3 < n) {
+    scatter_quad(p + e0, v);
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (e0 + r >= 0 && e0 + r < n) th_store(p + e0 + r, v[r]);
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) k_theta_pair(const T* __restrict__ th, int64_t n,
+                                                    int64_t tid0, uint64_t seed, float eps,
+                                                    T* __restrict__ plus, T* __restrict__ minus) {
+  const bool vec = (tid0 & 3) == 0;
+  const float me = -eps;
+  theta_quads(n, tid0, [&](int64_t q, int64_t e0) {
+    float z[4], w[4], vp[4], vm[4];
+    gauss_quad(seed, (uint64_t)q, 1u, z);
+    load_quad(th, e0, n, vec, w);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      vp[r] = fmaf(eps, z[r], w[r]);
+      vm[r] = fmaf(me, z[r], w[r]);
+    }
+    store_quad(plus, e0, n, vec, vp);
+    store_quad(minus, e0, n, vec, vm);
+  });
+}
+
+// theta <- rnd(fma(a, z, theta)), a = scal[0]; a non-finite coefficient (reported
+// by the coefficient kernel) leaves theta untouched, as for the latents.
+template <typename T>
+__global__ void __launch_bounds__(256) k_theta_update(T* __restrict__ th, int64_t n, int64_t tid0,
+                                                      uint64_t seed, const float* scal) {
+  const float a = scal[0];
+  if (!isfinite(a)) return;
+  const bool vec = (tid0 & 3) == 0;
+  theta_quads(n, tid0, [&](int64_t q, int64_t e0) {
+    float z[4], w[4];
+    gauss_quad(seed, (uint64_t)q, 1u, z);
+    load_quad(th, e0, n, vec, w);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = fmaf(a, z[r], w[r]);
+    store_quad(th, e0, n, vec, w);
+  });
+}
+
+// ---------------------------------------------------------------------------
 // Masked update: w_i <- round(fma(a, z_i, w_i)), a = -(lr g); exact delta of
 // the clean fixed-point sum.
 // ---------------------------------------------------------------------------
@@ -1105,6 +1213,37 @@ hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
                      c->d_act_off_tmp);
   hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(1), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
+  return hipGetLastError();
+}
+
+static unsigned theta_grid(const termezo_ctx* c, int64_t n, int64_t tid0) {
+  const int64_t quads = ((tid0 + n + 3) >> 2) - (tid0 >> 2);
+  const int64_t cap = (int64_t)(c->n_cu > 0 ? c->n_cu : 256) * 16;
+  return (unsigned)max((int64_t)1, min(cap, (quads + 255) / 256));
+}
+
+hipError_t launch_theta_pair(termezo_ctx* c, const ThetaHost& t, uint64_t seed, float eps) {
+  if (t.n <= 0) return hipSuccess;
+  const unsigned g = theta_grid(c, t.n, t.tid0);
+  if (t.dtype == TERMEZO_F32)
+    hipLaunchKernelGGL(k_theta_pair<float>, dim3(g), dim3(256), 0, c->stream, (const float*)t.data,
+                       t.n, t.tid0, seed, eps, (float*)t.plus, (float*)t.minus);
+  else
+    hipLaunchKernelGGL(k_theta_pair<uint16_t>, dim3(g), dim3(256), 0, c->stream,
+                       (const uint16_t*)t.data, t.n, t.tid0, seed, eps, (uint16_t*)t.plus,
+                       (uint16_t*)t.minus);
+  return hipGetLastError();
+}
+
+hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, uint64_t seed) {
+  if (t.n <= 0) return hipSuccess;
+  const unsigned g = theta_grid(c, t.n, t.tid0);
+  if (t.dtype == TERMEZO_F32)
+    hipLaunchKernelGGL(k_theta_update<float>, dim3(g), dim3(256), 0, c->stream, (float*)t.data, t.n,
+                       t.tid0, seed, (const float*)c->d_scal);
+  else
+    hipLaunchKernelGGL(k_theta_update<uint16_t>, dim3(g), dim3(256), 0, c->stream,
+                       (uint16_t*)t.data, t.n, t.tid0, seed, (const float*)c->d_scal);
   return hipGetLastError();
 }
 

@@ -34,6 +34,10 @@ class Layer(ctypes.Structure):
     _fields_ = [("latent", ctypes.c_void_p), ("d_out", ctypes.c_int64), ("d_in", ctypes.c_int64)]
 
 
+class Theta(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("n", ctypes.c_int64), ("dtype", ctypes.c_int32)]
+
+
 class ModelConfig(ctypes.Structure):
     _fields_ = [("n_blocks", ctypes.c_int32), ("d_model", ctypes.c_int32),
                 ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
@@ -65,7 +69,11 @@ _SIGS = {
     "termezo_active_count": [_P, ctypes.POINTER(_i64)],
     "termezo_gauss": [_P, _u64, _P, _i64, _P],
     "termezo_update_from_losses": [_P, _P, _P, _f32, _f32],
+    "termezo_theta_register": [_P, ctypes.POINTER(Theta), _i32],
+    "termezo_theta_current": [_P, _i32, ctypes.POINTER(_P)],
+    "termezo_theta_copy": [_P, _i32, _P],
     "termezo_model_create": [_P, _P, _P, ctypes.POINTER(_P)],
+    "termezo_model_set_norm_weights": [_P, _P],
     "termezo_model_destroy": [_P],
     "termezo_model_loss": [_P, _P, _i32, _i32, _P, _P, ctypes.POINTER(_f32)],
     "termezo_model_set_timing": [_P, _i32],
@@ -231,6 +239,31 @@ class Context:
         self._check(_lib.termezo_update_from_losses(self.handle, _ptr(loss_plus), _ptr(loss_minus),
                                                     eps, lr), "update_from_losses")
 
+    def theta_register(self, tensors):
+        """Register full-precision parameters theta (contiguous fp32 or bf16 device
+        tensors, kept alive by the caller): from now on perturb and update move them
+        with the latents (Algorithm 1)."""
+        for t in tensors:
+            if not t.is_cuda or not t.is_contiguous():
+                raise ValueError("theta tensors must be contiguous device tensors")
+        arr = (Theta * len(tensors))(*[Theta(t.data_ptr(), t.numel(), _dtype_code(t)) for t in tensors])
+        self._check(_lib.termezo_theta_register(self.handle, arr, len(tensors)), "theta_register")
+        self.theta = list(tensors)
+
+    def theta_current_ptr(self, i: int) -> int:
+        """Device address of the values the forward reads now for theta tensor i."""
+        out = _P()
+        self._check(_lib.termezo_theta_current(self.handle, i, ctypes.byref(out)), "theta_current")
+        return int(out.value)
+
+    def theta_current(self, i: int):
+        """A copy (new device tensor) of the values the forward reads now for theta
+        tensor i: the perturbed copy while a +- perturbation is current."""
+        import torch
+        out = torch.empty_like(self.theta[i])
+        self._check(_lib.termezo_theta_copy(self.handle, i, _ptr(out)), "theta_copy")
+        return out
+
     def mse_loss(self, y, target) -> float:
         out = _f32()
         self._check(_lib.termezo_mse_loss(self.handle, _ptr(y), _ptr(target), y.numel(),
@@ -257,6 +290,13 @@ class Model:
             raise TermezoError(st, "termezo_model_create failed")
         self.handle = out.value
         ctx._models.add(self)
+
+    def set_norm_weights(self, norm_weights):
+        """RMSNorm weights [2 n_blocks + 1, d_model] (device tensor in the activation
+        dtype, kept alive by the caller); None restores weights one."""
+        self.norm_weights = norm_weights
+        self.ctx._check(_lib.termezo_model_set_norm_weights(self.handle, _ptr(norm_weights)),
+                        "model_set_norm_weights")
 
     def loss(self, tokens, loss_dev=None, row_loss_dev=None, host: bool = True) -> Optional[float]:
         B, S = tokens.shape
