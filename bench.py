@@ -81,7 +81,7 @@ def measured_traffic():
     return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
 
 
-def cpu_baseline(c, rho, seed=0):
+def cpu_baseline(c, rho, seed=0, theta_n=0):
     """The oracle, as it stands, on a bounded sample of the same step; the
     full-step time is extrapolated by operation counts (stated in 'sample')."""
     import numpy as np
@@ -123,17 +123,28 @@ def cpu_baseline(c, rho, seed=0):
     logits = x.astype(np.float64) @ E.astype(np.float64).T
     dec.cross_entropy_rows(logits, np.zeros(n_pos, np.int64))
     t_head = time.perf_counter() - t0
+    # (4) theta: perturbation at both signs and the update on a sample of ids
+    t_theta, n_th = 0.0, 1 << 20
+    if theta_n:
+        th = synth.latents(seed + 5, [n_th], bf16=True)
+        t0 = time.perf_counter()
+        orc.theta_perturbed(th, 0, 1, 1e-3, 1, True)
+        orc.theta_perturbed(th, 0, 1, 1e-3, -1, True)
+        orc.theta_updated(th, 0, 1, 1e-4, 1.0, True)
+        t_theta = (time.perf_counter() - t0) * theta_n / n_th
     ntok = c["batch"] * c["seq"]
     t_fwd = c["n_blocks"] * c["batch"] * t_block + (ntok / n_pos) * t_head
-    t_step = 2 * t_fwd + t_latent
-    wall = t_latent * nsmp / D + t_block * n_seq + t_head
+    t_step = 2 * t_fwd + t_latent + t_theta
+    wall = t_latent * nsmp / D + t_block * n_seq + t_head + t_theta * n_th / max(theta_n, 1)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {
         "value": 1.0 / t_step, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
         "sample": (f"oracle perturb(+/-)+update+shrink on one block's 7 projections ({nsmp} bf16 "
                    f"latents) scaled to {D}; 1 decoder block x {n_seq} sequences of {c['seq']} tokens "
                    f"scaled x{c['n_blocks']} blocks x{c['batch'] / n_seq:g}; LM head+CE on {n_pos} "
-                   f"positions scaled x{ntok // n_pos}; two forwards per step; sample wall {wall:.1f}s"),
+                   f"positions scaled x{ntok // n_pos}; two forwards per step"
+                   + (f"; theta perturb(+/-)+update on {n_th} ids scaled to {theta_n}" if theta_n else "")
+                   + f"; sample wall {wall:.1f}s"),
         "extrapolated_step_s": t_step,
     }
 
@@ -161,7 +172,7 @@ def cpu_baseline_c1(n_steps=200, seed=0):
             "sample": f"{n_steps} full oracle steps of the same workload (single thread, C + numpy)"}
 
 
-def cpu_baseline_full(c, rho, n_steps=8, seed=0):
+def cpu_baseline_full(c, rho, n_steps=8, seed=0, theta=False):
     """The oracle's full decoder step (perturb +/-, two forwards, update) on the same
     workload, for configurations small enough to run whole."""
     import numpy as np
@@ -174,8 +185,11 @@ def cpu_baseline_full(c, rho, n_steps=8, seed=0):
                             n_kv_heads=c["n_kv_heads"], d_ffn=c["d_ffn"], vocab=c["vocab"], bf16=bf)
     shapes = cfg.layer_shapes()
     w = synth.latents(seed, [o * i for o, i in shapes], bf16=bf)
-    st = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w, bf16=bf)
     emb = synth.latents(seed + 1, [c["vocab"] * c["d_model"]], bf16=bf).reshape(c["vocab"], c["d_model"])
+    nE = emb.size
+    nw = np.ones((2 * c["n_blocks"] + 1) * c["d_model"], np.float32)
+    st = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w, bf16=bf,
+                           theta=np.concatenate([emb.ravel(), nw]) if theta else None, theta_bf16=bf)
     tok = synth.tokens(seed + 2, c["batch"], c["seq"], c["vocab"])
     st.build_mask(rho)
     t0 = time.perf_counter()
@@ -183,7 +197,8 @@ def cpu_baseline_full(c, rho, n_steps=8, seed=0):
         f = {}
         for sign in (1, -1):
             codes, _, betas = st.perturb(t, 1e-3, sign)
-            f[sign] = dec.mean_loss(dec.forward_row_losses(cfg, emb, tok, codes, betas))
+            e, n = ((st.theta_cur[:nE].reshape(emb.shape), st.theta_cur[nE:]) if theta else (emb, None))
+            f[sign] = dec.mean_loss(dec.forward_row_losses(cfg, e, tok, codes, betas, norm_w=n))
         st.update(orc.projected_grad(f[1], f[-1], 1e-3), c["lr"])
     dt = (time.perf_counter() - t0) / n_steps
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
@@ -444,6 +459,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", choices=["latent", "bitlinear", "all"],
                     help="run the kernel sweeps instead of the step benchmark")
+    ap.add_argument("--theta", action="store_true",
+                    help="also perturb and update the full-precision parameters (tied embedding and "
+                         "RMSNorm weights) with the latents, as Algorithm 1 does")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the measurement, copy 1 GiB device to device (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
@@ -490,6 +508,13 @@ def main():
     ctx = termezo.Context(layers)
     model = termezo.Model(ctx, c["n_blocks"], c["d_model"], c["n_heads"], c["n_kv_heads"],
                           c["d_ffn"], c["vocab"], E)
+    n_theta = 0
+    if args.theta:
+        NW = torch.ones((2 * c["n_blocks"] + 1, c["d_model"]), dtype=adt, device=dev)
+        model.set_norm_weights(NW)
+        ctx.theta_register([E, NW])
+        n_theta = E.numel() + NW.numel()
+        print(f"[bench] theta: {n_theta} full-precision parameters perturbed and updated", flush=True)
     t0 = time.perf_counter()
     k0, xi0 = ctx.build_mask(args.rho)
     mask_ms = (time.perf_counter() - t0) * 1e3
@@ -549,7 +574,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
-        cpu = cpu_baseline_full(c, args.rho) if args.config == "tiny" else cpu_baseline(c, args.rho)
+        cpu = (cpu_baseline_full(c, args.rho, theta=args.theta) if args.config == "tiny"
+               else cpu_baseline(c, args.rho, theta_n=n_theta))
         print(f"[bench] cpu baseline sample took {time.perf_counter() - t0:.1f} s", flush=True)
 
     metric = METRIC if args.config == "2b" else {
@@ -569,7 +595,9 @@ def main():
         "dtype": "int8xternary+f32" if fp32 else "int8xternary+bf16",
         "data": "synthetic",
         "config": {"workload": (f"termezo_zo_step_tiny_decoder" if args.config == "tiny"
-                                else f"termezo_zo_step_bitnet_{args.config}"),
+                                else f"termezo_zo_step_bitnet_{args.config}")
+                               + ("_with_theta" if args.theta else ""),
+                   "theta_params": n_theta,
                    **{k: v for k, v in c.items() if k not in ("rho", "lr", "fp32")},
                    "tokens_per_forward": c["batch"] * c["seq"], "latents": D,
                    "mask_ratio": args.rho, "k0": k0, "k_final": k_final, "eps": args.eps,
