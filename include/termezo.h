@@ -105,7 +105,8 @@ termezo_status termezo_build_mask(termezo_ctx* ctx, float rho0, float delta,
  * active set, w'_i = w_i elsewhere; tau' and beta' = 2 tau' are recomputed from
  * w' (the quantiser is applied on the fly to the perturbed latents, eq.
  * objective).  The latents themselves are not modified.  sign = 0 gives the
- * clean codes.  Records (seed, eps) for the following termezo_update.
+ * clean codes.  Registered theta tensors are perturbed too (see the theta
+ * section below).  Records (seed, eps) for the following termezo_update.
  * Errors: INVALID_ARG (sign not in {-1, 0, 1}; eps <= 0 or not finite),
  * STATE (no mask).  A perturbed |w'| >= 4 raises a deferred NUMERIC. */
 termezo_status termezo_perturb(termezo_ctx* ctx, uint64_t seed, float eps,
@@ -133,6 +134,7 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* ctx, int32_t layer,
  * (round = to nearest-even bf16 for BF16 latents, identity for F32); unmasked
  * latents are untouched.  Then tau^l is recomputed from the updated latents and
  * the active set keeps only the i with d_i <= xi0 (order preserved).
+ * Registered theta tensors are updated with the same g (theta section below).
  * proj_grad is g = (F+ - F-) / (2 eps) (eq. spsa).  k_out: host pointer
  * (nullable) receiving the new mask size; when non-NULL the call waits.
  * Invalidates the current codes.  Errors: INVALID_ARG (g or lr not finite),
