@@ -438,3 +438,42 @@ void orc_theta_update(float* theta, int64_t n, int64_t tid0, uint64_t seed, floa
     theta[i] = bf16_storage ? orc_round_bf16(v) : v;
   }
 }
+
+/* ------------------------------------------------------------------------ */
+/* K perturbation directions per step (Algorithm 1): the K estimates are     */
+/* taken at w_t, then the K updates w <- w - (eta/K) g_k m (.) z_k are       */
+/* applied in order.  Here the chain runs in fp32 and is rounded to the      */
+/* storage type once:  v = w;  v = fma(a_k, z_k, v) for k = 1..K;            */
+/* w = rnd(v),  with a_k = -((lr / K) g_k) (lr / K one fp32 division).       */
+/* For fp32 storage this equals K single updates applied one after another.  */
+/* ------------------------------------------------------------------------ */
+float orc_multi_coeff(float lr, int K, float g) {
+  float c = lr / (float)K;
+  return -(c * g);
+}
+
+void orc_update_layer_multi(float* w, const int64_t* act, int64_t k, int64_t gid0,
+                            const uint64_t* seeds, const float* g, int K, float lr,
+                            int bf16_storage) {
+  for (int64_t j = 0; j < k; ++j) {
+    int64_t i = act[j];
+    float v = w[i];
+    for (int q = 0; q < K; ++q) {
+      float z = orc_gauss_one(seeds[q], 0u, (uint64_t)(gid0 + i));
+      v = fmaf(orc_multi_coeff(lr, K, g[q]), z, v);
+    }
+    w[i] = bf16_storage ? orc_round_bf16(v) : v;
+  }
+}
+
+void orc_theta_update_multi(float* theta, int64_t n, int64_t tid0, const uint64_t* seeds,
+                            const float* g, int K, float lr, int bf16_storage) {
+  for (int64_t i = 0; i < n; ++i) {
+    float v = theta[i];
+    for (int q = 0; q < K; ++q) {
+      float z = orc_gauss_one(seeds[q], 1u, (uint64_t)(tid0 + i));
+      v = fmaf(orc_multi_coeff(lr, K, g[q]), z, v);
+    }
+    theta[i] = bf16_storage ? orc_round_bf16(v) : v;
+  }
+}

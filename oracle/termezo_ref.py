@@ -72,6 +72,9 @@ def lib():
         "orc_shrink_layer": (i64, [P, P, i64, f32, f32]),
         "orc_theta_perturbed": (None, [P, i64, i64, u64, f32, i32, i32, P]),
         "orc_theta_update": (None, [P, i64, i64, u64, f32, f32, i32]),
+        "orc_multi_coeff": (f32, [f32, i32, f32]),
+        "orc_update_layer_multi": (None, [P, P, i64, i64, P, P, i32, f32, i32]),
+        "orc_theta_update_multi": (None, [P, i64, i64, P, P, i32, f32, i32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -231,6 +234,11 @@ def theta_updated(theta: np.ndarray, tid0: int, seed: int, lr: float, g: float,
     lib().orc_theta_update(_p(theta), theta.size, int(tid0), seed & (2**64 - 1), float(lr),
                            float(g), int(bool(bf16)))
     return theta
+
+
+def multi_coeff(lr: float, K: int, g: float) -> float:
+    """a_k = -((lr / K) g_k) in fp32 (the coefficient of direction k)."""
+    return float(np.float32(lib().orc_multi_coeff(float(lr), int(K), float(g))))
 
 
 def shrink_layer(w: np.ndarray, act, tau: float, xi0: float) -> np.ndarray:
@@ -417,6 +425,32 @@ class TerMeZOOracle:
                               if sign != 0 else self.theta.copy())
         self.last_seed, self.last_eps = seed, eps
         return codes, taus, betas
+
+    # -- Algorithm 1 with K directions: all estimates at w_t, then the K updates
+    def update_multi(self, seeds: Sequence[int], gs: Sequence[float], lr: float) -> int:
+        """w <- rnd(fma chain over k of -(lr/K) g_k z_k) at the actives (and theta
+        densely, stream 1), then the thresholds and eq. selection_."""
+        K = len(seeds)
+        assert K == len(gs) and K >= 1
+        sd = np.array([s & (2**64 - 1) for s in seeds], dtype=np.uint64)
+        gg = np.array(gs, dtype=np.float32)
+        for l in range(len(self.layers)):
+            w = self.layer_w(l)
+            act = _i64(self.active[l])
+            lib().orc_update_layer_multi(_p(w), _p(act), act.size, int(self.offsets[l]), _p(sd),
+                                         _p(gg), K, float(lr), int(self.bf16))
+        if self.theta is not None:
+            lib().orc_theta_update_multi(_p(self.theta), self.theta.size, 0, _p(sd), _p(gg), K,
+                                         float(lr), int(self.theta_bf16))
+            self.theta_cur = self.theta.copy()
+        self._refresh_thresholds()
+        for l in range(len(self.layers)):
+            act = _i64(self.active[l]).copy()
+            n = lib().orc_shrink_layer(_p(self.layer_w(l)), _p(act), act.size,
+                                       float(self.tau[l]), float(self.xi0))
+            self.active[l] = act[:n].copy()
+        self.last_seed = None
+        return self.k
 
     # -- Algorithm 1: update, then eq. selection_ ---------------------------
     def update(self, g: float, lr: float) -> int:

@@ -383,6 +383,64 @@ def test_theta_bf16_storage_rounds_to_nearest_even(orc):
     assert np.max(np.abs(tu - (t0 - np.float32(1e-2 * 3.0) * zt))) <= np.max(_ulp32(t0)) * 2**16
 
 
+def test_k_direction_update_reduces_to_single_and_sequential_updates(orc):
+    """Algorithm 1 with K directions: (i) K = 1 is the single-direction update
+    (latents, theta, thresholds and mask identical); (ii) with fp32 storage the
+    fp32 fma chain equals K single updates with coefficient lr/K applied one
+    after another (checked through the layer-level update of one direction);
+    (iii) on a quadratic (quantiser bypassed) the update is
+    -(lr/K) sum_k g_k u_k with g_k = u_k'(Av + b)."""
+    shapes = [(8, 32), (16, 16)]
+    D = sum(o * i for o, i in shapes)
+    w0 = synth.latents(21, [D])
+    t0 = synth.latents(22, [40])
+    mk = lambda: orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w0, theta=t0)
+    a, b = mk(), mk()
+    a.build_mask(0.2)
+    b.build_mask(0.2)
+    a.perturb(5, 1e-3, 1)
+    b.perturb(5, 1e-3, 1)
+    assert a.update(0.75, 1e-2) == b.update_multi([5], [0.75], 1e-2)
+    assert np.array_equal(a.w, b.w) and np.array_equal(a.theta, b.theta)
+    assert a.tau == b.tau and all(np.array_equal(x, y) for x, y in zip(a.active, b.active))
+    # (ii) sequential single-direction updates, fp32 storage
+    seeds, gs, lr, K = [11, 12, 13], [0.5, -1.25, 2.0], 3e-2, 3
+    st = mk()
+    st.build_mask(0.2)
+    act = [x.copy() for x in st.active]
+    st.update_multi(seeds, gs, lr)
+    lrk = float(np.float32(np.float32(lr) / np.float32(K)))
+    for l in range(len(shapes)):
+        w = w0[st.offsets[l]: st.offsets[l + 1]].copy()
+        for sd, g in zip(seeds, gs):
+            w = orc.updated_layer_values(w, act[l], st.offsets[l], sd, lrk, g, bf16=False)
+        assert np.array_equal(w, st.layer_w(l)), f"layer {l}"
+    th = t0.copy()
+    for sd, g in zip(seeds, gs):
+        th = orc.theta_updated(th, 0, sd, lrk, g, bf16=False)
+    assert np.array_equal(th, st.theta)
+    # (iii) quadratic over (w, theta), K directions
+    Dw = D
+    A, bb = _quadratic_problem(Dw + t0.size, 9)
+    F = lambda v: 0.5 * v @ A @ v + bb @ v
+    st = mk()
+    st.build_mask(0.2)
+    act = np.concatenate([x + st.offsets[l] for l, x in enumerate(st.active)])
+    v0 = np.concatenate([w0, t0]).astype(np.float64)
+    eps, gsq, step = 1e-3, [], np.zeros(Dw + t0.size)
+    for sd in seeds:
+        u = np.zeros(Dw + t0.size)
+        u[act] = np.concatenate([orc.gauss(sd, st.active[l] + st.offsets[l]) for l in range(len(shapes))])
+        u[Dw:] = orc.gauss_range(sd, 0, t0.size, stream=1)
+        g = (F(v0 + eps * u) - F(v0 - eps * u)) / (2 * eps)
+        assert abs(g - u @ (A @ v0 + bb)) < 1e-6 * (1 + abs(g))
+        gsq.append(np.float32(g))
+        step += -(lr / K) * float(np.float32(g)) * u
+    st.update_multi(seeds, gsq, lr)
+    moved = np.concatenate([st.w, st.theta]).astype(np.float64) - v0
+    assert np.allclose(moved, step, rtol=1e-4, atol=1e-8)
+
+
 def test_smoothed_gradient_of_ternary_objective(orc):
     """F(w) = c'Q(w) with tau held fixed: the Gaussian-smoothed gradient has the
     closed form (c_i/eps)(phi((w_i-tau)/eps) + phi((w_i+tau)/eps)), and the
