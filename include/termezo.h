@@ -152,6 +152,30 @@ termezo_status termezo_update(termezo_ctx* ctx, float proj_grad, float lr,
 termezo_status termezo_update_from_losses(termezo_ctx* ctx, const float* loss_plus,
                                           const float* loss_minus, float eps, float lr);
 
+/* K perturbation directions per step (Algorithm 1: the K two-point estimates
+ * are all taken at w_t, then the K updates are applied).  After the caller has
+ * evaluated F+_k and F-_k for every seed s_k (termezo_perturb(s_k, eps, +1),
+ * loss, termezo_perturb(s_k, eps, -1), loss), one call applies, at every active
+ * latent (and every registered theta value),
+ *   v = fma(a_K, z_K, ... fma(a_1, z_1, w) ...) in fp32,  w <- round(v),
+ * with a_k = -((lr / K) * g_k) in fp32 and z_k regenerated from s_k, then the
+ * shrink of termezo_update.  With fp32 storage this equals the K updates of
+ * Algorithm 1 applied one after another; with bf16 storage the sum is rounded
+ * once.  seeds, proj_grads: host arrays of K entries, 1 <= K <= 32.
+ * k_out as for termezo_update.  Errors: INVALID_ARG (K out of range, null
+ * arrays, non-finite g or lr), STATE (no perturbation since the last update). */
+termezo_status termezo_update_multi(termezo_ctx* ctx, const uint64_t* seeds,
+                                    const float* proj_grads, int32_t K, float lr,
+                                    int64_t* k_out);
+
+/* The same with the projected gradients formed on the device from the losses
+ * (device fp32 [2K]: F+_1, F-_1, F+_2, F-_2, ...): g_k = (F+_k - F-_k) / (2 eps)
+ * in fp32; seeds is a host array.  Never waits.  A non-finite g_k skips the
+ * update and raises a deferred NUMERIC.  Errors as above (eps must be > 0). */
+termezo_status termezo_update_multi_from_losses(termezo_ctx* ctx, const uint64_t* seeds,
+                                                const float* losses, int32_t K, float eps,
+                                                float lr);
+
 /* ---- full-precision parameters theta (Sec. 3; Algorithm 1) ---------------------
  * Algorithm 1 perturbs and updates the full-precision parameters (embeddings,
  * normalisation weights, LM head) densely, together with the masked latents,

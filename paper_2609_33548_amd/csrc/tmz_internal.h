@@ -61,6 +61,18 @@ struct GemmOut {
   int nseg;
 };
 
+// Perturbation directions applied by one update (Algorithm 1: K per step),
+// passed to the update kernels by value; their coefficients a_k live on the
+// device (d_scal[0 .. K-1]).
+constexpr int kMaxK = 32;
+struct SeedList {
+  uint64_t s[kMaxK];
+  int32_t K;
+};
+// d_scal layout: coefficients a_k at [0, kMaxK), the last single-direction g at kMaxK
+constexpr int kScalG = kMaxK;
+constexpr int kScalLen = kMaxK + 2;
+
 // One registered full-precision parameter tensor (theta).
 struct ThetaHost {
   void* data;                        // caller's tensor (clean values, updated in place)
@@ -196,16 +208,21 @@ hipError_t launch_tile_ranges(termezo_ctx* c);            // d_act, d_act_off ->
 hipError_t launch_requant(termezo_ctx* c, int patch);
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se);
 hipError_t launch_set_coeff(termezo_ctx* c, float a);
+// K host coefficients to d_scal[0 .. K-1]
+hipError_t launch_set_coeffs(termezo_ctx* c, const float* a, int K);
 hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float* fm, float eps,
                                     float lr);
-// a from d_scal[0]; the updated values of the actives go to d_wp (list order)
-hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed);
+// a_k = -((lr / K) g_k), g_k = (F+_k - F-_k) / (2 eps) from device losses [2K] (F+_k, F-_k pairs)
+hipError_t launch_coeffs_multi_from_losses(termezo_ctx* c, const float* losses, int K, float eps,
+                                           float lr);
+// coefficients from d_scal[0 .. K-1]; the updated values of the actives go to d_wp (list order)
+hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds);
 // from d_wp (the updated values): d_act -> d_act_tmp, offsets -> tmp
 hipError_t launch_shrink(termezo_ctx* c, int64_t k);
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);
 // theta: both perturbed copies in one pass; in-place update with the coefficient in d_scal[0]
 hipError_t launch_theta_pair(termezo_ctx* c, const ThetaHost& t, uint64_t seed, float eps);
-hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, uint64_t seed);
+hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, const SeedList& seeds);
 hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z, hipStream_t s);
 hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hipStream_t s);
 

@@ -226,7 +226,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_tile_out, (size_t)c->T), "alloc");
   chk(dalloc(&c->d_tile_eqb, (size_t)c->T), "alloc");
   chk(dalloc(&c->d_loss, 4), "alloc");
-  chk(dalloc(&c->d_scal, 4), "alloc");
+  chk(dalloc(&c->d_scal, kScalLen), "alloc");
   chk(hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device),
       "device attribute");
   if (st == TERMEZO_OK) {
@@ -383,13 +383,26 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
 }
 
 namespace {
-// Update at the actives with the coefficient already in d_scal, then the new
+SeedList one_seed(uint64_t s) {
+  SeedList l = {};
+  l.s[0] = s;
+  l.K = 1;
+  return l;
+}
+SeedList seed_list(const uint64_t* s, int32_t K) {
+  SeedList l = {};
+  for (int32_t q = 0; q < K; ++q) l.s[q] = s[q];
+  l.K = K;
+  return l;
+}
+
+// Update at the actives with the coefficients already in d_scal, then the new
 // thresholds and the shrink; the compacted list replaces the old one.
-termezo_status finish_update(termezo_ctx* c, int64_t* k_out) {
-  TMZ_HIP(c, launch_update(c, c->k_bound, c->last_seed));
+termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_out) {
+  TMZ_HIP(c, launch_update(c, c->k_bound, seeds));
   c->theta_pair_valid = false;
   c->theta_sign = 0;
-  for (const ThetaHost& t : c->theta) TMZ_HIP(c, launch_theta_update(c, t, c->last_seed));
+  for (const ThetaHost& t : c->theta) TMZ_HIP(c, launch_theta_update(c, t, seeds));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_clean, c->d_tau, c->d_beta));
   TMZ_HIP(c, launch_shrink(c, c->k_bound));
   std::swap(c->d_act, c->d_act_tmp);
@@ -417,7 +430,7 @@ termezo_status termezo_update(termezo_ctx* c, float proj_grad, float lr, int64_t
   if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
   const float a = -(lr * proj_grad);
   TMZ_HIP(c, launch_set_coeff(c, a));
-  return finish_update(c, k_out);
+  return finish_update(c, one_seed(c->last_seed), k_out);
 }
 
 termezo_status termezo_update_from_losses(termezo_ctx* c, const float* loss_plus,
@@ -428,7 +441,37 @@ termezo_status termezo_update_from_losses(termezo_ctx* c, const float* loss_plus
     return fail(c, TERMEZO_ERR_INVALID_ARG, "eps must be > 0 and lr finite");
   if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
   TMZ_HIP(c, launch_coeff_from_losses(c, loss_plus, loss_minus, eps, lr));
-  return finish_update(c, nullptr);
+  return finish_update(c, one_seed(c->last_seed), nullptr);
+}
+
+termezo_status termezo_update_multi(termezo_ctx* c, const uint64_t* seeds, const float* proj_grads,
+                                    int32_t K, float lr, int64_t* k_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!seeds || !proj_grads || K < 1 || K > kMaxK)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "null seeds / gradients or K outside [1, 32]");
+  if (!finite(lr)) return fail(c, TERMEZO_ERR_INVALID_ARG, "lr must be finite");
+  for (int32_t q = 0; q < K; ++q)
+    if (!finite(proj_grads[q]))
+      return fail(c, TERMEZO_ERR_INVALID_ARG, "projected gradients must be finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  float a[kMaxK];
+  const float cK = lr / (float)K;
+  for (int32_t q = 0; q < K; ++q) a[q] = -(cK * proj_grads[q]);
+  TMZ_HIP(c, launch_set_coeffs(c, a, K));
+  return finish_update(c, seed_list(seeds, K), k_out);
+}
+
+termezo_status termezo_update_multi_from_losses(termezo_ctx* c, const uint64_t* seeds,
+                                                const float* losses, int32_t K, float eps,
+                                                float lr) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!seeds || !losses || K < 1 || K > kMaxK)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "null seeds / losses or K outside [1, 32]");
+  if (!finite(eps) || !(eps > 0.0f) || !finite(lr))
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "eps must be > 0 and lr finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  TMZ_HIP(c, launch_coeffs_multi_from_losses(c, losses, K, eps, lr));
+  return finish_update(c, seed_list(seeds, K), nullptr);
 }
 
 termezo_status termezo_theta_register(termezo_ctx* c, const termezo_theta* params, int32_t n) {

@@ -771,20 +771,29 @@ __global__ void __launch_bounds__(256) k_theta_pair(const T* __restrict__ th, in
   });
 }
 
-// theta <- rnd(fma(a, z, theta)), a = scal[0]; a non-finite coefficient (reported
-// by the coefficient kernel) leaves theta untouched, as for the latents.
+// True when every coefficient of the update is finite (a non-finite one, reported
+// by the coefficient kernel, leaves latents and theta untouched).
+__device__ __forceinline__ bool coeffs_ok(const float* scal, int K) {
+  bool ok = true;
+  for (int q = 0; q < K; ++q) ok = ok && isfinite(scal[q]);
+  return ok;
+}
+
+// theta <- rnd(v), v = fma(a_K, z_K, ... fma(a_1, z_1, theta)) in fp32, a_k = scal[k].
 template <typename T>
 __global__ void __launch_bounds__(256) k_theta_update(T* __restrict__ th, int64_t n, int64_t tid0,
-                                                      uint64_t seed, const float* scal) {
-  const float a = scal[0];
-  if (!isfinite(a)) return;
+                                                      SeedList seeds, const float* scal) {
+  if (!coeffs_ok(scal, seeds.K)) return;
   const bool vec = (tid0 & 3) == 0;
   theta_quads(n, tid0, [&](int64_t q, int64_t e0) {
     float z[4], w[4];
-    gauss_quad(seed, (uint64_t)q, 1u, z);
     load_quad(th, e0, n, vec, w);
+    for (int k = 0; k < seeds.K; ++k) {
+      const float a = scal[k];
+      gauss_quad(seeds.s[k], (uint64_t)q, 1u, z);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) w[r] = fmaf(a, z[r], w[r]);
+      for (int r = 0; r < 4; ++r) w[r] = fmaf(a, z[r], w[r]);
+    }
     store_quad(th, e0, n, vec, w);
   });
 }
@@ -795,7 +804,26 @@ __global__ void __launch_bounds__(256) k_theta_update(T* __restrict__ th, int64_
 // ---------------------------------------------------------------------------
 __global__ void k_set_coeff(float* scal, float a) {
   scal[0] = a;
-  scal[1] = 0.0f;
+  scal[kScalG] = 0.0f;
+}
+
+struct CoefList {
+  float a[kMaxK];
+};
+__global__ void k_set_coeffs(float* scal, CoefList c, int K) {
+  if ((int)threadIdx.x < K) scal[threadIdx.x] = c.a[threadIdx.x];
+}
+
+// K directions: g_k = (F+_k - F-_k) / (2 eps), a_k = -((lr / K) g_k), all fp32.
+__global__ void k_coeffs_multi_from_losses(const float* losses, int K, float eps, float lr,
+                                           float* scal, int32_t* err) {
+  const int k = threadIdx.x;
+  if (k >= K) return;
+  const float g = __fdiv_rn(losses[2 * k] - losses[2 * k + 1], 2.0f * eps);
+  const float c = __fdiv_rn(lr, (float)K);
+  const float a = -(c * g);
+  scal[k] = a;
+  if (!isfinite(a)) atomicOr(err, 2);
 }
 
 // g = (F+ - F-) / (2 eps) and a = -(lr g), in fp32 (eq. spsa).
@@ -804,7 +832,7 @@ __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps,
   const float g = __fdiv_rn(*fp - *fm, 2.0f * eps);
   const float a = -(lr * g);
   scal[0] = a;
-  scal[1] = g;
+  scal[kScalG] = g;
   if (!isfinite(a)) atomicOr(err, 2);
 }
 
@@ -813,12 +841,14 @@ __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps,
 // left untouched and wn holds their current values.
 template <typename T>
 __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __restrict__ act,
-                                                const int64_t* act_off, uint64_t seed,
+                                                const int64_t* act_off, SeedList seeds,
                                                 const float* scal, float* __restrict__ wn) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const float a = scal[0];
-  const bool a_ok = isfinite(a);
+  const uint64_t seed = seeds.s[0];
+  const int K = seeds.K;
+  const bool a_ok = coeffs_ok(scal, K);
   const int64_t k = aoff[st.L];
   const int64_t per = (k + gridDim.x - 1) / gridDim.x;
   const int64_t chunk = (per + 256 * kRun - 1) / (256 * kRun) * (256 * kRun);
@@ -850,7 +880,10 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       if (!one) wv[r] = load1(w, i[r]);
       nv[r] = wv[r];
       if (a_ok) {
-        nv[r] = storage_round(w, fmaf(a, zc.get(seed, (uint64_t)(st.gid0[l] + i[r])), wv[r]));
+        const uint64_t gid = (uint64_t)(st.gid0[l] + i[r]);
+        float v = fmaf(a, zc.get(seed, gid), wv[r]);
+        for (int q = 1; q < K; ++q) v = fmaf(scal[q], gauss_at(seeds.s[q], gid), v);
+        nv[r] = storage_round(w, v);
         if (!one) store1(w, i[r], nv[r]);
       }
       bad |= !in_fix_range(nv[r]);
@@ -1186,15 +1219,29 @@ hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float
   return hipGetLastError();
 }
 
-hipError_t launch_update(termezo_ctx* c, int64_t k, uint64_t seed) {
+hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds) {
   if (k <= 0) return hipSuccess;
   const int64_t g = sparse_grid(k);
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, (const float*)c->d_scal, c->d_wp);
+                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, (const float*)c->d_scal, c->d_wp);
+                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_coeffs(termezo_ctx* c, const float* a, int K) {
+  CoefList cl = {};
+  for (int q = 0; q < K && q < kMaxK; ++q) cl.a[q] = a[q];
+  hipLaunchKernelGGL(k_set_coeffs, dim3(1), dim3(kMaxK), 0, c->stream, c->d_scal, cl, K);
+  return hipGetLastError();
+}
+
+hipError_t launch_coeffs_multi_from_losses(termezo_ctx* c, const float* losses, int K, float eps,
+                                           float lr) {
+  hipLaunchKernelGGL(k_coeffs_multi_from_losses, dim3(1), dim3(kMaxK), 0, c->stream, losses, K,
+                     eps, lr, c->d_scal, c->d_err);
   return hipGetLastError();
 }
 
@@ -1235,15 +1282,15 @@ hipError_t launch_theta_pair(termezo_ctx* c, const ThetaHost& t, uint64_t seed, 
   return hipGetLastError();
 }
 
-hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, uint64_t seed) {
+hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, const SeedList& seeds) {
   if (t.n <= 0) return hipSuccess;
   const unsigned g = theta_grid(c, t.n, t.tid0);
   if (t.dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_theta_update<float>, dim3(g), dim3(256), 0, c->stream, (float*)t.data, t.n,
-                       t.tid0, seed, (const float*)c->d_scal);
+                       t.tid0, seeds, (const float*)c->d_scal);
   else
     hipLaunchKernelGGL(k_theta_update<uint16_t>, dim3(g), dim3(256), 0, c->stream,
-                       (uint16_t*)t.data, t.n, t.tid0, seed, (const float*)c->d_scal);
+                       (uint16_t*)t.data, t.n, t.tid0, seeds, (const float*)c->d_scal);
   return hipGetLastError();
 }
 

@@ -69,6 +69,8 @@ _SIGS = {
     "termezo_active_count": [_P, ctypes.POINTER(_i64)],
     "termezo_gauss": [_P, _u64, _P, _i64, _P],
     "termezo_update_from_losses": [_P, _P, _P, _f32, _f32],
+    "termezo_update_multi": [_P, _P, _P, _i32, _f32, ctypes.POINTER(_i64)],
+    "termezo_update_multi_from_losses": [_P, _P, _P, _i32, _f32, _f32],
     "termezo_theta_register": [_P, ctypes.POINTER(Theta), _i32],
     "termezo_theta_current": [_P, _i32, ctypes.POINTER(_P)],
     "termezo_theta_copy": [_P, _i32, _P],
@@ -263,6 +265,23 @@ class Context:
         out = torch.empty_like(self.theta[i])
         self._check(_lib.termezo_theta_copy(self.handle, i, _ptr(out)), "theta_copy")
         return out
+
+    def update_multi(self, seeds, proj_grads, lr: float, want_k: bool = True) -> Optional[int]:
+        """K directions (Algorithm 1): one update from the K seeds and projected gradients."""
+        K = len(seeds)
+        sd = (ctypes.c_uint64 * K)(*[s & (2**64 - 1) for s in seeds])
+        gg = (ctypes.c_float * K)(*[float(g) for g in proj_grads])
+        k = _i64()
+        self._check(_lib.termezo_update_multi(self.handle, sd, gg, K, lr,
+                                              ctypes.byref(k) if want_k else None), "update_multi")
+        return int(k.value) if want_k else None
+
+    def update_multi_from_losses(self, seeds, losses, eps: float, lr: float):
+        """K directions with g_k formed on the device from losses [2K] (F+_k, F-_k pairs)."""
+        K = len(seeds)
+        sd = (ctypes.c_uint64 * K)(*[s & (2**64 - 1) for s in seeds])
+        self._check(_lib.termezo_update_multi_from_losses(self.handle, sd, _ptr(losses), K, eps, lr),
+                    "update_multi_from_losses")
 
     def mse_loss(self, y, target) -> float:
         out = _f32()
