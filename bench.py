@@ -81,7 +81,7 @@ def measured_traffic():
     return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
 
 
-def cpu_baseline(c, rho, seed=0, theta_n=0):
+def cpu_baseline(c, rho, seed=0, theta_n=0, K=1):
     """The oracle, as it stands, on a bounded sample of the same step; the
     full-step time is extrapolated by operation counts (stated in 'sample')."""
     import numpy as np
@@ -134,7 +134,8 @@ def cpu_baseline(c, rho, seed=0, theta_n=0):
         t_theta = (time.perf_counter() - t0) * theta_n / n_th
     ntok = c["batch"] * c["seq"]
     t_fwd = c["n_blocks"] * c["batch"] * t_block + (ntok / n_pos) * t_head
-    t_step = 2 * t_fwd + t_latent + t_theta
+    # K directions: K perturbation pairs and 2K forwards; the update regenerates K directions
+    t_step = K * (2 * t_fwd + t_latent + t_theta)
     wall = t_latent * nsmp / D + t_block * n_seq + t_head + t_theta * n_th / max(theta_n, 1)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {
@@ -144,6 +145,7 @@ def cpu_baseline(c, rho, seed=0, theta_n=0):
                    f"scaled x{c['n_blocks']} blocks x{c['batch'] / n_seq:g}; LM head+CE on {n_pos} "
                    f"positions scaled x{ntok // n_pos}; two forwards per step"
                    + (f"; theta perturb(+/-)+update on {n_th} ids scaled to {theta_n}" if theta_n else "")
+                   + (f"; all of it x{K} directions" if K > 1 else "")
                    + f"; sample wall {wall:.1f}s"),
         "extrapolated_step_s": t_step,
     }
@@ -459,6 +461,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", choices=["latent", "bitlinear", "all"],
                     help="run the kernel sweeps instead of the step benchmark")
+    ap.add_argument("--K", type=int, default=1,
+                    help="perturbation directions per step (Algorithm 1; the paper's runs use 5)")
     ap.add_argument("--theta", action="store_true",
                     help="also perturb and update the full-precision parameters (tied embedding and "
                          "RMSNorm weights) with the latents, as Algorithm 1 does")
@@ -519,14 +523,23 @@ def main():
     k0, xi0 = ctx.build_mask(args.rho)
     mask_ms = (time.perf_counter() - t0) * 1e3
     print(f"[bench] mask: k0={k0} xi0={xi0:.3e} built in {mask_ms:.1f} ms", flush=True)
-    F = torch.zeros(2, device=dev)
+    F = torch.zeros(2 * args.K, device=dev)
 
     def step(t):
-        ctx.perturb(t, args.eps, 1)
-        model.loss(tok, loss_dev=F[0:1], host=False)
-        ctx.perturb(t, args.eps, -1)
-        model.loss(tok, loss_dev=F[1:2], host=False)
-        ctx.update_from_losses(F[0:1], F[1:2], args.eps, args.lr)
+        if args.K == 1:
+            ctx.perturb(t, args.eps, 1)
+            model.loss(tok, loss_dev=F[0:1], host=False)
+            ctx.perturb(t, args.eps, -1)
+            model.loss(tok, loss_dev=F[1:2], host=False)
+            ctx.update_from_losses(F[0:1], F[1:2], args.eps, args.lr)
+            return
+        seeds = [t * args.K + k for k in range(args.K)]     # seed s_{t,k}
+        for k, sd in enumerate(seeds):
+            ctx.perturb(sd, args.eps, 1)
+            model.loss(tok, loss_dev=F[2 * k: 2 * k + 1], host=False)
+            ctx.perturb(sd, args.eps, -1)
+            model.loss(tok, loss_dev=F[2 * k + 1: 2 * k + 2], host=False)
+        ctx.update_multi_from_losses(seeds, F, args.eps, args.lr)
 
     for t in range(args.warmup):
         step(t)
@@ -575,7 +588,7 @@ def main():
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         cpu = (cpu_baseline_full(c, args.rho, theta=args.theta) if args.config == "tiny"
-               else cpu_baseline(c, args.rho, theta_n=n_theta))
+               else cpu_baseline(c, args.rho, theta_n=n_theta, K=args.K))
         print(f"[bench] cpu baseline sample took {time.perf_counter() - t0:.1f} s", flush=True)
 
     metric = METRIC if args.config == "2b" else {
@@ -596,8 +609,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": (f"termezo_zo_step_tiny_decoder" if args.config == "tiny"
                                 else f"termezo_zo_step_bitnet_{args.config}")
-                               + ("_with_theta" if args.theta else ""),
-                   "theta_params": n_theta,
+                               + ("_with_theta" if args.theta else "")
+                               + (f"_K{args.K}" if args.K > 1 else ""),
+                   "theta_params": n_theta, "directions_per_step": args.K,
                    **{k: v for k, v in c.items() if k not in ("rho", "lr", "fp32")},
                    "tokens_per_forward": c["batch"] * c["seq"], "latents": D,
                    "mask_ratio": args.rho, "k0": k0, "k_final": k_final, "eps": args.eps,
