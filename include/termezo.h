@@ -112,6 +112,17 @@ termezo_status termezo_build_mask(termezo_ctx* ctx, float rho0, float delta,
 termezo_status termezo_perturb(termezo_ctx* ctx, uint64_t seed, float eps,
                                int32_t sign);
 
+/* Requantisation strategy of termezo_perturb (the codes are the same either way).
+ * By default a perturbation rewrites only the codes of the active latents while
+ * no frozen code can change: every frozen latent is tracked to lie at least a
+ * bound m^l (exactly, from xi0 and the threshold drift) from the threshold its
+ * code was computed with, and a layer whose perturbed threshold tau' moves by
+ * less than m^l keeps its frozen codes; other layers, and every layer when the
+ * active set exceeds 1/256 of the latents, are requantised densely.
+ * always_dense != 0 requantises every latent of every layer on each call
+ * (for measurement).  Errors: INVALID_ARG (null ctx). */
+termezo_status termezo_set_dense_requant(termezo_ctx* ctx, int32_t always_dense);
+
 /* BitLinear forward of one projection on its current codes (Sec. 1 and 3:
  * ternary weights with 8-bit activations).  x: device [M][d_in] (F32 or BF16);
  * y: device [M][d_out] (F32 or BF16).  Per token row m: a_m = max_k |x[m][k]|,

@@ -39,6 +39,9 @@ struct DevState {
   float* beta;                       // [L]
   float* tau_cur;                    // [L] threshold of the current codes
   float* beta_cur;                   // [L]
+  float* tau_ref;                    // [L] threshold the frozen codes were computed with
+  double* mref;                      // [L] lower bound of the frozen weights' distance to tau_ref
+  int32_t* need;                     // [L] 1: the layer needs the dense requantisation now
   int32_t* err;                      // deferred numeric error flag
   int32_t L;
   int64_t T;                         // number of tiles
@@ -118,7 +121,13 @@ struct termezo_ctx {
   float* d_beta = nullptr;
   float* d_tau_cur = nullptr;
   float* d_beta_cur = nullptr;
+  float* d_tau_ref = nullptr;
+  double* d_mref = nullptr;
+  int32_t* d_need = nullptr;
+  int64_t* d_dense_off = nullptr;    // [L+1] tiles of the layers needing the dense pass
   int32_t* d_err = nullptr;
+  int dense_requant = 0;             // 1: every perturbation re-quantises every latent
+  double xi_lo = 0.0;                // lower bound of the frozen weights' exact distance at build
 
   // mask
   uint32_t* d_act = nullptr;         // active local indices, ascending, layer after layer
@@ -185,6 +194,9 @@ struct termezo_ctx {
     s.beta = d_beta;
     s.tau_cur = d_tau_cur;
     s.beta_cur = d_beta_cur;
+    s.tau_ref = d_tau_ref;
+    s.mref = d_mref;
+    s.need = d_need;
     s.err = d_err;
     s.L = L;
     s.T = T;
@@ -206,6 +218,16 @@ hipError_t launch_mask_compact_write(termezo_ctx* c, int inclusive);   // -> act
 hipError_t launch_tile_ranges(termezo_ctx* c);            // d_act, d_act_off -> d_tile_act
 // codes of w with tau_cur; with patch, the actives' codes from their perturbed values d_wp
 hipError_t launch_requant(termezo_ctx* c, int patch);
+// Guarded requantisation of a perturbation: layers whose threshold moved less than
+// the frozen weights' distance keep their frozen codes and get only the actives'
+// codes (sparse); the others are re-quantised densely.
+hipError_t launch_requant_guarded(termezo_ctx* c, int force);
+// after a dense requantisation of every layer at tau_cur (mask build): frozen codes refer
+// to tau_cur; every frozen weight is at least xi_lo from it
+hipError_t launch_ref_init(termezo_ctx* c, double xi_lo);
+// after an update: weights leaving the set are frozen at tau_ref (their distance to the new
+// clean threshold exceeds xi0, so to tau_ref at least xi_lo - |tau - tau_ref|)
+hipError_t launch_ref_after_update(termezo_ctx* c, double xi_lo);
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se);
 hipError_t launch_set_coeff(termezo_ctx* c, float a);
 // K host coefficients to d_scal[0 .. K-1]

@@ -118,7 +118,7 @@ __device__ __forceinline__ void store8(float* p, const float v[8]) {
   reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
 }
 
-template <int MODE, typename T>
+template <int MODE, typename T, bool WEIGHTED = false>
 __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* __restrict__ u,
                                              int64_t M, int64_t K, float eps, int8_t* xq,
                                              float* xs, T* xf) {
@@ -162,13 +162,21 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
     float a = 0.0f;
 #pragma unroll
     for (int c = 0; c < kRowChunks; ++c) {
-      float wt[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
-      const int idx = c * 64 + lane;
-      if (u && idx < nch) load8(u + idx * 8, wt);
+      if constexpr (WEIGHTED) {            // RMSNorm weight row (the u argument)
+        float wt[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+        const int idx = c * 64 + lane;
+        if (idx < nch) load8(u + idx * 8, wt);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        v[c][j] = v[c][j] * r * wt[j];
-        a = fmaxf(a, fabsf(v[c][j]));
+        for (int j = 0; j < 8; ++j) {
+          v[c][j] = v[c][j] * r * wt[j];
+          a = fmaxf(a, fabsf(v[c][j]));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          v[c][j] = v[c][j] * r;
+          a = fmaxf(a, fabsf(v[c][j]));
+        }
       }
     }
     if (MODE == kRowNormStore) {
@@ -1540,23 +1548,24 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   // RMSNorm (weight row wr of the norm weights, one when there are none), then
   // the quantiser, or stored (the LM-head input)
   auto rmsq = [&](int8_t* xq, float* xs, void* xf, int wr) {
+#define TMZ_NORM(T, MD, W)                                                                   \
+  hipLaunchKernelGGL((k_row<MD, T, W>), dim3(rowg), dim3(256), 0, s, (const T*)m->h,          \
+                     nrm ? (const T*)nrm + (int64_t)wr * d : (const T*)nullptr, M, d, cf.norm_eps, \
+                     xq, xs, (T*)xf)
     if (bf) {
-      const uint16_t* w = nrm ? (const uint16_t*)nrm + (int64_t)wr * d : nullptr;
-      if (xf)
-        hipLaunchKernelGGL((k_row<kRowNormStore, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                           (const uint16_t*)m->h, w, M, d, cf.norm_eps, xq, xs, (uint16_t*)xf);
-      else
-        hipLaunchKernelGGL((k_row<kRowNormQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                           (const uint16_t*)m->h, w, M, d, cf.norm_eps, xq, xs, (uint16_t*)nullptr);
+      if (xf) {
+        if (nrm) TMZ_NORM(uint16_t, kRowNormStore, true); else TMZ_NORM(uint16_t, kRowNormStore, false);
+      } else {
+        if (nrm) TMZ_NORM(uint16_t, kRowNormQuant, true); else TMZ_NORM(uint16_t, kRowNormQuant, false);
+      }
     } else {
-      const float* w = nrm ? (const float*)nrm + (int64_t)wr * d : nullptr;
-      if (xf)
-        hipLaunchKernelGGL((k_row<kRowNormStore, float>), dim3(rowg), dim3(256), 0, s,
-                           (const float*)m->h, w, M, d, cf.norm_eps, xq, xs, (float*)xf);
-      else
-        hipLaunchKernelGGL((k_row<kRowNormQuant, float>), dim3(rowg), dim3(256), 0, s,
-                           (const float*)m->h, w, M, d, cf.norm_eps, xq, xs, (float*)nullptr);
+      if (xf) {
+        if (nrm) TMZ_NORM(float, kRowNormStore, true); else TMZ_NORM(float, kRowNormStore, false);
+      } else {
+        if (nrm) TMZ_NORM(float, kRowNormQuant, true); else TMZ_NORM(float, kRowNormQuant, false);
+      }
     }
+#undef TMZ_NORM
     chk(hipGetLastError());
   };
   for (int blk = 0; blk < cf.n_blocks; ++blk) {

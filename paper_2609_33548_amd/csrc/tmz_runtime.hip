@@ -114,6 +114,10 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_beta);
   dfree(c->d_tau_cur);
   dfree(c->d_beta_cur);
+  dfree(c->d_tau_ref);
+  dfree(c->d_mref);
+  dfree(c->d_need);
+  dfree(c->d_dense_off);
   dfree(c->d_err);
   dfree(c->d_act);
   dfree(c->d_act_tmp);
@@ -217,6 +221,10 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_beta, n_layers), "alloc");
   chk(dalloc(&c->d_tau_cur, n_layers), "alloc");
   chk(dalloc(&c->d_beta_cur, n_layers), "alloc");
+  chk(dalloc(&c->d_tau_ref, n_layers), "alloc");
+  chk(dalloc(&c->d_mref, n_layers), "alloc");
+  chk(dalloc(&c->d_need, n_layers), "alloc");
+  chk(dalloc(&c->d_dense_off, (size_t)n_layers + 1), "alloc");
   chk(dalloc(&c->d_err, 1), "alloc");
   chk(dalloc(&c->d_act_off, (size_t)n_layers + 1), "alloc");
   chk(dalloc(&c->d_act_off_tmp, (size_t)n_layers + 1), "alloc");
@@ -314,6 +322,10 @@ termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32
   float xi0;
   std::memcpy(&xi0, &sel.prefix, sizeof(float));
   c->xi0 = xi0;
+  // every inactive weight has fp32 distance >= xi0 to the clean threshold the codes were
+  // just computed with, so an exact distance >= xi0 - ulp(xi0) / 2
+  c->xi_lo = (double)xi0 - 0.5 * ((double)std::nextafter(xi0, INFINITY) - (double)xi0);
+  TMZ_HIP(c, launch_ref_init(c, c->xi_lo));
   c->k0 = total;
   c->k_bound = total;
   c->tie_inclusive = inclusive;
@@ -333,7 +345,11 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
   TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se));
   TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
-  TMZ_HIP(c, launch_requant(c, 1));
+  // guarded requantisation: the actives' codes only, while no frozen code can change
+  // (dense on request, or when the active set exceeds 1/256 of the latents: there the
+  // scattered code-word updates cost more than the dense stream)
+  const int force = c->dense_requant || c->k_bound * 256 > c->D;
+  TMZ_HIP(c, launch_requant_guarded(c, force));
   // theta: both signs of the pair come from one pass, so the second evaluation
   // of a pair (same seed and eps) only switches to the other copy
   if (!c->theta.empty() && sign != 0 &&
@@ -408,6 +424,7 @@ termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_o
   std::swap(c->d_act, c->d_act_tmp);
   std::swap(c->d_act_off, c->d_act_off_tmp);
   TMZ_HIP(c, launch_tile_ranges(c));
+  TMZ_HIP(c, launch_ref_after_update(c, c->xi_lo));
   c->codes_valid = false;
   c->pending_perturb = false;
   if (k_out) {
@@ -472,6 +489,12 @@ termezo_status termezo_update_multi_from_losses(termezo_ctx* c, const uint64_t* 
   if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
   TMZ_HIP(c, launch_coeffs_multi_from_losses(c, losses, K, eps, lr));
   return finish_update(c, seed_list(seeds, K), nullptr);
+}
+
+termezo_status termezo_set_dense_requant(termezo_ctx* c, int32_t always_dense) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  c->dense_requant = always_dense ? 1 : 0;
+  return TERMEZO_OK;
 }
 
 termezo_status termezo_theta_register(termezo_ctx* c, const termezo_theta* params, int32_t n) {

@@ -466,14 +466,13 @@ __device__ __forceinline__ uint32_t join_word(uint32_t w) {
 // one load instruction covers 1 KB of consecutive bytes; a code word's chunks
 // (2 for bf16, 4 for fp32) sit in adjacent lanes and are joined by shuffles.
 template <typename T, bool PATCH>
-__global__ void __launch_bounds__(kRqThreads) k_requant_tile(DevState st, const uint32_t* act,
-                                                            const float* wp) {
+__device__ __forceinline__ void requant_tile(const DevState& st, const uint32_t* act,
+                                             const float* wp, int64_t t) {
   constexpr int EPC = 16 / (int)sizeof(T);       // elements per 16-byte chunk
   constexpr int CPW = 16 / EPC;                  // chunks per code word
   constexpr int CPT = kTile / EPC / kRqThreads;  // chunks per thread
   __shared__ uint32_t words[kTile / 16];
   const int tid = threadIdx.x;
-  const int64_t t = blockIdx.x;
   const int l = st.tile_layer[t];
   const int64_t start = st.tile_start[t];
   const int cnt = (int)min((int64_t)kTile, st.n[l] - start);
@@ -556,6 +555,32 @@ __global__ void __launch_bounds__(kRqThreads) k_requant_tile(DevState st, const 
   for (int v = 0; v < CPT; ++v) {
     const int c = v * kRqThreads + tid;
     if (owner && c * EPC < cnt) out[c / CPW] = wd[v];
+  }
+}
+
+// One tile per block: every tile of every layer (mask build, dense requantisation).
+template <typename T, bool PATCH>
+__global__ void __launch_bounds__(kRqThreads) k_requant_tile(DevState st, const uint32_t* act,
+                                                            const float* wp) {
+  requant_tile<T, PATCH>(st, act, wp, blockIdx.x);
+}
+
+// The tiles of the layers the guard marked for the dense requantisation: dense_off[l]
+// is the position of layer l's first tile in that list (dense_off[L] tiles in all);
+// blocks stride over the list (none when every layer kept its frozen codes).
+template <typename T>
+__global__ void __launch_bounds__(kRqThreads) k_requant_list(DevState st, const uint32_t* act,
+                                                            const float* wp,
+                                                            const int64_t* dense_off) {
+  const int64_t total = dense_off[st.L];
+  for (int64_t i = blockIdx.x; i < total; i += gridDim.x) {
+    int lo = 0, hi = st.L - 1;                   // last layer with dense_off <= i
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (dense_off[mid] <= i) lo = mid; else hi = mid - 1;
+    }
+    __syncthreads();                             // the previous tile's LDS words are consumed
+    requant_tile<T, true>(st, act, wp, st.tile0[lo] + (i - dense_off[lo]));
   }
 }
 
@@ -898,6 +923,111 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
 }
 
 // ---------------------------------------------------------------------------
+// Guarded requantisation.  The codes of frozen (inactive) weights of layer l are
+// Q(w; tau_ref[l]); every frozen weight lies at least mref[l] (exactly, in fp64)
+// from tau_ref[l].  A perturbed threshold tau' with |tau' - tau_ref| < mref
+// cannot change a frozen code (the sign of |w| - tau is the same at tau_ref and
+// tau'), so the codes equal the dense requantisation at tau' once the actives'
+// codes are rewritten.  Otherwise the layer is requantised densely, its frozen
+// codes then refer to tau' and no bound is kept for it (mref < 0: dense until the
+// next mask build).
+// ---------------------------------------------------------------------------
+// One block: need[l] for every layer, then dense_off (the layers needing the dense
+// pass, their tiles listed in layer order).
+__global__ void __launch_bounds__(256) k_guard(DevState st, int force, int64_t* dense_off) {
+  __shared__ int64_t cnt[kMaxLayers + 1];
+  for (int l = threadIdx.x; l < st.L; l += blockDim.x) {
+    const float tc = st.tau_cur[l], tr = st.tau_ref[l];
+    const bool keep = !force && (tc == tr || fabs((double)tc - (double)tr) < st.mref[l]);
+    st.need[l] = keep ? 0 : 1;
+    if (!keep) {
+      st.tau_ref[l] = tc;
+      st.mref[l] = -1.0;
+    }
+    cnt[l] = keep ? 0 : (l + 1 < st.L ? st.tile0[l + 1] : st.T) - st.tile0[l];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {                        // exclusive scan in LDS
+    int64_t run = 0;
+    for (int l = 0; l < st.L; ++l) {
+      const int64_t c = cnt[l];
+      cnt[l] = run;
+      run += c;
+    }
+    cnt[st.L] = run;
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l <= st.L; l += blockDim.x) dense_off[l] = cnt[l];
+}
+
+// After a dense requantisation of every layer at tau_cur (the mask build): every
+// inactive weight's fp32 distance is at least xi0, so its exact distance is at
+// least xi_lo = xi0 - ulp(xi0)/2.
+__global__ void k_ref_init(DevState st, double xi_lo) {
+  const int l = blockIdx.x * blockDim.x + threadIdx.x;
+  if (l >= st.L) return;
+  st.tau_ref[l] = st.tau_cur[l];
+  st.mref[l] = xi_lo;
+}
+
+// After an update: a weight leaving the set has fp32 distance above xi0 to the new
+// clean threshold tau, so it lies at least xi_lo - |tau - tau_ref| from tau_ref
+// (its code is written at tau_ref by the shrink).
+__global__ void k_ref_after_update(DevState st, double xi_lo) {
+  const int l = blockIdx.x * blockDim.x + threadIdx.x;
+  if (l >= st.L || st.mref[l] < 0.0) return;
+  const double m = xi_lo - fabs((double)st.tau[l] - (double)st.tau_ref[l]);
+  st.mref[l] = fmin(st.mref[l], m);
+}
+
+// Rewrite the 2-bit code of local index i of layer l (other fields of the word may
+// be written concurrently by other threads: only the changed bits are flipped, with
+// one atomic; the word is read past the L1 cache).
+__device__ __forceinline__ void set_code(uint32_t* codes, int64_t code_off, uint32_t i,
+                                         uint32_t code) {
+  uint32_t* wp = codes + code_off + (i >> 4);
+  const int sh = code_shift((int)(i & 15u));
+  const uint32_t cur = __hip_atomic_load(wp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t diff = (((cur >> sh) & 3u) ^ code) << sh;
+  if (diff) atomicXor(wp, diff);
+}
+
+// The actives' codes at their perturbed values, for the layers that kept their frozen
+// codes.  Each thread walks kRun consecutive list entries.  An entry whose code word
+// holds no other active (its list neighbours lie in other words) is the word's only
+// writer and updates it with a plain read-modify-write; shared words take the atomic.
+__global__ void __launch_bounds__(256) k_patch_codes(DevState st, const uint32_t* __restrict__ act,
+                                                     const int64_t* act_off,
+                                                     const float* __restrict__ wp) {
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  load_offsets(aoff, act_off, st.L);
+  const int64_t k = aoff[st.L];
+  for (int64_t j0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kRun; j0 < k;
+       j0 += (int64_t)gridDim.x * 256 * kRun) {
+    uint32_t i[kRun + 2];                        // i[0], i[kRun+1]: the run's list neighbours
+    const int n = run_entries(act, j0, k, i + 1);
+    i[0] = j0 > 0 ? act[j0 - 1] : 0xFFFFFFFFu;
+    i[n + 1] = j0 + n < k ? act[j0 + n] : 0xFFFFFFFFu;
+    int l = layer_of(aoff, st.L, j0);
+    for (int r = 1; r <= n; ++r) {
+      const int64_t j = j0 + r - 1;
+      while (aoff[l + 1] <= j) ++l;
+      if (st.need[l]) continue;
+      const uint32_t idx = i[r], code = ternary_code(wp[j], st.tau_cur[l]);
+      const bool sole = (i[r - 1] >> 4) != (idx >> 4) && (i[r + 1] >> 4) != (idx >> 4);
+      if (sole) {
+        uint32_t* wptr = st.codes + st.code_off[l] + (idx >> 4);
+        const int sh = code_shift((int)(idx & 15u));
+        const uint32_t cur = *wptr, nw = (cur & ~(3u << sh)) | (code << sh);
+        if (nw != cur) *wptr = nw;
+      } else {
+        set_code(st.codes, st.code_off[l], idx, code);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Shrink-only set update: keep the actives with ||w| - tau| <= xi0.
 // Block b handles entries [b * 256 per, (b+1) * 256 per); thread t takes
 // entries b * 256 per + 256 r + t (r < per <= kShrinkPer), so reads and writes
@@ -1027,17 +1157,29 @@ __global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_
     const int64_t pos = boff + cnt[4 * r + wid] + __popcll(b & below);
     while (aoff[l + 1] <= j) ++l;
     if (j == aoff[l]) act_off_new[l] = pos;   // first entry of layer l
-    if (keep) act_new[pos] = act[j];
+    if (keep)
+      act_new[pos] = act[j];
+    else                                      // frozen from now on: its code at tau_ref
+      set_code(st.codes, st.code_off[l], act[j], ternary_code(wn[j], st.tau_ref[l]));
   }
 }
 
-// Layers that were empty before the shrink take the next layer's offset.
-__global__ void k_shrink_offsets(const int64_t* act_off, int64_t* act_off_new, int L,
-                                 const int64_t* total) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  act_off_new[L] = *total;
-  for (int l = L - 1; l >= 0; --l)
-    if (act_off[l] == act_off[l + 1]) act_off_new[l] = act_off_new[l + 1];
+// Layers that were empty before the shrink take the next layer's offset (one block:
+// both offset arrays in LDS, the backward pass over the layers there).
+__global__ void __launch_bounds__(256) k_shrink_offsets(const int64_t* act_off,
+                                                        int64_t* act_off_new, int L,
+                                                        const int64_t* total) {
+  __shared__ int64_t o[kMaxLayers + 1], n[kMaxLayers + 1];
+  for (int l = threadIdx.x; l <= L; l += blockDim.x) {
+    o[l] = act_off[l];
+    n[l] = l == L ? *total : act_off_new[l];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0)
+    for (int l = L - 1; l >= 0; --l)
+      if (o[l] == o[l + 1]) n[l] = n[l + 1];
+  __syncthreads();
+  for (int l = threadIdx.x; l <= L; l += blockDim.x) act_off_new[l] = n[l];
 }
 
 // ---------------------------------------------------------------------------
@@ -1166,13 +1308,19 @@ hipError_t launch_mask_compact_write(termezo_ctx* c, int inclusive) {
   return hipGetLastError();
 }
 
+static inline int64_t sparse_grid(int64_t k) {
+  return max((int64_t)1, min((int64_t)8192, (k + 256 * kRun - 1) / (256 * kRun)));
+}
+
 hipError_t launch_requant(termezo_ctx* c, int patch) {
   const dim3 g((unsigned)c->T), b(kRqThreads);
   if (c->dtype == TERMEZO_F32) {
     if (patch)
-      hipLaunchKernelGGL((k_requant_tile<float, true>), g, b, 0, c->stream, c->dev(), c->d_act, c->d_wp);
+      hipLaunchKernelGGL((k_requant_tile<float, true>), g, b, 0, c->stream, c->dev(), c->d_act,
+                         c->d_wp);
     else
-      hipLaunchKernelGGL((k_requant_tile<float, false>), g, b, 0, c->stream, c->dev(), c->d_act, c->d_wp);
+      hipLaunchKernelGGL((k_requant_tile<float, false>), g, b, 0, c->stream, c->dev(), c->d_act,
+                         c->d_wp);
   } else {
     if (patch)
       hipLaunchKernelGGL((k_requant_tile<uint16_t, true>), g, b, 0, c->stream, c->dev(), c->d_act,
@@ -1184,6 +1332,38 @@ hipError_t launch_requant(termezo_ctx* c, int patch) {
   return hipGetLastError();
 }
 
+hipError_t launch_requant_guarded(termezo_ctx* c, int force) {
+  hipLaunchKernelGGL(k_guard, dim3(1), dim3(256), 0, c->stream, c->dev(), force, c->d_dense_off);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (force) return launch_requant(c, 1);      // every layer: one block per tile
+  const unsigned g = (unsigned)min(c->T, (int64_t)(c->n_cu > 0 ? 8 * c->n_cu : 2048));
+  if (c->dtype == TERMEZO_F32)
+    hipLaunchKernelGGL((k_requant_list<float>), dim3(g), dim3(kRqThreads), 0, c->stream, c->dev(),
+                       c->d_act, c->d_wp, (const int64_t*)c->d_dense_off);
+  else
+    hipLaunchKernelGGL((k_requant_list<uint16_t>), dim3(g), dim3(kRqThreads), 0, c->stream,
+                       c->dev(), c->d_act, c->d_wp, (const int64_t*)c->d_dense_off);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (c->k_bound > 0)
+    hipLaunchKernelGGL(k_patch_codes, dim3((unsigned)sparse_grid(c->k_bound)), dim3(256), 0,
+                       c->stream, c->dev(), c->d_act, c->d_act_off, c->d_wp);
+  return hipGetLastError();
+}
+
+hipError_t launch_ref_init(termezo_ctx* c, double xi_lo) {
+  hipLaunchKernelGGL(k_ref_init, dim3((unsigned)((c->L + 255) / 256)), dim3(256), 0, c->stream,
+                     c->dev(), xi_lo);
+  return hipGetLastError();
+}
+
+hipError_t launch_ref_after_update(termezo_ctx* c, double xi_lo) {
+  hipLaunchKernelGGL(k_ref_after_update, dim3((unsigned)((c->L + 255) / 256)), dim3(256), 0,
+                     c->stream, c->dev(), xi_lo);
+  return hipGetLastError();
+}
+
 hipError_t launch_tile_ranges(termezo_ctx* c) {
   const int64_t g = max((int64_t)1, min((int64_t)2048, (c->T + 1 + 255) / 256));
   hipLaunchKernelGGL(k_tile_ranges, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
@@ -1191,9 +1371,6 @@ hipError_t launch_tile_ranges(termezo_ctx* c) {
   return hipGetLastError();
 }
 
-static inline int64_t sparse_grid(int64_t k) {
-  return max((int64_t)1, min((int64_t)8192, (k + 256 * kRun - 1) / (256 * kRun)));
-}
 
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se) {
   if (k <= 0) return hipSuccess;
@@ -1258,7 +1435,7 @@ hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
   hipLaunchKernelGGL(k_shrink_write, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act,
                      c->d_act_off, c->d_wp, c->xi0, per, c->d_blk_cnt, c->d_act_tmp,
                      c->d_act_off_tmp);
-  hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(1), 0, c->stream, c->d_act_off,
+  hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(256), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
   return hipGetLastError();
 }

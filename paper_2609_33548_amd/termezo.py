@@ -72,6 +72,7 @@ _SIGS = {
     "termezo_update_multi": [_P, _P, _P, _i32, _f32, ctypes.POINTER(_i64)],
     "termezo_update_multi_from_losses": [_P, _P, _P, _i32, _f32, _f32],
     "termezo_theta_register": [_P, ctypes.POINTER(Theta), _i32],
+    "termezo_set_dense_requant": [_P, _i32],
     "termezo_theta_current": [_P, _i32, ctypes.POINTER(_P)],
     "termezo_theta_copy": [_P, _i32, _P],
     "termezo_model_create": [_P, _P, _P, ctypes.POINTER(_P)],
@@ -240,6 +241,11 @@ class Context:
         """Device-side g = (F+ - F-) / (2 eps) and update; no host round trip."""
         self._check(_lib.termezo_update_from_losses(self.handle, _ptr(loss_plus), _ptr(loss_minus),
                                                     eps, lr), "update_from_losses")
+
+    def set_dense_requant(self, on: bool):
+        """Re-quantise every latent on each perturbation (default: only the actives'
+        codes while the threshold drift guard proves the frozen codes unchanged)."""
+        self._check(_lib.termezo_set_dense_requant(self.handle, int(bool(on))), "set_dense_requant")
 
     def theta_register(self, tensors):
         """Register full-precision parameters theta (contiguous fp32 or bf16 device

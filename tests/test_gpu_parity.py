@@ -92,7 +92,8 @@ def test_build_mask_matches_oracle(orc, shapes, bf16, rho0, inclusive):
 
 @pytest.mark.parametrize("shapes", [[(256, 256)], C2_LAYERS], ids=["c1", "c2"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-@pytest.mark.parametrize("rho0", [0.05, 0.9999, 1.0])   # 0.9999: fully active tiles after ragged ones
+# 0.002: the guarded path (actives' codes only); 0.9999: fully active tiles after ragged ones
+@pytest.mark.parametrize("rho0", [0.002, 0.05, 0.9999, 1.0])
 def test_perturb_codes_match_oracle(orc, shapes, bf16, rho0):
     print(f"perturb shapes={len(shapes)} bf16={bf16} rho0={rho0}", flush=True)
     ref, ctx, tensors = _setup(orc, shapes, bf16, seed=2)
@@ -189,7 +190,7 @@ def test_bitlinear_large_grid_sampled_rows(orc, M, K, N, ydt):
 
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
-@pytest.mark.parametrize("rho0", [0.01, 0.9999, 1.0])
+@pytest.mark.parametrize("rho0", [0.002, 0.01, 0.9999, 1.0])   # 0.002: guarded (actives-only) path
 def test_update_and_shrink_match_oracle(orc, bf16, rho0):
     print(f"update bf16={bf16} rho0={rho0}", flush=True)
     ref, ctx, tensors = _setup(orc, C2_LAYERS, bf16, seed=5)
@@ -284,3 +285,40 @@ def test_state_and_numeric_errors(orc):
     w[3, 5] = 0.0
     ctx.build_mask(0.1)                        # recovers once the latent is fixed
     ctx.close()
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("rho0,eps", [(0.003, 1e-3),    # drift far below xi0: actives only
+                                      (0.002, 0.5)])    # drift above xi0: dense fallback
+def test_guarded_requant_equals_dense_requant(orc, bf16, rho0, eps):
+    """The default perturbation (actives' codes only while the threshold-drift
+    guard proves every frozen code unchanged, dense otherwise) gives the codes of
+    the dense requantisation: two contexts on the same latents, one forced dense,
+    against each other and the oracle over five steps (perturb +, -, 0, update)."""
+    print(f"guarded requant bf16={bf16} rho0={rho0} eps={eps}", flush=True)
+    shapes = [(256, 256), (128, 512), (384, 128)]
+    ref, ctx, tensors = _setup(orc, shapes, bf16, seed=41)
+    _, ctx_d, tensors_d = _setup(orc, shapes, bf16, seed=41)
+    ctx_d.set_dense_requant(True)
+    ctx.build_mask(rho0)
+    ctx_d.build_mask(rho0)
+    ref.build_mask(rho0)
+    for t in range(5):
+        for sign in (1, -1, 0):
+            ctx.perturb(t, eps, sign)
+            ctx_d.perturb(t, eps, sign)
+            codes, taus, betas = ref.perturb(t, eps, sign)
+            for l in range(len(shapes)):
+                got, dense = ctx.codes(l), ctx_d.codes(l)
+                assert np.array_equal(dense, codes[l]), f"step {t} sign {sign} layer {l}: dense path"
+                bad = np.count_nonzero(got != codes[l])
+                assert bad == 0, f"step {t} sign {sign} layer {l}: {bad} codes differ"
+        g = 0.5 - 0.3 * t
+        ctx.perturb(t, eps, 1)
+        ctx_d.perturb(t, eps, 1)
+        ref.perturb(t, eps, 1)
+        assert ctx.update(g, 1e-2) == ctx_d.update(g, 1e-2) == ref.update(g, 1e-2)
+        assert np.array_equal(_latents_host(tensors), ref.w)
+        assert np.array_equal(_latents_host(tensors_d), ref.w)
+    ctx.close()
+    ctx_d.close()
