@@ -163,6 +163,34 @@ termezo_status termezo_update(termezo_ctx* ctx, float proj_grad, float lr,
 termezo_status termezo_update_from_losses(termezo_ctx* ctx, const float* loss_plus,
                                           const float* loss_minus, float eps, float lr);
 
+/* ---- memory-optimal storage (Sec. 5 eq. memory: frozen weights as 2-bit codes) ----
+ * After the mask is built, termezo_compact copies the active latents into a
+ * library-owned array in list order; from then on the context never reads or
+ * writes the caller's latent tensors (they may be freed).  Frozen latents live
+ * on only as their ternary codes.  Perturbation, update and shrink work on the
+ * compact array (contiguous instead of scattered accesses).  The codes are
+ * those of the dense semantics while every layer's threshold stays within its
+ * frozen margin (see termezo_set_dense_requant); if a perturbed threshold ever
+ * moves farther, the frozen codes are kept and a deferred NUMERIC error names
+ * the condition.  termezo_build_mask then fails with STATE (it needs the full
+ * latents).  Errors: STATE (no mask, already compact, pending perturbation),
+ * OOM.  Waits for the stream. */
+termezo_status termezo_compact(termezo_ctx* ctx);
+
+/* Values (fp32, host) of one layer's active latents in list order (ascending
+ * local index); *n receives the count.  Works with and without compact mode.
+ * Errors: INVALID_ARG (layer, null n, cap below the count), STATE (no mask).
+ * Waits for the stream. */
+termezo_status termezo_active_values(termezo_ctx* ctx, int32_t layer, float* values,
+                                     int64_t cap, int64_t* n);
+
+/* Device memory of the method's state (host values, nullable): library_bytes =
+ * the library-owned buffers (codes, mask lists, thresholds, tile tables,
+ * compact latents, theta copies, scratch); latent_bytes = the caller's latent
+ * tensors the context still needs (0 in compact mode). */
+termezo_status termezo_memory_footprint(termezo_ctx* ctx, int64_t* library_bytes,
+                                        int64_t* latent_bytes);
+
 /* K perturbation directions per step (Algorithm 1: the K two-point estimates
  * are all taken at w_t, then the K updates are applied).  After the caller has
  * evaluated F+_k and F-_k for every seed s_k (termezo_perturb(s_k, eps, +1),

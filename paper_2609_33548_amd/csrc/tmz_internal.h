@@ -138,6 +138,11 @@ struct termezo_ctx {
   std::vector<int64_t> h_act_off;    // host copy, valid when act_off_host_valid
   bool act_off_host_valid = false;
   float* d_wp = nullptr;             // perturbed values at the actives (act_cap)
+  // compact mode: the active latents in list order (latent dtype), library-owned; the
+  // caller's latent tensors are no longer read or written
+  bool compact = false;
+  void* d_wc = nullptr;
+  void* d_wc_tmp = nullptr;
 
   // scratch
   unsigned long long* d_hist = nullptr;      // kHistBins
@@ -242,6 +247,9 @@ hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds);
 // from d_wp (the updated values): d_act -> d_act_tmp, offsets -> tmp
 hipError_t launch_shrink(termezo_ctx* c, int64_t k);
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);
+// list entries [j0, j1): latent values (compact array when from_compact, else the layers)
+hipError_t launch_active_values(termezo_ctx* c, int64_t j0, int64_t j1, void* out, int to_f32,
+                                int from_compact);
 // theta: both perturbed copies in one pass; in-place update with the coefficient in d_scal[0]
 hipError_t launch_theta_pair(termezo_ctx* c, const ThetaHost& t, uint64_t seed, float eps);
 hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, const SeedList& seeds);

@@ -58,8 +58,13 @@ termezo_status sync_and_check(termezo_ctx* c) {
   if (err) {
     const int32_t zero = 0;
     TMZ_HIP(c, hipMemcpy(c->d_err, &zero, sizeof(zero), hipMemcpyHostToDevice));
-    return fail(c, TERMEZO_ERR_NUMERIC,
-                "a latent (or perturbed latent) is non-finite or has |w| >= 4");
+    std::string msg;
+    if (err & 1) msg += "a latent (or perturbed latent) is non-finite or has |w| >= 4; ";
+    if (err & 2) msg += "a projected gradient or update coefficient is not finite; ";
+    if (err & 4)
+      msg += "compact mode: a layer's threshold moved by more than its frozen latents' margin "
+             "(their codes were kept; rebuild the mask from full latents); ";
+    return fail(c, TERMEZO_ERR_NUMERIC, msg);
   }
   return TERMEZO_OK;
 }
@@ -134,6 +139,9 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_scal);
   dfree(c->d_xq);
   dfree(c->d_xs);
+  if (c->d_wc) (void)hipFree(c->d_wc);
+  if (c->d_wc_tmp) (void)hipFree(c->d_wc_tmp);
+  c->d_wc = c->d_wc_tmp = nullptr;
   for (ThetaHost& t : c->theta) {
     if (t.plus) (void)hipFree(t.plus);
     if (t.minus) (void)hipFree(t.minus);
@@ -281,6 +289,8 @@ termezo_status termezo_sync(termezo_ctx* c) {
 termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32_t tie_inclusive,
                                   int64_t* k0_out, float* xi0_out) {
   if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (c->compact)
+    return fail(c, TERMEZO_ERR_STATE, "build_mask needs the full latents (compact mode)");
   if (!finite(rho0) || !(rho0 > 0.0f) || rho0 > 1.0f)
     return fail(c, TERMEZO_ERR_INVALID_ARG, "rho0 must lie in (0, 1]");
   if (!finite(delta) || !(delta > 0.0f))
@@ -348,7 +358,7 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   // guarded requantisation: the actives' codes only, while no frozen code can change
   // (dense on request, or when the active set exceeds 1/256 of the latents: there the
   // scattered code-word updates cost more than the dense stream)
-  const int force = c->dense_requant || c->k_bound * 256 > c->D;
+  const int force = !c->compact && (c->dense_requant || c->k_bound * 256 > c->D);
   TMZ_HIP(c, launch_requant_guarded(c, force));
   // theta: both signs of the pair come from one pass, so the second evaluation
   // of a pair (same seed and eps) only switches to the other copy
@@ -423,6 +433,7 @@ termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_o
   TMZ_HIP(c, launch_shrink(c, c->k_bound));
   std::swap(c->d_act, c->d_act_tmp);
   std::swap(c->d_act_off, c->d_act_off_tmp);
+  if (c->compact) std::swap(c->d_wc, c->d_wc_tmp);
   TMZ_HIP(c, launch_tile_ranges(c));
   TMZ_HIP(c, launch_ref_after_update(c, c->xi_lo));
   c->codes_valid = false;
@@ -489,6 +500,75 @@ termezo_status termezo_update_multi_from_losses(termezo_ctx* c, const uint64_t* 
   if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
   TMZ_HIP(c, launch_coeffs_multi_from_losses(c, losses, K, eps, lr));
   return finish_update(c, seed_list(seeds, K), nullptr);
+}
+
+termezo_status termezo_compact(termezo_ctx* c) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "compact before build_mask");
+  if (c->compact) return fail(c, TERMEZO_ERR_STATE, "already compact");
+  if (c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "compact with a pending perturbation");
+  const size_t bytes = (size_t)(c->act_cap > 0 ? c->act_cap : 1) * dtype_size(c->dtype);
+  void *wc = nullptr, *wt = nullptr;
+  hipError_t e = hipMalloc(&wc, bytes);
+  if (e == hipSuccess) e = hipMalloc(&wt, bytes);
+  if (e != hipSuccess) {
+    if (wc) (void)hipFree(wc);
+    return hip_fail(c, e, "alloc compact latents");
+  }
+  int64_t k = 0;
+  TMZ_HIP(c, hipMemcpyAsync(&k, c->d_act_off + c->L, sizeof(int64_t), hipMemcpyDeviceToHost,
+                            c->stream));
+  TMZ_HIP(c, hipStreamSynchronize(c->stream));
+  c->d_wc = wc;
+  c->d_wc_tmp = wt;
+  TMZ_HIP(c, launch_active_values(c, 0, k, c->d_wc, 0, 0));
+  termezo_status st = sync_and_check(c);
+  if (st != TERMEZO_OK) return st;
+  c->compact = true;
+  c->k_bound = k;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_active_values(termezo_ctx* c, int32_t layer, float* values, int64_t cap,
+                                     int64_t* n) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= c->L || !n) return fail(c, TERMEZO_ERR_INVALID_ARG, "bad layer or n");
+  if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "no mask");
+  int64_t off[2];
+  TMZ_HIP(c, hipMemcpyAsync(off, c->d_act_off + layer, 2 * sizeof(int64_t), hipMemcpyDeviceToHost,
+                            c->stream));
+  TMZ_HIP(c, hipStreamSynchronize(c->stream));
+  const int64_t cnt = off[1] - off[0];
+  *n = cnt;
+  if (cnt == 0) return TERMEZO_OK;
+  if (!values || cap < cnt) return fail(c, TERMEZO_ERR_INVALID_ARG, "capacity below the count");
+  float* tmp = nullptr;
+  TMZ_HIP(c, hipMalloc(&tmp, (size_t)cnt * sizeof(float)));
+  hipError_t e = launch_active_values(c, off[0], off[1], tmp, 1, c->compact ? 1 : 0);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(values, tmp, (size_t)cnt * sizeof(float), hipMemcpyDeviceToHost, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  (void)hipFree(tmp);
+  if (e != hipSuccess) return hip_fail(c, e, "active values");
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
+                                        int64_t* latent_bytes) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  const int64_t L = c->L, T = c->T, cap = c->act_cap;
+  const int64_t dsz = (int64_t)dtype_size(c->dtype);
+  int64_t b = c->D / 4;                                          // 2-bit codes
+  b += L * (8 * 8 + 4 * 4 + 4 + 8 + 4 + 8) + 3 * (L + 1) * 8;    // per-layer state, offsets
+  b += T * (4 + 8 + 8 + 8 + 8 + 8) + 8;                          // tile tables and scratch
+  b += cap * (4 + 4 + 4) + c->blk_cap * 8;                       // index lists, w', shrink
+  if (c->compact) b += 2 * cap * dsz;                            // active latents (list order)
+  b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;
+  b += c->xq_cap + c->xs_cap * 4;                                // activation-quant scratch
+  for (const ThetaHost& t : c->theta) b += 2 * t.n * (int64_t)dtype_size(t.dtype);
+  if (library_bytes) *library_bytes = b;
+  if (latent_bytes) *latent_bytes = c->compact ? 0 : c->D * dsz;
+  return TERMEZO_OK;
 }
 
 termezo_status termezo_set_dense_requant(termezo_ctx* c, int32_t always_dense) {

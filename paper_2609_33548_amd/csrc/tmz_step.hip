@@ -656,11 +656,18 @@ __device__ __forceinline__ void put4(float* wp, int64_t j0, int n, const float v
   }
 }
 
+// wc (compact mode): the active latents in list order, read instead of the layers.
+template <typename T>
+__device__ __forceinline__ void list4(const T* wc, int64_t j0, int n, float v[4]) {
+  for (int r = 0; r < 4; ++r) v[r] = r < n ? load1(wc, j0 + r) : 0.0f;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
                                                        const uint32_t* __restrict__ act,
                                                        const int64_t* act_off, uint64_t seed,
-                                                       float se, float* __restrict__ wp) {
+                                                       float se, float* __restrict__ wp,
+                                                       const T* __restrict__ wc) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const int64_t k = aoff[st.L];
@@ -683,7 +690,10 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
     const int lr = layer_of(aoff, st.L, j0);
     const bool one = aoff[lr + 1] >= j0 + n;
     float wv[4], v[4];
-    if (one) gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
+    if (wc)
+      list4(wc, j0, n, wv);
+    else if (one)
+      gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
     for (int r = 0; r < n; ++r) {
       const int64_t j = j0 + r;
       if (l < 0) {
@@ -694,7 +704,7 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
         any = false;
         while (aoff[l + 1] <= j) ++l;
       }
-      if (!one) wv[r] = load1(reinterpret_cast<const T*>(st.w[l]), i[r]);
+      if (!wc && !one) wv[r] = load1(reinterpret_cast<const T*>(st.w[l]), i[r]);
       v[r] = se != 0.0f ? fmaf(se, zc.get(seed, (uint64_t)(st.gid0[l] + i[r])), wv[r]) : wv[r];
       bad |= !in_fix_range(v[r]);
       acc += (long long)fix_abs(v[r]) - (long long)fix_abs(wv[r]);
@@ -867,7 +877,8 @@ __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps,
 template <typename T>
 __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __restrict__ act,
                                                 const int64_t* act_off, SeedList seeds,
-                                                const float* scal, float* __restrict__ wn) {
+                                                const float* scal, float* __restrict__ wn,
+                                                T* __restrict__ wc) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const float a = scal[0];
@@ -890,7 +901,10 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
     const int lr = layer_of(aoff, st.L, j0);
     const bool one = aoff[lr + 1] >= j0 + n;
     float wv[4], nv[4];
-    if (one) gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
+    if (wc)
+      list4((const T*)wc, j0, n, wv);
+    else if (one)
+      gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
     for (int r = 0; r < n; ++r) {
       const int64_t j = j0 + r;
       if (l < 0) {
@@ -902,20 +916,23 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
         while (aoff[l + 1] <= j) ++l;
       }
       T* w = reinterpret_cast<T*>(const_cast<void*>(st.w[l]));
-      if (!one) wv[r] = load1(w, i[r]);
+      if (!wc && !one) wv[r] = load1(w, i[r]);
       nv[r] = wv[r];
       if (a_ok) {
         const uint64_t gid = (uint64_t)(st.gid0[l] + i[r]);
         float v = fmaf(a, zc.get(seed, gid), wv[r]);
         for (int q = 1; q < K; ++q) v = fmaf(scal[q], gauss_at(seeds.s[q], gid), v);
         nv[r] = storage_round(w, v);
-        if (!one) store1(w, i[r], nv[r]);
+        if (wc)
+          store1(wc, j, nv[r]);
+        else if (!one)
+          store1(w, i[r], nv[r]);
       }
       bad |= !in_fix_range(nv[r]);
       acc += (long long)fix_abs(nv[r]) - (long long)fix_abs(wv[r]);
       any = true;
     }
-    if (one && a_ok) scatter4(reinterpret_cast<T*>(const_cast<void*>(st.w[lr])), i, n, nv);
+    if (!wc && one && a_ok) scatter4(reinterpret_cast<T*>(const_cast<void*>(st.w[lr])), i, n, nv);
     put4(wn, j0, n, nv);
   }
   flush_delta((long long*)st.S_clean, l, acc, any);
@@ -934,11 +951,18 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
 // ---------------------------------------------------------------------------
 // One block: need[l] for every layer, then dense_off (the layers needing the dense
 // pass, their tiles listed in layer order).
-__global__ void __launch_bounds__(256) k_guard(DevState st, int force, int64_t* dense_off) {
+// Compact mode (no frozen latents kept): a layer that fails the guard cannot be
+// re-quantised; its frozen codes stay and the deferred error bit 4 is raised.
+__global__ void __launch_bounds__(256) k_guard(DevState st, int force, int64_t* dense_off,
+                                               int compact) {
   __shared__ int64_t cnt[kMaxLayers + 1];
   for (int l = threadIdx.x; l < st.L; l += blockDim.x) {
     const float tc = st.tau_cur[l], tr = st.tau_ref[l];
-    const bool keep = !force && (tc == tr || fabs((double)tc - (double)tr) < st.mref[l]);
+    bool keep = !force && (tc == tr || fabs((double)tc - (double)tr) < st.mref[l]);
+    if (compact && !keep) {
+      atomicOr(st.err, 4);
+      keep = true;
+    }
     st.need[l] = keep ? 0 : 1;
     if (!keep) {
       st.tau_ref[l] = tc;
@@ -1121,7 +1145,8 @@ __global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_
                                                       const float* __restrict__ wn, float xi0,
                                                       int per, const int64_t* blk_off,
                                                       uint32_t* __restrict__ act_new,
-                                                      int64_t* act_off_new) {
+                                                      int64_t* act_off_new, void* wc_new,
+                                                      int wc_bf16) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   __shared__ float tau[kMaxLayers];
   __shared__ int32_t cnt[kShrinkPer * 4];   // kept entries per (r, wave), then their offsets
@@ -1157,9 +1182,15 @@ __global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_
     const int64_t pos = boff + cnt[4 * r + wid] + __popcll(b & below);
     while (aoff[l + 1] <= j) ++l;
     if (j == aoff[l]) act_off_new[l] = pos;   // first entry of layer l
-    if (keep)
+    if (keep) {
       act_new[pos] = act[j];
-    else                                      // frozen from now on: its code at tau_ref
+      if (wc_new) {                           // compact mode: the kept latent, list order
+        if (wc_bf16)
+          reinterpret_cast<uint16_t*>(wc_new)[pos] = f32_to_bf16_rne(wn[j]);
+        else
+          reinterpret_cast<float*>(wc_new)[pos] = wn[j];
+      }
+    } else                                    // frozen from now on: its code at tau_ref
       set_code(st.codes, st.code_off[l], act[j], ternary_code(wn[j], st.tau_ref[l]));
   }
 }
@@ -1180,6 +1211,34 @@ __global__ void __launch_bounds__(256) k_shrink_offsets(const int64_t* act_off,
       if (o[l] == o[l + 1]) n[l] = n[l + 1];
   __syncthreads();
   for (int l = threadIdx.x; l <= L; l += blockDim.x) act_off_new[l] = n[l];
+}
+
+// ---------------------------------------------------------------------------
+// Active latents in list order: from the layers (compaction) or, in compact mode,
+// from the compact array; out in the latent dtype (to_f32 = 0) or as fp32.
+// Entries [j0, j1) of the list.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) k_active_values(DevState st, const uint32_t* act,
+                                                       const int64_t* act_off, const T* wc,
+                                                       int64_t j0, int64_t j1, void* out,
+                                                       int to_f32) {
+  __shared__ int64_t aoff[kMaxLayers + 1];
+  load_offsets(aoff, act_off, st.L);
+  for (int64_t j = j0 + (int64_t)blockIdx.x * 256 + threadIdx.x; j < j1;
+       j += (int64_t)gridDim.x * 256) {
+    float v;
+    if (wc) {
+      v = load1(wc, j);
+    } else {
+      const int l = layer_of(aoff, st.L, j);
+      v = load1(reinterpret_cast<const T*>(st.w[l]), act[j]);
+    }
+    if (to_f32)
+      reinterpret_cast<float*>(out)[j - j0] = v;
+    else
+      store1(reinterpret_cast<T*>(out), j - j0, v);   // exact: v is a T value
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1333,7 +1392,8 @@ hipError_t launch_requant(termezo_ctx* c, int patch) {
 }
 
 hipError_t launch_requant_guarded(termezo_ctx* c, int force) {
-  hipLaunchKernelGGL(k_guard, dim3(1), dim3(256), 0, c->stream, c->dev(), force, c->d_dense_off);
+  hipLaunchKernelGGL(k_guard, dim3(1), dim3(256), 0, c->stream, c->dev(), force, c->d_dense_off,
+                     c->compact ? 1 : 0);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (force) return launch_requant(c, 1);      // every layer: one block per tile
@@ -1377,10 +1437,10 @@ hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float 
   const int64_t g = sparse_grid(k);
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_perturb_delta<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, se, c->d_wp);
+                       c->d_act_off, seed, se, c->d_wp, (const float*)c->d_wc);
   else
     hipLaunchKernelGGL(k_perturb_delta<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(),
-                       c->d_act, c->d_act_off, seed, se, c->d_wp);
+                       c->d_act, c->d_act_off, seed, se, c->d_wp, (const uint16_t*)c->d_wc);
   return hipGetLastError();
 }
 
@@ -1401,10 +1461,10 @@ hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds) {
   const int64_t g = sparse_grid(k);
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp);
+                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)c->d_wc);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp);
+                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (uint16_t*)c->d_wc);
   return hipGetLastError();
 }
 
@@ -1434,7 +1494,7 @@ hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
   // offsets of layers without any entry are fixed afterwards
   hipLaunchKernelGGL(k_shrink_write, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act,
                      c->d_act_off, c->d_wp, c->xi0, per, c->d_blk_cnt, c->d_act_tmp,
-                     c->d_act_off_tmp);
+                     c->d_act_off_tmp, c->d_wc_tmp, c->dtype == TERMEZO_BF16 ? 1 : 0);
   hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(256), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
   return hipGetLastError();
@@ -1468,6 +1528,22 @@ hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, const SeedLis
   else
     hipLaunchKernelGGL(k_theta_update<uint16_t>, dim3(g), dim3(256), 0, c->stream,
                        (uint16_t*)t.data, t.n, t.tid0, seeds, (const float*)c->d_scal);
+  return hipGetLastError();
+}
+
+hipError_t launch_active_values(termezo_ctx* c, int64_t j0, int64_t j1, void* out, int to_f32,
+                                int from_compact) {
+  if (j1 <= j0) return hipSuccess;
+  const unsigned g = (unsigned)max((int64_t)1, min((int64_t)4096, (j1 - j0 + 255) / 256));
+  if (c->dtype == TERMEZO_F32)
+    hipLaunchKernelGGL(k_active_values<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
+                       c->d_act_off, from_compact ? (const float*)c->d_wc : (const float*)nullptr,
+                       j0, j1, out, to_f32);
+  else
+    hipLaunchKernelGGL(k_active_values<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(),
+                       c->d_act, c->d_act_off,
+                       from_compact ? (const uint16_t*)c->d_wc : (const uint16_t*)nullptr, j0, j1,
+                       out, to_f32);
   return hipGetLastError();
 }
 

@@ -73,6 +73,9 @@ _SIGS = {
     "termezo_update_multi_from_losses": [_P, _P, _P, _i32, _f32, _f32],
     "termezo_theta_register": [_P, ctypes.POINTER(Theta), _i32],
     "termezo_set_dense_requant": [_P, _i32],
+    "termezo_compact": [_P],
+    "termezo_active_values": [_P, _i32, _P, _i64, ctypes.POINTER(_i64)],
+    "termezo_memory_footprint": [_P, ctypes.POINTER(_i64), ctypes.POINTER(_i64)],
     "termezo_theta_current": [_P, _i32, ctypes.POINTER(_P)],
     "termezo_theta_copy": [_P, _i32, _P],
     "termezo_model_create": [_P, _P, _P, ctypes.POINTER(_P)],
@@ -241,6 +244,27 @@ class Context:
         """Device-side g = (F+ - F-) / (2 eps) and update; no host round trip."""
         self._check(_lib.termezo_update_from_losses(self.handle, _ptr(loss_plus), _ptr(loss_minus),
                                                     eps, lr), "update_from_losses")
+
+    def compact(self):
+        """Memory-optimal storage: keep only the active latents (library-owned); the
+        registered latent tensors are no longer read or written."""
+        self._check(_lib.termezo_compact(self.handle), "compact")
+
+    def active_values(self, layer: int) -> np.ndarray:
+        """fp32 values of one layer's active latents in list order."""
+        d_out, d_in = self.shapes[layer]
+        buf = np.empty(max(1, d_out * d_in), np.float32)
+        n = _i64()
+        self._check(_lib.termezo_active_values(self.handle, layer, buf.ctypes.data, buf.size,
+                                               ctypes.byref(n)), "active_values")
+        return buf[: n.value].copy()
+
+    def memory_footprint(self):
+        """(library-owned device bytes, caller latent bytes still needed)."""
+        lb, wb = _i64(), _i64()
+        self._check(_lib.termezo_memory_footprint(self.handle, ctypes.byref(lb), ctypes.byref(wb)),
+                    "memory_footprint")
+        return int(lb.value), int(wb.value)
 
     def set_dense_requant(self, on: bool):
         """Re-quantise every latent on each perturbation (default: only the actives'

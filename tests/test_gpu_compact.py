@@ -1,0 +1,104 @@
+"""GPU parity of the memory-optimal storage (compact mode: frozen latents kept only
+as their ternary codes, the active latents in a library-owned list-order array)
+against the CPU oracle, through the C ABI.
+
+Bar: codes, active latent values, thresholds, fixed-point sums and the shrunk mask
+bit-exact against the oracle's dense step, with the caller's latent tensors
+overwritten by NaN right after compaction (so any read of them would show)."""
+import numpy as np
+import pytest
+
+from paper_2609_33548_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _ctx(torch, termezo, shapes, w, bf16):
+    lat, off = [], 0
+    for o, i in shapes:
+        t = torch.from_numpy(np.ascontiguousarray(w[off: off + o * i]).reshape(o, i)).cuda()
+        lat.append(t.to(torch.bfloat16) if bf16 else t)
+        off += o * i
+    return termezo.Context(lat), lat
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("K", [1, 3])
+def test_compact_mode_matches_oracle(orc, bf16, K):
+    torch = _torch()
+    from paper_2609_33548_amd import termezo
+    print(f"compact bf16={bf16} K={K}", flush=True)
+    shapes = [(256, 512), (512, 256), (384, 384)]
+    w = synth.latents(81, [o * i for o, i in shapes], bf16=bf16)
+    th = synth.latents(82, [3001], bf16=bf16)
+    ref = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w, bf16=bf16, theta=th,
+                            theta_bf16=bf16)
+    ctx, lat = _ctx(torch, termezo, shapes, w, bf16)
+    T = torch.from_numpy(th).cuda().to(torch.bfloat16 if bf16 else torch.float32)
+    ctx.theta_register([T])
+    assert ctx.build_mask(0.003) == ref.build_mask(0.003)
+    lib_before, need_before = ctx.memory_footprint()
+    ctx.compact()
+    lib_after, need_after = ctx.memory_footprint()
+    assert need_after == 0 and need_before == sum(o * i for o, i in shapes) * (2 if bf16 else 4)
+    assert lib_after < lib_before + need_before
+    for x in lat:                       # the library must not read them any more
+        x.fill_(float("nan"))
+    # lr small enough that the threshold drift stays inside the frozen margin (the
+    # oracle's thresholds show the margin nearly untouched after four steps; at
+    # lr = 3e-2 a bf16 layer would exceed it, which compact mode reports)
+    eps, lr = 1e-3, 1e-3
+    for t in range(4):
+        seeds = [10 * t + k for k in range(K)]
+        gs = []
+        for k, sd in enumerate(seeds):
+            for sign in (1, -1, 0):
+                ctx.perturb(sd, eps, sign)
+                codes, _, _ = ref.perturb(sd, eps, sign)
+                for l in range(len(shapes)):
+                    assert np.array_equal(ctx.codes(l), codes[l]), f"step {t} dir {k} sign {sign} layer {l}"
+            ctx.perturb(sd, eps, 1)
+            ref.perturb(sd, eps, 1)
+            gs.append(0.8 - 0.5 * k + 0.2 * t)
+        if K == 1:
+            assert ctx.update(gs[0], lr) == ref.update(gs[0], lr)
+        else:
+            assert ctx.update_multi(seeds, gs, lr) == ref.update_multi(seeds, gs, lr)
+        for l in range(len(shapes)):
+            assert np.array_equal(ctx.mask(l), ref.active[l]), f"step {t} layer {l}: mask"
+            exp = ref.layer_w(l)[ref.active[l]]
+            assert np.array_equal(ctx.active_values(l), exp), f"step {t} layer {l}: active latents"
+            st = ctx.layer_stats(l)
+            assert st["S"] == ref.S[l] and st["tau"] == ref.tau[l], f"step {t} layer {l}: threshold"
+        assert np.array_equal(T.float().cpu().numpy(), ref.theta)
+    ctx.sync()
+    assert all(torch.isnan(x.float()).all() for x in lat)
+    ctx.close()
+
+
+def test_compact_mode_reports_a_margin_violation(orc):
+    """A perturbation far larger than the frozen margin (eps = 0.5 against xi0 of a
+    0.2% mask): compact mode keeps the frozen codes and reports NUMERIC; the full
+    latents were dropped, so the mask cannot be rebuilt (STATE)."""
+    torch = _torch()
+    from paper_2609_33548_amd import termezo
+    shapes = [(256, 256), (128, 512)]
+    w = synth.latents(83, [o * i for o, i in shapes], bf16=True)
+    ctx, lat = _ctx(torch, termezo, shapes, w, True)
+    ctx.build_mask(0.002)
+    ctx.compact()
+    ctx.perturb(5, 0.5, 1)
+    with pytest.raises(termezo.TermezoError) as e:
+        ctx.sync()
+    assert e.value.status == termezo.ERR_NUMERIC and "margin" in str(e.value)
+    with pytest.raises(termezo.TermezoError) as e:
+        ctx.build_mask(0.01)
+    assert e.value.status == termezo.ERR_STATE
+    ctx.close()
