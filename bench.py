@@ -354,6 +354,45 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
                "us": t_u * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_u / 1e9,
                "frac_hbm": b_u / t_u / 1e9 / HBM_PEAK_GBS, "cpu_baseline": cu})
     ctx.close()
+    # memory-optimal storage: a fresh context per ratio (the compact form is kept until the
+    # context ends); the actives live contiguously in list order
+    for r in SWEEP_RATIOS:
+        cc = termezo.Context(layers)
+        k0, _ = cc.build_mask(r)
+        cc.compact()
+        lib_b, _ = cc.memory_footprint()
+        cc.perturb(0, 1e-3, 1)
+        cc.update(1.0, 1e-5, want_k=False)
+        cc.perturb(1, 1e-3, 1)
+        torch.cuda.synchronize()
+        k = cc.active_count()
+        ev0.record(stream)
+        for t in range(reps):
+            cc.perturb(100 + t, 1e-3, 1 if t % 2 == 0 else -1)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        t_c = ev0.elapsed_time(ev1) / reps * 1e-3
+        up = 0.0
+        for t in range(reps):
+            cc.perturb(200 + t, 1e-3, 1)
+            ev0.record(stream)
+            cc.update(1.0, 1e-5, want_k=False)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            up += ev0.elapsed_time(ev1) * 1e-3
+        t_uc = up / reps
+        k_after = cc.active_count()
+        cc.sync()
+        cc.close()
+        b_g = k * 26
+        b_u = 16 * k
+        _emit({"sweep": "perturb_compact", "latents": D, "ratio": r, "k": k, "ms": t_c * 1e3,
+               "algorithmic_bytes": b_g, "GB/s": b_g / t_c / 1e9,
+               "frac_hbm": b_g / t_c / 1e9 / HBM_PEAK_GBS, "library_bytes": lib_b,
+               "protocol": "termezo_compact after the mask build; actives' codes only"})
+        _emit({"sweep": "update_compact", "latents": D, "ratio": r, "k": k, "k_after": k_after,
+               "us": t_uc * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_uc / 1e9,
+               "frac_hbm": b_u / t_uc / 1e9 / HBM_PEAK_GBS})
     del lat, layers
     torch.cuda.empty_cache()
 
@@ -481,6 +520,9 @@ def main():
                     help="run the kernel sweeps instead of the step benchmark")
     ap.add_argument("--K", type=int, default=1,
                     help="perturbation directions per step (Algorithm 1; the paper's runs use 5)")
+    ap.add_argument("--compact", action="store_true",
+                    help="memory-optimal storage: after the mask build keep only the active latents "
+                         "(the full latent tensor is freed)")
     ap.add_argument("--theta", action="store_true",
                     help="also perturb and update the full-precision parameters (tied embedding and "
                          "RMSNorm weights) with the latents, as Algorithm 1 does")
@@ -541,6 +583,19 @@ def main():
     k0, xi0 = ctx.build_mask(args.rho)
     mask_ms = (time.perf_counter() - t0) * 1e3
     print(f"[bench] mask: k0={k0} xi0={xi0:.3e} built in {mask_ms:.1f} ms", flush=True)
+    if args.compact:
+        ctx.compact()
+        del lat, layers                  # frozen latents live on only as their ternary codes
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    lib_b, lat_b = ctx.memory_footprint()
+    bsz = 4 if fp32 else 2
+    # eq. memory of the paper for the latent side: every latent as a 2-bit code, the active
+    # latents at full width, the mask as an index list or a bitmask (whichever is smaller)
+    idx_bits = math.ceil(math.log2(D))
+    eq_mem = D * 0.25 + k0 * bsz + min(-(-D // 8), -(-k0 * idx_bits // 8))
+    print(f"[bench] memory: library {lib_b / 2**20:.1f} MiB, caller latents {lat_b / 2**20:.1f} MiB, "
+          f"eq. memory estimate {eq_mem / 2**20:.1f} MiB", flush=True)
     F = torch.zeros(2 * args.K, device=dev)
 
     def step(t):
@@ -630,6 +685,7 @@ def main():
                                + ("_with_theta" if args.theta else "")
                                + (f"_K{args.K}" if args.K > 1 else ""),
                    "theta_params": n_theta, "directions_per_step": args.K,
+                   "storage": "compact" if args.compact else "full_latents",
                    **{k: v for k, v in c.items() if k not in ("rho", "lr", "fp32")},
                    "tokens_per_forward": c["batch"] * c["seq"], "latents": D,
                    "mask_ratio": args.rho, "k0": k0, "k_final": k_final, "eps": args.eps,
@@ -648,6 +704,10 @@ def main():
                                 "lm_head_ce": h_ms / args.steps,
                                 "event_timed_step_ms": timed_ms_per_step},
         "mask_build_ms": mask_ms,
+        "memory": {"library_bytes": lib_b, "latent_bytes_needed": lat_b,
+                   "method_state_bytes": lib_b + lat_b,
+                   "eq_memory_latent_side_bytes": int(eq_mem),
+                   "torch_allocated_bytes": int(torch.cuda.memory_allocated())},
         "cpu_baseline": cpu,
     }
     if args.config == "tiny":

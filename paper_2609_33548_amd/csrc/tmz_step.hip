@@ -950,21 +950,23 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
 // next mask build).
 // ---------------------------------------------------------------------------
 // One block: need[l] for every layer, then dense_off (the layers needing the dense
-// pass, their tiles listed in layer order).
+// pass, their tiles listed in layer order).  A layer whose weights are all active has
+// no frozen code and always passes.  force: every layer takes the dense pass.
 // Compact mode (no frozen latents kept): a layer that fails the guard cannot be
 // re-quantised; its frozen codes stay and the deferred error bit 4 is raised.
 __global__ void __launch_bounds__(256) k_guard(DevState st, int force, int64_t* dense_off,
-                                               int compact) {
+                                               int compact, const int64_t* act_off) {
   __shared__ int64_t cnt[kMaxLayers + 1];
   for (int l = threadIdx.x; l < st.L; l += blockDim.x) {
     const float tc = st.tau_cur[l], tr = st.tau_ref[l];
-    bool keep = !force && (tc == tr || fabs((double)tc - (double)tr) < st.mref[l]);
-    if (compact && !keep) {
-      atomicOr(st.err, 4);
-      keep = true;
-    }
+    const bool none_frozen = act_off[l + 1] - act_off[l] == st.n[l];
+    const bool pass = tc == tr || none_frozen || fabs((double)tc - (double)tr) < st.mref[l];
+    if (compact && !pass) atomicOr(st.err, 4);
+    // forced dense pass: a layer that passes rewrites its frozen codes unchanged, so
+    // its reference and bound stay valid
+    const bool keep = compact || (!force && pass);
     st.need[l] = keep ? 0 : 1;
-    if (!keep) {
+    if (!pass && !compact) {
       st.tau_ref[l] = tc;
       st.mref[l] = -1.0;
     }
@@ -1393,7 +1395,7 @@ hipError_t launch_requant(termezo_ctx* c, int patch) {
 
 hipError_t launch_requant_guarded(termezo_ctx* c, int force) {
   hipLaunchKernelGGL(k_guard, dim3(1), dim3(256), 0, c->stream, c->dev(), force, c->d_dense_off,
-                     c->compact ? 1 : 0);
+                     c->compact ? 1 : 0, (const int64_t*)c->d_act_off);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (force) return launch_requant(c, 1);      // every layer: one block per tile

@@ -249,6 +249,7 @@ class Context:
         """Memory-optimal storage: keep only the active latents (library-owned); the
         registered latent tensors are no longer read or written."""
         self._check(_lib.termezo_compact(self.handle), "compact")
+        self.latents = None                 # the caller may now free its latent tensors
 
     def active_values(self, layer: int) -> np.ndarray:
         """fp32 values of one layer's active latents in list order."""

@@ -102,3 +102,35 @@ def test_compact_mode_reports_a_margin_violation(orc):
         ctx.build_mask(0.01)
     assert e.value.status == termezo.ERR_STATE
     ctx.close()
+
+
+def test_compact_mode_all_active_has_no_margin(orc):
+    """rho0 = 1: no frozen latent exists, so even eps = 0.5 (far past any margin)
+    keeps compact mode exact: codes, active latents and thresholds equal the
+    oracle's dense step and no violation is reported."""
+    torch = _torch()
+    from paper_2609_33548_amd import termezo
+    shapes = [(256, 256), (128, 512)]
+    w = synth.latents(84, [o * i for o, i in shapes], bf16=True)
+    ref = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w, bf16=True)
+    ctx, lat = _ctx(torch, termezo, shapes, w, True)
+    assert ctx.build_mask(1.0) == ref.build_mask(1.0)
+    ctx.compact()
+    for x in lat:
+        x.fill_(float("nan"))
+    for sign in (1, -1):
+        ctx.perturb(5, 0.5, sign)
+        codes, _, _ = ref.perturb(5, 0.5, sign)
+        for l in range(len(shapes)):
+            assert np.array_equal(ctx.codes(l), codes[l]), f"sign {sign} layer {l}"
+    assert ctx.update(0.7, 1e-2) == ref.update(0.7, 1e-2)
+    for l in range(len(shapes)):
+        assert np.array_equal(ctx.mask(l), ref.active[l]), f"layer {l}: mask"
+        assert np.array_equal(ctx.active_values(l), ref.layer_w(l)[ref.active[l]])
+    # latents the update pushed past xi0 are frozen now: a small perturbation again
+    ctx.perturb(6, 1e-3, 1)
+    codes, _, _ = ref.perturb(6, 1e-3, 1)
+    for l in range(len(shapes)):
+        assert np.array_equal(ctx.codes(l), codes[l]), f"after update, layer {l}"
+    ctx.sync()
+    ctx.close()

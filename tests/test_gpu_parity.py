@@ -293,32 +293,45 @@ def test_state_and_numeric_errors(orc):
 def test_guarded_requant_equals_dense_requant(orc, bf16, rho0, eps):
     """The default perturbation (actives' codes only while the threshold-drift
     guard proves every frozen code unchanged, dense otherwise) gives the codes of
-    the dense requantisation: two contexts on the same latents, one forced dense,
-    against each other and the oracle over five steps (perturb +, -, 0, update)."""
+    the dense requantisation: three contexts on the same latents (default, forced
+    dense, and switching between the two at every perturbation, so a guarded pass
+    follows a forced one) against each other and the oracle over five steps
+    (perturb +, -, 0, update)."""
     print(f"guarded requant bf16={bf16} rho0={rho0} eps={eps}", flush=True)
     shapes = [(256, 256), (128, 512), (384, 128)]
     ref, ctx, tensors = _setup(orc, shapes, bf16, seed=41)
     _, ctx_d, tensors_d = _setup(orc, shapes, bf16, seed=41)
+    _, ctx_a, _ = _setup(orc, shapes, bf16, seed=41)
     ctx_d.set_dense_requant(True)
     ctx.build_mask(rho0)
     ctx_d.build_mask(rho0)
+    ctx_a.build_mask(rho0)
     ref.build_mask(rho0)
+    n_pert = 0
     for t in range(5):
         for sign in (1, -1, 0):
             ctx.perturb(t, eps, sign)
             ctx_d.perturb(t, eps, sign)
+            ctx_a.set_dense_requant(n_pert % 2 == 0)
+            ctx_a.perturb(t, eps, sign)
+            n_pert += 1
             codes, taus, betas = ref.perturb(t, eps, sign)
             for l in range(len(shapes)):
                 got, dense = ctx.codes(l), ctx_d.codes(l)
                 assert np.array_equal(dense, codes[l]), f"step {t} sign {sign} layer {l}: dense path"
                 bad = np.count_nonzero(got != codes[l])
                 assert bad == 0, f"step {t} sign {sign} layer {l}: {bad} codes differ"
+                bad = np.count_nonzero(ctx_a.codes(l) != codes[l])
+                assert bad == 0, f"step {t} sign {sign} layer {l}: {bad} codes differ (switching)"
         g = 0.5 - 0.3 * t
         ctx.perturb(t, eps, 1)
         ctx_d.perturb(t, eps, 1)
+        ctx_a.perturb(t, eps, 1)
         ref.perturb(t, eps, 1)
-        assert ctx.update(g, 1e-2) == ctx_d.update(g, 1e-2) == ref.update(g, 1e-2)
+        k_ref = ref.update(g, 1e-2)
+        assert ctx.update(g, 1e-2) == ctx_d.update(g, 1e-2) == ctx_a.update(g, 1e-2) == k_ref
         assert np.array_equal(_latents_host(tensors), ref.w)
         assert np.array_equal(_latents_host(tensors_d), ref.w)
     ctx.close()
     ctx_d.close()
+    ctx_a.close()
