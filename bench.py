@@ -81,7 +81,7 @@ def measured_traffic():
     return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
 
 
-def cpu_baseline(c, rho, seed=0, theta_n=0, K=1):
+def cpu_baseline(c, rho, seed=0, theta_n=0, K=1, es=0):
     """The oracle, as it stands, on a bounded sample of the same step; the
     full-step time is extrapolated by operation counts (stated in 'sample')."""
     import numpy as np
@@ -136,6 +136,8 @@ def cpu_baseline(c, rho, seed=0, theta_n=0, K=1):
     t_fwd = c["n_blocks"] * c["batch"] * t_block + (ntok / n_pos) * t_head
     # K directions: K perturbation pairs and 2K forwards; the update regenerates K directions
     t_step = K * (2 * t_fwd + t_latent + t_theta)
+    if es:     # ES: es one-sided members, one forward and one perturbation each
+        t_step = es * (t_fwd + 0.5 * (t_latent + t_theta))
     wall = t_latent * nsmp / D + t_block * n_seq + t_head + t_theta * n_th / max(theta_n, 1)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {
@@ -145,7 +147,9 @@ def cpu_baseline(c, rho, seed=0, theta_n=0, K=1):
                    f"scaled x{c['n_blocks']} blocks x{c['batch'] / n_seq:g}; LM head+CE on {n_pos} "
                    f"positions scaled x{ntok // n_pos}; two forwards per step"
                    + (f"; theta perturb(+/-)+update on {n_th} ids scaled to {theta_n}" if theta_n else "")
-                   + (f"; all of it x{K} directions" if K > 1 else "")
+                   + (f"; all of it x{K} directions" if K > 1 and not es else "")
+                   + (f"; ES: {es} members x (one forward + half the perturb/update sample)"
+                      if es else "")
                    + f"; sample wall {wall:.1f}s"),
         "extrapolated_step_s": t_step,
     }
@@ -520,6 +524,9 @@ def main():
                     help="run the kernel sweeps instead of the step benchmark")
     ap.add_argument("--K", type=int, default=1,
                     help="perturbation directions per step (Algorithm 1; the paper's runs use 5)")
+    ap.add_argument("--es", type=int, default=0,
+                    help="evolution strategies on the mask (RL appendix): N one-sided population "
+                         "members per step, rewards = -loss, standardised")
     ap.add_argument("--compact", action="store_true",
                     help="memory-optimal storage: after the mask build keep only the active latents "
                          "(the full latent tensor is freed)")
@@ -596,9 +603,17 @@ def main():
     eq_mem = D * 0.25 + k0 * bsz + min(-(-D // 8), -(-k0 * idx_bits // 8))
     print(f"[bench] memory: library {lib_b / 2**20:.1f} MiB, caller latents {lat_b / 2**20:.1f} MiB, "
           f"eq. memory estimate {eq_mem / 2**20:.1f} MiB", flush=True)
-    F = torch.zeros(2 * args.K, device=dev)
+    F = torch.zeros(max(2 * args.K, args.es), device=dev)
 
     def step(t):
+        if args.es:
+            seeds = [t * args.es + n for n in range(args.es)]
+            for n, sd in enumerate(seeds):
+                ctx.perturb(sd, args.eps, 1)
+                model.loss(tok, loss_dev=F[n: n + 1], host=False)
+            # the losses are the rewards of the descent: -lr ascends on -loss
+            ctx.es_update_from_rewards(seeds, F[:args.es], -args.lr)
+            return
         if args.K == 1:
             ctx.perturb(t, args.eps, 1)
             model.loss(tok, loss_dev=F[0:1], host=False)
@@ -661,7 +676,7 @@ def main():
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         cpu = (cpu_baseline_full(c, args.rho, theta=args.theta) if args.config == "tiny"
-               else cpu_baseline(c, args.rho, theta_n=n_theta, K=args.K))
+               else cpu_baseline(c, args.rho, theta_n=n_theta, K=args.K, es=args.es))
         print(f"[bench] cpu baseline sample took {time.perf_counter() - t0:.1f} s", flush=True)
 
     metric = METRIC if args.config == "2b" else {
@@ -683,8 +698,12 @@ def main():
         "config": {"workload": (f"termezo_zo_step_tiny_decoder" if args.config == "tiny"
                                 else f"termezo_zo_step_bitnet_{args.config}")
                                + ("_with_theta" if args.theta else "")
-                               + (f"_K{args.K}" if args.K > 1 else ""),
-                   "theta_params": n_theta, "directions_per_step": args.K,
+                               + (f"_K{args.K}" if args.K > 1 and not args.es else "")
+                               + (f"_es{args.es}" if args.es else "")
+                               + ("_compact" if args.compact else ""),
+                   "theta_params": n_theta,
+                   "directions_per_step": args.es if args.es else args.K,
+                   "estimator": "es_one_sided" if args.es else "spsa_two_point",
                    "storage": "compact" if args.compact else "full_latents",
                    **{k: v for k, v in c.items() if k not in ("rho", "lr", "fp32")},
                    "tokens_per_forward": c["batch"] * c["seq"], "latents": D,

@@ -215,6 +215,29 @@ termezo_status termezo_update_multi_from_losses(termezo_ctx* ctx, const uint64_t
                                                 const float* losses, int32_t K, float eps,
                                                 float lr);
 
+/* ---- evolution strategies on the mask (appendix on RL-based fine-tuning) -------
+ * The RL variant evaluates N one-sided perturbations w + sigma m (.) z_n
+ * (termezo_perturb(s_n, sigma, +1), then the caller's reward R_n) and updates
+ * with the reward-weighted sum of the directions, restricted to the mask:
+ *   v = fma(a_N, z_N, ... fma(a_1, z_1, w) ...) in fp32,  w <- round(v),
+ * a_n = (lr / N) * Rt_n in fp32 (lr / N one fp32 division), at every active
+ * latent (and every registered theta value, stream 1), then the shrink of
+ * termezo_update.  standardize != 0: Rt_n = fp32((R_n - mu) / sd) with mu and
+ * the population deviation sd computed in fp64 in index order (all Rt zero when
+ * sd = 0, so N = 1 or equal rewards leave the weights unchanged); standardize
+ * = 0: Rt_n = R_n.  seeds: host array of N entries, 1 <= N <= 32.  A negative
+ * lr descends instead of ascends (rewards = losses).
+ * Errors: INVALID_ARG (N out of range, null arrays, non-finite reward, lr or
+ * coefficient), STATE (no perturbation since the last update). */
+termezo_status termezo_es_update(termezo_ctx* ctx, const uint64_t* seeds, const float* rewards,
+                                 int32_t N, float lr, int32_t standardize, int64_t* k_out);
+
+/* The same with the rewards in device memory (fp32 [N]); never waits.  A
+ * non-finite coefficient skips the update and raises a deferred NUMERIC. */
+termezo_status termezo_es_update_from_rewards(termezo_ctx* ctx, const uint64_t* seeds,
+                                              const float* rewards, int32_t N, float lr,
+                                              int32_t standardize);
+
 /* ---- full-precision parameters theta (Sec. 3; Algorithm 1) ---------------------
  * Algorithm 1 perturbs and updates the full-precision parameters (embeddings,
  * normalisation weights, LM head) densely, together with the masked latents,

@@ -477,3 +477,56 @@ void orc_theta_update_multi(float* theta, int64_t n, int64_t tid0, const uint64_
     theta[i] = bf16_storage ? orc_round_bf16(v) : v;
   }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Evolution strategies restricted to the mask (appendix on RL-based        */
+/* fine-tuning): N one-sided perturbations w + sigma m (.) z_n, a reward R_n */
+/* for each, then the reward-weighted sum of the directions,                 */
+/*   w <- w + (eta / N) sum_n Rt_n m (.) z_n,                                */
+/* where Rt are the rewards standardised over the population (z-score, the   */
+/* population standard deviation; all zero when that deviation is zero, so   */
+/* N = 1 or equal rewards leave w unchanged), or the raw rewards.            */
+/* Standardisation in fp64, in index order:                                  */
+/*   mu = (sum R) / N;  var = (sum (R - mu)^2) / N;  sd = sqrt(var);         */
+/*   Rt_n = fp32((R_n - mu) / sd).                                           */
+/* Coefficients a_n = (eta / N) * Rt_n in fp32 (eta / N one fp32 division); */
+/* the fp32 chain v = fma(a_n, z_n, v) over n, rounded to storage once.     */
+/* ------------------------------------------------------------------------ */
+void orc_es_standardize(const float* r, int N, float* out) {
+  double mu = 0.0, var = 0.0;
+  for (int n = 0; n < N; ++n) mu += (double)r[n];
+  mu /= (double)N;
+  for (int n = 0; n < N; ++n) {
+    double d = (double)r[n] - mu;
+    var += d * d;
+  }
+  var /= (double)N;
+  double sd = sqrt(var);
+  for (int n = 0; n < N; ++n) out[n] = sd > 0.0 ? (float)(((double)r[n] - mu) / sd) : 0.0f;
+}
+
+void orc_es_coeffs(const float* r, int N, float lr, int standardize, float* a) {
+  float c = lr / (float)N;
+  for (int n = 0; n < N; ++n) a[n] = r[n];
+  if (standardize) orc_es_standardize(r, N, a);
+  for (int n = 0; n < N; ++n) a[n] = c * a[n];
+}
+
+void orc_update_layer_coeffs(float* w, const int64_t* act, int64_t k, int64_t gid0,
+                             const uint64_t* seeds, const float* a, int N, int bf16_storage) {
+  for (int64_t j = 0; j < k; ++j) {
+    int64_t i = act[j];
+    float v = w[i];
+    for (int n = 0; n < N; ++n) v = fmaf(a[n], orc_gauss_one(seeds[n], 0u, (uint64_t)(gid0 + i)), v);
+    w[i] = bf16_storage ? orc_round_bf16(v) : v;
+  }
+}
+
+void orc_theta_update_coeffs(float* theta, int64_t n, int64_t tid0, const uint64_t* seeds,
+                             const float* a, int N, int bf16_storage) {
+  for (int64_t i = 0; i < n; ++i) {
+    float v = theta[i];
+    for (int q = 0; q < N; ++q) v = fmaf(a[q], orc_gauss_one(seeds[q], 1u, (uint64_t)(tid0 + i)), v);
+    theta[i] = bf16_storage ? orc_round_bf16(v) : v;
+  }
+}

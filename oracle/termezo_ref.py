@@ -75,6 +75,10 @@ def lib():
         "orc_multi_coeff": (f32, [f32, i32, f32]),
         "orc_update_layer_multi": (None, [P, P, i64, i64, P, P, i32, f32, i32]),
         "orc_theta_update_multi": (None, [P, i64, i64, P, P, i32, f32, i32]),
+        "orc_es_standardize": (None, [P, i32, P]),
+        "orc_es_coeffs": (None, [P, i32, f32, i32, P]),
+        "orc_update_layer_coeffs": (None, [P, P, i64, i64, P, P, i32, i32]),
+        "orc_theta_update_coeffs": (None, [P, i64, i64, P, P, i32, i32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -239,6 +243,23 @@ def theta_updated(theta: np.ndarray, tid0: int, seed: int, lr: float, g: float,
 def multi_coeff(lr: float, K: int, g: float) -> float:
     """a_k = -((lr / K) g_k) in fp32 (the coefficient of direction k)."""
     return float(np.float32(lib().orc_multi_coeff(float(lr), int(K), float(g))))
+
+
+def es_standardize(rewards) -> np.ndarray:
+    """Population z-score of the rewards (fp64, index order), rounded to fp32;
+    all zero when the standard deviation is zero (RL appendix, ES reading)."""
+    r = _f32(np.asarray(rewards)).ravel()
+    out = np.empty(r.size, np.float32)
+    lib().orc_es_standardize(_p(r), r.size, _p(out))
+    return out
+
+
+def es_coeffs(rewards, lr: float, standardize: bool = True) -> np.ndarray:
+    """a_n = (lr / N) * Rt_n in fp32 (Rt: standardised or raw rewards)."""
+    r = _f32(np.asarray(rewards)).ravel()
+    out = np.empty(r.size, np.float32)
+    lib().orc_es_coeffs(_p(r), r.size, float(lr), int(bool(standardize)), _p(out))
+    return out
 
 
 def shrink_layer(w: np.ndarray, act, tau: float, xi0: float) -> np.ndarray:
@@ -442,6 +463,33 @@ class TerMeZOOracle:
         if self.theta is not None:
             lib().orc_theta_update_multi(_p(self.theta), self.theta.size, 0, _p(sd), _p(gg), K,
                                          float(lr), int(self.theta_bf16))
+            self.theta_cur = self.theta.copy()
+        self._refresh_thresholds()
+        for l in range(len(self.layers)):
+            act = _i64(self.active[l]).copy()
+            n = lib().orc_shrink_layer(_p(self.layer_w(l)), _p(act), act.size,
+                                       float(self.tau[l]), float(self.xi0))
+            self.active[l] = act[:n].copy()
+        self.last_seed = None
+        return self.k
+
+    def es_update(self, seeds: Sequence[int], rewards: Sequence[float], lr: float,
+                  standardize: bool = True) -> int:
+        """Evolution strategies on the mask (RL appendix): w <- rnd(fma chain over n
+        of a_n z_n) at the actives (theta densely, stream 1), a_n = (lr/N) Rt_n,
+        then the thresholds and eq. selection_ as after any update."""
+        N = len(seeds)
+        assert N == len(rewards) and N >= 1
+        sd = np.array([s & (2**64 - 1) for s in seeds], dtype=np.uint64)
+        a = es_coeffs(rewards, lr, standardize)
+        for l in range(len(self.layers)):
+            w = self.layer_w(l)
+            act = _i64(self.active[l])
+            lib().orc_update_layer_coeffs(_p(w), _p(act), act.size, int(self.offsets[l]), _p(sd),
+                                          _p(a), N, int(self.bf16))
+        if self.theta is not None:
+            lib().orc_theta_update_coeffs(_p(self.theta), self.theta.size, 0, _p(sd), _p(a), N,
+                                          int(self.theta_bf16))
             self.theta_cur = self.theta.copy()
         self._refresh_thresholds()
         for l in range(len(self.layers)):

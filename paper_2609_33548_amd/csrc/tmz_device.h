@@ -22,8 +22,10 @@ __device__ __forceinline__ U4 philox10(uint32_t c0, uint32_t c1, uint32_t c2, ui
                                        uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t hA = __umulhi(0xD2511F53u, c0), lA = 0xD2511F53u * c0;
-    const uint32_t hB = __umulhi(0xCD9E8D57u, c2), lB = 0xCD9E8D57u * c2;
+    // full 64-bit products (one v_mad_u64_u32 each instead of a mul_hi / mul_lo pair)
+    const uint64_t pA = (uint64_t)0xD2511F53u * c0, pB = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t hA = (uint32_t)(pA >> 32), lA = (uint32_t)pA;
+    const uint32_t hB = (uint32_t)(pB >> 32), lB = (uint32_t)pB;
     const uint32_t n0 = hB ^ c1 ^ k0;
     const uint32_t n2 = hA ^ c3 ^ k1;
     c0 = n0;

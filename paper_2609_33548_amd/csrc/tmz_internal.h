@@ -152,6 +152,8 @@ struct termezo_ctx {
   int64_t* d_tile_eqb = nullptr;             // T      equal keys before the tile
   int64_t* d_blk_cnt = nullptr;              // shrink block counts
   int64_t blk_cap = 0;
+  uint64_t* d_shrink_flags = nullptr;        // shrink keep flags, one word per thread
+  int64_t flag_cap = 0;
   double* d_loss = nullptr;                  // loss accumulators
   float* d_scal = nullptr;                   // [0] update coefficient a, [1] g
   int n_cu = 0;                              // compute units of the device
@@ -240,6 +242,8 @@ hipError_t launch_set_coeffs(termezo_ctx* c, const float* a, int K);
 hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float* fm, float eps,
                                     float lr);
 // a_k = -((lr / K) g_k), g_k = (F+_k - F-_k) / (2 eps) from device losses [2K] (F+_k, F-_k pairs)
+hipError_t launch_es_coeffs(termezo_ctx* c, const float* rewards, int N, float lr,
+                            int standardize);
 hipError_t launch_coeffs_multi_from_losses(termezo_ctx* c, const float* losses, int K, float eps,
                                            float lr);
 // coefficients from d_scal[0 .. K-1]; the updated values of the actives go to d_wp (list order)

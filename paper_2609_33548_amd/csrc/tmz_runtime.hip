@@ -75,6 +75,7 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   dfree(c->d_act_tmp);
   dfree(c->d_wp);
   dfree(c->d_blk_cnt);
+  dfree(c->d_shrink_flags);
   c->act_cap = 0;
   const int64_t cap = k > 0 ? k : 1;
   TMZ_HIP(c, dalloc(&c->d_act, (size_t)cap));
@@ -82,6 +83,9 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   TMZ_HIP(c, dalloc(&c->d_wp, (size_t)cap));
   c->blk_cap = cap / 1024 + 2;   // shrink blocks hold at least 1024 entries (4 per thread)
   TMZ_HIP(c, dalloc(&c->d_blk_cnt, (size_t)c->blk_cap));
+  // shrink flags, one word per thread: at most 2048 blocks below 64 entries per thread
+  c->flag_cap = std::max((int64_t)2048 * 256, cap / 64) + 256;
+  TMZ_HIP(c, dalloc(&c->d_shrink_flags, (size_t)c->flag_cap));
   c->act_cap = cap;
   return TERMEZO_OK;
 }
@@ -135,6 +139,7 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_tile_out);
   dfree(c->d_tile_eqb);
   dfree(c->d_blk_cnt);
+  dfree(c->d_shrink_flags);
   dfree(c->d_loss);
   dfree(c->d_scal);
   dfree(c->d_xq);
@@ -502,6 +507,55 @@ termezo_status termezo_update_multi_from_losses(termezo_ctx* c, const uint64_t* 
   return finish_update(c, seed_list(seeds, K), nullptr);
 }
 
+// Evolution strategies on the mask: the coefficients a_n = (lr / N) Rt_n (Rt: the
+// population z-score of the rewards in fp64, index order, or the raw rewards),
+// then the K-direction update with the N seeds.
+termezo_status termezo_es_update(termezo_ctx* c, const uint64_t* seeds, const float* rewards,
+                                 int32_t N, float lr, int32_t standardize, int64_t* k_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!seeds || !rewards || N < 1 || N > kMaxK)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "null seeds / rewards or N outside [1, 32]");
+  if (!finite(lr)) return fail(c, TERMEZO_ERR_INVALID_ARG, "lr must be finite");
+  for (int32_t n = 0; n < N; ++n)
+    if (!finite(rewards[n])) return fail(c, TERMEZO_ERR_INVALID_ARG, "rewards must be finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  float rt[kMaxK];
+  for (int32_t n = 0; n < N; ++n) rt[n] = rewards[n];
+  if (standardize) {
+    double mu = 0.0, var = 0.0;
+    for (int32_t n = 0; n < N; ++n) mu += (double)rewards[n];
+    mu /= (double)N;
+    for (int32_t n = 0; n < N; ++n) {
+      const double d = (double)rewards[n] - mu;
+      var += d * d;
+    }
+    var /= (double)N;
+    const double sd = std::sqrt(var);
+    for (int32_t n = 0; n < N; ++n)
+      rt[n] = sd > 0.0 ? (float)(((double)rewards[n] - mu) / sd) : 0.0f;
+  }
+  const float cN = lr / (float)N;
+  float a[kMaxK];
+  for (int32_t n = 0; n < N; ++n) {
+    a[n] = cN * rt[n];
+    if (!finite(a[n])) return fail(c, TERMEZO_ERR_INVALID_ARG, "ES coefficient is not finite");
+  }
+  TMZ_HIP(c, launch_set_coeffs(c, a, N));
+  return finish_update(c, seed_list(seeds, N), k_out);
+}
+
+termezo_status termezo_es_update_from_rewards(termezo_ctx* c, const uint64_t* seeds,
+                                              const float* rewards, int32_t N, float lr,
+                                              int32_t standardize) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!seeds || !rewards || N < 1 || N > kMaxK)
+    return fail(c, TERMEZO_ERR_INVALID_ARG, "null seeds / rewards or N outside [1, 32]");
+  if (!finite(lr)) return fail(c, TERMEZO_ERR_INVALID_ARG, "lr must be finite");
+  if (!c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "update without a perturbation");
+  TMZ_HIP(c, launch_es_coeffs(c, rewards, N, lr, standardize ? 1 : 0));
+  return finish_update(c, seed_list(seeds, N), nullptr);
+}
+
 termezo_status termezo_compact(termezo_ctx* c) {
   if (!c) return TERMEZO_ERR_INVALID_ARG;
   if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "compact before build_mask");
@@ -561,7 +615,7 @@ termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
   int64_t b = c->D / 4;                                          // 2-bit codes
   b += L * (8 * 8 + 4 * 4 + 4 + 8 + 4 + 8) + 3 * (L + 1) * 8;    // per-layer state, offsets
   b += T * (4 + 8 + 8 + 8 + 8 + 8) + 8;                          // tile tables and scratch
-  b += cap * (4 + 4 + 4) + c->blk_cap * 8;                       // index lists, w', shrink
+  b += cap * (4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;     // index lists, w', shrink
   if (c->compact) b += 2 * cap * dsz;                            // active latents (list order)
   b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;
   b += c->xq_cap + c->xs_cap * 4;                                // activation-quant scratch

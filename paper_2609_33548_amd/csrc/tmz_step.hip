@@ -584,6 +584,15 @@ __global__ void __launch_bounds__(kRqThreads) k_requant_list(DevState st, const 
   }
 }
 
+// The four draws of Philox counter quad q on a stream: one Philox call and one
+// Box-Muller pair per two ids -- the operations of gauss_at, so the values are the same.
+__device__ __forceinline__ void gauss_quad(uint64_t seed, uint64_t q, uint32_t stream, float z[4]) {
+  const U4 x = philox10((uint32_t)q, (uint32_t)(q >> 32), stream, 0u, (uint32_t)seed,
+                        (uint32_t)(seed >> 32));
+  box_muller(x.a, x.b, z[0], z[1]);     // ids 4q, 4q+1: cos, sin of the pair (x0, x1)
+  box_muller(x.c, x.d, z[2], z[3]);     // ids 4q+2, 4q+3: cos, sin of the pair (x2, x3)
+}
+
 // ---------------------------------------------------------------------------
 // Perturbation at the actives: w' = fma(se, z, w), stored compactly; the
 // exact change of the fixed-point |w| sum goes to S_cur (initialised to
@@ -694,6 +703,26 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
       list4(wc, j0, n, wv);
     else if (one)
       gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
+    const uint64_t g0 = one ? (uint64_t)(st.gid0[lr] + i[0]) : 0ull;
+    if (one && n == 4 && i[3] == i[0] + 3 && (g0 & 3u) == 0) {
+      // a whole Philox quad (dense runs): one draw, no per-entry layer walk
+      if (l != lr) {
+        if (any) atomicAdd((unsigned long long*)&st.S_cur[l], (unsigned long long)acc);
+        acc = 0;
+        l = lr;
+      }
+      float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (se != 0.0f) gauss_quad(seed, g0 >> 2, 0u, z);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[r] = se != 0.0f ? fmaf(se, z[r], wv[r]) : wv[r];
+        bad |= !in_fix_range(v[r]);
+        acc += (long long)fix_abs(v[r]) - (long long)fix_abs(wv[r]);
+      }
+      any = true;
+      put4(wp, j0, 4, v);
+      continue;
+    }
     for (int r = 0; r < n; ++r) {
       const int64_t j = j0 + r;
       if (l < 0) {
@@ -724,13 +753,6 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
 // the same.  Both perturbed copies theta +- eps z (rounded to the storage
 // type) come from one pass; the update is in place.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void gauss_quad(uint64_t seed, uint64_t q, uint32_t stream, float z[4]) {
-  const U4 x = philox10((uint32_t)q, (uint32_t)(q >> 32), stream, 0u, (uint32_t)seed,
-                        (uint32_t)(seed >> 32));
-  box_muller(x.a, x.b, z[0], z[1]);     // ids 4q, 4q+1: cos, sin of the pair (x0, x1)
-  box_muller(x.c, x.d, z[2], z[3]);     // ids 4q+2, 4q+3: cos, sin of the pair (x2, x3)
-}
-
 __device__ __forceinline__ float th_load(const float* p) { return *p; }
 __device__ __forceinline__ float th_load(const uint16_t* p) { return bf16_to_f32(*p); }
 __device__ __forceinline__ void th_store(float* p, float v) { *p = v; }
@@ -861,6 +883,39 @@ __global__ void k_coeffs_multi_from_losses(const float* losses, int K, float eps
   if (!isfinite(a)) atomicOr(err, 2);
 }
 
+// Evolution strategies on the mask (appendix on RL-based fine-tuning): a_n =
+// (lr / N) Rt_n in fp32, Rt the population z-score of the rewards in fp64 (index
+// order; zero when the deviation is zero) or the raw rewards.  One thread: the
+// sums run in a fixed order.  A non-finite coefficient skips the update (the
+// update kernels test every coefficient) and raises the deferred error bit 2.
+__global__ void k_es_coeffs(const float* rewards, int N, float lr, int standardize, float* scal,
+                            int32_t* err) {
+  if (threadIdx.x != 0) return;
+  float rt[kMaxK];
+  for (int n = 0; n < N; ++n) rt[n] = rewards[n];
+  if (standardize) {
+    double mu = 0.0, var = 0.0;
+    for (int n = 0; n < N; ++n) mu += (double)rewards[n];
+    mu /= (double)N;
+    for (int n = 0; n < N; ++n) {
+      const double d = (double)rewards[n] - mu;
+      var += d * d;
+    }
+    var /= (double)N;
+    const double sd = sqrt(var);
+    for (int n = 0; n < N; ++n)
+      rt[n] = sd > 0.0 ? (float)(((double)rewards[n] - mu) / sd) : (isfinite(sd) ? 0.0f : NAN);
+  }
+  const float c = __fdiv_rn(lr, (float)N);
+  bool ok = true;
+  for (int n = 0; n < N; ++n) {
+    const float a = c * rt[n];
+    scal[n] = a;
+    ok &= isfinite(a) != 0;
+  }
+  if (!ok) atomicOr(err, 2);
+}
+
 // g = (F+ - F-) / (2 eps) and a = -(lr g), in fp32 (eq. spsa).
 __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps, float lr,
                                     float* scal, int32_t* err) {
@@ -905,6 +960,45 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       list4((const T*)wc, j0, n, wv);
     else if (one)
       gather4(reinterpret_cast<const T*>(st.w[lr]), i, n, wv);
+    const uint64_t g0 = one ? (uint64_t)(st.gid0[lr] + i[0]) : 0ull;
+    if (one && n == 4 && i[3] == i[0] + 3 && (g0 & 3u) == 0) {
+      // a whole Philox quad (dense runs): one draw per direction, same fma chain
+      if (l != lr) {
+        if (any) atomicAdd((unsigned long long*)&st.S_clean[l], (unsigned long long)acc);
+        acc = 0;
+        l = lr;
+      }
+      T* w = reinterpret_cast<T*>(const_cast<void*>(st.w[lr]));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) nv[r] = wv[r];
+      if (a_ok) {
+        float z[4], v[4];
+        gauss_quad(seed, g0 >> 2, 0u, z);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaf(a, z[r], wv[r]);
+        for (int q = 1; q < K; ++q) {
+          gauss_quad(seeds.s[q], g0 >> 2, 0u, z);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = fmaf(scal[q], z[r], v[r]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) nv[r] = storage_round(w, v[r]);
+        if (wc) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) store1((T*)wc, j0 + r, nv[r]);
+        } else {
+          scatter4(w, i, 4, nv);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        bad |= !in_fix_range(nv[r]);
+        acc += (long long)fix_abs(nv[r]) - (long long)fix_abs(wv[r]);
+      }
+      any = true;
+      put4(wn, j0, 4, nv);
+      continue;
+    }
     for (int r = 0; r < n; ++r) {
       const int64_t j = j0 + r;
       if (l < 0) {
@@ -1072,6 +1166,10 @@ __device__ __forceinline__ void load_layer_lds(int64_t* aoff, float* tau, const 
   __syncthreads();
 }
 
+// Keep flags of a thread's entries (bit r: entry base + 256 r + t); the loads go
+// out sixteen at a time.
+constexpr int kShrinkBatch = 16;
+
 __device__ __forceinline__ uint64_t shrink_flags(const int64_t* aoff, const float* tau, int L,
                                                  const float* __restrict__ wn, int64_t k,
                                                  int64_t base, int per, float xi0) {
@@ -1079,24 +1177,37 @@ __device__ __forceinline__ uint64_t shrink_flags(const int64_t* aoff, const floa
   const int64_t j0 = base + threadIdx.x;
   if (j0 >= k) return 0;
   int l = layer_of(aoff, L, j0);
-  for (int r = 0; r < per; ++r) {
-    const int64_t j = j0 + 256 * r;
-    if (j >= k) break;
-    while (aoff[l + 1] <= j) ++l;
-    if (fabsf(fabsf(wn[j]) - tau[l]) <= xi0) m |= 1ull << r;
+  int64_t nxt = aoff[l + 1];
+  for (int r0 = 0; r0 < per; r0 += kShrinkBatch) {
+    float v[kShrinkBatch];
+#pragma unroll
+    for (int u = 0; u < kShrinkBatch; ++u) {
+      const int64_t j = j0 + 256 * (int64_t)(r0 + u);
+      v[u] = (r0 + u < per && j < k) ? wn[j] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kShrinkBatch; ++u) {
+      const int64_t j = j0 + 256 * (int64_t)(r0 + u);
+      if (r0 + u >= per || j >= k) break;
+      while (nxt <= j) nxt = aoff[++l + 1];
+      if (fabsf(fabsf(v[u]) - tau[l]) <= xi0) m |= 1ull << (r0 + u);
+    }
   }
   return m;
 }
 
+// Pass 1: the flags of every thread (kept for pass 2) and the block's kept count.
 __global__ void __launch_bounds__(256) k_shrink_count(DevState st, const int64_t* act_off,
                                                       const float* __restrict__ wn, float xi0,
-                                                      int per, int64_t* blk_cnt) {
+                                                      int per, int64_t* blk_cnt,
+                                                      uint64_t* __restrict__ flags) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   __shared__ float tau[kMaxLayers];
   __shared__ unsigned long long red[4];
   load_layer_lds(aoff, tau, act_off, st.tau, st.L);
   const int64_t k = aoff[st.L];
   const uint64_t m = shrink_flags(aoff, tau, st.L, wn, k, (int64_t)blockIdx.x * 256 * per, per, xi0);
+  flags[(int64_t)blockIdx.x * 256 + threadIdx.x] = m;
   const unsigned long long s = block_sum_u64(__popcll(m), red);
   if (threadIdx.x == 0) blk_cnt[blockIdx.x] = (int64_t)s;
 }
@@ -1142,20 +1253,22 @@ __global__ void __launch_bounds__(1024) k_blocks_scan(int64_t* blk_cnt, int64_t 
   if (tid == 0) *total = carry;
 }
 
+// Pass 2: kept entries to their new positions (ordered r, then wave, then lane within
+// a block), dropped ones get their code at tau_ref.
 __global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_t* __restrict__ act,
                                                       const int64_t* act_off,
-                                                      const float* __restrict__ wn, float xi0,
-                                                      int per, const int64_t* blk_off,
+                                                      const float* __restrict__ wn, int per,
+                                                      const int64_t* blk_off,
+                                                      const uint64_t* __restrict__ flags,
                                                       uint32_t* __restrict__ act_new,
                                                       int64_t* act_off_new, void* wc_new,
                                                       int wc_bf16) {
   __shared__ int64_t aoff[kMaxLayers + 1];
-  __shared__ float tau[kMaxLayers];
   __shared__ int32_t cnt[kShrinkPer * 4];   // kept entries per (r, wave), then their offsets
-  load_layer_lds(aoff, tau, act_off, st.tau, st.L);
-  const int64_t k = aoff[st.L];
+  for (int i = threadIdx.x; i <= st.L; i += blockDim.x) aoff[i] = act_off[i];
+  const int64_t k = act_off[st.L];
   const int64_t base = (int64_t)blockIdx.x * 256 * per;
-  const uint64_t m = shrink_flags(aoff, tau, st.L, wn, k, base, per, xi0);
+  const uint64_t m = flags[(int64_t)blockIdx.x * 256 + threadIdx.x];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const unsigned long long below = (1ull << lane) - 1ull;
   for (int r = 0; r < per; ++r) {
@@ -1176,24 +1289,40 @@ __global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_
   if (j0 >= k) return;
   const int64_t boff = blk_off[blockIdx.x];
   int l = layer_of(aoff, st.L, j0);
-  for (int r = 0; r < per; ++r) {
-    const int64_t j = j0 + 256 * r;
-    const bool keep = (m >> r) & 1ull;
-    const unsigned long long b = __ballot(keep);
-    if (j >= k) break;
-    const int64_t pos = boff + cnt[4 * r + wid] + __popcll(b & below);
-    while (aoff[l + 1] <= j) ++l;
-    if (j == aoff[l]) act_off_new[l] = pos;   // first entry of layer l
-    if (keep) {
-      act_new[pos] = act[j];
-      if (wc_new) {                           // compact mode: the kept latent, list order
-        if (wc_bf16)
-          reinterpret_cast<uint16_t*>(wc_new)[pos] = f32_to_bf16_rne(wn[j]);
-        else
-          reinterpret_cast<float*>(wc_new)[pos] = wn[j];
+  int64_t cur = aoff[l], nxt = aoff[l + 1];
+  for (int r0 = 0; r0 < per; r0 += kShrinkBatch) {
+    uint32_t a[kShrinkBatch];
+#pragma unroll
+    for (int u = 0; u < kShrinkBatch; ++u) {
+      const int64_t j = j0 + 256 * (int64_t)(r0 + u);
+      a[u] = (r0 + u < per && j < k) ? act[j] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kShrinkBatch; ++u) {
+      const int r = r0 + u;
+      if (r >= per) break;
+      const int64_t j = j0 + 256 * (int64_t)r;
+      const bool keep = (m >> r) & 1ull;
+      const unsigned long long b = __ballot(keep);
+      if (j >= k) break;
+      const int64_t pos = boff + cnt[4 * r + wid] + __popcll(b & below);
+      while (nxt <= j) {
+        cur = nxt;
+        nxt = aoff[++l + 1];
       }
-    } else                                    // frozen from now on: its code at tau_ref
-      set_code(st.codes, st.code_off[l], act[j], ternary_code(wn[j], st.tau_ref[l]));
+      if (j == cur) act_off_new[l] = pos;     // first entry of layer l
+      if (keep) {
+        act_new[pos] = a[u];
+        if (wc_new) {                         // compact mode: the kept latent, list order
+          if (wc_bf16)
+            reinterpret_cast<uint16_t*>(wc_new)[pos] = f32_to_bf16_rne(wn[j]);
+          else
+            reinterpret_cast<float*>(wc_new)[pos] = wn[j];
+        }
+      } else {                                // frozen from now on: its code at tau_ref
+        set_code(st.codes, st.code_off[l], a[u], ternary_code(wn[j], st.tau_ref[l]));
+      }
+    }
   }
 }
 
@@ -1477,6 +1606,13 @@ hipError_t launch_set_coeffs(termezo_ctx* c, const float* a, int K) {
   return hipGetLastError();
 }
 
+hipError_t launch_es_coeffs(termezo_ctx* c, const float* rewards, int N, float lr,
+                            int standardize) {
+  hipLaunchKernelGGL(k_es_coeffs, dim3(1), dim3(64), 0, c->stream, rewards, N, lr, standardize,
+                     c->d_scal, c->d_err);
+  return hipGetLastError();
+}
+
 hipError_t launch_coeffs_multi_from_losses(termezo_ctx* c, const float* losses, int K, float eps,
                                            float lr) {
   hipLaunchKernelGGL(k_coeffs_multi_from_losses, dim3(1), dim3(kMaxK), 0, c->stream, losses, K,
@@ -1490,13 +1626,15 @@ hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
   while (per < kShrinkPer && k > (int64_t)2048 * 256 * per) per *= 2;
   const int64_t nb = max((int64_t)1, (k + 256 * per - 1) / (256 * per));
   int64_t* total = c->d_blk_cnt + nb;  // blk_cap >= nb + 1
+  if (nb > c->blk_cap - 1 || nb * 256 > c->flag_cap) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_shrink_count, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act_off,
-                     c->d_wp, c->xi0, per, c->d_blk_cnt);
+                     c->d_wp, c->xi0, per, c->d_blk_cnt, c->d_shrink_flags);
   hipLaunchKernelGGL(k_blocks_scan, dim3(1), dim3(1024), 0, c->stream, c->d_blk_cnt, nb, total);
   // offsets of layers without any entry are fixed afterwards
   hipLaunchKernelGGL(k_shrink_write, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                     c->d_act_off, c->d_wp, c->xi0, per, c->d_blk_cnt, c->d_act_tmp,
-                     c->d_act_off_tmp, c->d_wc_tmp, c->dtype == TERMEZO_BF16 ? 1 : 0);
+                     c->d_act_off, c->d_wp, per, c->d_blk_cnt,
+                     (const uint64_t*)c->d_shrink_flags, c->d_act_tmp, c->d_act_off_tmp,
+                     c->d_wc_tmp, c->dtype == TERMEZO_BF16 ? 1 : 0);
   hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(256), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
   return hipGetLastError();

@@ -71,6 +71,8 @@ _SIGS = {
     "termezo_update_from_losses": [_P, _P, _P, _f32, _f32],
     "termezo_update_multi": [_P, _P, _P, _i32, _f32, ctypes.POINTER(_i64)],
     "termezo_update_multi_from_losses": [_P, _P, _P, _i32, _f32, _f32],
+    "termezo_es_update": [_P, _P, _P, _i32, _f32, _i32, ctypes.POINTER(_i64)],
+    "termezo_es_update_from_rewards": [_P, _P, _P, _i32, _f32, _i32],
     "termezo_theta_register": [_P, ctypes.POINTER(Theta), _i32],
     "termezo_set_dense_requant": [_P, _i32],
     "termezo_compact": [_P],
@@ -313,6 +315,26 @@ class Context:
         sd = (ctypes.c_uint64 * K)(*[s & (2**64 - 1) for s in seeds])
         self._check(_lib.termezo_update_multi_from_losses(self.handle, sd, _ptr(losses), K, eps, lr),
                     "update_multi_from_losses")
+
+    def es_update(self, seeds, rewards, lr: float, standardize: bool = True,
+                  want_k: bool = True) -> Optional[int]:
+        """Evolution strategies on the mask: the reward-weighted sum of the N
+        directions (host rewards), then the shrink."""
+        N = len(seeds)
+        sd = (ctypes.c_uint64 * N)(*[s & (2**64 - 1) for s in seeds])
+        rr = (ctypes.c_float * N)(*[float(r) for r in rewards])
+        k = _i64()
+        self._check(_lib.termezo_es_update(self.handle, sd, rr, N, lr, int(bool(standardize)),
+                                           ctypes.byref(k) if want_k else None), "es_update")
+        return int(k.value) if want_k else None
+
+    def es_update_from_rewards(self, seeds, rewards, lr: float, standardize: bool = True):
+        """The same with the rewards in a device fp32 tensor [N]; never waits."""
+        N = len(seeds)
+        sd = (ctypes.c_uint64 * N)(*[s & (2**64 - 1) for s in seeds])
+        self._check(_lib.termezo_es_update_from_rewards(self.handle, sd, _ptr(rewards), N, lr,
+                                                        int(bool(standardize))),
+                    "es_update_from_rewards")
 
     def mse_loss(self, y, target) -> float:
         out = _f32()

@@ -441,6 +441,87 @@ def test_k_direction_update_reduces_to_single_and_sequential_updates(orc):
     assert np.allclose(moved, step, rtol=1e-4, atol=1e-8)
 
 
+def _zscore_decimal(r):
+    """Population z-score of fp32 rewards in 50-digit decimal arithmetic."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 50
+    d = [Decimal(float(x)) for x in r]
+    n = Decimal(len(d))
+    mu = sum(d) / n
+    var = sum((x - mu) ** 2 for x in d) / n
+    if var == 0:
+        return np.zeros(len(d))
+    sd = var.sqrt()
+    return np.array([float((x - mu) / sd) for x in d])
+
+
+def test_es_standardisation_is_population_zscore(orc):
+    """RL appendix (ES reading): the rewards are standardised over the population
+    with the population standard deviation; checked against 50-digit decimal
+    arithmetic (within one fp32 ulp), the zero-mean / unit-variance property,
+    invariance under a positive affine map of the rewards, order preservation,
+    and the degenerate populations (N = 1, equal rewards) that give zero."""
+    rng = np.random.default_rng(5)
+    for N in (2, 5, 30, 32):
+        r = rng.normal(0.3, 2.0, N).astype(np.float32)
+        got = orc.es_standardize(r)
+        ref = _zscore_decimal(r)
+        assert np.all(np.abs(got - ref) <= _ulp32(ref)), N
+        assert abs(float(np.sum(got.astype(np.float64)))) < 1e-5 * N
+        assert abs(float(np.mean(got.astype(np.float64) ** 2)) - 1.0) < 1e-6
+        assert np.array_equal(np.argsort(got, kind="stable"), np.argsort(r, kind="stable"))
+        aff = (np.float64(r) * 3.5 - 7.0).astype(np.float32)
+        assert np.all(np.abs(orc.es_standardize(aff) - _zscore_decimal(aff)) <= _ulp32(got) * 2 + 1e-6)
+    assert np.array_equal(orc.es_standardize([4.25] * 7), np.zeros(7, np.float32))
+    assert np.array_equal(orc.es_standardize([1.5]), np.zeros(1, np.float32))
+    # binary rewards: +-1 exactly (two equal groups)
+    assert np.array_equal(orc.es_standardize([1, 0, 0, 1]), np.array([1, -1, -1, 1], np.float32))
+    # coefficients: (lr / N) Rt in fp32; raw rewards when not standardised
+    c = np.float32(np.float32(0.3) / np.float32(4))
+    assert np.array_equal(orc.es_coeffs([1, 0, 0, 1], 0.3), c * np.array([1, -1, -1, 1], np.float32))
+    assert np.array_equal(orc.es_coeffs([2, -3, 0, 1], 0.3, standardize=False),
+                          c * np.array([2, -3, 0, 1], np.float32))
+
+
+@pytest.mark.parametrize("standardize", [True, False])
+def test_es_update_is_reward_weighted_sum_on_the_mask(orc, standardize):
+    """RL appendix: the ES update moves the masked latents (and theta, densely)
+    by (lr / N) sum_n Rt_n z_n, with the same z_n that perturbed them (one-sided
+    w + sigma z_n); unmasked latents stay bit-identical; N = 1 with
+    standardisation leaves everything unchanged."""
+    shapes = [(8, 32), (16, 16)]
+    D = sum(o * i for o, i in shapes)
+    w0 = synth.latents(31, [D])
+    t0 = synth.latents(32, [48])
+    st = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w0, theta=t0)
+    st.build_mask(0.25)
+    act = np.concatenate([x + st.offsets[l] for l, x in enumerate(st.active)])
+    seeds = [101, 102, 103, 104, 105]
+    rewards = np.array([0.2, -1.0, 0.7, 0.7, 3.1], np.float32)
+    for sd in seeds:                             # one-sided population members
+        st.perturb(sd, 1e-3, 1)
+    lr = 5e-2
+    rt = _zscore_decimal(rewards) if standardize else rewards.astype(np.float64)
+    step = np.zeros(D + t0.size)
+    for sd, rn in zip(seeds, rt):
+        u = np.zeros(D + t0.size)
+        u[act] = orc.gauss(sd, act)
+        u[D:] = orc.gauss_range(sd, 0, t0.size, stream=1)
+        step += (lr / len(seeds)) * rn * u
+    st.es_update(seeds, rewards, lr, standardize)
+    moved = np.concatenate([st.w, st.theta]).astype(np.float64) - np.concatenate([w0, t0])
+    assert np.allclose(moved, step, rtol=1e-4, atol=1e-9)
+    frozen = np.setdiff1d(np.arange(D), act)
+    assert np.array_equal(st.w[frozen], w0[frozen])
+    assert np.count_nonzero(moved[act]) > 0.9 * act.size
+    # one member, standardised: no move
+    one = orc.TerMeZOOracle([orc.Layer(o, i) for o, i in shapes], w0, theta=t0)
+    one.build_mask(0.25)
+    one.perturb(7, 1e-3, 1)
+    one.es_update([7], [2.5], lr)
+    assert np.array_equal(one.w, w0) and np.array_equal(one.theta, t0)
+
+
 def test_smoothed_gradient_of_ternary_objective(orc):
     """F(w) = c'Q(w) with tau held fixed: the Gaussian-smoothed gradient has the
     closed form (c_i/eps)(phi((w_i-tau)/eps) + phi((w_i+tau)/eps)), and the
