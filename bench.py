@@ -309,12 +309,14 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         k = ctx.active_count()
 
         def time_perturb(dense):
+            # pairs as in a step: (s, +eps) then (s, -eps); the second call of a pair
+            # reuses the values the first one wrote
             ctx.set_dense_requant(dense)
             ctx.perturb(99, 1e-3, 1)
             torch.cuda.synchronize()
             ev0.record(stream)
             for t in range(reps):
-                ctx.perturb(100 + t, 1e-3, 1 if t % 2 == 0 else -1)
+                ctx.perturb(100 + t // 2, 1e-3, 1 if t % 2 == 0 else -1)
             ev1.record(stream)
             torch.cuda.synchronize()
             return ev0.elapsed_time(ev1) / reps * 1e-3
@@ -342,7 +344,8 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         _emit({"sweep": "perturb_requant", "latents": D, "ratio": r, "k": k, "ms": t_p * 1e3,
                "algorithmic_bytes": b_p, "GB/s": b_p / t_p / 1e9,
                "frac_hbm": b_p / t_p / 1e9 / HBM_PEAK_GBS,
-               "protocol": "dense requantisation of every latent (termezo_set_dense_requant)",
+               "protocol": "dense requantisation of every latent (termezo_set_dense_requant); "
+                           "mean over 5 (+eps, -eps) pairs of one seed each",
                "cpu_baseline": cp})
         # default path: the same codes; only the actives' codes are rewritten while the
         # threshold-drift guard holds (per active: 4 B index + 2 B latent read, 4 B w' written,
@@ -353,7 +356,7 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
                "frac_hbm": b_g / t_g / 1e9 / HBM_PEAK_GBS,
                "speedup_vs_dense": t_p / t_g,
                "protocol": "default termezo_perturb (guarded: dense where the guard fails and "
-                           "for every layer when k > D/256)"})
+                           "for every layer when k > D/256); mean over 5 (+eps, -eps) pairs"})
         _emit({"sweep": "update", "latents": D, "ratio": r, "k": k, "k_after": k_after,
                "us": t_u * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_u / 1e9,
                "frac_hbm": b_u / t_u / 1e9 / HBM_PEAK_GBS, "cpu_baseline": cu})
@@ -372,7 +375,7 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         k = cc.active_count()
         ev0.record(stream)
         for t in range(reps):
-            cc.perturb(100 + t, 1e-3, 1 if t % 2 == 0 else -1)
+            cc.perturb(100 + t // 2, 1e-3, 1 if t % 2 == 0 else -1)
         ev1.record(stream)
         torch.cuda.synchronize()
         t_c = ev0.elapsed_time(ev1) / reps * 1e-3
@@ -393,7 +396,8 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         _emit({"sweep": "perturb_compact", "latents": D, "ratio": r, "k": k, "ms": t_c * 1e3,
                "algorithmic_bytes": b_g, "GB/s": b_g / t_c / 1e9,
                "frac_hbm": b_g / t_c / 1e9 / HBM_PEAK_GBS, "library_bytes": lib_b,
-               "protocol": "termezo_compact after the mask build; actives' codes only"})
+               "protocol": "termezo_compact after the mask build; actives' codes only; mean over "
+                           "5 (+eps, -eps) pairs"})
         _emit({"sweep": "update_compact", "latents": D, "ratio": r, "k": k, "k_after": k_after,
                "us": t_uc * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_uc / 1e9,
                "frac_hbm": b_u / t_uc / 1e9 / HBM_PEAK_GBS})

@@ -138,6 +138,15 @@ struct termezo_ctx {
   std::vector<int64_t> h_act_off;    // host copy, valid when act_off_host_valid
   bool act_off_host_valid = false;
   float* d_wp = nullptr;             // perturbed values at the actives (act_cap)
+  // perturbation pair: the first call of a (seed, eps) pair also writes the other sign's
+  // values (d_wpm, its |w| sums in d_S_alt) and z (d_zc), all in list order
+  float* d_wpm = nullptr;
+  float* d_zc = nullptr;
+  int64_t* d_S_alt = nullptr;        // [L]
+  bool pair_valid = false;
+  uint64_t pair_seed = 0;
+  float pair_eps = 0.f;
+  int pair_sign = 0;                 // sign whose values d_wp / d_S_cur hold
   // compact mode: the active latents in list order (latent dtype), library-owned; the
   // caller's latent tensors are no longer read or written
   bool compact = false;
@@ -235,7 +244,7 @@ hipError_t launch_ref_init(termezo_ctx* c, double xi_lo);
 // after an update: weights leaving the set are frozen at tau_ref (their distance to the new
 // clean threshold exceeds xi0, so to tau_ref at least xi_lo - |tau - tau_ref|)
 hipError_t launch_ref_after_update(termezo_ctx* c, double xi_lo);
-hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se);
+hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se, bool pair);
 hipError_t launch_set_coeff(termezo_ctx* c, float a);
 // K host coefficients to d_scal[0 .. K-1]
 hipError_t launch_set_coeffs(termezo_ctx* c, const float* a, int K);
@@ -247,7 +256,7 @@ hipError_t launch_es_coeffs(termezo_ctx* c, const float* rewards, int N, float l
 hipError_t launch_coeffs_multi_from_losses(termezo_ctx* c, const float* losses, int K, float eps,
                                            float lr);
 // coefficients from d_scal[0 .. K-1]; the updated values of the actives go to d_wp (list order)
-hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds);
+hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds, const float* zc);
 // from d_wp (the updated values): d_act -> d_act_tmp, offsets -> tmp
 hipError_t launch_shrink(termezo_ctx* c, int64_t k);
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);

@@ -74,13 +74,18 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   dfree(c->d_act);
   dfree(c->d_act_tmp);
   dfree(c->d_wp);
+  dfree(c->d_wpm);
+  dfree(c->d_zc);
   dfree(c->d_blk_cnt);
   dfree(c->d_shrink_flags);
   c->act_cap = 0;
+  c->pair_valid = false;
   const int64_t cap = k > 0 ? k : 1;
   TMZ_HIP(c, dalloc(&c->d_act, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_act_tmp, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_wp, (size_t)cap));
+  TMZ_HIP(c, dalloc(&c->d_wpm, (size_t)cap));
+  TMZ_HIP(c, dalloc(&c->d_zc, (size_t)cap));
   c->blk_cap = cap / 1024 + 2;   // shrink blocks hold at least 1024 entries (4 per thread)
   TMZ_HIP(c, dalloc(&c->d_blk_cnt, (size_t)c->blk_cap));
   // shrink flags, one word per thread: at most 2048 blocks below 64 entries per thread
@@ -119,6 +124,7 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_codes);
   dfree(c->d_S_clean);
   dfree(c->d_S_cur);
+  dfree(c->d_S_alt);
   dfree(c->d_tau);
   dfree(c->d_beta);
   dfree(c->d_tau_cur);
@@ -133,6 +139,8 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_act_off);
   dfree(c->d_act_off_tmp);
   dfree(c->d_wp);
+  dfree(c->d_wpm);
+  dfree(c->d_zc);
   dfree(c->d_hist);
   dfree(c->d_sel);
   dfree(c->d_tile_cnt);
@@ -230,6 +238,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_codes, (size_t)words), "alloc codes");
   chk(dalloc(&c->d_S_clean, n_layers), "alloc");
   chk(dalloc(&c->d_S_cur, n_layers), "alloc");
+  chk(dalloc(&c->d_S_alt, n_layers), "alloc");
   chk(dalloc(&c->d_tau, n_layers), "alloc");
   chk(dalloc(&c->d_beta, n_layers), "alloc");
   chk(dalloc(&c->d_tau_cur, n_layers), "alloc");
@@ -304,6 +313,7 @@ termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32
   if (k0 <= 0) return fail(c, TERMEZO_ERR_STATE, "rho0 * D rounds down to an empty mask");
 
   c->has_mask = false;
+  c->pair_valid = false;
   c->codes_valid = false;
   c->pending_perturb = false;
   c->delta = delta;
@@ -357,8 +367,25 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   if (!finite(eps) || !(eps > 0.0f)) return fail(c, TERMEZO_ERR_INVALID_ARG, "eps must be > 0");
   if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "perturb before build_mask");
   const float se = (float)sign * eps;
-  TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
-  TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se));
+  if (sign != 0 && c->pair_valid && c->pair_seed == seed && c->pair_eps == eps) {
+    // the other sign of a pair: its values and sums came with the first call
+    if (sign != c->pair_sign) {
+      std::swap(c->d_wp, c->d_wpm);
+      std::swap(c->d_S_cur, c->d_S_alt);
+      c->pair_sign = sign;
+    }
+  } else {
+    c->pair_valid = false;
+    TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
+    if (sign != 0) TMZ_HIP(c, launch_copy_i64(c->d_S_alt, c->d_S_clean, c->L, c->stream));
+    TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se, sign != 0));
+    if (sign != 0) {
+      c->pair_valid = true;
+      c->pair_seed = seed;
+      c->pair_eps = eps;
+      c->pair_sign = sign;
+    }
+  }
   TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
   // guarded requantisation: the actives' codes only, while no frozen code can change
   // (dense on request, or when the active set exceeds 1/256 of the latents: there the
@@ -430,7 +457,10 @@ SeedList seed_list(const uint64_t* s, int32_t K) {
 // Update at the actives with the coefficients already in d_scal, then the new
 // thresholds and the shrink; the compacted list replaces the old one.
 termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_out) {
-  TMZ_HIP(c, launch_update(c, c->k_bound, seeds));
+  // the first direction's z is kept by the perturbation pass of that seed
+  const bool cached = c->pair_valid && c->pair_seed == seeds.s[0];
+  TMZ_HIP(c, launch_update(c, c->k_bound, seeds, cached ? c->d_zc : nullptr));
+  c->pair_valid = false;
   c->theta_pair_valid = false;
   c->theta_sign = 0;
   for (const ThetaHost& t : c->theta) TMZ_HIP(c, launch_theta_update(c, t, seeds));
@@ -579,6 +609,7 @@ termezo_status termezo_compact(termezo_ctx* c) {
   termezo_status st = sync_and_check(c);
   if (st != TERMEZO_OK) return st;
   c->compact = true;
+  c->pair_valid = false;
   c->k_bound = k;
   return TERMEZO_OK;
 }
@@ -615,7 +646,8 @@ termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
   int64_t b = c->D / 4;                                          // 2-bit codes
   b += L * (8 * 8 + 4 * 4 + 4 + 8 + 4 + 8) + 3 * (L + 1) * 8;    // per-layer state, offsets
   b += T * (4 + 8 + 8 + 8 + 8 + 8) + 8;                          // tile tables and scratch
-  b += cap * (4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;     // index lists, w', shrink
+  b += cap * (4 + 4 + 4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;  // lists, w' pair, z, shrink
+  b += L * 8;                                                    // |w| sums of the other sign
   if (c->compact) b += 2 * cap * dsz;                            // active latents (list order)
   b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;
   b += c->xq_cap + c->xs_cap * 4;                                // activation-quant scratch

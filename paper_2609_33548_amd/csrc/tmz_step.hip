@@ -656,12 +656,22 @@ __device__ __forceinline__ void scatter4(uint16_t* w, const uint32_t i[4], int n
       if (r < n) w[i[r]] = f32_to_bf16_rne(v[r]);
   }
 }
-// Four values to wp[j0 ..]: one 16-byte store for a whole run.
+// Four values to wp[j0 ..]: one 16-byte store for a whole run (8 bytes for bf16
+// values, which the bf16 variant stores exactly).
 __device__ __forceinline__ void put4(float* wp, int64_t j0, int n, const float v[4]) {
   if (n == 4) {
     *reinterpret_cast<float4*>(wp + j0) = make_float4(v[0], v[1], v[2], v[3]);
   } else {
     for (int r = 0; r < n; ++r) wp[j0 + r] = v[r];
+  }
+}
+__device__ __forceinline__ void put4(uint16_t* wp, int64_t j0, int n, const float v[4]) {
+  if (n == 4) {
+    const uint32_t lo = (uint32_t)f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+    const uint32_t hi = (uint32_t)f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+    *reinterpret_cast<uint2*>(wp + j0) = make_uint2(lo, hi);
+  } else {
+    for (int r = 0; r < n; ++r) wp[j0 + r] = f32_to_bf16_rne(v[r]);
   }
 }
 
@@ -671,12 +681,18 @@ __device__ __forceinline__ void list4(const T* wc, int64_t j0, int n, float v[4]
   for (int r = 0; r < 4; ++r) v[r] = r < n ? load1(wc, j0 + r) : 0.0f;
 }
 
-template <typename T>
+// PAIR: both signs of the perturbation from one pass -- w' at +se to wp with its
+// delta in S_cur, w' at -se to wpm with its delta in S_alt, and z to zout (list
+// order), so the other sign of the pair and the update need no generator pass.
+template <typename T, bool PAIR>
 __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
                                                        const uint32_t* __restrict__ act,
                                                        const int64_t* act_off, uint64_t seed,
                                                        float se, float* __restrict__ wp,
-                                                       const T* __restrict__ wc) {
+                                                       const T* __restrict__ wc,
+                                                       float* __restrict__ wpm,
+                                                       float* __restrict__ zout,
+                                                       int64_t* S_alt) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const int64_t k = aoff[st.L];
@@ -688,17 +704,28 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
   const int64_t jb = (int64_t)blockIdx.x * chunk, je = min(k, jb + chunk);
   bool bad = false, any = false;
   int l = -1;
-  long long acc = 0;
+  long long acc = 0, acc2 = 0;
   GaussCache zc;
-  for (int64_t base = jb; base < je; base += 256 * kRun) {
-    const int64_t j0 = base + (int64_t)threadIdx.x * kRun;
-    if (j0 >= je) continue;
-    uint32_t i[4];
-    const int n = run_entries(act, j0, je, i);
+  auto flush_layer = [&]() __attribute__((always_inline)) {
+    if (any) {
+      atomicAdd((unsigned long long*)&st.S_cur[l], (unsigned long long)acc);
+      if (PAIR) atomicAdd((unsigned long long*)&S_alt[l], (unsigned long long)acc2);
+    }
+    acc = 0;
+    acc2 = 0;
+  };
+  // the next run's indices are loaded one iteration ahead
+  uint32_t inx[4] = {0u, 0u, 0u, 0u};
+  int nnx = jb + (int64_t)threadIdx.x * kRun < je
+                ? run_entries(act, jb + (int64_t)threadIdx.x * kRun, je, inx) : 0;
+  for (int64_t j0 = jb + (int64_t)threadIdx.x * kRun; j0 < je; j0 += 256 * kRun) {
+    uint32_t i[4] = {inx[0], inx[1], inx[2], inx[3]};
+    const int n = nnx;
+    nnx = j0 + 256 * kRun < je ? run_entries(act, j0 + 256 * kRun, je, inx) : 0;
     // the run lies in one layer, or it is handled entry by entry
     const int lr = layer_of(aoff, st.L, j0);
     const bool one = aoff[lr + 1] >= j0 + n;
-    float wv[4], v[4];
+    float wv[4], v[4], vm[4], z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (wc)
       list4(wc, j0, n, wv);
     else if (one)
@@ -707,20 +734,28 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
     if (one && n == 4 && i[3] == i[0] + 3 && (g0 & 3u) == 0) {
       // a whole Philox quad (dense runs): one draw, no per-entry layer walk
       if (l != lr) {
-        if (any) atomicAdd((unsigned long long*)&st.S_cur[l], (unsigned long long)acc);
-        acc = 0;
+        flush_layer();
         l = lr;
       }
-      float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
       if (se != 0.0f) gauss_quad(seed, g0 >> 2, 0u, z);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         v[r] = se != 0.0f ? fmaf(se, z[r], wv[r]) : wv[r];
         bad |= !in_fix_range(v[r]);
-        acc += (long long)fix_abs(v[r]) - (long long)fix_abs(wv[r]);
+        const long long f0 = (long long)fix_abs(wv[r]);
+        acc += (long long)fix_abs(v[r]) - f0;
+        if (PAIR) {
+          vm[r] = fmaf(-se, z[r], wv[r]);
+          bad |= !in_fix_range(vm[r]);
+          acc2 += (long long)fix_abs(vm[r]) - f0;
+        }
       }
       any = true;
       put4(wp, j0, 4, v);
+      if (PAIR) {
+        put4(wpm, j0, 4, vm);
+        put4(zout, j0, 4, z);
+      }
       continue;
     }
     for (int r = 0; r < n; ++r) {
@@ -728,20 +763,31 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
       if (l < 0) {
         l = layer_of(aoff, st.L, j);
       } else if (aoff[l + 1] <= j) {        // into a later layer
-        if (any) atomicAdd((unsigned long long*)&st.S_cur[l], (unsigned long long)acc);
-        acc = 0;
+        flush_layer();
         any = false;
         while (aoff[l + 1] <= j) ++l;
       }
       if (!wc && !one) wv[r] = load1(reinterpret_cast<const T*>(st.w[l]), i[r]);
-      v[r] = se != 0.0f ? fmaf(se, zc.get(seed, (uint64_t)(st.gid0[l] + i[r])), wv[r]) : wv[r];
+      if (se != 0.0f) z[r] = zc.get(seed, (uint64_t)(st.gid0[l] + i[r]));
+      v[r] = se != 0.0f ? fmaf(se, z[r], wv[r]) : wv[r];
       bad |= !in_fix_range(v[r]);
-      acc += (long long)fix_abs(v[r]) - (long long)fix_abs(wv[r]);
+      const long long f0 = (long long)fix_abs(wv[r]);
+      acc += (long long)fix_abs(v[r]) - f0;
+      if (PAIR) {
+        vm[r] = fmaf(-se, z[r], wv[r]);
+        bad |= !in_fix_range(vm[r]);
+        acc2 += (long long)fix_abs(vm[r]) - f0;
+      }
       any = true;
     }
     put4(wp, j0, n, v);
+    if (PAIR) {
+      put4(wpm, j0, n, vm);
+      put4(zout, j0, n, z);
+    }
   }
   flush_delta((long long*)st.S_cur, l, acc, any);
+  if (PAIR) flush_delta((long long*)S_alt, l, acc2, any);
   if (bad) atomicOr(st.err, 1);
 }
 
@@ -926,14 +972,17 @@ __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps,
   if (!isfinite(a)) atomicOr(err, 2);
 }
 
-// The new values also go, in list order, to wn (read by the shrink).  With a
-// non-finite coefficient (reported by the coefficient kernel) the latents are
-// left untouched and wn holds their current values.
+// The new values also go, in list order and the latent dtype, to wn (read by the
+// shrink).  With a non-finite coefficient (reported by the coefficient kernel) the
+// latents are left untouched and wn holds their current values.  zcache (list
+// order, or null): the first direction's z, kept by the perturbation pass of the
+// same seed.
 template <typename T>
 __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __restrict__ act,
                                                 const int64_t* act_off, SeedList seeds,
-                                                const float* scal, float* __restrict__ wn,
-                                                T* __restrict__ wc) {
+                                                const float* scal, T* __restrict__ wn,
+                                                T* __restrict__ wc,
+                                                const float* __restrict__ zcache) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const float a = scal[0];
@@ -948,11 +997,14 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
   int l = -1;
   long long acc = 0;
   GaussCache zc;
-  for (int64_t base = jb; base < je; base += 256 * kRun) {
-    const int64_t j0 = base + (int64_t)threadIdx.x * kRun;
-    if (j0 >= je) continue;
-    uint32_t i[4];
-    const int n = run_entries(act, j0, je, i);
+  // the next run's indices are loaded one iteration ahead
+  uint32_t inx[4] = {0u, 0u, 0u, 0u};
+  int nnx = jb + (int64_t)threadIdx.x * kRun < je
+                ? run_entries(act, jb + (int64_t)threadIdx.x * kRun, je, inx) : 0;
+  for (int64_t j0 = jb + (int64_t)threadIdx.x * kRun; j0 < je; j0 += 256 * kRun) {
+    uint32_t i[4] = {inx[0], inx[1], inx[2], inx[3]};
+    const int n = nnx;
+    nnx = j0 + 256 * kRun < je ? run_entries(act, j0 + 256 * kRun, je, inx) : 0;
     const int lr = layer_of(aoff, st.L, j0);
     const bool one = aoff[lr + 1] >= j0 + n;
     float wv[4], nv[4];
@@ -973,7 +1025,12 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       for (int r = 0; r < 4; ++r) nv[r] = wv[r];
       if (a_ok) {
         float z[4], v[4];
-        gauss_quad(seed, g0 >> 2, 0u, z);
+        if (zcache) {
+          const float4 zz = *reinterpret_cast<const float4*>(zcache + j0);
+          z[0] = zz.x; z[1] = zz.y; z[2] = zz.z; z[3] = zz.w;
+        } else {
+          gauss_quad(seed, g0 >> 2, 0u, z);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] = fmaf(a, z[r], wv[r]);
         for (int q = 1; q < K; ++q) {
@@ -1014,7 +1071,7 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       nv[r] = wv[r];
       if (a_ok) {
         const uint64_t gid = (uint64_t)(st.gid0[l] + i[r]);
-        float v = fmaf(a, zc.get(seed, gid), wv[r]);
+        float v = fmaf(a, zcache ? zcache[j] : zc.get(seed, gid), wv[r]);
         for (int q = 1; q < K; ++q) v = fmaf(scal[q], gauss_at(seeds.s[q], gid), v);
         nv[r] = storage_round(w, v);
         if (wc)
@@ -1149,10 +1206,13 @@ __global__ void __launch_bounds__(256) k_patch_codes(DevState st, const uint32_t
 
 // ---------------------------------------------------------------------------
 // Shrink-only set update: keep the actives with ||w| - tau| <= xi0.
-// Block b handles entries [b * 256 per, (b+1) * 256 per); thread t takes
-// entries b * 256 per + 256 r + t (r < per <= kShrinkPer), so reads and writes
-// of a wave are contiguous; per grows with the list so that small lists still
-// spread over many blocks.  The updated values come from wn (list order).
+// Block b handles entries [b * 256 per, (b+1) * 256 per); thread t takes the
+// four consecutive entries b * 256 per + 4 (256 r + t) + e (r < per / 4, e < 4,
+// per <= kShrinkPer), so a lane's values and indices are one 8- or 16-byte load
+// and a wave's are contiguous; per grows with the list so that small lists still
+// spread over many blocks.  Kept entries keep the list order (r, wave, lane, e).
+// The updated values come from wn (list order, in the latent dtype: the rounded
+// new values are exact there).
 // ---------------------------------------------------------------------------
 constexpr int kShrinkPer = 64;                // entries per thread at most (block: 256 * per)
 
@@ -1166,39 +1226,69 @@ __device__ __forceinline__ void load_layer_lds(int64_t* aoff, float* tau, const 
   __syncthreads();
 }
 
-// Keep flags of a thread's entries (bit r: entry base + 256 r + t); the loads go
-// out sixteen at a time.
-constexpr int kShrinkBatch = 16;
+// Four consecutive list entries j .. j+3 (j % 4 == 0) below k: one vector load
+// when all four exist.
+__device__ __forceinline__ void load_quad4(const float* p, int64_t j, int64_t k, float v[4]) {
+  if (j + 3 < k) {
+    const float4 a = *reinterpret_cast<const float4*>(p + j);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  } else {
+    for (int e = 0; e < 4; ++e) v[e] = j + e < k ? p[j + e] : 0.0f;
+  }
+}
+__device__ __forceinline__ void load_quad4(const uint16_t* p, int64_t j, int64_t k, float v[4]) {
+  if (j + 3 < k) {
+    const uint2 a = *reinterpret_cast<const uint2*>(p + j);
+    v[0] = __uint_as_float(a.x << 16);
+    v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(a.y << 16);
+    v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+  } else {
+    for (int e = 0; e < 4; ++e) v[e] = j + e < k ? bf16_to_f32(p[j + e]) : 0.0f;
+  }
+}
 
+// Keep flags of a thread's entries (bit 4 r + e); four quads in flight at a time.
+template <typename T>
 __device__ __forceinline__ uint64_t shrink_flags(const int64_t* aoff, const float* tau, int L,
-                                                 const float* __restrict__ wn, int64_t k,
+                                                 const T* __restrict__ wn, int64_t k,
                                                  int64_t base, int per, float xi0) {
   uint64_t m = 0;
-  const int64_t j0 = base + threadIdx.x;
+  const int64_t j0 = base + 4 * (int64_t)threadIdx.x;
   if (j0 >= k) return 0;
   int l = layer_of(aoff, L, j0);
   int64_t nxt = aoff[l + 1];
-  for (int r0 = 0; r0 < per; r0 += kShrinkBatch) {
-    float v[kShrinkBatch];
+  const int R = per / 4;
+  for (int r0 = 0; r0 < R; r0 += 4) {
+    float v[4][4];
 #pragma unroll
-    for (int u = 0; u < kShrinkBatch; ++u) {
-      const int64_t j = j0 + 256 * (int64_t)(r0 + u);
-      v[u] = (r0 + u < per && j < k) ? wn[j] : 0.0f;
+    for (int u = 0; u < 4; ++u) {
+      const int64_t j = j0 + 1024 * (int64_t)(r0 + u);
+      if (r0 + u < R && j < k)
+        load_quad4(wn, j, k, v[u]);
+      else
+        v[u][0] = v[u][1] = v[u][2] = v[u][3] = 0.0f;
     }
 #pragma unroll
-    for (int u = 0; u < kShrinkBatch; ++u) {
-      const int64_t j = j0 + 256 * (int64_t)(r0 + u);
-      if (r0 + u >= per || j >= k) break;
-      while (nxt <= j) nxt = aoff[++l + 1];
-      if (fabsf(fabsf(v[u]) - tau[l]) <= xi0) m |= 1ull << (r0 + u);
+    for (int u = 0; u < 4; ++u) {
+      const int64_t jq = j0 + 1024 * (int64_t)(r0 + u);
+      if (r0 + u >= R || jq >= k) break;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t j = jq + e;
+        if (j >= k) break;
+        while (nxt <= j) nxt = aoff[++l + 1];
+        if (fabsf(fabsf(v[u][e]) - tau[l]) <= xi0) m |= 1ull << (4 * (r0 + u) + e);
+      }
     }
   }
   return m;
 }
 
 // Pass 1: the flags of every thread (kept for pass 2) and the block's kept count.
+template <typename T>
 __global__ void __launch_bounds__(256) k_shrink_count(DevState st, const int64_t* act_off,
-                                                      const float* __restrict__ wn, float xi0,
+                                                      const T* __restrict__ wn, float xi0,
                                                       int per, int64_t* blk_cnt,
                                                       uint64_t* __restrict__ flags) {
   __shared__ int64_t aoff[kMaxLayers + 1];
@@ -1253,74 +1343,80 @@ __global__ void __launch_bounds__(1024) k_blocks_scan(int64_t* blk_cnt, int64_t 
   if (tid == 0) *total = carry;
 }
 
-// Pass 2: kept entries to their new positions (ordered r, then wave, then lane within
-// a block), dropped ones get their code at tau_ref.
+// Pass 2: kept entries to their new positions (ordered r, then wave, then lane,
+// then e within a block), dropped ones get their code at tau_ref.
+template <typename T>
 __global__ void __launch_bounds__(256) k_shrink_write(DevState st, const uint32_t* __restrict__ act,
                                                       const int64_t* act_off,
-                                                      const float* __restrict__ wn, int per,
+                                                      const T* __restrict__ wn, int per,
                                                       const int64_t* blk_off,
                                                       const uint64_t* __restrict__ flags,
                                                       uint32_t* __restrict__ act_new,
-                                                      int64_t* act_off_new, void* wc_new,
-                                                      int wc_bf16) {
+                                                      int64_t* act_off_new, T* wc_new) {
   __shared__ int64_t aoff[kMaxLayers + 1];
-  __shared__ int32_t cnt[kShrinkPer * 4];   // kept entries per (r, wave), then their offsets
+  __shared__ int32_t cnt[kShrinkPer];       // kept entries per (r, wave), then their offsets
   for (int i = threadIdx.x; i <= st.L; i += blockDim.x) aoff[i] = act_off[i];
   const int64_t k = act_off[st.L];
   const int64_t base = (int64_t)blockIdx.x * 256 * per;
+  const int R = per / 4;
   const uint64_t m = flags[(int64_t)blockIdx.x * 256 + threadIdx.x];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const unsigned long long below = (1ull << lane) - 1ull;
-  for (int r = 0; r < per; ++r) {
-    const unsigned long long b = __ballot((m >> r) & 1ull);
-    if (lane == 0) cnt[4 * r + wid] = __popcll(b);
+  for (int r = 0; r < R; ++r) {
+    const int c = __popcll(m >> (4 * r) & 0xFull);
+    // wave total of the lanes' counts: one ballot per bit of the count
+    int tot = 0;
+#pragma unroll
+    for (int b = 0; b < 3; ++b) tot += __popcll(__ballot((c >> b) & 1)) << b;
+    if (lane == 0) cnt[4 * r + wid] = tot;
   }
   __syncthreads();
   if (threadIdx.x == 0) {                    // entries are ordered r, then wave, then lane
     int32_t run = 0;
-    for (int i = 0; i < per * 4; ++i) {
+    for (int i = 0; i < R * 4; ++i) {
       const int32_t c = cnt[i];
       cnt[i] = run;
       run += c;
     }
   }
   __syncthreads();
-  const int64_t j0 = base + threadIdx.x;
+  const int64_t j0 = base + 4 * (int64_t)threadIdx.x;
   if (j0 >= k) return;
   const int64_t boff = blk_off[blockIdx.x];
   int l = layer_of(aoff, st.L, j0);
   int64_t cur = aoff[l], nxt = aoff[l + 1];
-  for (int r0 = 0; r0 < per; r0 += kShrinkBatch) {
-    uint32_t a[kShrinkBatch];
+  for (int r = 0; r < R; ++r) {
+    const int64_t jq = j0 + 1024 * (int64_t)r;
+    const uint32_t q = (uint32_t)(m >> (4 * r)) & 0xFu;
+    const int c = __popc(q);
+    // kept entries of the lower lanes of the wave for this r
+    int before = 0;
 #pragma unroll
-    for (int u = 0; u < kShrinkBatch; ++u) {
-      const int64_t j = j0 + 256 * (int64_t)(r0 + u);
-      a[u] = (r0 + u < per && j < k) ? act[j] : 0u;
+    for (int b = 0; b < 3; ++b) before += __popcll(__ballot((c >> b) & 1) & below) << b;
+    if (jq >= k) break;
+    uint32_t a[4];
+    if (jq + 3 < k) {
+      const uint4 v = *reinterpret_cast<const uint4*>(act + jq);
+      a[0] = v.x; a[1] = v.y; a[2] = v.z; a[3] = v.w;
+    } else {
+      for (int e = 0; e < 4; ++e) a[e] = jq + e < k ? act[jq + e] : 0u;
     }
+    int64_t pos = boff + cnt[4 * r + wid] + before;
 #pragma unroll
-    for (int u = 0; u < kShrinkBatch; ++u) {
-      const int r = r0 + u;
-      if (r >= per) break;
-      const int64_t j = j0 + 256 * (int64_t)r;
-      const bool keep = (m >> r) & 1ull;
-      const unsigned long long b = __ballot(keep);
+    for (int e = 0; e < 4; ++e) {
+      const int64_t j = jq + e;
       if (j >= k) break;
-      const int64_t pos = boff + cnt[4 * r + wid] + __popcll(b & below);
       while (nxt <= j) {
         cur = nxt;
         nxt = aoff[++l + 1];
       }
       if (j == cur) act_off_new[l] = pos;     // first entry of layer l
-      if (keep) {
-        act_new[pos] = a[u];
-        if (wc_new) {                         // compact mode: the kept latent, list order
-          if (wc_bf16)
-            reinterpret_cast<uint16_t*>(wc_new)[pos] = f32_to_bf16_rne(wn[j]);
-          else
-            reinterpret_cast<float*>(wc_new)[pos] = wn[j];
-        }
+      if ((q >> e) & 1u) {
+        act_new[pos] = a[e];
+        if (wc_new) wc_new[pos] = wn[j];      // compact mode: the kept latent, list order
+        ++pos;
       } else {                                // frozen from now on: its code at tau_ref
-        set_code(st.codes, st.code_off[l], a[u], ternary_code(wn[j], st.tau_ref[l]));
+        set_code(st.codes, st.code_off[l], a[e], ternary_code(load1(wn, j), st.tau_ref[l]));
       }
     }
   }
@@ -1563,15 +1659,31 @@ hipError_t launch_tile_ranges(termezo_ctx* c) {
 }
 
 
-hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se) {
+hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se, bool pair) {
   if (k <= 0) return hipSuccess;
   const int64_t g = sparse_grid(k);
-  if (c->dtype == TERMEZO_F32)
-    hipLaunchKernelGGL(k_perturb_delta<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seed, se, c->d_wp, (const float*)c->d_wc);
-  else
-    hipLaunchKernelGGL(k_perturb_delta<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(),
-                       c->d_act, c->d_act_off, seed, se, c->d_wp, (const uint16_t*)c->d_wc);
+  float* wpm = pair ? c->d_wpm : nullptr;
+  float* zo = pair ? c->d_zc : nullptr;
+  int64_t* sa = pair ? c->d_S_alt : nullptr;
+  if (c->dtype == TERMEZO_F32) {
+    if (pair)
+      hipLaunchKernelGGL((k_perturb_delta<float, true>), dim3(g), dim3(256), 0, c->stream,
+                         c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
+                         (const float*)c->d_wc, wpm, zo, sa);
+    else
+      hipLaunchKernelGGL((k_perturb_delta<float, false>), dim3(g), dim3(256), 0, c->stream,
+                         c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
+                         (const float*)c->d_wc, wpm, zo, sa);
+  } else {
+    if (pair)
+      hipLaunchKernelGGL((k_perturb_delta<uint16_t, true>), dim3(g), dim3(256), 0, c->stream,
+                         c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
+                         (const uint16_t*)c->d_wc, wpm, zo, sa);
+    else
+      hipLaunchKernelGGL((k_perturb_delta<uint16_t, false>), dim3(g), dim3(256), 0, c->stream,
+                         c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
+                         (const uint16_t*)c->d_wc, wpm, zo, sa);
+  }
   return hipGetLastError();
 }
 
@@ -1587,15 +1699,17 @@ hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float
   return hipGetLastError();
 }
 
-hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds) {
+hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds, const float* zc) {
   if (k <= 0) return hipSuccess;
   const int64_t g = sparse_grid(k);
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)c->d_wc);
+                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)c->d_wc,
+                       zc);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (uint16_t*)c->d_wc);
+                       c->d_act_off, seeds, (const float*)c->d_scal, (uint16_t*)c->d_wp,
+                       (uint16_t*)c->d_wc, zc);
   return hipGetLastError();
 }
 
@@ -1627,14 +1741,27 @@ hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
   const int64_t nb = max((int64_t)1, (k + 256 * per - 1) / (256 * per));
   int64_t* total = c->d_blk_cnt + nb;  // blk_cap >= nb + 1
   if (nb > c->blk_cap - 1 || nb * 256 > c->flag_cap) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_shrink_count, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act_off,
-                     c->d_wp, c->xi0, per, c->d_blk_cnt, c->d_shrink_flags);
+  const bool bf = c->dtype == TERMEZO_BF16;
+  if (bf)
+    hipLaunchKernelGGL(k_shrink_count<uint16_t>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
+                       c->d_act_off, (const uint16_t*)c->d_wp, c->xi0, per, c->d_blk_cnt,
+                       c->d_shrink_flags);
+  else
+    hipLaunchKernelGGL(k_shrink_count<float>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
+                       c->d_act_off, (const float*)c->d_wp, c->xi0, per, c->d_blk_cnt,
+                       c->d_shrink_flags);
   hipLaunchKernelGGL(k_blocks_scan, dim3(1), dim3(1024), 0, c->stream, c->d_blk_cnt, nb, total);
   // offsets of layers without any entry are fixed afterwards
-  hipLaunchKernelGGL(k_shrink_write, dim3(nb), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                     c->d_act_off, c->d_wp, per, c->d_blk_cnt,
-                     (const uint64_t*)c->d_shrink_flags, c->d_act_tmp, c->d_act_off_tmp,
-                     c->d_wc_tmp, c->dtype == TERMEZO_BF16 ? 1 : 0);
+  if (bf)
+    hipLaunchKernelGGL(k_shrink_write<uint16_t>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
+                       c->d_act, c->d_act_off, (const uint16_t*)c->d_wp, per, c->d_blk_cnt,
+                       (const uint64_t*)c->d_shrink_flags, c->d_act_tmp, c->d_act_off_tmp,
+                       (uint16_t*)c->d_wc_tmp);
+  else
+    hipLaunchKernelGGL(k_shrink_write<float>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
+                       c->d_act, c->d_act_off, (const float*)c->d_wp, per, c->d_blk_cnt,
+                       (const uint64_t*)c->d_shrink_flags, c->d_act_tmp, c->d_act_off_tmp,
+                       (float*)c->d_wc_tmp);
   hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(256), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
   return hipGetLastError();

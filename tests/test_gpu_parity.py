@@ -335,3 +335,34 @@ def test_guarded_requant_equals_dense_requant(orc, bf16, rho0, eps):
     ctx.close()
     ctx_d.close()
     ctx_a.close()
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("rho0", [0.01, 1.0])
+def test_perturbation_pair_reuse(orc, bf16, rho0):
+    """The first call of a (seed, eps) pair also produces the other sign's values
+    and z; the other sign, a repeat of either sign, a pair that starts with -1, a
+    new eps for the same seed, sign 0 in between, and the update after the pair
+    (z kept from the perturbation) all give the oracle's codes, thresholds and
+    latents."""
+    print(f"pair reuse bf16={bf16} rho0={rho0}", flush=True)
+    shapes = [(256, 256), (128, 512), (64, 128)]
+    ref, ctx, tensors = _setup(orc, shapes, bf16, seed=17)
+    assert ctx.build_mask(rho0) == ref.build_mask(rho0)
+    calls = [(3, 1e-3, 1), (3, 1e-3, -1), (3, 1e-3, 1), (3, 1e-3, 1), (3, 2e-3, -1),
+             (3, 2e-3, 1), (3, 2e-3, 0), (3, 2e-3, -1), (4, 1e-3, -1), (4, 1e-3, 1)]
+    lr = 1e-2
+    for step in range(2):
+        for sd, eps, sign in calls:
+            sd += 10 * step
+            ctx.perturb(sd, eps, sign)
+            codes, taus, betas = ref.perturb(sd, eps, sign)
+            for l in range(len(shapes)):
+                assert np.array_equal(ctx.codes(l), codes[l]), f"{(sd, eps, sign)} layer {l}"
+                st = ctx.layer_stats(l)
+                assert st["tau_cur"] == taus[l] and st["beta_cur"] == betas[l], f"{(sd, eps, sign)}"
+        g = 0.7 - step
+        assert ctx.update(g, lr) == ref.update(g, lr)
+        assert np.array_equal(_latents_host(tensors), ref.w), f"step {step}: latents"
+        _check_mask(ref, ctx)
+    ctx.close()
