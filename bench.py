@@ -350,13 +350,13 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         # default path: the same codes; only the actives' codes are rewritten while the
         # threshold-drift guard holds (per active: 4 B index + 2 B latent read, 4 B w' written,
         # index and w' read again, the code word read and, where the code changes, written)
-        b_g = k * 26 if k * 256 <= D else b_p
+        b_g = k * 26 if k * 64 <= D else b_p
         _emit({"sweep": "perturb_guarded", "latents": D, "ratio": r, "k": k, "ms": t_g * 1e3,
                "algorithmic_bytes": b_g, "GB/s": b_g / t_g / 1e9,
                "frac_hbm": b_g / t_g / 1e9 / HBM_PEAK_GBS,
                "speedup_vs_dense": t_p / t_g,
                "protocol": "default termezo_perturb (guarded: dense where the guard fails and "
-                           "for every layer when k > D/256); mean over 5 (+eps, -eps) pairs"})
+                           "for every layer when k > D/64); mean over 5 (+eps, -eps) pairs"})
         _emit({"sweep": "update", "latents": D, "ratio": r, "k": k, "k_after": k_after,
                "us": t_u * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_u / 1e9,
                "frac_hbm": b_u / t_u / 1e9 / HBM_PEAK_GBS, "cpu_baseline": cu})
