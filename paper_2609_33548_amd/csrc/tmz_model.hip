@@ -118,18 +118,141 @@ __device__ __forceinline__ void store8(float* p, const float v[8]) {
   reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
 }
 
-template <int MODE, typename T, bool WEIGHTED = false>
+// Eight bf16 values of a 16-byte chunk to fp32, and back (exact: the values are
+// bf16 numbers).
+__device__ __forceinline__ void unpack8(const uint4 r, float v[8]) {
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = __uint_as_float(w[j] << 16);
+    v[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ uint4 pack8(const float v[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    w[j] = (__float_as_uint(v[2 * j]) >> 16) | (__float_as_uint(v[2 * j + 1]) & 0xFFFF0000u);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Long bf16 rows: the row stays in registers as packed bf16 (4 registers per chunk:
+// the input, or for the SwiGLU the rounded product, both bf16 numbers); the RMSNorm
+// output is recomputed from it where it is needed, with the same operations.  (For
+// rows of up to 8 chunks per lane the fp32 copy below leaves enough waves per SIMD
+// and measured faster.)
+template <int MODE, bool WEIGHTED, int CH>
+__device__ __forceinline__ void row_bf16(const uint16_t* __restrict__ x,
+                                         const uint16_t* __restrict__ u, int64_t m, int64_t K,
+                                         float eps, int8_t* xq, float* xs, uint16_t* xf) {
+  const int lane = threadIdx.x & 63;
+  const int nch = (int)(K / 8);
+  uint4 raw[CH];
+  float acc = 0.0f;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int idx = c * 64 + lane;
+    raw[c] = make_uint4(0u, 0u, 0u, 0u);
+    if (idx < nch) {
+      raw[c] = *reinterpret_cast<const uint4*>(x + m * K + idx * 8);
+      float v[8];
+      unpack8(raw[c], v);
+      if (MODE == kRowSwiGLU) {
+        float uu[8];
+        load8(u + m * K + idx * 8, uu);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          v[j] = round_to(x, silu_mul(v[j], uu[j]));   // the product is an activation
+          acc = fmaxf(acc, fabsf(v[j]));
+        }
+        raw[c] = pack8(v);
+      } else if (MODE == kRowQuant) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = fmaxf(acc, fabsf(v[j]));
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = fmaf(v[j], v[j], acc);
+      }
+    }
+  }
+  float r = 1.0f;
+  // the values the quantiser sees, for chunk c (the RMSNorm output, or the row itself)
+  auto values = [&](int c, float v[8]) __attribute__((always_inline)) {
+    unpack8(raw[c], v);
+    if (MODE == kRowNormQuant || MODE == kRowNormStore) {
+      if constexpr (WEIGHTED) {            // RMSNorm weight row (the u argument)
+        float wt[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+        const int idx = c * 64 + lane;
+        if (idx < nch) load8(u + idx * 8, wt);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = v[j] * r * wt[j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = v[j] * r;
+      }
+    }
+  };
+  float amax;
+  if (MODE == kRowSwiGLU || MODE == kRowQuant) {
+    amax = wmax(acc);
+  } else {
+    const float ss = wsum(acc);
+    r = __fdiv_rn(1.0f, sqrt_rn(ss / (float)K + eps));
+    float a = 0.0f;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int idx = c * 64 + lane;
+      if (idx < nch) {
+        float v[8];
+        values(c, v);
+        if (MODE == kRowNormStore) {
+          store8(xf + m * K + idx * 8, v);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) a = fmaxf(a, fabsf(v[j]));
+        }
+      }
+    }
+    if (MODE == kRowNormStore) return;
+    amax = wmax(a);
+  }
+  const float sc = __fdiv_rn(127.0f, fmaxf(amax, 1e-5f));
+  if (lane == 0) xs[m] = sc;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int idx = c * 64 + lane;
+    if (idx < nch) {
+      float v[8];
+      values(c, v);
+      uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        w0 |= ((uint32_t)(uint8_t)q8(v[j], sc)) << (8 * j);
+        w1 |= ((uint32_t)(uint8_t)q8(v[4 + j], sc)) << (8 * j);
+      }
+      *reinterpret_cast<uint2*>(xq + m * K + idx * 8) = make_uint2(w0, w1);
+    }
+  }
+}
+
+// CH: chunks per lane the row needs at most (the kernel is instantiated for a few
+// row lengths so that the registers holding the row match it).
+template <int MODE, typename T, bool WEIGHTED = false, int CH = kRowChunks>
 __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* __restrict__ u,
                                              int64_t M, int64_t K, float eps, int8_t* xq,
                                              float* xs, T* xf) {
   const int lane = threadIdx.x & 63;
   const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (m >= M) return;                       // whole wave
+  if constexpr (sizeof(T) == 2 && CH > 8) {   // long rows: half the registers
+    row_bf16<MODE, WEIGHTED, CH>(x, u, m, K, eps, xq, xs, xf);
+    return;
+  }
   const int nch = (int)(K / 8);
-  float v[kRowChunks][8];
+  float v[CH][8];
   float acc = 0.0f;
 #pragma unroll
-  for (int c = 0; c < kRowChunks; ++c) {
+  for (int c = 0; c < CH; ++c) {
     const int idx = c * 64 + lane;
     if (idx < nch) {
       load8(x + m * K + idx * 8, v[c]);
@@ -161,7 +284,7 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
     const float r = __fdiv_rn(1.0f, sqrt_rn(ss / (float)K + eps));
     float a = 0.0f;
 #pragma unroll
-    for (int c = 0; c < kRowChunks; ++c) {
+    for (int c = 0; c < CH; ++c) {
       if constexpr (WEIGHTED) {            // RMSNorm weight row (the u argument)
         float wt[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
         const int idx = c * 64 + lane;
@@ -181,7 +304,7 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
     }
     if (MODE == kRowNormStore) {
 #pragma unroll
-      for (int c = 0; c < kRowChunks; ++c) {
+      for (int c = 0; c < CH; ++c) {
         const int idx = c * 64 + lane;
         if (idx < nch) store8(xf + m * K + idx * 8, v[c]);
       }
@@ -192,7 +315,7 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
   const float sc = __fdiv_rn(127.0f, fmaxf(amax, 1e-5f));
   if (lane == 0) xs[m] = sc;
 #pragma unroll
-  for (int c = 0; c < kRowChunks; ++c) {
+  for (int c = 0; c < CH; ++c) {
     const int idx = c * 64 + lane;
     if (idx < nch) {
       uint32_t w0 = 0, w1 = 0;
@@ -204,6 +327,25 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
       *reinterpret_cast<uint2*>(xq + m * K + idx * 8) = make_uint2(w0, w1);
     }
   }
+}
+
+// One row kernel launch (4 rows per block), instantiated for the chunks per lane
+// the row length needs: 3 (up to 1536 elements), 5 (2560), 8 (4096), 14 (7168),
+// else kRowChunks.
+template <int MODE, typename T, bool W = false>
+static void row_launch(unsigned grid, hipStream_t s, const T* x, const T* u, int64_t M, int64_t K,
+                       float eps, int8_t* xq, float* xs, T* xf) {
+  const int64_t need = (K / 8 + 63) / 64;
+  if (need <= 3)
+    hipLaunchKernelGGL((k_row<MODE, T, W, 3>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+  else if (need <= 5)
+    hipLaunchKernelGGL((k_row<MODE, T, W, 5>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+  else if (need <= 8)
+    hipLaunchKernelGGL((k_row<MODE, T, W, 8>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+  else if (need <= 14)
+    hipLaunchKernelGGL((k_row<MODE, T, W, 14>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+  else
+    hipLaunchKernelGGL((k_row<MODE, T, W>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
 }
 
 // ---------------------------------------------------------------------------
@@ -1549,9 +1691,9 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   // the quantiser, or stored (the LM-head input)
   auto rmsq = [&](int8_t* xq, float* xs, void* xf, int wr) {
 #define TMZ_NORM(T, MD, W)                                                                   \
-  hipLaunchKernelGGL((k_row<MD, T, W>), dim3(rowg), dim3(256), 0, s, (const T*)m->h,          \
-                     nrm ? (const T*)nrm + (int64_t)wr * d : (const T*)nullptr, M, d, cf.norm_eps, \
-                     xq, xs, (T*)xf)
+  row_launch<MD, T, W>(rowg, s, (const T*)m->h,                                              \
+                       nrm ? (const T*)nrm + (int64_t)wr * d : (const T*)nullptr, M, d,      \
+                       cf.norm_eps, xq, xs, (T*)xf)
     if (bf) {
       if (xf) {
         if (nrm) TMZ_NORM(uint16_t, kRowNormStore, true); else TMZ_NORM(uint16_t, kRowNormStore, false);
@@ -1596,13 +1738,11 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     chk(run_attention(m, batch, seq, s));
     span_end(m, sp, s);
     if (bf)
-      hipLaunchKernelGGL((k_row<kRowQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                         (const uint16_t*)m->attn, (const uint16_t*)nullptr, M, dq, 0.0f, m->xq,
-                         m->xs, (uint16_t*)nullptr);
+      row_launch<kRowQuant, uint16_t>(rowg, s, (const uint16_t*)m->attn, (const uint16_t*)nullptr,
+                                      M, dq, 0.0f, m->xq, m->xs, (uint16_t*)nullptr);
     else
-      hipLaunchKernelGGL((k_row<kRowQuant, float>), dim3(rowg), dim3(256), 0, s,
-                         (const float*)m->attn, (const float*)nullptr, M, dq, 0.0f, m->xq, m->xs,
-                         (float*)nullptr);
+      row_launch<kRowQuant, float>(rowg, s, (const float*)m->attn, (const float*)nullptr, M, dq,
+                                   0.0f, m->xq, m->xs, (float*)nullptr);
     chk(hipGetLastError());
     GemmOut oo = {};
     oo.nseg = 1;
@@ -1627,17 +1767,14 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                        fused ? kGemmSwiGLU : kGemmStore, nullptr, c->n_cu, s));
     span_end(m, sp, s);
     if (fused)
-      hipLaunchKernelGGL((k_row<kRowQuant, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                         (const uint16_t*)m->g, (const uint16_t*)nullptr, M, F, 0.0f, m->xq, m->xs,
-                         (uint16_t*)nullptr);
+      row_launch<kRowQuant, uint16_t>(rowg, s, (const uint16_t*)m->g, (const uint16_t*)nullptr, M,
+                                      F, 0.0f, m->xq, m->xs, (uint16_t*)nullptr);
     else if (bf)
-      hipLaunchKernelGGL((k_row<kRowSwiGLU, uint16_t>), dim3(rowg), dim3(256), 0, s,
-                         (const uint16_t*)m->g, (const uint16_t*)m->u, M, F, 0.0f, m->xq, m->xs,
-                         (uint16_t*)nullptr);
+      row_launch<kRowSwiGLU, uint16_t>(rowg, s, (const uint16_t*)m->g, (const uint16_t*)m->u, M,
+                                       F, 0.0f, m->xq, m->xs, (uint16_t*)nullptr);
     else
-      hipLaunchKernelGGL((k_row<kRowSwiGLU, float>), dim3(rowg), dim3(256), 0, s,
-                         (const float*)m->g, (const float*)m->u, M, F, 0.0f, m->xq, m->xs,
-                         (float*)nullptr);
+      row_launch<kRowSwiGLU, float>(rowg, s, (const float*)m->g, (const float*)m->u, M, F, 0.0f,
+                                    m->xq, m->xs, (float*)nullptr);
     chk(hipGetLastError());
     GemmOut od = {};
     od.nseg = 1;
