@@ -142,6 +142,7 @@ def cpu_baseline(c, rho, seed=0, theta_n=0, K=1, es=0):
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {
         "value": 1.0 / t_step, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+        "host": host_cpu(),
         "sample": (f"oracle perturb(+/-)+update+shrink on one block's 7 projections ({nsmp} bf16 "
                    f"latents) scaled to {D}; 1 decoder block x {n_seq} sequences of {c['seq']} tokens "
                    f"scaled x{c['n_blocks']} blocks x{c['batch'] / n_seq:g}; LM head+CE on {n_pos} "
@@ -174,7 +175,7 @@ def cpu_baseline_c1(n_steps=200, seed=0):
             f[sign] = orc.mse(y, tgt)
         st.update(orc.projected_grad(f[1], f[-1], C1["eps"]), C1["lr"])
     dt = (time.perf_counter() - t0) / n_steps
-    return {"value": 1.0 / dt, "unit": "steps/s", "cores": 1, "kind": "oracle",
+    return {"value": 1.0 / dt, "unit": "steps/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"{n_steps} full oracle steps of the same workload (single thread, C + numpy)"}
 
 
@@ -209,6 +210,7 @@ def cpu_baseline_full(c, rho, n_steps=8, seed=0, theta=False):
     dt = (time.perf_counter() - t0) / n_steps
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": 1.0 / dt, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "host": host_cpu(),
             "sample": f"{n_steps} full oracle steps of the same workload"}
 
 
@@ -263,6 +265,24 @@ def run_c1(args, torch, termezo, synth, dev):
 # small and large token counts.  Each point prints one JSON line.
 # ---------------------------------------------------------------------------
 HBM_PEAK_GBS = 8000.0
+
+
+def host_cpu():
+    """Model name of the host CPU and the logical CPUs this process may use."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return {"model": name, "logical_cpus": n}
 SWEEP_LAYER = (6912, 2560)           # 136 layers of this shape: 2,406,481,920 latents
 SWEEP_LAYERS = 136
 SWEEP_RATIOS = (1e-4, 1e-3, 1e-2, 1.0)
