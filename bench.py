@@ -104,7 +104,7 @@ def cpu_baseline(c, rho, seed=0, theta_n=0, K=1, es=0):
     st.update(1.0, 1e-4)
     t_latent = (time.perf_counter() - t0) * D / nsmp
     # (2) one decoder block on n_seq sequences (vocab shrunk so the head is negligible)
-    n_seq = 4
+    n_seq = 16
     cfg1 = dec.DecoderConfig(n_blocks=1, d_model=c["d_model"], n_heads=c["n_heads"],
                              n_kv_heads=c["n_kv_heads"], d_ffn=c["d_ffn"], vocab=64, bf16=True)
     rng = np.random.default_rng(seed)
@@ -116,7 +116,7 @@ def cpu_baseline(c, rho, seed=0, theta_n=0, K=1, es=0):
     dec.forward_row_losses(cfg1, emb, tok, codes, betas)
     t_block = (time.perf_counter() - t0) / n_seq
     # (3) LM head + cross-entropy for n_pos positions over the full vocabulary
-    n_pos = 512
+    n_pos = 2048
     E = synth.latents(seed + 3, [c["vocab"] * c["d_model"]], bf16=True).reshape(c["vocab"], c["d_model"])
     x = synth.activations(seed + 4, n_pos, c["d_model"], bf16=True)
     t0 = time.perf_counter()
