@@ -24,6 +24,7 @@ Step by step (paper section in brackets):
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence, Tuple
@@ -328,6 +329,21 @@ def projected_grad(f_plus: float, f_minus: float, eps: float) -> float:
 # --------------------------------------------------------------------------
 # Algorithm-1 state
 # --------------------------------------------------------------------------
+def eq_memory(m_mezo: float, d: float, rho0: float, B: float = 2.0, B_Q: float = 0.25,
+              mask: str = "min") -> float:
+    """Peak memory of TerMeZO in bytes from that of MeZO (Sec. 5, eq. memory): the frozen
+    fraction of the d latents drops from B to B_Q bytes, the rho0 d active ones keep a
+    B_Q-byte quantised copy besides their B bytes, plus the mask -- a bitmask of ceil(d/8)
+    bytes, an index list of ceil(rho0 d ceil(log2 d) / 8) bytes, or the smaller of the two
+    ("min", as the paper states it)."""
+    frozen = math.ceil(d * (1.0 - rho0) * (B - B_Q))
+    active_codes = math.ceil(rho0 * d * B_Q)
+    bitmask = math.ceil(d / 8.0)
+    index_list = math.ceil(rho0 * d * math.ceil(math.log2(d)) / 8.0)
+    m_mask = {"bitmask": bitmask, "index": index_list, "min": min(bitmask, index_list)}[mask]
+    return m_mezo - frozen + active_codes + m_mask
+
+
 @dataclass
 class Layer:
     d_out: int
