@@ -370,13 +370,15 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         # default path: the same codes; only the actives' codes are rewritten while the
         # threshold-drift guard holds (per active: 4 B index + 2 B latent read, 4 B w' written,
         # index and w' read again, the code word read and, where the code changes, written)
-        b_g = k * 26 if k * 64 <= D else b_p
+        # (above 1/256 active: the code words of the tiles with actives read and written,
+        # 0.5 B per weight, plus 4 B index + 4 B w' + 6 B for the delta per active)
+        b_g = k * 26 if k * 256 <= D else D * 0.5 + k * 14
         _emit({"sweep": "perturb_guarded", "latents": D, "ratio": r, "k": k, "ms": t_g * 1e3,
                "algorithmic_bytes": b_g, "GB/s": b_g / t_g / 1e9,
                "frac_hbm": b_g / t_g / 1e9 / HBM_PEAK_GBS,
                "speedup_vs_dense": t_p / t_g,
-               "protocol": "default termezo_perturb (guarded: dense where the guard fails and "
-                           "for every layer when k > D/64); mean over 5 (+eps, -eps) pairs"})
+               "protocol": "default termezo_perturb (guarded: dense where the guard fails, "
+                           "code words tile by tile when k > D/256); mean over 5 (+eps, -eps) pairs"})
         _emit({"sweep": "update", "latents": D, "ratio": r, "k": k, "k_after": k_after,
                "us": t_u * 1e6, "algorithmic_bytes": b_u, "GB/s": b_u / t_u / 1e9,
                "frac_hbm": b_u / t_u / 1e9 / HBM_PEAK_GBS, "cpu_baseline": cu})
@@ -411,7 +413,7 @@ def sweep_latent(torch, termezo, synth, dev, cpu):
         k_after = cc.active_count()
         cc.sync()
         cc.close()
-        b_g = k * 26
+        b_g = k * 26 if k * 256 <= D else D * 0.5 + k * 14
         b_u = 16 * k
         _emit({"sweep": "perturb_compact", "latents": D, "ratio": r, "k": k, "ms": t_c * 1e3,
                "algorithmic_bytes": b_g, "GB/s": b_g / t_c / 1e9,

@@ -123,8 +123,9 @@ termezo_status termezo_perturb(termezo_ctx* ctx, uint64_t seed, float eps,
  * no frozen code can change: every frozen latent is tracked to lie at least a
  * bound m^l (exactly, from xi0 and the threshold drift) from the threshold its
  * code was computed with, and a layer whose perturbed threshold tau' moves by
- * less than m^l keeps its frozen codes; other layers, and every layer when the
- * active set exceeds 1/64 of the latents, are requantised densely.
+ * less than m^l keeps its frozen codes (the actives' codes are rewritten one by
+ * one, or, above 1/256 active, tile by tile over the code words); other layers
+ * are requantised densely.
  * always_dense != 0 requantises every latent of every layer on each call
  * (for measurement).  Errors: INVALID_ARG (null ctx). */
 termezo_status termezo_set_dense_requant(termezo_ctx* ctx, int32_t always_dense);

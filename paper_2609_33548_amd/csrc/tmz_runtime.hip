@@ -388,9 +388,8 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   }
   TMZ_HIP(c, launch_thresholds(c, c->d_S_cur, c->d_tau_cur, c->d_beta_cur));
   // guarded requantisation: the actives' codes only, while no frozen code can change
-  // (dense on request, or when the active set exceeds 1/64 of the latents: there the
-  // scattered code-word updates cost more than the dense stream)
-  const int force = !c->compact && (c->dense_requant || c->k_bound * 64 > c->D);
+  // (every latent re-quantised on request)
+  const int force = !c->compact && c->dense_requant;
   TMZ_HIP(c, launch_requant_guarded(c, force));
   // theta: both signs of the pair come from one pass, so the second evaluation
   // of a pair (same seed and eps) only switches to the other copy

@@ -1204,6 +1204,83 @@ __global__ void __launch_bounds__(256) k_patch_codes(DevState st, const uint32_t
   }
 }
 
+// The same codes tile by tile, for denser sets (one block per tile): a tile with
+// actives reads its code words back into LDS (one 16-byte load per thread), rewrites
+// the actives' codes there and stores the words (the frozen codes are reused, so the
+// latents are not read); a fully active tile takes every code from w'; tiles without
+// actives, and the tiles of layers that take the dense pass, are not touched.
+__global__ void __launch_bounds__(kRqThreads) k_patch_tiles(DevState st,
+                                                            const uint32_t* __restrict__ act,
+                                                            const float* __restrict__ wp) {
+  __shared__ uint32_t words[kTile / 16];
+  const int tid = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  const int l = st.tile_layer[t];
+  const int64_t a0 = st.tile_act[t], a1 = st.tile_act[t + 1];
+  if (st.need[l] || a1 == a0) return;            // block-uniform
+  const int64_t start = st.tile_start[t];
+  const int cnt = (int)min((int64_t)kTile, st.n[l] - start);   // a multiple of 16
+  const int nw = cnt / 16;
+  const float tau = st.tau_cur[l];
+  const int64_t woff = st.code_off[l] + start / 16;
+  gu32* out = (gu32*)(st.codes + woff);
+  if (a1 - a0 == cnt) {                          // every element active: codes from w'
+    constexpr int FC = kTile / 4 / kRqThreads;
+    const float* src = wp + a0;
+    const bool vec = (a0 & 3) == 0;
+#pragma unroll
+    for (int v = 0; v < FC; ++v) {
+      const int c = v * kRqThreads + tid;
+      const int e = c * 4;
+      float x[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (e < cnt) {
+        if (vec) {
+          const v4u b = __builtin_nontemporal_load((gv4u_c*)(src + e));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] = __uint_as_float(b[r]);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] = src[e + r];
+        }
+      }
+      const uint32_t wd = join_word<4>(partial_word<4>(x, c & 3, tau));
+      if ((tid & 3) == 0 && e < cnt) out[c / 4] = wd;
+    }
+    return;
+  }
+  static_assert(kTile / 16 == 4 * kRqThreads, "one 16-byte chunk of words per thread");
+  const bool vec = (woff & 3) == 0;
+  const int i0 = 4 * tid;
+  // the first active entry of this thread is loaded together with the words
+  const int64_t jf = a0 + tid;
+  const uint32_t af = jf < a1 ? act[jf] : 0u;
+  const float wf = jf < a1 ? wp[jf] : 0.0f;
+  if (vec && i0 + 3 < nw) {
+    const v4u v = *(gv4u_c*)(out + i0);
+    words[i0] = v[0]; words[i0 + 1] = v[1]; words[i0 + 2] = v[2]; words[i0 + 3] = v[3];
+  } else {
+    for (int r = 0; r < 4; ++r)
+      if (i0 + r < nw) words[i0 + r] = out[i0 + r];
+  }
+  __syncthreads();
+  auto patch = [&](uint32_t idx, float x) __attribute__((always_inline)) {
+    const uint32_t li = idx - (uint32_t)start;
+    const uint32_t code = ternary_code(x, tau);
+    const int sh = code_shift((int)(li & 15u));
+    atomicAnd(&words[li >> 4], ~(3u << sh));
+    if (code) atomicOr(&words[li >> 4], code << sh);
+  };
+  if (jf < a1) patch(af, wf);
+  for (int64_t jj = jf + kRqThreads; jj < a1; jj += kRqThreads) patch(act[jj], wp[jj]);
+  __syncthreads();
+  if (vec && i0 + 3 < nw) {
+    *(gv4u*)(out + i0) = v4u{words[i0], words[i0 + 1], words[i0 + 2], words[i0 + 3]};
+  } else {
+    for (int r = 0; r < 4; ++r)
+      if (i0 + r < nw) out[i0 + r] = words[i0 + r];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Shrink-only set update: keep the actives with ||w| - tau| <= xi0.
 // Block b handles entries [b * 256 per, (b+1) * 256 per); thread t takes the
@@ -1633,9 +1710,15 @@ hipError_t launch_requant_guarded(termezo_ctx* c, int force) {
                        c->dev(), c->d_act, c->d_wp, (const int64_t*)c->d_dense_off);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (c->k_bound > 0)
+  if (c->k_bound <= 0) return hipSuccess;
+  // sparse sets: one scattered code-word update per active; above 1/256 active the
+  // code words of the tiles with actives are rewritten whole (0.5 byte per weight)
+  if (c->k_bound * 256 <= c->D)
     hipLaunchKernelGGL(k_patch_codes, dim3((unsigned)sparse_grid(c->k_bound)), dim3(256), 0,
                        c->stream, c->dev(), c->d_act, c->d_act_off, c->d_wp);
+  else
+    hipLaunchKernelGGL(k_patch_tiles, dim3((unsigned)c->T), dim3(kRqThreads), 0, c->stream,
+                       c->dev(), c->d_act, c->d_wp);
   return hipGetLastError();
 }
 

@@ -31,10 +31,11 @@ def _ctx(torch, termezo, shapes, w, bf16):
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
 @pytest.mark.parametrize("K", [1, 3])
-def test_compact_mode_matches_oracle(orc, bf16, K):
+@pytest.mark.parametrize("rho0", [0.003, 0.012])   # codes one by one / tile by tile
+def test_compact_mode_matches_oracle(orc, bf16, K, rho0):
     torch = _torch()
     from paper_2609_33548_amd import termezo
-    print(f"compact bf16={bf16} K={K}", flush=True)
+    print(f"compact bf16={bf16} K={K} rho0={rho0}", flush=True)
     shapes = [(256, 512), (512, 256), (384, 384)]
     w = synth.latents(81, [o * i for o, i in shapes], bf16=bf16)
     th = synth.latents(82, [3001], bf16=bf16)
@@ -43,7 +44,7 @@ def test_compact_mode_matches_oracle(orc, bf16, K):
     ctx, lat = _ctx(torch, termezo, shapes, w, bf16)
     T = torch.from_numpy(th).cuda().to(torch.bfloat16 if bf16 else torch.float32)
     ctx.theta_register([T])
-    assert ctx.build_mask(0.003) == ref.build_mask(0.003)
+    assert ctx.build_mask(rho0) == ref.build_mask(rho0)
     lib_before, need_before = ctx.memory_footprint()
     ctx.compact()
     lib_after, need_after = ctx.memory_footprint()

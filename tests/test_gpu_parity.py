@@ -289,7 +289,8 @@ def test_state_and_numeric_errors(orc):
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
 @pytest.mark.parametrize("rho0,eps", [(0.003, 1e-3),    # drift far below xi0: actives only
-                                      (0.012, 1e-3),    # denser set, still actives only
+                                      (0.012, 1e-3),    # denser set: code words tile by tile
+                                      (0.02, 0.5),      # tile-by-tile and dense fallback
                                       (0.002, 0.5)])    # drift above xi0: dense fallback
 def test_guarded_requant_equals_dense_requant(orc, bf16, rho0, eps):
     """The default perturbation (actives' codes only while the threshold-drift
