@@ -368,3 +368,32 @@ def test_perturbation_pair_reuse(orc, bf16, rho0):
         assert np.array_equal(_latents_host(tensors), ref.w), f"step {step}: latents"
         _check_mask(ref, ctx)
     ctx.close()
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+def test_degenerate_active_sets(orc, bf16):
+    """A single active latent (k0 = 1), then updates large enough that the shrink
+    empties the set: with k = 0 a perturbation gives the clean codes of the current
+    latents, an update changes nothing, and both sides agree throughout (codes,
+    thresholds, latents, masks)."""
+    print(f"degenerate sets bf16={bf16}", flush=True)
+    shapes = [(64, 128), (32, 256)]
+    D = sum(o * i for o, i in shapes)
+    ref, ctx, tensors = _setup(orc, shapes, bf16, seed=23)
+    assert ctx.build_mask(1.0 / D) == ref.build_mask(1.0 / D)
+    assert ref.k == 1
+    emptied = False
+    for t in range(12):
+        for sign in (1, -1):
+            ctx.perturb(t, 1e-3, sign)
+            codes, taus, betas = ref.perturb(t, 1e-3, sign)
+            for l in range(len(shapes)):
+                assert np.array_equal(ctx.codes(l), codes[l]), f"step {t} sign {sign} layer {l}"
+        g = 50.0 if t % 2 == 0 else -50.0
+        assert ctx.update(g, 1e-2) == ref.update(g, 1e-2)
+        assert np.array_equal(_latents_host(tensors), ref.w), f"step {t}"
+        _check_mask(ref, ctx)
+        _check_stats(ref, ctx)
+        emptied = emptied or ref.k == 0
+    assert emptied, "the set did not empty; the case is not exercised"
+    ctx.close()
