@@ -26,18 +26,18 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 CONFIGS = {
-    # config 4 (headline): BitNet b1.58 2B shape, bf16 latents and activations
+    # headline workload: BitNet b1.58 2B shape, bf16 latents and activations
     "2b": dict(n_blocks=30, d_model=2560, n_heads=20, n_kv_heads=5, d_ffn=6912, vocab=128256,
                seq=512, batch=16, rho=1e-3, lr=1e-5),
-    # config 3: 700M-class shape, 16 heads of 96 (MHA), bf16
+    # 700M-class shape, 16 heads of 96 (MHA), bf16
     "700m": dict(n_blocks=24, d_model=1536, n_heads=16, n_kv_heads=16, d_ffn=4096, vocab=32000,
                  seq=512, batch=8, rho=1e-3, lr=1e-5),
-    # config 2: tiny decoder, fp32 latents and activations
+    # tiny decoder, fp32 latents and activations
     "tiny": dict(n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4, d_ffn=688, vocab=1024,
                  seq=64, batch=4, rho=1e-2, lr=1e-4, fp32=True),
 }
-# config 1: one 256 x 256 BitLinear (fp32 latents), 8 token rows, MSE to a target
-C1 = dict(d_out=256, d_in=256, tokens=8, rho=1e-2, eps=1e-3, lr=1e-4)
+# single-layer workload: one 256 x 256 BitLinear (fp32 latents), 8 token rows, MSE to a target
+LAYER = dict(d_out=256, d_in=256, tokens=8, rho=1e-2, eps=1e-3, lr=1e-4)
 PEAK_INT8_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 # HBM traffic of the GEMM launches measured with rocprofv3 counters (FETCH_SIZE,
 # WRITE_SIZE), valid only for the kernel source it was measured on.
@@ -155,25 +155,25 @@ def cpu_baseline(c, rho, seed=0, theta_n=0, K=1, es=0):
         "extrapolated_step_s": t_step,
     }
 
-def cpu_baseline_c1(n_steps=200, seed=0):
-    """The oracle's full config-1 step (perturb +/-, BitLinear, MSE, update), timed."""
+def cpu_baseline_layer(n_steps=200, seed=0):
+    """The oracle's full single-layer step (perturb +/-, BitLinear, MSE, update), timed."""
     import numpy as np
     from oracle import termezo_ref as orc
     from paper_2609_33548_amd import synth
-    w = synth.latents(seed, [C1["d_out"] * C1["d_in"]])
-    st = orc.TerMeZOOracle([orc.Layer(C1["d_out"], C1["d_in"])], w)
-    x = synth.activations(100, C1["tokens"], C1["d_in"])
-    tgt = synth.activations(101, C1["tokens"], C1["d_out"])
-    st.build_mask(C1["rho"])
+    w = synth.latents(seed, [LAYER["d_out"] * LAYER["d_in"]])
+    st = orc.TerMeZOOracle([orc.Layer(LAYER["d_out"], LAYER["d_in"])], w)
+    x = synth.activations(100, LAYER["tokens"], LAYER["d_in"])
+    tgt = synth.activations(101, LAYER["tokens"], LAYER["d_out"])
+    st.build_mask(LAYER["rho"])
     xq, s = orc.act_quant(x)
     t0 = time.perf_counter()
     for t in range(n_steps):
         f = {}
         for sign in (1, -1):
-            codes, _, betas = st.perturb(t, C1["eps"], sign)
+            codes, _, betas = st.perturb(t, LAYER["eps"], sign)
             _, y = orc.bitlinear(xq, s, codes[0], betas[0], want_acc=False)
             f[sign] = orc.mse(y, tgt)
-        st.update(orc.projected_grad(f[1], f[-1], C1["eps"]), C1["lr"])
+        st.update(orc.projected_grad(f[1], f[-1], LAYER["eps"]), LAYER["lr"])
     dt = (time.perf_counter() - t0) / n_steps
     return {"value": 1.0 / dt, "unit": "steps/s", "cores": 1, "kind": "oracle", "host": host_cpu(),
             "sample": f"{n_steps} full oracle steps of the same workload (single thread, C + numpy)"}
@@ -214,27 +214,27 @@ def cpu_baseline_full(c, rho, n_steps=8, seed=0, theta=False):
             "sample": f"{n_steps} full oracle steps of the same workload"}
 
 
-def run_c1(args, torch, termezo, synth, dev):
-    """Config 1: one BitLinear 256 x 256 with fp32 latents, 8 token rows, MSE to a
+def run_layer(args, torch, termezo, synth, dev):
+    """Single-layer workload: one BitLinear 256 x 256 with fp32 latents, 8 token rows, MSE to a
     N(0, 1) target, mask ratio 1e-2; a step is perturb +/-, two forwards with the MSE
     read back, g on the host and the masked update."""
     import numpy as np
-    w = synth.torch_latents(0, C1["d_out"] * C1["d_in"], torch.float32, dev).view(C1["d_out"], C1["d_in"])
-    x = torch.from_numpy(synth.activations(100, C1["tokens"], C1["d_in"])).to(dev)
-    tgt = torch.from_numpy(synth.activations(101, C1["tokens"], C1["d_out"])).to(dev)
-    y = torch.empty((C1["tokens"], C1["d_out"]), device=dev)
+    w = synth.torch_latents(0, LAYER["d_out"] * LAYER["d_in"], torch.float32, dev).view(LAYER["d_out"], LAYER["d_in"])
+    x = torch.from_numpy(synth.activations(100, LAYER["tokens"], LAYER["d_in"])).to(dev)
+    tgt = torch.from_numpy(synth.activations(101, LAYER["tokens"], LAYER["d_out"])).to(dev)
+    y = torch.empty((LAYER["tokens"], LAYER["d_out"]), device=dev)
     ctx = termezo.Context([w])
-    k0, _ = ctx.build_mask(C1["rho"])
-    eps32, two = np.float32(C1["eps"]), np.float32(2.0)
+    k0, _ = ctx.build_mask(LAYER["rho"])
+    eps32, two = np.float32(LAYER["eps"]), np.float32(2.0)
 
     def step(t):
         f = {}
         for sign in (1, -1):
-            ctx.perturb(t, C1["eps"], sign)
+            ctx.perturb(t, LAYER["eps"], sign)
             ctx.bitlinear_forward(0, x, y)
             f[sign] = np.float32(ctx.mse_loss(y, tgt))
         g = np.float32((f[1] - f[-1]) / (two * eps32))      # projected gradient, fp32
-        ctx.update(float(g), C1["lr"], want_k=False)
+        ctx.update(float(g), LAYER["lr"], want_k=False)
 
     for t in range(args.warmup):
         step(t)
@@ -244,12 +244,12 @@ def run_c1(args, torch, termezo, synth, dev):
         step(t)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
-    cpu = None if args.no_cpu_baseline else cpu_baseline_c1()
+    cpu = None if args.no_cpu_baseline else cpu_baseline_layer()
     out = {"metric": "ZO steps/sec, single BitLinear with MSE loss", "value": 1000.0 / ms,
            "unit": "steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "int8xternary+f32", "data": "synthetic",
-           "config": {"workload": "termezo_zo_step_bitlinear_256x256_mse", **C1, "k0": k0,
+           "config": {"workload": "termezo_zo_step_bitlinear_256x256_mse", **LAYER, "k0": k0,
                       "parallelism": "single_gpu"},
            "roofline": None,
            "note": "launch-latency bound (two host read-backs of the loss per step); "
@@ -540,8 +540,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="2b", choices=sorted(CONFIGS) + ["c1"],
-                    help="2b (default, config 4), 700m (config 3), tiny (config 2), c1 (config 1)")
+    ap.add_argument("--config", default="2b", choices=sorted(CONFIGS) + ["layer"],
+                    help="2b (default: the 2B decoder), 700m (700M-class decoder), tiny (tiny "
+                         "fp32 decoder), layer (one 256 x 256 BitLinear with an MSE loss)")
     ap.add_argument("--rho", type=float, default=None, help="mask ratio (default: the config's)")
     ap.add_argument("--eps", type=float, default=1e-3)
     ap.add_argument("--lr", type=float, default=None, help="learning rate (default: the config's)")
@@ -579,8 +580,8 @@ def main():
         if args.sweep in ("bitlinear", "all"):
             sweep_bitlinear(torch, termezo, synth, dev, not args.no_cpu_baseline)
         return
-    if args.config == "c1":
-        run_c1(args, torch, termezo, synth, dev)
+    if args.config == "layer":
+        run_layer(args, torch, termezo, synth, dev)
         return
     c = CONFIGS[args.config]
     if args.rho is None:

@@ -314,7 +314,7 @@ def bitlinear_matmul(xq: np.ndarray, s: np.ndarray, codes: np.ndarray, beta: flo
 
 
 def mse(y: np.ndarray, target: np.ndarray) -> float:
-    """Config-1 loss: e = y - t and e^2 in fp32, the mean accumulated in fp64."""
+    """MSE loss of the single-layer workload: e = y - t and e^2 in fp32, the mean accumulated in fp64."""
     e = (_f32(y) - _f32(target)).astype(np.float32)
     e2 = (e * e).astype(np.float32)
     return float(np.float32(np.sum(e2.astype(np.float64)) / e2.size))

@@ -1569,7 +1569,7 @@ hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z
   return hipGetLastError();
 }
 
-// Config-1 loss: one block, fixed reduction order (deterministic).
+// MSE loss of the single-layer workload: one block, fixed reduction order (deterministic).
 __global__ void __launch_bounds__(256) k_mse(const float* y, const float* t, int64_t n,
                                              double* out) {
   __shared__ double lds[256];

@@ -12,8 +12,8 @@ from paper_2609_33548_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-C2_LAYERS = [(256, 256)] * 4 + [(688, 256), (688, 256), (256, 688)]
-C2_LAYERS = C2_LAYERS * 2
+TINY_DECODER_LAYERS = [(256, 256)] * 4 + [(688, 256), (688, 256), (256, 688)]
+TINY_DECODER_LAYERS = TINY_DECODER_LAYERS * 2
 
 
 def _torch():
@@ -74,7 +74,7 @@ def test_gauss_is_bit_identical_to_oracle(orc):
                                f"gpu {z[bad[0]]!r} oracle {rz[bad[0]]!r}")
 
 
-@pytest.mark.parametrize("shapes", [[(256, 256)], C2_LAYERS], ids=["c1", "c2"])
+@pytest.mark.parametrize("shapes", [[(256, 256)], TINY_DECODER_LAYERS], ids=["single_layer", "tiny_decoder"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
 @pytest.mark.parametrize("rho0,inclusive", [(0.01, False), (0.001, False), (0.01, True),
                                            (1.0, False)])
@@ -90,7 +90,7 @@ def test_build_mask_matches_oracle(orc, shapes, bf16, rho0, inclusive):
         assert np.array_equal(ctx.codes(l), ref.clean_codes(l))
 
 
-@pytest.mark.parametrize("shapes", [[(256, 256)], C2_LAYERS], ids=["c1", "c2"])
+@pytest.mark.parametrize("shapes", [[(256, 256)], TINY_DECODER_LAYERS], ids=["single_layer", "tiny_decoder"])
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
 # 0.002: the guarded path (actives' codes only); 0.9999: fully active tiles after ragged ones
 @pytest.mark.parametrize("rho0", [0.002, 0.05, 0.9999, 1.0])
@@ -193,7 +193,7 @@ def test_bitlinear_large_grid_sampled_rows(orc, M, K, N, ydt):
 @pytest.mark.parametrize("rho0", [0.002, 0.01, 0.9999, 1.0])   # 0.002: guarded (actives-only) path
 def test_update_and_shrink_match_oracle(orc, bf16, rho0):
     print(f"update bf16={bf16} rho0={rho0}", flush=True)
-    ref, ctx, tensors = _setup(orc, C2_LAYERS, bf16, seed=5)
+    ref, ctx, tensors = _setup(orc, TINY_DECODER_LAYERS, bf16, seed=5)
     ctx.build_mask(rho0)
     ref.build_mask(rho0)
     gs = [40.0, -25.0, 60.0, -80.0, 10.0, 120.0]
@@ -217,7 +217,7 @@ def test_update_and_shrink_match_oracle(orc, bf16, rho0):
         _check_stats(ref, ctx)
 
 
-def test_config1_trajectory_is_bit_exact(orc):
+def test_single_layer_trajectory_is_bit_exact(orc):
     """Single BitLinear 256x256, fp32 latents, 8 token rows, MSE to a N(0,1)
     target, rho0 = 1%, eps = 1e-3, lr = 1e-4, seeds s_t = t, 100 steps."""
     torch = _torch()
