@@ -85,8 +85,8 @@ void termezo_destroy(termezo_ctx* ctx);
 /* Message describing the last failure on ctx ("" if none).  Owned by ctx. */
 const char* termezo_last_error(const termezo_ctx* ctx);
 
-/* Initial mask (Sec. 3, eq. distance and eq. selection_init; Algorithm 1,
- * first two statements).  Computes tau^l = 0.5 (mean|w^l| + delta) per layer,
+/* Initial mask (Sec. 3, eq. distance and eq. selection_init; the initial
+ * threshold and selection of Algorithm 1).  Computes tau^l = 0.5 (mean|w^l| + delta) per layer,
  * the distance d_i = min(|w_i - tau|, |w_i + tau|) of every latent, the global
  * budget k0 = floor(rho0 * D) and xi0, the k0-th smallest distance over all
  * layers (ties at xi0 broken by ascending gid; tie_inclusive != 0 keeps every
