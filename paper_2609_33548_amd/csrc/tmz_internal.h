@@ -150,8 +150,13 @@ struct termezo_ctx {
   // compact mode: the active latents in list order (latent dtype), library-owned; the
   // caller's latent tensors are no longer read or written
   bool compact = false;
+  // mirror: d_wc holds the active latents in list order and is kept current (always in
+  // compact mode; otherwise for sparse sets, where it replaces the scattered reads of the
+  // latents; the update then writes both)
+  bool mirror = false;
   void* d_wc = nullptr;
   void* d_wc_tmp = nullptr;
+  int64_t wc_cap = 0;
 
   // scratch
   unsigned long long* d_hist = nullptr;      // kHistBins

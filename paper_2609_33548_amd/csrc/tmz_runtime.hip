@@ -95,6 +95,20 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   return TERMEZO_OK;
 }
 
+// The list-order copy of the active latents (and the buffer the shrink compacts it into).
+termezo_status ensure_wc_capacity(termezo_ctx* c, int64_t k) {
+  if (k <= c->wc_cap && c->d_wc) return TERMEZO_OK;
+  if (c->d_wc) (void)hipFree(c->d_wc);
+  if (c->d_wc_tmp) (void)hipFree(c->d_wc_tmp);
+  c->d_wc = c->d_wc_tmp = nullptr;
+  c->wc_cap = 0;
+  const size_t bytes = (size_t)(k > 0 ? k : 1) * dtype_size(c->dtype);
+  TMZ_HIP(c, hipMalloc(&c->d_wc, bytes));
+  TMZ_HIP(c, hipMalloc(&c->d_wc_tmp, bytes));
+  c->wc_cap = k > 0 ? k : 1;
+  return TERMEZO_OK;
+}
+
 termezo_status ensure_xq_capacity(termezo_ctx* c, int64_t M, int64_t K) {
   const int64_t need = M * K;
   if (need > c->xq_cap) {
@@ -334,6 +348,15 @@ termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32
   if (st != TERMEZO_OK) return st;
   TMZ_HIP(c, launch_mask_compact_write(c, inclusive));
   TMZ_HIP(c, launch_tile_ranges(c));
+  // sparse sets: keep the active latents in list order as well (contiguous reads in the
+  // perturbation and the update instead of gathers; the update writes both copies)
+  c->mirror = false;
+  if (total > 0 && total * 8 <= c->D) {
+    st = ensure_wc_capacity(c, total);
+    if (st != TERMEZO_OK) return st;
+    TMZ_HIP(c, launch_active_values(c, 0, total, c->d_wc, 0, 0));
+    c->mirror = true;
+  }
 
   // clean codes: current = clean
   TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
@@ -467,7 +490,7 @@ termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_o
   TMZ_HIP(c, launch_shrink(c, c->k_bound));
   std::swap(c->d_act, c->d_act_tmp);
   std::swap(c->d_act_off, c->d_act_off_tmp);
-  if (c->compact) std::swap(c->d_wc, c->d_wc_tmp);
+  if (c->mirror) std::swap(c->d_wc, c->d_wc_tmp);
   TMZ_HIP(c, launch_tile_ranges(c));
   TMZ_HIP(c, launch_ref_after_update(c, c->xi_lo));
   c->codes_valid = false;
@@ -590,23 +613,18 @@ termezo_status termezo_compact(termezo_ctx* c) {
   if (!c->has_mask) return fail(c, TERMEZO_ERR_STATE, "compact before build_mask");
   if (c->compact) return fail(c, TERMEZO_ERR_STATE, "already compact");
   if (c->pending_perturb) return fail(c, TERMEZO_ERR_STATE, "compact with a pending perturbation");
-  const size_t bytes = (size_t)(c->act_cap > 0 ? c->act_cap : 1) * dtype_size(c->dtype);
-  void *wc = nullptr, *wt = nullptr;
-  hipError_t e = hipMalloc(&wc, bytes);
-  if (e == hipSuccess) e = hipMalloc(&wt, bytes);
-  if (e != hipSuccess) {
-    if (wc) (void)hipFree(wc);
-    return hip_fail(c, e, "alloc compact latents");
-  }
   int64_t k = 0;
   TMZ_HIP(c, hipMemcpyAsync(&k, c->d_act_off + c->L, sizeof(int64_t), hipMemcpyDeviceToHost,
                             c->stream));
   TMZ_HIP(c, hipStreamSynchronize(c->stream));
-  c->d_wc = wc;
-  c->d_wc_tmp = wt;
-  TMZ_HIP(c, launch_active_values(c, 0, k, c->d_wc, 0, 0));
+  if (!c->mirror) {                              // dense sets: the copy is made now
+    termezo_status st = ensure_wc_capacity(c, k);
+    if (st != TERMEZO_OK) return st;
+    TMZ_HIP(c, launch_active_values(c, 0, k, c->d_wc, 0, 0));
+  }
   termezo_status st = sync_and_check(c);
   if (st != TERMEZO_OK) return st;
+  c->mirror = true;
   c->compact = true;
   c->pair_valid = false;
   c->k_bound = k;
@@ -647,7 +665,7 @@ termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
   b += T * (4 + 8 + 8 + 8 + 8 + 8) + 8;                          // tile tables and scratch
   b += cap * (4 + 4 + 4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;  // lists, w' pair, z, shrink
   b += L * 8;                                                    // |w| sums of the other sign
-  if (c->compact) b += 2 * cap * dsz;                            // active latents (list order)
+  if (c->mirror) b += 2 * c->wc_cap * dsz;                       // active latents (list order)
   b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;
   b += c->xq_cap + c->xs_cap * 4;                                // activation-quant scratch
   for (const ThetaHost& t : c->theta) b += 2 * t.n * (int64_t)dtype_size(t.dtype);

@@ -676,9 +676,25 @@ __device__ __forceinline__ void put4(uint16_t* wp, int64_t j0, int n, const floa
 }
 
 // wc (compact mode): the active latents in list order, read instead of the layers.
-template <typename T>
-__device__ __forceinline__ void list4(const T* wc, int64_t j0, int n, float v[4]) {
-  for (int r = 0; r < 4; ++r) v[r] = r < n ? load1(wc, j0 + r) : 0.0f;
+// (j0 % 4 == 0: a whole run is one 8- or 16-byte load)
+__device__ __forceinline__ void list4(const float* wc, int64_t j0, int n, float v[4]) {
+  if (n == 4) {
+    const float4 a = *reinterpret_cast<const float4*>(wc + j0);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  } else {
+    for (int r = 0; r < 4; ++r) v[r] = r < n ? wc[j0 + r] : 0.0f;
+  }
+}
+__device__ __forceinline__ void list4(const uint16_t* wc, int64_t j0, int n, float v[4]) {
+  if (n == 4) {
+    const uint2 a = *reinterpret_cast<const uint2*>(wc + j0);
+    v[0] = __uint_as_float(a.x << 16);
+    v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(a.y << 16);
+    v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+  } else {
+    for (int r = 0; r < 4; ++r) v[r] = r < n ? bf16_to_f32(wc[j0 + r]) : 0.0f;
+  }
 }
 
 // PAIR: both signs of the perturbation from one pass -- w' at +se to wp with its
@@ -982,7 +998,8 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
                                                 const int64_t* act_off, SeedList seeds,
                                                 const float* scal, T* __restrict__ wn,
                                                 T* __restrict__ wc,
-                                                const float* __restrict__ zcache) {
+                                                const float* __restrict__ zcache,
+                                                int write_latents) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const float a = scal[0];
@@ -1040,12 +1057,8 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) nv[r] = storage_round(w, v[r]);
-        if (wc) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) store1((T*)wc, j0 + r, nv[r]);
-        } else {
-          scatter4(w, i, 4, nv);
-        }
+        if (wc) put4(wc, j0, 4, nv);
+        if (write_latents) scatter4(w, i, 4, nv);
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -1074,16 +1087,14 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
         float v = fmaf(a, zcache ? zcache[j] : zc.get(seed, gid), wv[r]);
         for (int q = 1; q < K; ++q) v = fmaf(scal[q], gauss_at(seeds.s[q], gid), v);
         nv[r] = storage_round(w, v);
-        if (wc)
-          store1(wc, j, nv[r]);
-        else if (!one)
-          store1(w, i[r], nv[r]);
+        if (wc) store1(wc, j, nv[r]);
+        if (write_latents && !one) store1(w, i[r], nv[r]);
       }
       bad |= !in_fix_range(nv[r]);
       acc += (long long)fix_abs(nv[r]) - (long long)fix_abs(wv[r]);
       any = true;
     }
-    if (!wc && one && a_ok) scatter4(reinterpret_cast<T*>(const_cast<void*>(st.w[lr])), i, n, nv);
+    if (write_latents && one && a_ok) scatter4(reinterpret_cast<T*>(const_cast<void*>(st.w[lr])), i, n, nv);
     put4(wn, j0, n, nv);
   }
   flush_delta((long long*)st.S_clean, l, acc, any);
@@ -1745,6 +1756,7 @@ hipError_t launch_tile_ranges(termezo_ctx* c) {
 hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float se, bool pair) {
   if (k <= 0) return hipSuccess;
   const int64_t g = sparse_grid(k);
+  const void* wcp = c->mirror ? c->d_wc : nullptr;
   float* wpm = pair ? c->d_wpm : nullptr;
   float* zo = pair ? c->d_zc : nullptr;
   int64_t* sa = pair ? c->d_S_alt : nullptr;
@@ -1752,20 +1764,20 @@ hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float 
     if (pair)
       hipLaunchKernelGGL((k_perturb_delta<float, true>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const float*)c->d_wc, wpm, zo, sa);
+                         (const float*)wcp, wpm, zo, sa);
     else
       hipLaunchKernelGGL((k_perturb_delta<float, false>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const float*)c->d_wc, wpm, zo, sa);
+                         (const float*)wcp, wpm, zo, sa);
   } else {
     if (pair)
       hipLaunchKernelGGL((k_perturb_delta<uint16_t, true>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const uint16_t*)c->d_wc, wpm, zo, sa);
+                         (const uint16_t*)wcp, wpm, zo, sa);
     else
       hipLaunchKernelGGL((k_perturb_delta<uint16_t, false>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const uint16_t*)c->d_wc, wpm, zo, sa);
+                         (const uint16_t*)wcp, wpm, zo, sa);
   }
   return hipGetLastError();
 }
@@ -1785,14 +1797,16 @@ hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float
 hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds, const float* zc) {
   if (k <= 0) return hipSuccess;
   const int64_t g = sparse_grid(k);
+  void* wcp = c->mirror ? c->d_wc : nullptr;
+  const int wl = c->compact ? 0 : 1;           // the caller's latents, unless dropped
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
-                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)c->d_wc,
-                       zc);
+                       c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)wcp,
+                       zc, wl);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
                        c->d_act_off, seeds, (const float*)c->d_scal, (uint16_t*)c->d_wp,
-                       (uint16_t*)c->d_wc, zc);
+                       (uint16_t*)wcp, zc, wl);
   return hipGetLastError();
 }
 
@@ -1839,12 +1853,12 @@ hipError_t launch_shrink(termezo_ctx* c, int64_t k) {
     hipLaunchKernelGGL(k_shrink_write<uint16_t>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
                        c->d_act, c->d_act_off, (const uint16_t*)c->d_wp, per, c->d_blk_cnt,
                        (const uint64_t*)c->d_shrink_flags, c->d_act_tmp, c->d_act_off_tmp,
-                       (uint16_t*)c->d_wc_tmp);
+                       (uint16_t*)(c->mirror ? c->d_wc_tmp : nullptr));
   else
     hipLaunchKernelGGL(k_shrink_write<float>, dim3(nb), dim3(256), 0, c->stream, c->dev(),
                        c->d_act, c->d_act_off, (const float*)c->d_wp, per, c->d_blk_cnt,
                        (const uint64_t*)c->d_shrink_flags, c->d_act_tmp, c->d_act_off_tmp,
-                       (float*)c->d_wc_tmp);
+                       (float*)(c->mirror ? c->d_wc_tmp : nullptr));
   hipLaunchKernelGGL(k_shrink_offsets, dim3(1), dim3(256), 0, c->stream, c->d_act_off,
                      c->d_act_off_tmp, c->L, total);
   return hipGetLastError();
