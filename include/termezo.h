@@ -108,11 +108,11 @@ termezo_status termezo_build_mask(termezo_ctx* ctx, float rho0, float delta,
  * clean codes.  Registered theta tensors are perturbed too (see the theta
  * section below).  Records (seed, eps) for the following termezo_update.
  * Perturbation pairs: the first call with a (seed, eps) and sign +-1 also forms
- * the values of the other sign and keeps z (list order, 8 bytes per active
- * latent of library memory); a following call with the same seed and eps and
- * either sign reuses them, and the update after it reads z instead of drawing
- * it.  Any other seed or eps, sign 0, an update or a mask rebuild starts afresh;
- * the caller must not write the latents in between (they are borrowed).
+ * the perturbed values of the other sign (list order, 4 bytes per active latent
+ * of library memory; z itself is never stored); a following call with the same
+ * seed and eps and either sign reuses them.  Any other seed or eps, sign 0, an
+ * update or a mask rebuild starts afresh; the caller must not write the latents
+ * in between (they are borrowed).
  * Errors: INVALID_ARG (sign not in {-1, 0, 1}; eps <= 0 or not finite),
  * STATE (no mask).  A perturbed |w'| >= 4 raises a deferred NUMERIC. */
 termezo_status termezo_perturb(termezo_ctx* ctx, uint64_t seed, float eps,

@@ -139,9 +139,8 @@ struct termezo_ctx {
   bool act_off_host_valid = false;
   float* d_wp = nullptr;             // perturbed values at the actives (act_cap)
   // perturbation pair: the first call of a (seed, eps) pair also writes the other sign's
-  // values (d_wpm, its |w| sums in d_S_alt) and z (d_zc), all in list order
+  // values (d_wpm, its |w| sums in d_S_alt), in list order
   float* d_wpm = nullptr;
-  float* d_zc = nullptr;
   int64_t* d_S_alt = nullptr;        // [L]
   bool pair_valid = false;
   uint64_t pair_seed = 0;
@@ -261,7 +260,7 @@ hipError_t launch_es_coeffs(termezo_ctx* c, const float* rewards, int N, float l
 hipError_t launch_coeffs_multi_from_losses(termezo_ctx* c, const float* losses, int K, float eps,
                                            float lr);
 // coefficients from d_scal[0 .. K-1]; the updated values of the actives go to d_wp (list order)
-hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds, const float* zc);
+hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds);
 // from d_wp (the updated values): d_act -> d_act_tmp, offsets -> tmp
 hipError_t launch_shrink(termezo_ctx* c, int64_t k);
 hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev);

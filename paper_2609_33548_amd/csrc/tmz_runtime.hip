@@ -75,7 +75,6 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   dfree(c->d_act_tmp);
   dfree(c->d_wp);
   dfree(c->d_wpm);
-  dfree(c->d_zc);
   dfree(c->d_blk_cnt);
   dfree(c->d_shrink_flags);
   c->act_cap = 0;
@@ -85,7 +84,6 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   TMZ_HIP(c, dalloc(&c->d_act_tmp, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_wp, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_wpm, (size_t)cap));
-  TMZ_HIP(c, dalloc(&c->d_zc, (size_t)cap));
   c->blk_cap = cap / 1024 + 2;   // shrink blocks hold at least 1024 entries (4 per thread)
   TMZ_HIP(c, dalloc(&c->d_blk_cnt, (size_t)c->blk_cap));
   // shrink flags, one word per thread: at most 2048 blocks below 64 entries per thread
@@ -154,7 +152,6 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_act_off_tmp);
   dfree(c->d_wp);
   dfree(c->d_wpm);
-  dfree(c->d_zc);
   dfree(c->d_hist);
   dfree(c->d_sel);
   dfree(c->d_tile_cnt);
@@ -479,9 +476,7 @@ SeedList seed_list(const uint64_t* s, int32_t K) {
 // Update at the actives with the coefficients already in d_scal, then the new
 // thresholds and the shrink; the compacted list replaces the old one.
 termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_out) {
-  // the first direction's z is kept by the perturbation pass of that seed
-  const bool cached = c->pair_valid && c->pair_seed == seeds.s[0];
-  TMZ_HIP(c, launch_update(c, c->k_bound, seeds, cached ? c->d_zc : nullptr));
+  TMZ_HIP(c, launch_update(c, c->k_bound, seeds));
   c->pair_valid = false;
   c->theta_pair_valid = false;
   c->theta_sign = 0;
@@ -663,7 +658,7 @@ termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
   int64_t b = c->D / 4;                                          // 2-bit codes
   b += L * (8 * 8 + 4 * 4 + 4 + 8 + 4 + 8) + 3 * (L + 1) * 8;    // per-layer state, offsets
   b += T * (4 + 8 + 8 + 8 + 8 + 8) + 8;                          // tile tables and scratch
-  b += cap * (4 + 4 + 4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;  // lists, w' pair, z, shrink
+  b += cap * (4 + 4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;  // lists, w' of both signs, shrink
   b += L * 8;                                                    // |w| sums of the other sign
   if (c->mirror) b += 2 * c->wc_cap * dsz;                       // active latents (list order)
   b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;

@@ -698,8 +698,8 @@ __device__ __forceinline__ void list4(const uint16_t* wc, int64_t j0, int n, flo
 }
 
 // PAIR: both signs of the perturbation from one pass -- w' at +se to wp with its
-// delta in S_cur, w' at -se to wpm with its delta in S_alt, and z to zout (list
-// order), so the other sign of the pair and the update need no generator pass.
+// delta in S_cur, w' at -se to wpm with its delta in S_alt (list order), so the other
+// sign of the pair needs no generator pass.  z itself is never stored.
 template <typename T, bool PAIR>
 __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
                                                        const uint32_t* __restrict__ act,
@@ -707,7 +707,6 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
                                                        float se, float* __restrict__ wp,
                                                        const T* __restrict__ wc,
                                                        float* __restrict__ wpm,
-                                                       float* __restrict__ zout,
                                                        int64_t* S_alt) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
@@ -768,10 +767,7 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
       }
       any = true;
       put4(wp, j0, 4, v);
-      if (PAIR) {
-        put4(wpm, j0, 4, vm);
-        put4(zout, j0, 4, z);
-      }
+      if (PAIR) put4(wpm, j0, 4, vm);
       continue;
     }
     for (int r = 0; r < n; ++r) {
@@ -797,10 +793,7 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
       any = true;
     }
     put4(wp, j0, n, v);
-    if (PAIR) {
-      put4(wpm, j0, n, vm);
-      put4(zout, j0, n, z);
-    }
+    if (PAIR) put4(wpm, j0, n, vm);
   }
   flush_delta((long long*)st.S_cur, l, acc, any);
   if (PAIR) flush_delta((long long*)S_alt, l, acc2, any);
@@ -990,15 +983,12 @@ __global__ void k_coeff_from_losses(const float* fp, const float* fm, float eps,
 
 // The new values also go, in list order and the latent dtype, to wn (read by the
 // shrink).  With a non-finite coefficient (reported by the coefficient kernel) the
-// latents are left untouched and wn holds their current values.  zcache (list
-// order, or null): the first direction's z, kept by the perturbation pass of the
-// same seed.
+// latents are left untouched and wn holds their current values.
 template <typename T>
 __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __restrict__ act,
                                                 const int64_t* act_off, SeedList seeds,
                                                 const float* scal, T* __restrict__ wn,
                                                 T* __restrict__ wc,
-                                                const float* __restrict__ zcache,
                                                 int write_latents) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
@@ -1042,12 +1032,7 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       for (int r = 0; r < 4; ++r) nv[r] = wv[r];
       if (a_ok) {
         float z[4], v[4];
-        if (zcache) {
-          const float4 zz = *reinterpret_cast<const float4*>(zcache + j0);
-          z[0] = zz.x; z[1] = zz.y; z[2] = zz.z; z[3] = zz.w;
-        } else {
-          gauss_quad(seed, g0 >> 2, 0u, z);
-        }
+        gauss_quad(seed, g0 >> 2, 0u, z);
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] = fmaf(a, z[r], wv[r]);
         for (int q = 1; q < K; ++q) {
@@ -1084,7 +1069,7 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       nv[r] = wv[r];
       if (a_ok) {
         const uint64_t gid = (uint64_t)(st.gid0[l] + i[r]);
-        float v = fmaf(a, zcache ? zcache[j] : zc.get(seed, gid), wv[r]);
+        float v = fmaf(a, zc.get(seed, gid), wv[r]);
         for (int q = 1; q < K; ++q) v = fmaf(scal[q], gauss_at(seeds.s[q], gid), v);
         nv[r] = storage_round(w, v);
         if (wc) store1(wc, j, nv[r]);
@@ -1758,26 +1743,25 @@ hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float 
   const int64_t g = sparse_grid(k);
   const void* wcp = c->mirror ? c->d_wc : nullptr;
   float* wpm = pair ? c->d_wpm : nullptr;
-  float* zo = pair ? c->d_zc : nullptr;
   int64_t* sa = pair ? c->d_S_alt : nullptr;
   if (c->dtype == TERMEZO_F32) {
     if (pair)
       hipLaunchKernelGGL((k_perturb_delta<float, true>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const float*)wcp, wpm, zo, sa);
+                         (const float*)wcp, wpm, sa);
     else
       hipLaunchKernelGGL((k_perturb_delta<float, false>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const float*)wcp, wpm, zo, sa);
+                         (const float*)wcp, wpm, sa);
   } else {
     if (pair)
       hipLaunchKernelGGL((k_perturb_delta<uint16_t, true>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const uint16_t*)wcp, wpm, zo, sa);
+                         (const uint16_t*)wcp, wpm, sa);
     else
       hipLaunchKernelGGL((k_perturb_delta<uint16_t, false>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const uint16_t*)wcp, wpm, zo, sa);
+                         (const uint16_t*)wcp, wpm, sa);
   }
   return hipGetLastError();
 }
@@ -1794,7 +1778,7 @@ hipError_t launch_coeff_from_losses(termezo_ctx* c, const float* fp, const float
   return hipGetLastError();
 }
 
-hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds, const float* zc) {
+hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds) {
   if (k <= 0) return hipSuccess;
   const int64_t g = sparse_grid(k);
   void* wcp = c->mirror ? c->d_wc : nullptr;
@@ -1802,11 +1786,11 @@ hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds, const
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
                        c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)wcp,
-                       zc, wl);
+                       wl);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
                        c->d_act_off, seeds, (const float*)c->d_scal, (uint16_t*)c->d_wp,
-                       (uint16_t*)wcp, zc, wl);
+                       (uint16_t*)wcp, wl);
   return hipGetLastError();
 }
 

@@ -342,11 +342,10 @@ def test_guarded_requant_equals_dense_requant(orc, bf16, rho0, eps):
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
 @pytest.mark.parametrize("rho0", [0.01, 1.0])
 def test_perturbation_pair_reuse(orc, bf16, rho0):
-    """The first call of a (seed, eps) pair also produces the other sign's values
-    and z; the other sign, a repeat of either sign, a pair that starts with -1, a
-    new eps for the same seed, sign 0 in between, and the update after the pair
-    (z kept from the perturbation) all give the oracle's codes, thresholds and
-    latents."""
+    """The first call of a (seed, eps) pair also produces the other sign's values;
+    the other sign, a repeat of either sign, a pair that starts with -1, a new eps
+    for the same seed, sign 0 in between, and the update after the pair all give
+    the oracle's codes, thresholds and latents."""
     print(f"pair reuse bf16={bf16} rho0={rho0}", flush=True)
     shapes = [(256, 256), (128, 512), (64, 128)]
     ref, ctx, tensors = _setup(orc, shapes, bf16, seed=17)
