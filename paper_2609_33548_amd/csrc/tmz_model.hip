@@ -445,6 +445,17 @@ __global__ void __launch_bounds__(256) k_kv_prep(uint16_t* __restrict__ k,
   const int s0 = blockIdx.x * 64, bh = blockIdx.y;
   const int b = bh / Hkv, h = bh % Hkv;
   const int64_t rowkv = (int64_t)Hkv * HD;
+  // V rows first (64 tokens in 16-byte chunks, into registers): their latency overlaps the
+  // rotation of K below
+  constexpr int VPT = 64 * HD / 8 / 256;     // chunks per thread
+  uint4 vreg[VPT];
+#pragma unroll
+  for (int q = 0; q < VPT; ++q) {
+    const int i = q * 256 + threadIdx.x;
+    const int r = i / (HD / 8), c8 = (i % (HD / 8)) * 8;
+    vreg[q] = make_uint4(0, 0, 0, 0);
+    if (s0 + r < S) vreg[q] = *reinterpret_cast<const uint4*>(v + ((int64_t)b * S + s0 + r) * rowkv + (int64_t)h * HD + c8);
+  }
   // K: rotary chunk pairs, in place
   for (int e = threadIdx.x; e < 64 * HALF / 8; e += 256) {
     const int r = e / (HALF / 8), dc = (e % (HALF / 8)) * 8;
@@ -456,12 +467,12 @@ __global__ void __launch_bounds__(256) k_kv_prep(uint16_t* __restrict__ k,
     *reinterpret_cast<uint4*>(kp + dc) = rope_chunk(lo, hi, true, rope_c + ti, rope_s + ti);
     *reinterpret_cast<uint4*>(kp + dc + HALF) = rope_chunk(hi, lo, false, rope_c + ti, rope_s + ti);
   }
-  // V^T: 64 token rows in 16-byte chunks into LDS, then 8 tokens of one dim per 16-byte store
-  for (int i = threadIdx.x; i < 64 * HD / 8; i += 256) {
+  // V^T: the token rows into LDS, then 8 tokens of one dim per 16-byte store
+#pragma unroll
+  for (int q = 0; q < VPT; ++q) {
+    const int i = q * 256 + threadIdx.x;
     const int r = i / (HD / 8), c8 = (i % (HD / 8)) * 8;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (s0 + r < S) val = *reinterpret_cast<const uint4*>(v + ((int64_t)b * S + s0 + r) * rowkv + (int64_t)h * HD + c8);
-    *reinterpret_cast<uint4*>(&t[r][c8]) = val;
+    *reinterpret_cast<uint4*>(&t[r][c8]) = vreg[q];
   }
   __syncthreads();
   for (int i = threadIdx.x; i < HD * 8; i += 256) {
