@@ -73,7 +73,16 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, int64_t d, T* h) {
   const int64_t m = blockIdx.x;
   const T* src = E + (int64_t)tok[m] * d;
-  for (int64_t i = threadIdx.x; i < d; i += 256) h[m * d + i] = src[i];
+  T* dst = h + m * d;
+  constexpr int EPC = 16 / (int)sizeof(T);    // elements per 16-byte chunk
+  const bool vec = d % EPC == 0 && reinterpret_cast<uintptr_t>(E) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(h) % 16 == 0;
+  if (vec) {
+    for (int64_t c = threadIdx.x; c < d / EPC; c += 256)
+      reinterpret_cast<uint4*>(dst)[c] = reinterpret_cast<const uint4*>(src)[c];
+  } else {
+    for (int64_t i = threadIdx.x; i < d; i += 256) dst[i] = src[i];
+  }
 }
 
 // ---------------------------------------------------------------------------
