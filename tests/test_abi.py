@@ -73,3 +73,14 @@ def test_null_context_calls_are_rejected():
     assert T.lib.termezo_bitlinear_forward(None, 0, None, 0, 1, None, 0, None, None, None) \
         == T.ERR_INVALID_ARG
     T.lib.termezo_destroy(None)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one MI355X: --gpus above 1 exits with status 2 and says so,
+    before importing torch or touching a device."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
