@@ -126,3 +126,117 @@ def test_bf16_storage_rounds_every_stored_activation():
     r32 = dec.forward_row_losses(cfg32, emb, tok, codes, betas)
     assert not np.array_equal(r16, r32)
     assert np.allclose(r16, r32, rtol=2e-2)
+
+
+# --------------------------------------------------------------------------
+# Block composition, written independently with torch fp64 library routines
+# --------------------------------------------------------------------------
+def _torch_rows(cfg, emb, tokens, codes, betas, mutant=None):
+    """Per-position next-token cross-entropy of the pre-norm BitNet decoder, composed
+    from torch CPU routines (F.embedding, F.rms_norm, rotate-half RoPE, SDPA with K/V
+    heads repeated, F.silu, F.cross_entropy); the ternary projections use the oracle's
+    activation quantiser (pinned on its own) and an int64 matmul.  Rounding points: the
+    activation dtype wherever a tensor is stored (fp32 first, then bf16), the RMSNorm
+    output feeding a projection kept at fp32.  `mutant` swaps in one plausible wiring
+    mistake, to show the comparison detects it."""
+    from oracle import termezo_ref as orc
+    f64 = torch.float64
+    act = torch.bfloat16 if cfg.bf16 else torch.float32
+
+    def stored(x):
+        return x.to(torch.float32).to(act).to(f64)
+
+    def bitlinear(x, c, beta):
+        xq, s = orc.act_quant(x.to(torch.float32).numpy())
+        acc = torch.from_numpy(xq).to(torch.int64) @ torch.from_numpy(c).to(torch.int64).T
+        r = torch.tensor(beta, dtype=torch.float32) / torch.from_numpy(s)
+        return (acc.to(torch.float32) * r[:, None]).to(f64)
+
+    B, S = tokens.shape
+    d, Hq, Hkv, hd = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    E = torch.from_numpy(emb).to(f64)
+    tok = torch.from_numpy(tokens).to(torch.int64)
+    half = hd // 2
+    inv = cfg.rope_base ** (-torch.arange(half, dtype=f64) * 2.0 / hd)
+    ang = torch.arange(S, dtype=f64)[:, None] * inv[None, :]
+    cos = torch.cat([ang.cos(), ang.cos()], -1)           # [S, hd]
+    sin = torch.cat([ang.sin(), ang.sin()], -1)
+
+    def rope(x, H):                                         # x [B, S, H*hd]
+        x = x.view(B, S, H, hd)
+        if mutant == "interleaved_rope":                    # pairs (2i, 2i+1) instead
+            x1, x2 = x[..., 0::2], x[..., 1::2]
+            a = ang[None, :, None, :]
+            y = torch.stack([x1 * a.cos() - x2 * a.sin(), x1 * a.sin() + x2 * a.cos()], -1)
+            return y.reshape(B, S, H * hd)
+        rot = torch.cat([-x[..., half:], x[..., :half]], -1)
+        return (x * cos[None, :, None, :] + rot * sin[None, :, None, :]).reshape(B, S, H * hd)
+
+    def norm(h):
+        return F.rms_norm(h, (d,), eps=cfg.norm_eps)
+
+    h = stored(F.embedding(tok, E))                         # [B, S, d]
+    for blk in range(cfg.n_blocks):
+        c = codes[7 * blk: 7 * blk + 7]
+        be = betas[7 * blk: 7 * blk + 7]
+        x = norm(h).reshape(B * S, d)
+        q = stored(rope(stored(bitlinear(x, c[0], be[0])).view(B, S, -1), Hq))
+        k = stored(rope(stored(bitlinear(x, c[1], be[1])).view(B, S, -1), Hkv))
+        v = stored(bitlinear(x, c[2], be[2])).view(B, S, -1)
+        qh = q.view(B, S, Hq, hd).transpose(1, 2)
+        kh = k.view(B, S, Hkv, hd).transpose(1, 2)
+        vh = v.view(B, S, Hkv, hd).transpose(1, 2)
+        if mutant == "gqa_modulo":                          # query head h reads kv head h % Hkv
+            kh = kh.repeat(1, Hq // Hkv, 1, 1)
+            vh = vh.repeat(1, Hq // Hkv, 1, 1)
+        else:
+            kh = kh.repeat_interleave(Hq // Hkv, dim=1)
+            vh = vh.repeat_interleave(Hq // Hkv, dim=1)
+        a = F.scaled_dot_product_attention(qh, kh, vh, is_causal=(mutant != "no_causal_mask"))
+        a = stored(a.transpose(1, 2).reshape(B * S, Hq * hd))
+        o = stored(bitlinear(a, c[3], be[3])).view(B, S, d)
+        h = stored(h + o)
+        x = (h if mutant == "no_mlp_norm" else norm(h)).reshape(B * S, d)
+        g = stored(bitlinear(x, c[4], be[4]))
+        u = stored(bitlinear(x, c[5], be[5]))
+        m = stored(F.silu(g) * u) if mutant != "gate_up_swapped" else stored(F.silu(u) * g)
+        dn = stored(bitlinear(m, c[6], be[6])).view(B, S, d)
+        h = stored(h + dn)
+    xf = stored(norm(h)).reshape(B * S, d)
+    logits = xf @ E.T
+    labels = torch.zeros(B, S, dtype=torch.int64)
+    labels[:, :-1] = tok[:, 1:]
+    rows = F.cross_entropy(logits, labels.reshape(-1), reduction="none").view(B, S)
+    rows[:, -1] = 0.0
+    return rows.numpy()
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_block_composition_matches_independent_torch_composition(bf16):
+    """Pins the wiring of the decoder oracle (pre-norm order, residual adds, RoPE pairs,
+    GQA head mapping, causal mask, SwiGLU, tied head, rounding points) against a
+    composition of library routines; each mutant of that composition, one wiring
+    mistake each, must differ from the oracle far beyond the agreement bar."""
+    cfg = dec.DecoderConfig(n_blocks=2, d_model=64, n_heads=4, n_kv_heads=2, d_ffn=96,
+                            vocab=50, bf16=bf16)
+    rng = np.random.default_rng(3)
+    codes = [rng.integers(-1, 2, size=s).astype(np.int8) for s in cfg.layer_shapes()]
+    betas = [0.05] * len(codes)
+    # embedding of std 0.25 (logits of std ~2) so the losses vary strongly from position
+    # to position without saturating
+    emb = dec.store(synth.activations(21, cfg.vocab, cfg.d_model) * np.float32(0.25), bf16)
+    tok = synth.tokens(22, 2, 16, cfg.vocab)
+    ref = dec.forward_row_losses(cfg, emb, tok, codes, betas)
+    got = _torch_rows(cfg, emb, tok, codes, betas)
+    assert np.all(got[:, -1] == 0.0)
+    # relative error, on a floor of 1 nat (a position whose label is the current token
+    # has a loss near zero with a tied head)
+    rel = np.abs(got[:, :-1] - ref[:, :-1]) / np.maximum(np.abs(ref[:, :-1]), 1.0)
+    # the same rounding points and integer decisions on both sides: only fp64 summation
+    # order differs (observed 1e-15)
+    assert rel.max() <= 1e-12, rel.max()
+    for mutant in ("interleaved_rope", "gqa_modulo", "no_causal_mask", "no_mlp_norm",
+                   "gate_up_swapped"):
+        bad = _torch_rows(cfg, emb, tok, codes, betas, mutant=mutant)
+        drel = np.abs(bad[:, :-1] - ref[:, :-1]) / np.maximum(np.abs(ref[:, :-1]), 1.0)
+        assert drel.max() > 1e-3, mutant

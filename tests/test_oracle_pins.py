@@ -173,16 +173,30 @@ def test_distance_is_min_of_both_boundaries(orc):
 # --------------------------------------------------------------------------
 # Mask: initial selection and shrink (eq. selection_init, eq. selection_)
 # --------------------------------------------------------------------------
-def _brute_force_mask(w_layers, delta, rho0):
+def _brute_force_tau(w, delta):
+    """tau = fp32((mean|w| + delta) / 2) from the exact rational mean."""
+    gamma = sum(Fraction(float(abs(v))) for v in w) / len(w)
+    return float(np.float32(float((gamma + Fraction(float(np.float32(delta)))) / 2)))
+
+
+def _brute_force_distances(w, tau):
+    """fp32 of the exact min(|w - tau|, |w + tau|) for every latent (the fp64
+    differences of two fp32 numbers this close in magnitude are exact)."""
+    return [float(np.float32(min(abs(float(v) - tau), abs(float(v) + tau)))) for v in w]
+
+
+def _brute_force_keys(w_layers, delta):
     keys = []
     gid = 0
     for w in w_layers:
-        gamma = sum(Fraction(float(abs(v))) for v in w) / len(w)
-        tau = float(np.float32(float((gamma + Fraction(float(np.float32(delta)))) / 2)))
-        for v in w:
-            dv = min(abs(float(v) - tau), abs(float(v) + tau))
-            keys.append((float(np.float32(dv)), gid))
+        for dv in _brute_force_distances(w, _brute_force_tau(w, delta)):
+            keys.append((dv, gid))
             gid += 1
+    return keys
+
+
+def _brute_force_mask(w_layers, delta, rho0):
+    keys = _brute_force_keys(w_layers, delta)
     k0 = math.floor(float(np.float32(rho0)) * len(keys))
     keys.sort()
     return sorted(g for _, g in keys[:k0]), keys[k0 - 1][0]
@@ -230,6 +244,74 @@ def test_mask_invariants_and_global_quantile(orc):
     st2 = orc.TerMeZOOracle(layers, w)
     k_inc, xi_inc = st2.build_mask(rho0, inclusive=True)
     assert xi_inc == xi0 and k_inc >= k0
+
+
+def _tie_layers():
+    """bf16 latents: every value class shares one distance, so ties at xi0 occur."""
+    sizes = [(16, 32), (8, 64), (32, 16)]
+    w_layers = [synth.latents(300 + i, [a * b], bf16=True) for i, (a, b) in enumerate(sizes)]
+    return sizes, w_layers
+
+
+def test_inclusive_selection_matches_brute_force_with_ties(orc):
+    """eq. selection_init read literally: every latent with d <= xi0, where xi0 is the
+    k0-th smallest distance.  Budgets are chosen so that the tie class at xi0 runs past
+    the k0-th entry (an exact-k branch would return k0 and fail), plus one without."""
+    sizes, w_layers = _tie_layers()
+    keys = _brute_force_keys(w_layers, 1e-5)
+    srt = sorted(keys)
+    D = len(keys)
+    tied = [k for k in range(1, D) if srt[k - 1][0] == srt[k][0]]
+    untied = [k for k in range(1, D) if srt[k - 1][0] != srt[k][0]]
+    cases = [tied[0], tied[len(tied) // 2], tied[-1], untied[len(untied) // 3]]
+    n_past = 0
+    for k0 in cases:
+        rho0 = (k0 + 0.5) / D                   # floor(fp32(rho0) * D) = k0
+        assert math.floor(float(np.float32(rho0)) * D) == k0
+        xi0 = srt[k0 - 1][0]
+        inc = sorted(g for dv, g in keys if dv <= xi0)
+        n_past += len(inc) > k0
+        st = orc.TerMeZOOracle([orc.Layer(a, b) for a, b in sizes], np.concatenate(w_layers),
+                               bf16=True)
+        k, xi = st.build_mask(rho0, inclusive=True)
+        got = np.concatenate([a + st.offsets[l] for l, a in enumerate(st.active)])
+        assert xi == xi0 and k == len(inc) and got.tolist() == inc, k0
+        # the exact-k reading of the same budget is a strict subset when ties run past k0
+        st2 = orc.TerMeZOOracle([orc.Layer(a, b) for a, b in sizes], np.concatenate(w_layers),
+                                bf16=True)
+        assert st2.build_mask(rho0)[0] == k0
+    assert n_past == 3
+
+
+def test_shrink_keep_side_matches_brute_force_with_ties(orc):
+    """eq. selection_: S_t = {i in S_(t-1) : d_i(w_t) <= xi0}, d from the threshold of the
+    unperturbed updated latents.  The brute force takes tau from the exact rational mean
+    of each layer and keeps entries whose fp32 distance is at most xi0, ties included.
+    Step 0 applies g = 0 (latents and thresholds unchanged), so every entry of S_0 must
+    stay, the k0-th among them at exactly xi0; bf16 value classes add more ties."""
+    sizes, w_layers = _tie_layers()
+    layers = [orc.Layer(a, b) for a, b in sizes]
+    srt = sorted(_brute_force_keys(w_layers, 1e-5))
+    D = len(srt)
+    # a budget whose last two entries tie at xi0
+    k0 = next(k for k in range(D // 5, D) if srt[k - 2][0] == srt[k - 1][0])
+    st = orc.TerMeZOOracle(layers, np.concatenate(w_layers), bf16=True)
+    assert st.build_mask((k0 + 0.5) / D)[0] == k0
+    n_at_xi0 = 0
+    for t, g in enumerate([0.0, 40.0, -25.0, 60.0, 0.0]):
+        prev = [a.copy() for a in st.active]
+        st.perturb(t, 1e-3, 1)
+        st.update(g, 2e-3)
+        for l in range(len(layers)):
+            w = st.layer_w(l)
+            d = _brute_force_distances(w, _brute_force_tau(w, 1e-5))
+            keep = [int(i) for i in prev[l] if d[i] <= st.xi0]
+            n_at_xi0 += sum(1 for i in prev[l] if d[i] == st.xi0)
+            assert st.active[l].tolist() == keep, (t, l)
+        if t == 0:
+            assert [a.tolist() for a in st.active] == [a.tolist() for a in prev]
+            assert n_at_xi0 >= 2
+    assert st.k < st.k0                          # the nonzero steps did shrink the set
 
 
 def test_mask_band_matches_continuous_approximation(orc):
