@@ -42,7 +42,9 @@ PEAK_INT8_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 # HBM traffic of the GEMM launches measured with rocprofv3 counters (FETCH_SIZE,
 # WRITE_SIZE), valid only for the kernel source it was measured on.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bitlinear_gemm_traffic_2b_step.txt")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2609_33548_amd", "csrc", "tmz_bitlinear.hip")
+# the GEMM kernels and every header they include (tile order, direct-to-LDS loads, unpacking)
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2609_33548_amd", "csrc", f)
+                for f in ("tmz_bitlinear.hip", "tmz_device.h", "tmz_internal.h")]
 METRIC = "ZO steps/sec at 2B BitNet shape; perturb+requant GB/s; BitLinear int8 TOPS"
 
 
@@ -67,16 +69,23 @@ def gemm_algorithmic_bytes(c):
     return total / len(launches)
 
 
+def gemm_source_digest():
+    """SHA-256 over the GEMM's source files, concatenated in a fixed order."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """Counter-measured HBM bytes per GEMM launch, or None when the counters
     were taken on another version of the kernel source."""
-    import hashlib
     try:
         kv = dict(line.split(":", 1) for line in open(TRAFFIC_FILE) if ":" in line)
     except OSError:
         return None
-    src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
-    if kv.get("source_sha256", "").strip() != src:
+    if kv.get("source_sha256", "").strip() != gemm_source_digest():
         return None
     return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
 

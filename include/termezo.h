@@ -17,8 +17,9 @@
  *   - A context is not thread-safe.  All device work is ordered on the HIP
  *     stream given at creation.  Only the calls that return host values
  *     (build_mask, update with k_out, mse_loss, model_loss, sync and the
- *     exports) wait for the stream; they also report a deferred NUMERIC error
- *     raised by an earlier kernel on that context.
+ *     exports) wait for the stream; they also report a deferred error
+ *     raised by an earlier kernel on that context (NUMERIC, or INVALID_ARG for
+ *     a token id out of range).
  *   - Device pointers are plain device addresses of memory owned by the
  *     caller (for example PyTorch tensors); host pointers are noted as such.
  *   - Latent weights are BORROWED: the caller owns them and they must outlive
@@ -330,10 +331,14 @@ void termezo_model_destroy(termezo_model* model);
 /* Batch loss of eq. objective_est with next-token cross-entropy: the mean over
  * the batch * (seq - 1) labelled positions of logsumexp(logits) - logit[next
  * token], with the current codes (clean or perturbed).  tokens: device int32
- * [batch][seq].  Outputs (all optional): loss_dev (device fp32 scalar),
- * row_loss_dev (device fp32 [batch*seq], 0 at each sequence's last position),
- * loss_host (host; the call then waits).  Errors: INVALID_ARG, STATE (no
- * current codes), OOM. */
+ * [batch][seq]; every id must lie in [0, vocab).  Outputs (all optional):
+ * loss_dev (device fp32 scalar), row_loss_dev (device fp32 [batch*seq], 0 at
+ * each sequence's last position), loss_host (host; the call then waits and
+ * reports deferred errors).  An id outside [0, vocab) is read as id 0 (the
+ * embedding is never read out of bounds) and raises a deferred INVALID_ARG,
+ * reported by this call when loss_host is given, else by the next waiting
+ * call (termezo_sync, ...); the losses of that call are then meaningless.
+ * Errors: INVALID_ARG, STATE (no current codes), OOM. */
 termezo_status termezo_model_loss(termezo_model* model, const int32_t* tokens, int32_t batch,
                                   int32_t seq, float* loss_dev, float* row_loss_dev,
                                   float* loss_host);

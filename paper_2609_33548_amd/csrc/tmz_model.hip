@@ -1,9 +1,13 @@
 // BitNet decoder forward around the ternary BitLinear projections, and the
 // next-token cross-entropy that TerMeZO evaluates at w +/- eps z (Sec. 3,
-// eq. objective_est).  The full-precision parameters (token embedding tied to
-// the LM head, unit-weight RMSNorms) are frozen.  Activations are stored in
-// fp32 or bf16 between kernels; the RMSNorm output and the SwiGLU product are
-// handed to the int8 activation quantiser in fp32 without being stored.
+// eq. objective_est).  The full-precision parameters are the token embedding
+// (tied to the LM head) and the RMSNorm weights (one unless the caller gives a
+// weight table); when they are registered as theta the forward reads their
+// current, possibly perturbed, values.  Activations are stored in fp32 or bf16
+// between kernels.  The RMSNorm output feeding a projection goes to the int8
+// activation quantiser in fp32 without being stored; the SwiGLU product
+// silu(g) * u is stored in the activation dtype (by the fused gate|up GEMM
+// epilogue for bf16, by a row kernel otherwise) and then quantised.
 #include <algorithm>
 #include <cmath>
 #include <new>
@@ -67,12 +71,19 @@ __device__ __forceinline__ int8_t q8(float x, float s) {
 
 
 // ---------------------------------------------------------------------------
-// h[m] = E[tok[m]]
+// h[m] = E[tok[m]].  An id outside [0, V) reads row 0 instead and sets bit 8 of
+// the deferred error word, so the embedding is never read out of bounds.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, int64_t d, T* h) {
+__global__ void __launch_bounds__(256) k_embed(const int32_t* tok, const T* E, int64_t d,
+                                               int64_t V, T* h, int32_t* err) {
   const int64_t m = blockIdx.x;
-  const T* src = E + (int64_t)tok[m] * d;
+  int64_t t = tok[m];
+  if (t < 0 || t >= V) {
+    if (threadIdx.x == 0) atomicOr(err, 8);
+    t = 0;
+  }
+  const T* src = E + t * d;
   T* dst = h + m * d;
   constexpr int EPC = 16 / (int)sizeof(T);    // elements per 16-byte chunk
   const bool vec = d % EPC == 0 && reinterpret_cast<uintptr_t>(E) % 16 == 0 &&
@@ -1368,10 +1379,21 @@ __global__ void __launch_bounds__(256) k_loss_mean(const float* row_loss, int64_
   }
 }
 
-__global__ void k_labels(const int32_t* tok, int64_t M, int S, int32_t* labels) {
+// Next-token label of every position (-1 at the last position of a sequence); an
+// id outside [0, V) becomes label 0 and sets bit 8 of the deferred error word.
+__global__ void k_labels(const int32_t* tok, int64_t M, int S, int64_t V, int32_t* labels,
+                         int32_t* err) {
   const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (m >= M) return;
-  labels[m] = ((m % S) != S - 1) ? tok[m + 1] : -1;
+  int32_t t = -1;
+  if ((m % S) != S - 1) {
+    t = tok[m + 1];
+    if (t < 0 || (int64_t)t >= V) {
+      atomicOr(err, 8);
+      t = 0;
+    }
+  }
+  labels[m] = t;
 }
 
 }  // namespace tmz
@@ -1699,13 +1721,13 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
 
   if (bf)
     hipLaunchKernelGGL(k_embed<uint16_t>, dim3((unsigned)M), dim3(256), 0, s, tokens,
-                       (const uint16_t*)emb, d, (uint16_t*)m->h);
+                       (const uint16_t*)emb, d, (int64_t)cf.vocab, (uint16_t*)m->h, c->d_err);
   else
     hipLaunchKernelGGL(k_embed<float>, dim3((unsigned)M), dim3(256), 0, s, tokens,
-                       (const float*)emb, d, (float*)m->h);
+                       (const float*)emb, d, (int64_t)cf.vocab, (float*)m->h, c->d_err);
   chk(hipGetLastError());
   hipLaunchKernelGGL(k_labels, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, tokens, M, seq,
-                     m->labels);
+                     (int64_t)cf.vocab, m->labels, c->d_err);
   const unsigned rowg = (unsigned)((M + 3) / 4);
   // RMSNorm (weight row wr of the norm weights, one when there are none), then
   // the quantiser, or stored (the LM-head input)
@@ -1836,9 +1858,10 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   }
   if (loss_host) {
     double v = 0.0;
-    if (hipMemcpyAsync(&v, m->loss64, 8, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (hipMemcpyAsync(&v, m->loss64, 8, hipMemcpyDeviceToHost, s) != hipSuccess)
       return TERMEZO_ERR_DEVICE;
+    const termezo_status ds = termezo_sync(c);     // waits; reports deferred errors
+    if (ds != TERMEZO_OK) return ds;
     *loss_host = (float)v;
   }
   return TERMEZO_OK;

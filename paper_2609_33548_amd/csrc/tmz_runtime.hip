@@ -64,7 +64,8 @@ termezo_status sync_and_check(termezo_ctx* c) {
     if (err & 4)
       msg += "compact mode: a layer's threshold moved by more than its frozen latents' margin "
              "(their codes were kept; rebuild the mask from full latents); ";
-    return fail(c, TERMEZO_ERR_NUMERIC, msg);
+    if (err & 8) msg += "model_loss: a token id lies outside [0, vocab) (read as id 0); ";
+    return fail(c, (err & ~8) ? TERMEZO_ERR_NUMERIC : TERMEZO_ERR_INVALID_ARG, msg);
   }
   return TERMEZO_OK;
 }

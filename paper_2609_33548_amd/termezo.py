@@ -415,9 +415,3 @@ def gauss(seed: int, gids, stream=None):
     if st != OK:
         raise TermezoError(st, "termezo_gauss failed")
     return z
-
-
-def projected_grad(f_plus: float, f_minus: float, eps: float) -> float:
-    """g = (F+ - F-) / (2 eps) in fp32 (eq. spsa); host scalar arithmetic."""
-    fp, fm, e = np.float32(f_plus), np.float32(f_minus), np.float32(eps)
-    return float(np.float32(np.float32(fp - fm) / np.float32(np.float32(2.0) * e)))

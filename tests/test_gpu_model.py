@@ -130,3 +130,27 @@ def test_device_side_update_matches_host_update(orc):
         assert np.array_equal(got, ref.w), f"step {t}"
     model.close()
     ctx.close()
+
+
+def test_out_of_range_token_ids_are_reported(orc):
+    """A token id outside [0, vocab) is read as id 0 by the embedding and label
+    kernels (never out of bounds) and reported as INVALID_ARG by the waiting call;
+    the next call with valid ids is clean."""
+    torch = _torch()
+    from oracle import decoder_ref as dec
+    from paper_2609_33548_amd import termezo
+    cfg = dec.DecoderConfig(n_blocks=1, d_model=128, n_heads=2, n_kv_heads=1, d_ffn=256, vocab=200,
+                            bf16=True)
+    ref, ctx, model, tensors, emb, E, tok, tokd = _build(orc, dec, cfg, 60, 2, 64)
+    ctx.build_mask(0.02)
+    ctx.perturb(1, 1e-3, 1)
+    clean = model.loss(tokd)
+    for bad_id, pos in ((cfg.vocab, 5), (-3, 63), (1 << 30, 0)):
+        bad = tokd.clone()
+        bad[1, pos] = bad_id
+        with pytest.raises(termezo.TermezoError) as ei:
+            model.loss(bad)
+        assert ei.value.status == termezo.ERR_INVALID_ARG and "token id" in str(ei.value)
+        assert model.loss(tokd) == clean
+    model.close()
+    ctx.close()
