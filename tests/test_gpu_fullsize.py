@@ -8,18 +8,29 @@ the device's xi0 by counting: fewer than k0 distances lie below it and at
 least k0 at or below it, which makes it the k0-th smallest.  The mask that
 follows from xi0 (everything below it, then ties in id order up to k0) is
 compared with the device's on sampled layers; perturbed codes, updated
-latents and the shrunk mask are compared bit for bit on sampled layers; the
-decoder loss is compared per position on one sequence, all 210 layers'
-perturbed codes coming from the oracle.  Loss bar: the sequence mean within
-1e-3 relative, each position within 2e-2 relative -- the device rounds the
+latents and the shrunk mask are compared bit for bit on sampled layers.
+
+The batch losses F+ and F- are those the step consumes: the device evaluates
+all 16 sequences (the bench's call); the oracle, every layer's perturbed codes
+its own, evaluates the first 4 sequences (all 16 would take the fp64 oracle
+several minutes per sign).  Bars: the mean over those 4 sequences within 1e-3
+relative, each position within 2e-2 relative -- the device rounds the
 activations to bf16 at eight points per block through 30 blocks (2^-9
 relative each) and evaluates attention and exp in another order than the
-fp64 oracle (observed: median 2.6e-3, max 1.3e-2 per position, 1.6e-4 on
-the mean)."""
+fp64 oracle (observed in earlier runs: max 1.3e-2 per position, 1.6e-4 on a
+sequence mean).  The device's batch F is checked to be the mean of its own
+per-position losses over all 16 sequences.  F+ - F- (over the same 4 sequences)
+is about 5e-4 of F here, of the order of the bf16 storage error each loss may
+carry; the two evaluations share every activation the perturbation does not
+reach, so their errors largely cancel in the difference (observed: device and
+oracle differences within 4% of each other).  The test requires the same sign
+and agreement within 25%, a check on the direction g moves the weights in; the
+fp32 decoders bound g itself, and the update given g is bit-exact."""
 import numpy as np
 import pytest
 
 import bench
+import fullsize_common as fc
 from paper_2609_33548_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -28,6 +39,7 @@ C = bench.CONFIGS["2b"]
 SHAPES = bench.layer_shapes(C)
 SAMPLED = (0, 1, 4, 6, 104, 209)        # q, k, gate, down of block 0; up of block 14; down of block 29
 RHO, EPS, SEED, LR = 1e-3, 1e-3, 7, 1e-5
+N_SEQ = 4                                # sequences the oracle evaluates
 
 
 def _torch():
@@ -41,47 +53,21 @@ def _torch():
 def full(orc):
     torch = _torch()
     from paper_2609_33548_amd import termezo
-    D = sum(o * i for o, i in SHAPES)
-    lat = synth.torch_latents(1234, D, torch.bfloat16, "cuda")
-    views, off, offs = [], 0, []
-    for o, i in SHAPES:
-        views.append(lat[off: off + o * i].view(o, i))
-        offs.append(off)
-        off += o * i
-    ctx = termezo.Context(views)
-    st = {"ctx": ctx, "lat": lat, "views": views, "offs": offs, "D": D}
+    st = fc.build(torch, termezo, SHAPES)
     yield st
-    ctx.close()
+    if "model" in st:
+        st["model"].close()
+    st["ctx"].close()
+    del st
+    torch.cuda.empty_cache()
 
 
 def _host(view):
-    return view.float().cpu().numpy().ravel()
+    return fc.host(view)
 
 
 def _oracle_mask(full, orc, xi0):
-    """The mask xi0 defines: every layer's actives from the oracle's distances."""
-    k0 = int(np.floor(np.float64(np.float32(RHO)) * np.float64(full["D"])))
-    less, leq, ties, taus, acts_lt = 0, 0, [], [], []
-    for l, v in enumerate(full["views"]):
-        if l % 30 == 0:
-            print(f"  oracle distances, layer {l}", flush=True)
-        w = _host(v)
-        tau, _ = orc.threshold(orc.layer_abs_sum(w), w.size, 1e-5)
-        d = orc.distance(w, tau)
-        lt = np.nonzero(d < np.float32(xi0))[0]
-        eq = np.nonzero(d == np.float32(xi0))[0]
-        less += lt.size
-        leq += lt.size + eq.size
-        taus.append(tau)
-        acts_lt.append(lt)
-        ties.append(eq)
-    quota = k0 - less
-    acts = []
-    for l in range(len(SHAPES)):
-        take = ties[l][: max(0, min(quota, ties[l].size))]
-        quota -= take.size
-        acts.append(np.sort(np.concatenate([acts_lt[l], take])).astype(np.int64))
-    return k0, less, leq, taus, acts
+    return fc.oracle_mask(full, orc, RHO, xi0)
 
 
 def test_fullsize_mask(full, orc):
@@ -114,47 +100,45 @@ def test_fullsize_perturbed_codes(full, orc):
         assert bad == 0, f"layer {l}: {bad} codes differ"
 
 
-def test_fullsize_decoder_loss(full, orc):
-    """Per-position losses of sequence 0 at w + eps z, every layer's codes and
-    scales from the oracle (its mask, perturbation and requantisation)."""
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("sign", [1, -1])
+def test_fullsize_batch_loss(full, orc, sign):
+    """F at w + sign eps z as the bench computes it (all 16 sequences, device scalar),
+    against the oracle on the first 4 sequences with every layer's codes its own."""
     torch = _torch()
     from oracle import decoder_ref as dec
     from paper_2609_33548_amd import termezo
     ctx = full["ctx"]
     assert "acts" in full, "needs the mask test"
-    print("full-size decoder loss", flush=True)
-    E = (synth.torch_normal(1235, (C["vocab"], C["d_model"]), torch.float32, "cuda")
-         * synth.LATENT_STD).to(torch.bfloat16)
-    tok = synth.torch_tokens(1236, C["batch"], C["seq"], C["vocab"], "cuda")
-    model = termezo.Model(ctx, C["n_blocks"], C["d_model"], C["n_heads"], C["n_kv_heads"],
-                          C["d_ffn"], C["vocab"], E)
+    print(f"full-size batch loss, sign {sign}", flush=True)
+    if "model" not in full:
+        E = (synth.torch_normal(1235, (C["vocab"], C["d_model"]), torch.float32, "cuda")
+             * synth.LATENT_STD).to(torch.bfloat16)
+        full["E"] = E
+        full["tok"] = synth.torch_tokens(1236, C["batch"], C["seq"], C["vocab"], "cuda")
+        full["model"] = termezo.Model(ctx, C["n_blocks"], C["d_model"], C["n_heads"],
+                                      C["n_kv_heads"], C["d_ffn"], C["vocab"], E)
+    model, tok = full["model"], full["tok"]
     rows = torch.empty(C["batch"] * C["seq"], device="cuda")
-    ctx.perturb(SEED, EPS, 1)
-    model.loss(tok, row_loss_dev=rows)
-    got = rows.cpu().numpy().reshape(C["batch"], C["seq"])[0]
-    codes, betas = [], []
-    for l, v in enumerate(full["views"]):
-        if l % 30 == 0:
-            print(f"  oracle codes, layer {l}", flush=True)
-        w = _host(v)
-        wp = orc.perturbed_layer_values(w, full["acts"][l], full["offs"][l], SEED, EPS, 1)
-        tau, beta = orc.threshold(orc.layer_abs_sum(wp), w.size, 1e-5)
-        codes.append(orc.quantize(wp, tau).reshape(SHAPES[l]))
-        betas.append(beta)
-    cfg = dec.DecoderConfig(n_blocks=C["n_blocks"], d_model=C["d_model"], n_heads=C["n_heads"],
-                            n_kv_heads=C["n_kv_heads"], d_ffn=C["d_ffn"], vocab=C["vocab"],
-                            bf16=True)
-    emb = E.float().cpu().numpy()
-    print("  oracle decoder forward (1 sequence)", flush=True)
-    ref = dec.forward_row_losses(cfg, emb, tok[:1].cpu().numpy(), codes, betas)[0]
-    model.close()
-    assert got[-1] == 0.0 and ref[-1] == 0.0
-    rel = np.abs(got[:-1] - ref[:-1]) / np.abs(ref[:-1])
-    seq_rel = abs(got[:-1].mean() - ref[:-1].mean()) / abs(ref[:-1].mean())
-    print(f"per-position max rel {rel.max():.2e} median {np.median(rel):.2e}; sequence mean rel "
-          f"{seq_rel:.2e}", flush=True)
-    assert seq_rel <= 1e-3
-    assert rel.max() <= 2e-2
+    Fd = torch.zeros(1, device="cuda")
+    ctx.perturb(SEED, EPS, sign)
+    model.loss(tok, loss_dev=Fd, row_loss_dev=rows, host=False)
+    got = rows.cpu().numpy().reshape(C["batch"], C["seq"])
+    F = float(Fd.cpu()[0])
+    codes, betas = fc.oracle_codes(full, orc, SEED, EPS, sign)
+    print("  oracle decoder forward (4 sequences)", flush=True)
+    ref = dec.forward_row_losses(fc.decoder_config(dec, C), full["E"].float().cpu().numpy(),
+                                 tok[:N_SEQ].cpu().numpy(), codes, betas)
+    del codes
+    full.setdefault("F", {})[sign] = fc.compare_losses(got, ref, F, N_SEQ, f"2B F(sign {sign})",
+                                                       2e-2, 1e-3)
+    if len(full["F"]) == 2:
+        (dp, rp), (dm, rm) = full["F"][1], full["F"][-1]
+        print(f"  F+ - F- over {N_SEQ} sequences: device {dp - dm:.3e}, oracle {rp - rm:.3e}",
+              flush=True)
+        full["model"].close()
+        assert (dp - dm) * (rp - rm) > 0
+        assert abs((dp - dm) - (rp - rm)) <= 0.25 * abs(rp - rm)
 
 
 def test_fullsize_update_and_shrink(full, orc):

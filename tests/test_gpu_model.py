@@ -1,10 +1,18 @@
 """GPU parity of the decoder step (the loss TerMeZO evaluates at w +/- eps z)
 against the decoder oracle, through the C ABI.
 
-Bar (losses): 1e-3 relative on the batch loss; per-position losses 5e-3
-relative (bf16 storage of activations and bf16 attention probabilities on the
-device, fp64 on the oracle).  Updated latents: bit-exact when both sides use
-the same projected gradient."""
+Bars (losses).  fp32 decoder: 1e-5 relative on the batch loss, 1e-3 per position.
+The device evaluates in fp32 what the oracle evaluates in fp64 (median per-position
+difference 4e-8); the larger per-position differences come from the activation
+quantiser, whose round-to-nearest decision on an fp32 input can fall the other
+way when that input differs from the oracle's in its last bit: one int8 value
+then moves by one step, which moves that token's projection by about
+1/(127 sqrt(K)) relative (observed up to 6.6e-4 on a position's loss); the batch
+mean over 252 positions stays below 1e-5 (observed up to 5.9e-6).  bf16 decoder:
+1e-3 on the batch loss and 5e-3 per position (bf16 storage of activations and
+bf16 attention probabilities on the device, fp64 on the oracle).  Updated
+latents: bit-exact when both sides use the same projected gradient; the
+projected gradient itself is compared in its own test."""
 import numpy as np
 import pytest
 
@@ -40,13 +48,16 @@ def _build(orc, dec, cfg, seed, B, S):
     return ref, ctx, model, tensors, emb, E, tok, torch.from_numpy(tok).cuda()
 
 
-def _compare(dec, cfg, ref, emb, tok, rows_gpu, loss_gpu, codes, betas, rtol_rows):
+def _compare(dec, cfg, ref, emb, tok, rows_gpu, loss_gpu, codes, betas, rtol_rows,
+             rtol_loss=1e-3):
     rrows = dec.forward_row_losses(cfg, emb, tok, codes, betas)
     rl = dec.mean_loss(rrows)
-    assert abs(loss_gpu - rl) <= 1e-3 * abs(rl), (loss_gpu, rl)
     lab = rrows[:, :-1]
     got = rows_gpu.reshape(rrows.shape)[:, :-1]
     rel = np.abs(got - lab) / np.abs(lab)
+    print(f"  loss rel {abs(loss_gpu - rl) / abs(rl):.2e}; per position max {rel.max():.2e} "
+          f"median {np.median(rel):.2e}", flush=True)
+    assert abs(loss_gpu - rl) <= rtol_loss * abs(rl), (loss_gpu, rl)
     assert rel.max() <= rtol_rows, f"max rel {rel.max()} at {np.unravel_index(rel.argmax(), rel.shape)}"
     assert np.all(rows_gpu.reshape(rrows.shape)[:, -1] == 0.0)
     return rl
@@ -69,11 +80,50 @@ def test_tiny_decoder_fp32_steps(orc):
             ctx.perturb(t, eps, sign)
             F[sign] = model.loss(tokd, row_loss_dev=rows)
             codes, _, betas = ref.perturb(t, eps, sign)
-            _compare(dec, cfg, ref, emb, tok, rows.cpu().numpy(), F[sign], codes, betas, 2e-3)
+            _compare(dec, cfg, ref, emb, tok, rows.cpu().numpy(), F[sign], codes, betas, 1e-3,
+                     rtol_loss=1e-5)
         g = orc.projected_grad(F[1], F[-1], eps)     # the device's losses drive both updates
         assert ctx.update(g, lr) == ref.update(g, lr)
         got = np.concatenate([x.cpu().numpy().ravel() for x in tensors])
         assert np.array_equal(got, ref.w)
+    model.close()
+    ctx.close()
+
+
+def test_tiny_decoder_fp32_projected_gradient(orc):
+    """The scalar that drives every update: g = (F+ - F-) / (2 eps) from the device's
+    losses against g from the oracle's losses (Algorithm 1, eq. spsa), over several
+    seeds of the tiny fp32 decoder (the single-layer and bf16 cases are covered by the
+    bit-exact trajectory and by the device-side update test).  Bound: each batch loss
+    agrees within r_F relative (fp32 evaluation against the fp64 oracle), so
+    |g_dev - g_orc| <= r_F (|F+| + |F-|) / (2 eps)."""
+    torch = _torch()
+    from oracle import decoder_ref as dec
+    cfg = dec.DecoderConfig(n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4, d_ffn=688, vocab=1024)
+    B, S = 4, 64
+    ref, ctx, model, tensors, emb, E, tok, tokd = _build(orc, dec, cfg, 31, B, S)
+    assert ctx.build_mask(0.01) == ref.build_mask(0.01)
+    Fd = torch.zeros(2, device="cuda")
+    eps, r_F = 1e-3, 1e-5
+    errs = []
+    for seed in range(20, 28):
+        rf = {}
+        for j, sign in enumerate((1, -1)):
+            ctx.perturb(seed, eps, sign)
+            model.loss(tokd, loss_dev=Fd[j: j + 1], host=False)
+            codes, _, betas = ref.perturb(seed, eps, sign)
+            rf[sign] = dec.mean_loss(dec.forward_row_losses(cfg, emb, tok, codes, betas))
+        fp, fm = (float(v) for v in Fd.cpu())
+        g_dev = orc.projected_grad(fp, fm, eps)
+        g_orc = orc.projected_grad(rf[1], rf[-1], eps)
+        bound = r_F * (abs(rf[1]) + abs(rf[-1])) / (2 * eps)
+        print(f"  seed {seed}: F+ {fp:.7f}/{rf[1]:.7f} F- {fm:.7f}/{rf[-1]:.7f} "
+              f"dF {fp - fm:.3e}/{rf[1] - rf[-1]:.3e} g {g_dev:.5f}/{g_orc:.5f} "
+              f"bound {bound:.3e}", flush=True)
+        for v, r in ((fp, rf[1]), (fm, rf[-1])):
+            assert abs(v - r) <= r_F * abs(r)
+        assert abs(g_dev - g_orc) <= bound
+        errs.append(abs(g_dev - g_orc))
     model.close()
     ctx.close()
 
