@@ -381,6 +381,11 @@ termezo_status termezo_layer_stats(termezo_ctx* ctx, int32_t layer, float* tau,
 termezo_status termezo_mse_loss(termezo_ctx* ctx, const float* y, const float* target,
                                 int64_t n, float* out);
 
+/* The same mean squared error written to a device fp32 scalar (loss_dev), e.g.
+ * for termezo_update_from_losses; never waits.  Errors: INVALID_ARG. */
+termezo_status termezo_mse_loss_dev(termezo_ctx* ctx, const float* y, const float* target,
+                                    int64_t n, float* loss_dev);
+
 /* Gaussian directions z_i for n global ids (device uint64 gids, device fp32
  * z), exactly as the perturbation and the update regenerate them from seed.
  * hip_stream: a hipStream_t (NULL = default stream); no synchronisation. */

@@ -10,7 +10,11 @@
  *
  * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -shared -fPIC
  * (no contraction: every floating-point operation below is one IEEE-754
- * correctly rounded operation, and fmaf is used only where written).
+ * correctly rounded operation, and fmaf is used only where written).  A second
+ * build of the same source with -fopenmp runs the loops marked "omp parallel
+ * for" over several host threads; each iteration of those loops writes only its
+ * own outputs (the one reduction is an exact integer sum), so both builds give
+ * identical results.  The plain build ignores the pragmas.
  *
  * Arithmetic conventions fixed here (the paper leaves them open; each reading
  * is listed in the design notes):
@@ -30,11 +34,26 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define ORC_OK 0
 #define ORC_ERR_INVALID 1
 #define ORC_ERR_STATE 2
 #define ORC_ERR_NUMERIC 5
+
+/* Host threads the parallel loops use: n > 0 sets it (OpenMP build only);
+ * returns the count in effect (1 for the plain build). */
+int orc_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x32-10 (Salmon, Moraes, Dror, Shaw: "Parallel random numbers: as   */
@@ -188,11 +207,13 @@ float orc_gauss_one(uint64_t seed, uint32_t stream, uint64_t gid) {
 
 void orc_gauss(uint64_t seed, uint32_t stream, const int64_t* gids, int64_t n,
                float* z) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) z[i] = orc_gauss_one(seed, stream, (uint64_t)gids[i]);
 }
 
 void orc_gauss_range(uint64_t seed, uint32_t stream, int64_t gid0, int64_t n,
                      float* z) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) z[i] = orc_gauss_one(seed, stream, (uint64_t)(gid0 + i));
 }
 
@@ -216,11 +237,15 @@ int64_t orc_fix_abs(float w) {
 /* Exact integer sum S = sum_i floor(|w_i| 2^36).  Every |w_i| must be finite
  * and below 4 so that S stays inside int64 for layers of up to 2^25 weights. */
 int orc_layer_abs_sum(const float* w, int64_t n, int64_t* S_out) {
-  int64_t S = 0;
+  int64_t S = 0, bad = 0;
+#pragma omp parallel for reduction(+ : S, bad)
   for (int64_t i = 0; i < n; ++i) {
-    if (!isfinite(w[i]) || fabsf(w[i]) >= 4.0f) return ORC_ERR_NUMERIC;
-    S += orc_fix_abs(w[i]);
+    if (!isfinite(w[i]) || fabsf(w[i]) >= 4.0f)
+      bad += 1;
+    else
+      S += orc_fix_abs(w[i]);
   }
+  if (bad) return ORC_ERR_NUMERIC;
   *S_out = S;
   return ORC_OK;
 }
@@ -235,6 +260,7 @@ void orc_threshold(int64_t S, int64_t n, float delta, float* tau, float* beta) {
 
 /* Ternary quantiser Q (eq. quant): +1 above tau, -1 below -tau, 0 otherwise. */
 void orc_quantize(const float* w, int64_t n, float tau, int8_t* codes) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) {
     if (w[i] > tau)
       codes[i] = 1;
@@ -247,6 +273,7 @@ void orc_quantize(const float* w, int64_t n, float tau, int8_t* codes) {
 
 /* Boundary distance (eq. distance): min(|w - tau|, |w + tau|) = ||w| - tau|. */
 void orc_distance(const float* w, int64_t n, float tau, float* d) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) d[i] = fabsf(fabsf(w[i]) - tau);
 }
 
@@ -315,6 +342,7 @@ void orc_perturbed_layer(const float* w, int64_t n, const int64_t* act, int64_t 
                          int64_t gid0, uint64_t seed, float eps, int sign, float* w_out) {
   float se = (float)sign * eps;
   memcpy(w_out, w, (size_t)n * sizeof(float));
+#pragma omp parallel for
   for (int64_t j = 0; j < k; ++j) {
     int64_t i = act[j];
     float z = orc_gauss_one(seed, 0u, (uint64_t)(gid0 + i));
@@ -330,6 +358,7 @@ void orc_perturbed_layer(const float* w, int64_t n, const int64_t* act, int64_t 
 /* y[m][n] = float(acc) * (beta / s_m).                                      */
 /* ------------------------------------------------------------------------ */
 void orc_act_quant(const float* x, int64_t M, int64_t K, int8_t* xq, float* s) {
+#pragma omp parallel for
   for (int64_t m = 0; m < M; ++m) {
     const float* row = x + m * K;
     float a = 0.0f;
@@ -347,6 +376,7 @@ void orc_act_quant(const float* x, int64_t M, int64_t K, int8_t* xq, float* s) {
 
 void orc_bitlinear(const int8_t* xq, const float* s, const int8_t* codes, float beta,
                    int64_t M, int64_t K, int64_t N, int32_t* acc, float* y) {
+#pragma omp parallel for
   for (int64_t m = 0; m < M; ++m) {
     float r = beta / s[m];
     for (int64_t n = 0; n < N; ++n) {
@@ -382,12 +412,14 @@ static float orc_round_bf16(float v) {
 }
 
 void orc_bf16_round_array(const float* x, int64_t n, float* y) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) y[i] = orc_round_bf16(x[i]);
 }
 
 void orc_update_layer(float* w, const int64_t* act, int64_t k, int64_t gid0,
                       uint64_t seed, float lr, float g, int bf16_storage) {
   float a = -(lr * g);
+#pragma omp parallel for
   for (int64_t j = 0; j < k; ++j) {
     int64_t i = act[j];
     float z = orc_gauss_one(seed, 0u, (uint64_t)(gid0 + i));
@@ -422,6 +454,7 @@ int64_t orc_shrink_layer(const float* w, int64_t* act, int64_t k, float tau, flo
 void orc_theta_perturbed(const float* theta, int64_t n, int64_t tid0, uint64_t seed,
                          float eps, int sign, int bf16_storage, float* out) {
   float se = (float)sign * eps;
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) {
     float z = orc_gauss_one(seed, 1u, (uint64_t)(tid0 + i));
     float v = fmaf(se, z, theta[i]);
@@ -432,6 +465,7 @@ void orc_theta_perturbed(const float* theta, int64_t n, int64_t tid0, uint64_t s
 void orc_theta_update(float* theta, int64_t n, int64_t tid0, uint64_t seed, float lr, float g,
                       int bf16_storage) {
   float a = -(lr * g);
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) {
     float z = orc_gauss_one(seed, 1u, (uint64_t)(tid0 + i));
     float v = fmaf(a, z, theta[i]);
@@ -455,6 +489,7 @@ float orc_multi_coeff(float lr, int K, float g) {
 void orc_update_layer_multi(float* w, const int64_t* act, int64_t k, int64_t gid0,
                             const uint64_t* seeds, const float* g, int K, float lr,
                             int bf16_storage) {
+#pragma omp parallel for
   for (int64_t j = 0; j < k; ++j) {
     int64_t i = act[j];
     float v = w[i];
@@ -468,6 +503,7 @@ void orc_update_layer_multi(float* w, const int64_t* act, int64_t k, int64_t gid
 
 void orc_theta_update_multi(float* theta, int64_t n, int64_t tid0, const uint64_t* seeds,
                             const float* g, int K, float lr, int bf16_storage) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) {
     float v = theta[i];
     for (int q = 0; q < K; ++q) {
@@ -514,6 +550,7 @@ void orc_es_coeffs(const float* r, int N, float lr, int standardize, float* a) {
 
 void orc_update_layer_coeffs(float* w, const int64_t* act, int64_t k, int64_t gid0,
                              const uint64_t* seeds, const float* a, int N, int bf16_storage) {
+#pragma omp parallel for
   for (int64_t j = 0; j < k; ++j) {
     int64_t i = act[j];
     float v = w[i];
@@ -524,6 +561,7 @@ void orc_update_layer_coeffs(float* w, const int64_t* act, int64_t k, int64_t gi
 
 void orc_theta_update_coeffs(float* theta, int64_t n, int64_t tid0, const uint64_t* seeds,
                              const float* a, int N, int bf16_storage) {
+#pragma omp parallel for
   for (int64_t i = 0; i < n; ++i) {
     float v = theta[i];
     for (int q = 0; q < N; ++q) v = fmaf(a[q], orc_gauss_one(seeds[q], 1u, (uint64_t)(tid0 + i)), v);

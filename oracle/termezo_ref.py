@@ -33,24 +33,25 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_LIB_OMP_PATH = os.path.join(_HERE, "liboracle_omp.so")
 _lib = None
+_loaded = {}
 
 OK, ERR_INVALID, ERR_STATE, ERR_NUMERIC = 0, 1, 2, 5
 
 
-def lib():
-    """Load (building on first use if absent) the C oracle library."""
-    global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(_LIB_PATH):
+def _load(path):
+    if path in _loaded:
+        return _loaded[path]
+    if not os.path.exists(path):
         from . import build_oracle  # type: ignore
         build_oracle.build()
-    L = ctypes.CDLL(_LIB_PATH)
+    L = ctypes.CDLL(path)
     P = ctypes.c_void_p
     i64, u64, u32, f32, i32 = (ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint32,
                                ctypes.c_float, ctypes.c_int)
     sig = {
+        "orc_set_threads": (i32, [i32]),
         "orc_philox4x32_10": (None, [P, P, P]),
         "orc_ln": (f32, [f32]),
         "orc_ln_array": (None, [P, i64, P]),
@@ -85,8 +86,29 @@ def lib():
         fn = getattr(L, name)
         fn.restype = res
         fn.argtypes = args
-    _lib = L
+    _loaded[path] = L
     return L
+
+
+def lib():
+    """The C oracle library in use (built on first use if absent): the plain
+    single-threaded build unless use_threads() chose the OpenMP one."""
+    global _lib
+    if _lib is None:
+        _lib = _load(_LIB_PATH)
+    return _lib
+
+
+def use_threads(n: int) -> int:
+    """Run the oracle's independent-iteration loops on n host threads (the OpenMP
+    build of the same source; n = 1 selects the plain single-threaded build).
+    Results do not depend on it.  Returns the thread count in effect."""
+    global _lib
+    if n <= 1:
+        _lib = _load(_LIB_PATH)
+        return 1
+    _lib = _load(_LIB_OMP_PATH)
+    return int(_lib.orc_set_threads(int(n)))
 
 
 def _p(a: np.ndarray):

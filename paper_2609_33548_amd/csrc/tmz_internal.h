@@ -271,7 +271,8 @@ hipError_t launch_active_values(termezo_ctx* c, int64_t j0, int64_t j1, void* ou
 hipError_t launch_theta_pair(termezo_ctx* c, const ThetaHost& t, uint64_t seed, float eps);
 hipError_t launch_theta_update(termezo_ctx* c, const ThetaHost& t, const SeedList& seeds);
 hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z, hipStream_t s);
-hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hipStream_t s);
+hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, float* mean32,
+                      hipStream_t s);
 
 // BitLinear
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,

@@ -810,12 +810,19 @@ termezo_status termezo_layer_stats(termezo_ctx* c, int32_t layer, float* tau, fl
 termezo_status termezo_mse_loss(termezo_ctx* c, const float* y, const float* target, int64_t n,
                                 float* out) {
   if (!c || !y || !target || !out || n <= 0) return TERMEZO_ERR_INVALID_ARG;
-  TMZ_HIP(c, launch_mse(y, target, n, c->d_loss, c->stream));
+  TMZ_HIP(c, launch_mse(y, target, n, c->d_loss, nullptr, c->stream));
   double sum = 0.0;
   TMZ_HIP(c, hipMemcpyAsync(&sum, c->d_loss, sizeof(double), hipMemcpyDeviceToHost, c->stream));
   termezo_status st = sync_and_check(c);
   if (st != TERMEZO_OK) return st;
   *out = (float)(sum / (double)n);
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_mse_loss_dev(termezo_ctx* c, const float* y, const float* target,
+                                    int64_t n, float* loss_dev) {
+  if (!c || !y || !target || !loss_dev || n <= 0) return TERMEZO_ERR_INVALID_ARG;
+  TMZ_HIP(c, launch_mse(y, target, n, c->d_loss, loss_dev, c->stream));
   return TERMEZO_OK;
 }
 

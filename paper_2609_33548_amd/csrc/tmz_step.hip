@@ -1566,8 +1566,10 @@ hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z
 }
 
 // MSE loss of the single-layer workload: one block, fixed reduction order (deterministic).
+// Sum of squared errors in fp64 (e = y - t and e * e in fp32), into *out; with
+// out32 non-null also the mean rounded to fp32.
 __global__ void __launch_bounds__(256) k_mse(const float* y, const float* t, int64_t n,
-                                             double* out) {
+                                             double* out, float* out32) {
   __shared__ double lds[256];
   double acc = 0.0;
   for (int64_t i = threadIdx.x; i < n; i += 256) {
@@ -1581,7 +1583,10 @@ __global__ void __launch_bounds__(256) k_mse(const float* y, const float* t, int
     if ((int)threadIdx.x < off) lds[threadIdx.x] += lds[threadIdx.x + off];
     __syncthreads();
   }
-  if (threadIdx.x == 0) *out = lds[0];
+  if (threadIdx.x == 0) {
+    *out = lds[0];
+    if (out32) *out32 = (float)(lds[0] / (double)n);
+  }
 }
 
 // ===========================================================================
@@ -1903,8 +1908,9 @@ hipError_t launch_unpack_layer(termezo_ctx* c, int layer, int8_t* out_dev) {
   return hipGetLastError();
 }
 
-hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, hipStream_t s) {
-  hipLaunchKernelGGL(k_mse, dim3(1), dim3(256), 0, s, y, t, n, acc);
+hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, float* mean32,
+                      hipStream_t s) {
+  hipLaunchKernelGGL(k_mse, dim3(1), dim3(256), 0, s, y, t, n, acc, mean32);
   return hipGetLastError();
 }
 

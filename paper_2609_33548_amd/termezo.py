@@ -66,6 +66,7 @@ _SIGS = {
     "termezo_layer_stats": [_P, _i32, ctypes.POINTER(_f32), ctypes.POINTER(_f32),
                             ctypes.POINTER(_i64), ctypes.POINTER(_f32), ctypes.POINTER(_f32)],
     "termezo_mse_loss": [_P, _P, _P, _i64, ctypes.POINTER(_f32)],
+    "termezo_mse_loss_dev": [_P, _P, _P, _i64, _P],
     "termezo_active_count": [_P, ctypes.POINTER(_i64)],
     "termezo_gauss": [_P, _u64, _P, _i64, _P],
     "termezo_update_from_losses": [_P, _P, _P, _f32, _f32],
@@ -341,6 +342,11 @@ class Context:
         self._check(_lib.termezo_mse_loss(self.handle, _ptr(y), _ptr(target), y.numel(),
                                           ctypes.byref(out)), "mse_loss")
         return float(np.float32(out.value))
+
+    def mse_loss_dev(self, y, target, loss_dev):
+        """The same loss written to the device fp32 scalar loss_dev (no wait)."""
+        self._check(_lib.termezo_mse_loss_dev(self.handle, _ptr(y), _ptr(target), y.numel(),
+                                              _ptr(loss_dev)), "mse_loss_dev")
 
 
 class Model:

@@ -250,6 +250,43 @@ def test_single_layer_trajectory_is_bit_exact(orc):
     _check_mask(ref, ctx)
 
 
+def test_single_layer_device_side_trajectory_is_bit_exact(orc):
+    """The single-layer step as the bench runs it, with nothing on the host: MSE
+    losses written to device scalars, g = (F+ - F-)/(2 eps) and the update formed on
+    the device (Algorithm 1).  The oracle runs the same 100 steps from its own losses;
+    losses, mask sizes and latents agree bit for bit."""
+    torch = _torch()
+    shapes = [(256, 256)]
+    ref, ctx, tensors = _setup(orc, shapes, bf16=False, seed=0)
+    x = synth.activations(100, 8, 256)
+    tgt = synth.activations(101, 8, 256)
+    xd = torch.from_numpy(x).cuda()
+    td = torch.from_numpy(tgt).cuda()
+    y = torch.empty((8, 256), device="cuda")
+    Fd = torch.zeros(2, device="cuda")
+    eps, lr = 1e-3, 1e-4
+    assert ctx.build_mask(0.01) == ref.build_mask(0.01)
+    xq, s = orc.act_quant(x)
+    losses = []
+    for t in range(100):
+        rf = {}
+        for j, sign in enumerate((1, -1)):
+            ctx.perturb(t, eps, sign)
+            ctx.bitlinear_forward(0, xd, y)
+            ctx.mse_loss_dev(y, td, Fd[j: j + 1])
+            codes, _, betas = ref.perturb(t, eps, sign)
+            _, ry = orc.bitlinear(xq, s, codes[0], betas[0], want_acc=False)
+            rf[sign] = orc.mse(ry, tgt)
+        ctx.update_from_losses(Fd[0:1], Fd[1:2], eps, lr)
+        losses.append(Fd.cpu().numpy().copy())
+        ref.update(orc.projected_grad(rf[1], rf[-1], eps), lr)
+        assert losses[-1].tolist() == [rf[1], rf[-1]], f"step {t}"
+        if t % 25 == 0:
+            assert ctx.active_count() == ref.k
+    assert np.array_equal(_latents_host(tensors), ref.w)
+    _check_mask(ref, ctx)
+
+
 def test_state_and_numeric_errors(orc):
     torch = _torch()
     from paper_2609_33548_amd import termezo as T

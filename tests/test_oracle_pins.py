@@ -810,3 +810,24 @@ def test_eq_memory_reproduces_the_memory_table(orc):
     d = 1.0e9
     assert orc.eq_memory(5e9, d, 1.0, mask="bitmask") == 5e9 + d * 0.25 + d / 8
     assert orc.eq_memory(5e9, d, 0.0, mask="bitmask") == 5e9 - d * 1.75 + d / 8
+
+
+def test_openmp_build_gives_identical_results(orc):
+    """The oracle's OpenMP build (used only to time it on all host cores) computes
+    exactly what the plain build computes: a dense-mask step, bf16 storage."""
+    w = synth.latents(13, [96 * 64, 64 * 96], bf16=True)
+    out = []
+    for n in (1, 4):
+        orc.use_threads(n)
+        try:
+            st = orc.TerMeZOOracle([orc.Layer(96, 64), orc.Layer(64, 96)], w, bf16=True)
+            st.build_mask(1.0)
+            codes, taus, betas = st.perturb(3, 1e-3, -1)
+            k = st.update(12.5, 1e-3)
+            out.append((codes, taus, betas, k, st.w.copy(), [a.copy() for a in st.active]))
+        finally:
+            orc.use_threads(1)
+    (c1, t1, b1, k1, w1, a1), (c2, t2, b2, k2, w2, a2) = out
+    assert all(np.array_equal(x, y) for x, y in zip(c1, c2))
+    assert t1 == t2 and b1 == b2 and k1 == k2 and np.array_equal(w1, w2)
+    assert all(np.array_equal(x, y) for x, y in zip(a1, a2))
