@@ -147,6 +147,24 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* ctx, int32_t layer,
                                          int8_t* xq_out, float* xscale_out,
                                          int32_t* acc_out);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same BitLinear
+ * forward as termezo_bitlinear_forward (same kernels, same results) without the
+ * inspection outputs, whose activation-quantisation scratch (int8 x_q and the
+ * per-token scales) lives in a fixed 16 MiB device array inside the library
+ * instead of context buffers grown on demand.  The call allocates nothing.
+ * Limit: M * d_in bytes rounded up to 256, plus 4 * M, at most 16 MiB (for
+ * example M <= 6543 at d_in = 2560, M <= 2425 at d_in = 6912).  Each GPU holds
+ * one copy of the array, shared by every context and call on that GPU: calls
+ * whose work overlaps on one GPU (different streams, or different host
+ * threads) race on it; calls ordered on one stream do not.  Nothing in the
+ * array needs to start at zero.  Errors: as termezo_bitlinear_forward, and
+ * INVALID_ARG when M exceeds the limit; DEVICE if the array's address could
+ * not be obtained at context creation. */
+termezo_status termezo_bitlinear_forward_noalloc(termezo_ctx* ctx, int32_t layer, const void* x,
+                                                 termezo_dtype x_dtype, int64_t M, void* y,
+                                                 termezo_dtype y_dtype);
+
 /* Masked projected-gradient update (Algorithm 1, last loop, K = 1) followed by
  * the shrink-only set update (eq. selection_).  With the seed of the last
  * termezo_perturb: for every active i, w_i <- round(fma(-(lr * g), z_i, w_i))

@@ -170,6 +170,7 @@ struct termezo_ctx {
   double* d_loss = nullptr;                  // loss accumulators
   float* d_scal = nullptr;                   // [0] update coefficient a, [1] g
   int n_cu = 0;                              // compute units of the device
+  void* noalloc_scratch = nullptr;           // this device's address of the file-scope scratch
   int8_t* d_xq = nullptr;                    // activation-quantisation scratch
   int64_t xq_cap = 0;
   float* d_xs = nullptr;

@@ -1,6 +1,7 @@
 // C ABI of the TerMeZO library: validation, buffer ownership, launch order.
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -8,7 +9,33 @@
 
 using namespace tmz;
 
+// Scratch of termezo_bitlinear_forward_noalloc: the int8 activations [M][d_in] of one
+// call, then (at the next 256-byte boundary) its per-token scales [M].  Each device
+// holds its own copy until the process ends.  In host code the name is only a
+// host-side stand-in: the device address comes from hipGetSymbolAddress, taken once
+// per device at context creation.
+constexpr int64_t kNoAllocScratchBytes = int64_t(16) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device`, which must be the current device.
+hipError_t noalloc_scratch_address(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[device] = p;
+  }
+  *out = g_scratch_addr[device];
+  return hipSuccess;
+}
 
 termezo_status fail(termezo_ctx* c, termezo_status st, const std::string& msg) {
   if (c) c->last_error = msg;
@@ -260,6 +287,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   chk(dalloc(&c->d_need, n_layers), "alloc");
   chk(dalloc(&c->d_dense_off, (size_t)n_layers + 1), "alloc");
   chk(dalloc(&c->d_err, 1), "alloc");
+  chk(noalloc_scratch_address(c->device, &c->noalloc_scratch), "hipGetSymbolAddress(scratch)");
   chk(dalloc(&c->d_act_off, (size_t)n_layers + 1), "alloc");
   chk(dalloc(&c->d_act_off_tmp, (size_t)n_layers + 1), "alloc");
   chk(dalloc(&c->d_hist, kHistBins), "alloc");
@@ -430,11 +458,10 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
   return TERMEZO_OK;
 }
 
-termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const void* x,
-                                         termezo_dtype x_dtype, int64_t M, void* y,
-                                         termezo_dtype y_dtype, int8_t* xq_out, float* xscale_out,
-                                         int32_t* acc_out) {
-  if (!c) return TERMEZO_ERR_INVALID_ARG;
+namespace {
+termezo_status check_forward_args(termezo_ctx* c, int32_t layer, const void* x,
+                                  termezo_dtype x_dtype, int64_t M, const void* y,
+                                  termezo_dtype y_dtype) {
   if (layer < 0 || layer >= c->L) return fail(c, TERMEZO_ERR_INVALID_ARG, "layer out of range");
   if (M <= 0 || !x || !y) return fail(c, TERMEZO_ERR_INVALID_ARG, "M <= 0 or null x / y");
   if ((x_dtype != TERMEZO_F32 && x_dtype != TERMEZO_BF16) ||
@@ -442,9 +469,20 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
     return fail(c, TERMEZO_ERR_INVALID_ARG, "x and y must be F32 or BF16");
   if ((reinterpret_cast<uintptr_t>(x) & 15u) != 0)
     return fail(c, TERMEZO_ERR_INVALID_ARG, "x must be 16-byte aligned");
+  if (!c->codes_valid) return fail(c, TERMEZO_ERR_STATE, "no current codes (perturb first)");
+  return TERMEZO_OK;
+}
+}  // namespace
+
+termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const void* x,
+                                         termezo_dtype x_dtype, int64_t M, void* y,
+                                         termezo_dtype y_dtype, int8_t* xq_out, float* xscale_out,
+                                         int32_t* acc_out) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
   if (xq_out && (reinterpret_cast<uintptr_t>(xq_out) & 15u) != 0)
     return fail(c, TERMEZO_ERR_INVALID_ARG, "xq_out must be 16-byte aligned");
-  if (!c->codes_valid) return fail(c, TERMEZO_ERR_STATE, "no current codes (perturb first)");
+  const termezo_status ck = check_forward_args(c, layer, x, x_dtype, M, y, y_dtype);
+  if (ck != TERMEZO_OK) return ck;
   const LayerHost& L = c->layers[layer];
   int8_t* xq = xq_out;
   float* xs = xscale_out;
@@ -457,6 +495,28 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
   TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->stream));
   TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
                                    L.d_in, L.d_out, y, y_dtype, acc_out, c->n_cu, c->stream));
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_bitlinear_forward_noalloc(termezo_ctx* c, int32_t layer, const void* x,
+                                                 termezo_dtype x_dtype, int64_t M, void* y,
+                                                 termezo_dtype y_dtype) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  const termezo_status ck = check_forward_args(c, layer, x, x_dtype, M, y, y_dtype);
+  if (ck != TERMEZO_OK) return ck;
+  const LayerHost& L = c->layers[layer];
+  // int8 activations, then the scales at the next 256-byte boundary
+  const int64_t xq_bytes = M <= kNoAllocScratchBytes ? ((M * L.d_in + 255) / 256) * 256 : -1;
+  if (xq_bytes < 0 || xq_bytes + 4 * M > kNoAllocScratchBytes)
+    return fail(c, TERMEZO_ERR_INVALID_ARG,
+                "bitlinear_forward_noalloc: M * d_in + 4 M bytes (256-aligned) exceed the "
+                "16 MiB scratch");
+  if (!c->noalloc_scratch) return fail(c, TERMEZO_ERR_DEVICE, "no scratch address");
+  int8_t* xq = static_cast<int8_t*>(c->noalloc_scratch);
+  float* xs = reinterpret_cast<float*>(static_cast<char*>(c->noalloc_scratch) + xq_bytes);
+  TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->stream));
+  TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
+                                   L.d_in, L.d_out, y, y_dtype, nullptr, c->n_cu, c->stream));
   return TERMEZO_OK;
 }
 

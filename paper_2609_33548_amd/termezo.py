@@ -67,6 +67,7 @@ _SIGS = {
                             ctypes.POINTER(_i64), ctypes.POINTER(_f32), ctypes.POINTER(_f32)],
     "termezo_mse_loss": [_P, _P, _P, _i64, ctypes.POINTER(_f32)],
     "termezo_mse_loss_dev": [_P, _P, _P, _i64, _P],
+    "termezo_bitlinear_forward_noalloc": [_P, _i32, _P, _i32, _i64, _P, _i32],
     "termezo_active_count": [_P, ctypes.POINTER(_i64)],
     "termezo_gauss": [_P, _u64, _P, _i64, _P],
     "termezo_update_from_losses": [_P, _P, _P, _f32, _f32],
@@ -204,6 +205,13 @@ class Context:
         self._check(_lib.termezo_bitlinear_forward(
             self.handle, layer, _ptr(x), _dtype_code(x), M, _ptr(y), _dtype_code(y),
             _ptr(xq_out), _ptr(xscale_out), _ptr(acc_out)), "bitlinear_forward")
+
+    def bitlinear_forward_noalloc(self, layer: int, x, y):
+        """BitLinear forward whose quantisation scratch is the library's fixed device
+        array (no allocation; M * d_in + 4 M bytes must fit 16 MiB)."""
+        self._check(_lib.termezo_bitlinear_forward_noalloc(
+            self.handle, layer, _ptr(x), _dtype_code(x), x.shape[0], _ptr(y), _dtype_code(y)),
+            "bitlinear_forward_noalloc")
 
     def update(self, proj_grad: float, lr: float, want_k: bool = True) -> Optional[int]:
         k = _i64()
