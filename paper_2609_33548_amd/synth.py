@@ -16,10 +16,14 @@ LATENT_STD = 0.02
 
 
 def to_bf16_values(x: np.ndarray) -> np.ndarray:
-    """Round fp32 values to the nearest bfloat16 (ties to even), kept as fp32."""
-    b = np.ascontiguousarray(x, np.float32).view(np.uint32).astype(np.uint64)
-    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
-    return b.astype(np.uint32).view(np.float32)
+    """Round finite fp32 values to the nearest bfloat16 (ties to even), kept as fp32.
+    (In 32-bit unsigned arithmetic: a finite value's bits plus 0x8000 stay below 2^32.)"""
+    b = np.array(x, dtype=np.float32, copy=True, order="C").view(np.uint32)
+    lsb = (b >> np.uint32(16)) & np.uint32(1)
+    b += np.uint32(0x7FFF)
+    b += lsb
+    b &= np.uint32(0xFFFF0000)
+    return b.view(np.float32)
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
