@@ -329,27 +329,40 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 // ---------------------------------------------------------------------------
 // Full-tile GEMM with direct global -> LDS loads (global_load_lds_dwordx4:
 // lane i of a wave writes its 16 bytes at the wave's LDS base + 16 i, no VGPRs)
-// and a 3-stage LDS ring, so step k+2 is in flight while step k is computed.
-//   A stage: BM rows x 128 bytes, 16-byte chunk c of row r stored at chunk
-//            c ^ ((r >> 1) & 7).
-//   B stage: BN rows x 32 bytes of packed 2-bit codes, 16-byte half h of
-//            row r stored at half h ^ bit2(r) ^ bit3(r).
+// into a ring of NST stages of BK = 128 or 256 K values each; the loads of
+// step k + NST - 1 are issued as step k starts, so they have NST - 1 steps of
+// compute to land, and one barrier per step publishes them.
+//   A stage: BM rows x BK bytes; 16-byte chunk c of row r stored at chunk
+//            c ^ swz(r) (128: (r >> 1) & 7; 256: r & 15).
+//   B stage: BN rows x BK / 4 bytes of packed 2-bit codes; 16-byte unit u of
+//            row r stored at unit u ^ bswz(r) (128: bit 2 ^ bit 3 of r;
+//            256: (r >> 2) & 3).
 // The swizzles keep the 16-byte fragment reads of 8 or 16 consecutive rows on
 // distinct banks.  8 waves as 2 x 4, WM x WN per wave,
 // v_mfma_i32_32x32x32_i8 with the codes as the first operand, so the
 // accumulator tile is Y^T (lane column = token).
-// K assignment: in sub-step ks (32 wide) of a K step, lane l supplies the 16
-// values at k = 16 (4 (l / 32) + ks) for both operands, so one 16-byte read
-// gives a lane the codes of all four sub-steps.  The codes of sub-step ks+1
-// are unpacked between the MFMAs of sub-step ks.
+// K assignment: in sub-step ks (32 wide) of a K step of KS = BK / 32 sub-steps,
+// lane l supplies the 16 values at k = 16 (KS (l / 32) + ks) for both operands,
+// so one 16-byte read gives a lane the codes of four sub-steps.  The codes of sub-step ks+1 are
+// unpacked between the MFMAs of sub-step ks.  The per-token output scales
+// beta' / s_m are formed in the epilogue from s_m loaded into registers at the
+// start.
 //
 // Tiles are 256 x 256 (128 x 64 per wave).  When the last round of tiles
 // would fill at most half of the compute units, its tiles are instead cut
 // into four 128 x 128 tiles (64 x 32 per wave), so the tail takes about a
-// quarter of a round instead of a whole one.
-// Requires M % 256 == 0, N % 256 == 0, K % 128 == 0.
+// quarter of a round instead of a whole one.  K step 256 (two stages of 80 KB,
+// the whole LDS) when K allows, else 128 (three stages).
+// Requires M % 256 == 0, N % 256 == 0, K % BK == 0.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int bswz(int row) { return ((row >> 2) ^ (row >> 3)) & 1; }
+template <int BK>
+__device__ __forceinline__ int aswz(int row) {
+  return BK == 256 ? (row & 15) : ((row >> 1) & 7);
+}
+template <int BK>
+__device__ __forceinline__ int bswz(int row) {
+  return BK == 256 ? ((row >> 2) & 3) : (((row >> 2) ^ (row >> 3)) & 1);
+}
 
 __device__ __forceinline__ v4i unpack16(uint32_t w) {
   uint32_t o[4];
@@ -358,49 +371,54 @@ __device__ __forceinline__ v4i unpack16(uint32_t w) {
 }
 
 constexpr int kDmaBM = 256, kDmaBN = 256;
-constexpr int kDmaLds = 3 * (kDmaBM * 128 + kDmaBN * 32);
+template <int BK, int NST>
+constexpr int dma_lds_bytes(int BM, int BN) { return NST * (BM * BK + BN * BK / 4); }
 
-template <int BM, int BN, int WM, int WN, typename TY, int MODE>
+template <int BM, int BN, int WM, int WN, typename TY, int MODE, int BK, int NST>
 __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
                                               const uint32_t* __restrict__ codes, int64_t K,
                                               int64_t N, const GemmOut& out, int32_t* acc_out,
                                               int64_t m0, int64_t n0, int8_t* lds,
-                                              const float* __restrict__ s, int rows,
-                                              float (*rrow)[kDmaBM]) {
+                                              const float* __restrict__ s) {
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int AROW = 128;                       // bytes per A row per stage (no pad)
-  constexpr int BROW = 32;                        // bytes of packed codes per B row per stage
+  constexpr int AROW = BK;                        // bytes per A row per stage (no pad)
+  constexpr int BROW = BK / 4;                    // bytes of packed codes per B row per stage
+  constexpr int ACH = BK / 16;                    // 16-byte chunks per A row
+  constexpr int BU = BROW / 16;                   // 16-byte units per B row
   constexpr int ASTAGE = BM * AROW, BSTAGE = BN * BROW;
-  constexpr int KS = kBK / 32;                    // MFMA sub-steps per K step
+  constexpr int KS = BK / 32;                     // MFMA sub-steps per K step
+  constexpr int HK = KS / 4;                      // 16-byte code reads per lane per fragment
   constexpr int NW = (BM / WM) * (BN / WN);       // waves per block
-  constexpr int AJ = BM / (8 * NW);               // A loads per wave per stage
-  constexpr int BW = BN / 32 < NW ? BN / 32 : NW; // waves holding distinct B rows
-  constexpr int BJ = BN / 32 > NW ? BN / (32 * NW) : 1;   // B loads per wave per stage
+  constexpr int ARPI = 1024 / AROW;               // A rows per 1 KB load instruction
+  constexpr int BRPI = 1024 / BROW;               // B rows per 1 KB load instruction
+  constexpr int AJ = BM / (ARPI * NW);            // A loads per wave per stage
+  constexpr int BW = BN / BRPI < NW ? BN / BRPI : NW;      // waves holding distinct B rows
+  constexpr int BJ = BN / BRPI > NW ? BN / (BRPI * NW) : 1;  // B loads per wave per stage
   constexpr int DJ = AJ + BJ;                     // direct loads per wave per stage
-  static_assert(AJ >= 1 && BM % (8 * NW) == 0 && (BN / 32 <= NW || BN % (32 * NW) == 0) &&
-                    DJ < 16, "tile");
+  static_assert(AJ >= 1 && BM % (ARPI * NW) == 0 && (BN / BRPI <= NW || BN % (BRPI * NW) == 0) &&
+                    DJ * (NST - 1) < 64 && (BK == 128 || BK == 256), "tile");
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
   const int64_t KW = K / 16;
-  const int nk = (int)(K / kBK);
+  const int nk = (int)(K / BK);
 
   // Per-lane global sources.  A: wave w fills 1 KB chunks AJ w .. AJ w + AJ-1
-  // (8 rows each); lane i -> row 8 j + i / 8, physical chunk i % 8.  B: wave
-  // w fills the 32-row blocks BJ (w % BW) .. + BJ-1, two lanes (physical halves)
-  // per row (with BW < NW several waves write the same bytes).
+  // (ARPI rows each); lane i -> row ARPI j + i / ACH, physical chunk i % ACH.
+  // B: wave w fills the BRPI-row blocks BJ (w % BW) .. + BJ-1, BU lanes
+  // (physical units) per row (with BW < NW several waves write the same bytes).
   const int8_t* asrc[AJ];
 #pragma unroll
   for (int j = 0; j < AJ; ++j) {
-    const int row = 8 * (AJ * wid + j) + (lane >> 3);
-    const int chunk = (lane & 7) ^ ((row >> 1) & 7);
+    const int row = ARPI * (AJ * wid + j) + lane / ACH;
+    const int chunk = (lane % ACH) ^ aswz<BK>(row);
     asrc[j] = xq + (m0 + row) * K + 16 * chunk;
   }
   const int bw = wid % BW;
   const uint32_t* bsrc[BJ];
 #pragma unroll
   for (int j = 0; j < BJ; ++j) {
-    const int brow_l = 32 * (BJ * bw + j) + (lane >> 1);
+    const int brow_l = BRPI * (BJ * bw + j) + lane / BU;
     int64_t crow = n0 + brow_l;                   // code row of tile row brow_l
     if constexpr (MODE == kGemmSwiGLU) {
       // column 32 p + c holds gate row 16 p + c (c < 16) or up row F + 16 p + c - 16, so a
@@ -408,13 +426,21 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
       const int64_t p = crow >> 5, c = crow & 31;
       crow = c < 16 ? 16 * p + c : (N >> 1) + 16 * p + (c - 16);
     }
-    bsrc[j] = codes + crow * KW + 4 * ((lane & 1) ^ bswz(brow_l));
+    bsrc[j] = codes + crow * KW + 4 * ((lane % BU) ^ bswz<BK>(brow_l));
   }
+
+  // per-token input scales of this lane's tokens and the segments' beta', for the epilogue
+  const int ml = lane & 31;                          // token of the lane (h: register half)
+  float sreg[TM], bet[kMaxSeg];
+#pragma unroll
+  for (int a = 0; a < TM; ++a) sreg[a] = s[m0 + wm * WM + 32 * a + ml];
+#pragma unroll
+  for (int sg = 0; sg < kMaxSeg; ++sg) bet[sg] = sg < out.nseg ? *out.beta[sg] : 0.0f;
 
   const uint32_t wa = __builtin_amdgcn_readfirstlane(wid);   // wave-uniform
   const uint32_t wb = __builtin_amdgcn_readfirstlane(bw);
   auto issue = [&](int kt, int8_t* Ad, uint32_t* Bd) __attribute__((always_inline)) {
-    const int64_t koff = (int64_t)kt * kBK;
+    const int64_t koff = (int64_t)kt * BK;
     const uint32_t abase = lds_offset(Ad) + 1024u * AJ * wa;
 #pragma unroll
     for (int j = 0; j < AJ; ++j) dma16(asrc[j] + koff, abase + 1024u * j);
@@ -436,30 +462,33 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   const int brow0 = wn * WN + (lane & 31);
   auto compute = [&](const int8_t* As, const uint32_t* Bs) __attribute__((always_inline)) {
     v4i af[2][TM];
-    v4i bq[TN], bfc[TN], bfn[TN];
+    v4i bq[HK][TN], bfc[TN], bfn[TN];
 #pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      const int row = brow0 + 32 * b;
-      bq[b] = *reinterpret_cast<const v4i*>(Bs + row * (BROW / 4) + 4 * (h ^ bswz(row)));
-    }
+    for (int q = 0; q < HK; ++q)
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int row = brow0 + 32 * b;
+        bq[q][b] = *reinterpret_cast<const v4i*>(Bs + row * (BROW / 4) +
+                                                 4 * ((HK * h + q) ^ bswz<BK>(row)));
+      }
     auto afrag = [&](int ks, int slot) __attribute__((always_inline)) {
-      const int c = 4 * h + ks;                      // logical 16-byte chunk
+      const int c = (ACH / 2) * h + ks;              // logical 16-byte chunk
 #pragma unroll
       for (int a = 0; a < TM; ++a) {
         const int row = arow0 + 32 * a;
-        af[slot][a] = *reinterpret_cast<const v4i*>(As + row * AROW + 16 * (c ^ ((row >> 1) & 7)));
+        af[slot][a] = *reinterpret_cast<const v4i*>(As + row * AROW + 16 * (c ^ aswz<BK>(row)));
       }
     };
     afrag(0, 0);
 #pragma unroll
-    for (int b = 0; b < TN; ++b) bfc[b] = unpack16((uint32_t)bq[b][0]);
+    for (int b = 0; b < TN; ++b) bfc[b] = unpack16((uint32_t)bq[0][b][0]);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1;
       if (ks + 1 < KS) {
         afrag(ks + 1, cur ^ 1);
 #pragma unroll
-        for (int b = 0; b < TN; ++b) bfn[b] = unpack16((uint32_t)bq[b][ks + 1]);
+        for (int b = 0; b < TN; ++b) bfn[b] = unpack16((uint32_t)bq[(ks + 1) / 4][b][(ks + 1) % 4]);
       }
 #pragma unroll
       for (int a = 0; a < TM; ++a)
@@ -481,26 +510,22 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   };
 
   auto Ast = [&](int st) { return lds + st * ASTAGE; };
-  auto Bst = [&](int st) { return reinterpret_cast<uint32_t*>(lds + 3 * ASTAGE + st * BSTAGE); };
-  // prologue: stages 0 and 1 in flight, stage 0 complete before the loop
-  issue(0, Ast(0), Bst(0));
-  if (nk > 1) issue(1, Ast(1), Bst(1));
-  // per-token output scales beta'/s_m while the first stages load (published to
-  // all waves by the loop's barriers)
-  for (int i = tid; i < kMaxSeg * kDmaBM; i += NW * 64) {
-    const int sg = i / kDmaBM, r = i % kDmaBM;
-    rrow[sg][r] = (sg < out.nseg && r < rows) ? __fdiv_rn(*out.beta[sg], s[m0 + r]) : 0.0f;
-  }
-  if (nk > 1) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
+  auto Bst = [&](int st) { return reinterpret_cast<uint32_t*>(lds + NST * ASTAGE + st * BSTAGE); };
+  // prologue: stages 0 .. NST-2 in flight, stage 0 complete before the loop
+#pragma unroll
+  for (int p = 0; p < NST - 1; ++p)
+    if (p < nk) issue(p, Ast(p), Bst(p));
+  if (NST == 3 && nk > 1) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int cur = 0;
   for (int kt = 0; kt < nk; ++kt) {
-    const int nxt2 = cur == 0 ? 2 : cur - 1;     // (kt + 2) % 3
-    if (kt + 2 < nk) issue(kt + 2, Ast(nxt2), Bst(nxt2));
+    const int nxt = cur == 0 ? NST - 1 : cur - 1;     // (kt + NST - 1) % NST
+    if (kt + NST - 1 < nk) issue(kt + NST - 1, Ast(nxt), Bst(nxt));
     compute(Ast(cur), Bst(cur));
-    if (kt + 2 < nk) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
+    // the loads of step kt + 1 have landed (NST = 3: those of kt + 2 may still be in flight)
+    if (NST == 3 && kt + 2 < nk) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    cur = cur == 2 ? 0 : cur + 1;
+    cur = cur == NST - 1 ? 0 : cur + 1;
   }
 
   // ---- epilogue.  Each wave stages one 32-token slice (MFMA row tile a) of its
@@ -509,13 +534,13 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   // 64 / UPR tokens of UPR * 16 contiguous bytes each instead of 32 tokens of 8
   // bytes.  Unit u of staged row r sits at unit u ^ (r % UPR).  The LDS writes
   // and reads of one wave need no barrier: a wave's LDS operations are ordered.
-  const int ml = lane & 31;                          // token of the lane (h: register half)
   constexpr int OW = MODE == kGemmSwiGLU ? WN / 2 : WN;   // outputs per staged row
   constexpr int UB = 16 / (int)sizeof(TY);                // outputs per 16-byte unit
   constexpr int UPR = OW / UB;                            // units per staged row
   constexpr int RB = OW * (int)sizeof(TY);                // bytes per staged row
   constexpr int RPL = 32 * UPR / 64;                      // units read per lane
-  static_assert(NW * 32 * RB <= 3 * (ASTAGE + BSTAGE) && RPL >= 1 && UPR <= 16, "epilogue staging");
+  static_assert(NW * 32 * RB <= NST * (ASTAGE + BSTAGE) && RPL >= 1 && UPR <= 16,
+                "epilogue staging");
   int8_t* wl = lds + wid * 32 * RB;
   auto stage4 = [&](int f, const float v[4]) __attribute__((always_inline)) {
     // four consecutive outputs f..f+3 of staged row ml
@@ -556,7 +581,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     if constexpr (MODE == kGemmSwiGLU) {
       // registers 0..7 of a 32-column block p are gate features 16 p + 8 (r / 4) + 4 h + r % 4,
       // registers 8..15 the up values of the same features
-      const float rg = rrow[0][mloc], ru = rrow[1][mloc];
+      const float rg = __fdiv_rn(bet[0], sreg[a]), ru = __fdiv_rn(bet[1], sreg[a]);
 #pragma unroll
       for (int b = 0; b < TN; ++b)
 #pragma unroll
@@ -577,7 +602,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
       for (int b = 0; b < TN; ++b) {
         const int64_t nb = n0 + wn * WN + b * 32;
         const int sg = (out.nseg > 2 && nb >= out.nstart[2]) ? 2 : (out.nseg > 1 && nb >= out.nstart[1]) ? 1 : 0;
-        const float rr = rrow[sg][mloc];
+        const float rr = __fdiv_rn(bet[sg], sreg[a]);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           float v4[4];
@@ -611,13 +636,13 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
 // Blocks [0, full) take 256 x 256 tiles [0, full) of the grouped order (XCD
 // aware); the following blocks take the four 128 x 128 quarters of each tile
 // in [full, T).
-template <typename TY, int MODE>
+template <typename TY, int MODE, int BK>
 __global__ void __launch_bounds__(512)
     k_gemm_i8_dma(const int8_t* __restrict__ xq, const float* __restrict__ s,
                   const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
                   int64_t full, int32_t* __restrict__ acc_out) {
-  __shared__ __attribute__((aligned(1024))) int8_t lds[kDmaLds];
-  __shared__ float rrow[kMaxSeg][kDmaBM];
+  constexpr int NST = BK == 256 ? 2 : 3;
+  __shared__ __attribute__((aligned(1024))) int8_t lds[dma_lds_bytes<BK, NST>(kDmaBM, kDmaBN)];
   const int64_t nb_m = M / kDmaBM, nb_n = N / kDmaBN;
   const bool quarter = (int64_t)blockIdx.x >= full;
   int64_t t, tm, tn;
@@ -633,9 +658,9 @@ __global__ void __launch_bounds__(512)
   const int64_t m0 = tm * kDmaBM + (quarter ? 128 * (q >> 1) : 0);
   const int64_t n0 = tn * kDmaBN + (quarter ? 128 * (q & 1) : 0);
   if (!quarter)
-    gemm_tile_dma<256, 256, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, s, 256, rrow);
+    gemm_tile_dma<256, 256, 128, 64, TY, MODE, BK, NST>(xq, codes, K, N, out, acc_out, m0, n0, lds, s);
   else
-    gemm_tile_dma<128, 128, 64, 32, TY, MODE>(xq, codes, K, N, out, acc_out, m0, n0, lds, s, 128, rrow);
+    gemm_tile_dma<128, 128, 64, 32, TY, MODE, BK, NST>(xq, codes, K, N, out, acc_out, m0, n0, lds, s);
 }
 
 // Two blocks per compute unit: 128 x 256 tiles of 4 waves (128 x 64 per wave, the
@@ -643,19 +668,17 @@ __global__ void __launch_bounds__(512)
 // block's barriers, prologue and epilogue overlap the other block's MFMAs and a
 // block left alone on a compute unit at the end of the grid runs at its full rate.
 constexpr int kHalfBM = 128, kHalfBN = 256;
-constexpr int kHalfLds = 3 * (kHalfBM * 128 + kHalfBN * 32);
 
 template <typename TY, int MODE>
 __global__ void __launch_bounds__(256, 2)
     k_gemm_i8_dma_h(const int8_t* __restrict__ xq, const float* __restrict__ s,
                     const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
                     int32_t* __restrict__ acc_out) {
-  __shared__ __attribute__((aligned(1024))) int8_t lds[kHalfLds];
-  __shared__ float rrow[kMaxSeg][kDmaBM];
+  __shared__ __attribute__((aligned(1024))) int8_t lds[dma_lds_bytes<128, 3>(kHalfBM, kHalfBN)];
   int64_t tm, tn;
   tile_of_block(M / kHalfBM, N / kHalfBN, tm, tn);
-  gemm_tile_dma<kHalfBM, kHalfBN, 128, 64, TY, MODE>(xq, codes, K, N, out, acc_out, tm * kHalfBM,
-                                                     tn * kHalfBN, lds, s, kHalfBM, rrow);
+  gemm_tile_dma<kHalfBM, kHalfBN, 128, 64, TY, MODE, 128, 3>(xq, codes, K, N, out, acc_out,
+                                                             tm * kHalfBM, tn * kHalfBN, lds, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -880,9 +903,14 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
     if (use_half_tiles(M, T, n_cu))
       hipLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)(2 * T)), dim3(256),
                          0, st, xq, s, codes, M, K, N, out, acc);
+    else if (K % 256 == 0)
+      hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU, 256>),
+                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, codes, M, K,
+                         N, out, full, acc);
     else
-      hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU>), dim3((unsigned)(full + 4 * (T - full))),
-                         dim3(512), 0, st, xq, s, codes, M, K, N, out, full, acc);
+      hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU, 128>),
+                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, codes, M, K,
+                         N, out, full, acc);
     return hipGetLastError();
   }
   if (M <= kGemvMaxM) {
@@ -935,21 +963,19 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
       // fewer full tiles than compute units: every tile as four 128 x 128 quarters
       const int64_t full = T < n_cu ? 0 : dma_full_tiles(T, n_cu);
       dim3 grid((unsigned)(full + 4 * (T - full)));
+#define TMZ_DMA(TY, MD, BK) \
+  hipLaunchKernelGGL((k_gemm_i8_dma<TY, MD, BK>), grid, dim3(512), 0, st, xq, s, codes, M, K, N, out, full, acc)
+#define TMZ_DMA_K(TY, MD) \
+  do {                                                 \
+    if (K % 256 == 0) TMZ_DMA(TY, MD, 256); else TMZ_DMA(TY, MD, 128); \
+  } while (0)
       if (ydt == TERMEZO_F32) {
-        if (mode == kGemmStore)
-          hipLaunchKernelGGL((k_gemm_i8_dma<float, kGemmStore>), grid, dim3(512), 0, st, xq, s, codes,
-                             M, K, N, out, full, acc);
-        else
-          hipLaunchKernelGGL((k_gemm_i8_dma<float, kGemmResidual>), grid, dim3(512), 0, st, xq, s,
-                             codes, M, K, N, out, full, acc);
+        if (mode == kGemmStore) TMZ_DMA_K(float, kGemmStore); else TMZ_DMA_K(float, kGemmResidual);
       } else {
-        if (mode == kGemmStore)
-          hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmStore>), grid, dim3(512), 0, st, xq, s,
-                             codes, M, K, N, out, full, acc);
-        else
-          hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmResidual>), grid, dim3(512), 0, st, xq, s,
-                             codes, M, K, N, out, full, acc);
+        if (mode == kGemmStore) TMZ_DMA_K(uint16_t, kGemmStore); else TMZ_DMA_K(uint16_t, kGemmResidual);
       }
+#undef TMZ_DMA_K
+#undef TMZ_DMA
       return hipGetLastError();
     }
     return launch_tile<256, 256, 128, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);

@@ -118,7 +118,12 @@ def test_perturb_codes_match_oracle(orc, shapes, bf16, rho0):
                                    # small-M kernel: ragged features, K not a multiple of 64,
                                    # a partial token group, the largest token count, K = 16
                                    (1, 2560, 6912), (17, 688, 100), (128, 6912, 2560),
-                                   (3, 16, 48), (100, 256, 200)])
+                                   (3, 16, 48), (100, 256, 200),
+                                   # more decode-sized shapes: the largest projection K at 16
+                                   # tokens, a long K on few features, K not a multiple of 64,
+                                   # features not a multiple of 4
+                                   (16, 6912, 2560), (1, 7168, 64), (5, 688, 100), (1, 256, 37),
+                                   (2, 7184, 48)])
 @pytest.mark.parametrize("xdt,ydt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
 def test_bitlinear_matches_oracle(orc, M, K, N, xdt, ydt):
     torch = _torch()
