@@ -178,7 +178,8 @@ def two_legs(fn, st_kw, mt_kw):
     st = run_leg(1, fn, **st_kw)
     mt = run_leg(n, fn, **mt_kw)
     log(f"cpu baseline ({fn.__name__}) took {time.perf_counter() - t0:.1f} s")
-    return combine_legs(st, mt, n), st, mt
+    combined = combine_legs(st, mt, n) if "value" in st else None   # nested results: caller combines
+    return combined, st, mt
 
 
 _INPUTS = {}

@@ -1025,6 +1025,9 @@ __global__ void __launch_bounds__(256) k_lmhead_f32(const float* x, const float*
 constexpr int kLmBK = 64;                  // bf16 elements per K step
 constexpr int kLmStride = 2 * kLmBK + 16;  // bytes per LDS row
 constexpr int kLmTile = 256;               // rows and vocab columns per block
+// direct-load LM head: ring stages, stage width, waves along N (8 waves of 128 x 64; four
+// waves of 128 x 128 measured 17% slower at the 2B shape)
+constexpr int kLmDmaStages = 2, kLmDmaBK = 64, kLmDmaNWN = 4;
 
 template <bool FULL>
 __global__ void __launch_bounds__(512) k_lmhead_bf16(const uint16_t* __restrict__ x,
@@ -1174,8 +1177,8 @@ __global__ void __launch_bounds__(512) k_lmhead_bf16(const uint16_t* __restrict_
 }
 
 // LM head + cross-entropy partials on full tiles with direct global -> LDS
-// loads: 256 tokens x 256 vocabulary columns per block, 8 waves as 2 x 4
-// (128 tokens x 64 columns per wave), v_mfma_f32_32x32x16_bf16 with the
+// loads: 256 tokens x 256 vocabulary columns per block, 2 x NWN waves of 128
+// tokens x 256 / NWN columns each, v_mfma_f32_32x32x16_bf16 with the
 // embedding rows as the first operand, so the accumulator is the transpose
 // of the logits: a lane owns one token and 16 of its columns per 32 x 32
 // tile, and a token's max and sum of exp over the block's columns reduce in
@@ -1186,19 +1189,19 @@ __global__ void __launch_bounds__(512) k_lmhead_bf16(const uint16_t* __restrict_
 // banks.  K assignment: in sub-step ks, lane half h supplies chunk
 // h * (2 BK / 32) + ks of its row for both operands.
 // Requires M % 256 == 0, V % 256 == 0, d % BK == 0.
-template <int STAGES, int BK>
-__global__ void __launch_bounds__(512) k_lmhead_dma(const uint16_t* __restrict__ x,
-                                                    const uint16_t* __restrict__ E, int64_t M,
-                                                    int64_t d, int64_t V,
-                                                    const int32_t* __restrict__ labels,
-                                                    float* pmax, float* psum, float* lab,
-                                                    int64_t nvt) {
-  constexpr int BM = 256, BN = 256, WM = 128, WN = 64, NT = 512;
+template <int STAGES, int BK, int NWN>
+__global__ void __launch_bounds__(128 * NWN) k_lmhead_dma(const uint16_t* __restrict__ x,
+                                                          const uint16_t* __restrict__ E, int64_t M,
+                                                          int64_t d, int64_t V,
+                                                          const int32_t* __restrict__ labels,
+                                                          float* pmax, float* psum, float* lab,
+                                                          int64_t nvt) {
+  constexpr int BM = 256, BN = 256, WM = 128, WN = BN / NWN, NT = 128 * NWN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int ROWB = 2 * BK, CPR = ROWB / 16;   // bytes and 16-byte chunks per stage row
   constexpr int OPB = BM * ROWB;                  // bytes per operand per stage
   constexpr int KS = CPR / 2;                     // MFMA sub-steps per stage
-  constexpr int IPW = CPR / 2;                    // loads per operand per wave per stage
+  constexpr int IPW = BM * CPR / NT;              // loads per operand per wave per stage
   static_assert(CPR == 8 || CPR == 4, "stage width");
   static_assert(STAGES >= 2 && STAGES * 2 * OPB <= 152 * 1024, "LDS");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES * 2 * OPB];
@@ -1215,15 +1218,19 @@ __global__ void __launch_bounds__(512) k_lmhead_dma(const uint16_t* __restrict__
   const int nk = (int)(d / BK);
   for (int i = tid; i < BM; i += NT) lbl[i] = labels[m0 + i];
 
-  // load j of wave w fills the 64 LDS chunks (w * IPW + j) * 64 .. + 63 of an operand
-  const uint8_t* asrc[IPW];
-  const uint8_t* bsrc[IPW];
+  // load j of wave w fills the 64 LDS chunks (w * IPW + j) * 64 .. + 63 of an operand:
+  // RPL rows of CPR chunks.  The chunk swizzle of those rows depends on j only through
+  // its parity, so two per-lane sources per operand serve every load (the rest of the
+  // offset is wave-uniform).
+  constexpr int RPL = 64 / CPR;                   // rows per 1 KB load
+  static_assert(IPW % 2 == 0, "loads per wave");
+  const uint8_t* asrc[2];
+  const uint8_t* bsrc[2];
 #pragma unroll
-  for (int j = 0; j < IPW; ++j) {
-    const int q = (wid * IPW + j) * 64 + lane;
-    const int row = q / CPR, lc = (q % CPR) ^ sw(row);
-    asrc[j] = reinterpret_cast<const uint8_t*>(x) + (m0 + row) * d * 2 + 16 * lc;
-    bsrc[j] = reinterpret_cast<const uint8_t*>(E) + (n0 + row) * d * 2 + 16 * lc;
+  for (int p = 0; p < 2; ++p) {
+    const int row = (wid * IPW + p) * RPL + lane / CPR, lc = (lane % CPR) ^ sw(row);
+    asrc[p] = reinterpret_cast<const uint8_t*>(x) + (m0 + row) * d * 2 + 16 * lc;
+    bsrc[p] = reinterpret_cast<const uint8_t*>(E) + (n0 + row) * d * 2 + 16 * lc;
   }
   const uint32_t wbase = __builtin_amdgcn_readfirstlane(wid) * IPW * 1024u;
   auto Ast = [&](int st) { return lds + st * 2 * OPB; };
@@ -1232,8 +1239,9 @@ __global__ void __launch_bounds__(512) k_lmhead_dma(const uint16_t* __restrict__
     const uint32_t ab = lds_offset(Ast(st)) + wbase, bb = ab + OPB;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
-      dma16(asrc[j] + koff, ab + 1024u * j);
-      dma16(bsrc[j] + koff, bb + 1024u * j);
+      const int64_t roff = (int64_t)(j & ~1) * RPL * d * 2 + koff;
+      dma16(asrc[j & 1] + roff, ab + 1024u * j);
+      dma16(bsrc[j & 1] + roff, bb + 1024u * j);
     }
   };
 
@@ -1832,7 +1840,8 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   if (bf) {
     const unsigned nb = (unsigned)(nvt * ((M + kLmTile - 1) / kLmTile));
     if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % 64 == 0)
-      hipLaunchKernelGGL((k_lmhead_dma<2, 64>), dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
+      hipLaunchKernelGGL((k_lmhead_dma<kLmDmaStages, kLmDmaBK, kLmDmaNWN>), dim3(nb), dim3(128 * kLmDmaNWN), 0, s,
+                         (const uint16_t*)m->xf,
                          (const uint16_t*)emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
                          m->psum, m->lab, nvt);
     else

@@ -84,3 +84,24 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_bench_cpu_baseline_legs_are_combined_by_direction():
+    """The two oracle legs (one thread, all host cores) are both reported with their
+    thread counts; the headline value is the faster one (higher rate, or lower time for
+    time-like units); nested results are left to the caller."""
+    import bench
+    calls = []
+
+    def rate(value):
+        calls.append(value)
+        return {"value": value, "unit": "steps/s", "sample": "s", "_fwd": 1.0}
+
+    out, st, mt = bench.two_legs(rate, {"value": 2.0}, {"value": 5.0})
+    assert out["value"] == 5.0 and out["cores"] == bench.all_cores()
+    assert out["single_thread"]["cores"] == 1 and out["all_cores"]["value"] == 5.0
+    assert "_fwd" not in out and st["_fwd"] == 1.0
+    t = bench.combine_legs({"value": 3.0, "unit": "us"}, {"value": 7.0, "unit": "us"}, 16)
+    assert t["value"] == 3.0 and t["cores"] == 1 and t["all_cores"]["cores"] == 16
+    nested, a, b = bench.two_legs(lambda: {"perturb": {"value": 1.0, "unit": "GB/s"}}, {}, {})
+    assert nested is None and a["perturb"]["value"] == 1.0
