@@ -102,6 +102,18 @@ def measured_traffic():
     return float(kv["fetch_bytes_per_launch"]) + float(kv["write_bytes_per_launch"])
 
 
+def calibration_copy(torch, dev):
+    """A 1 GiB device-to-device copy: a kernel of known traffic, by which hardware
+    byte counters taken in the same run are scaled to bytes."""
+    src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log("calibration copy: 1073741824 bytes read, 1073741824 bytes written")
+    del src, dst
+
+
 def log(msg):
     print(f"[bench] {msg}", flush=True)
 
@@ -471,13 +483,7 @@ def run_decoder(torch, termezo, synth, dev, c, rho, eps, lr, steps, warmup, thet
           "D": D, "c": c, "n_theta": n_theta}
     res = measure_steps(torch, st, rho, eps, lr, steps, warmup, K=K, es=es, compact=compact)
     if calib_copy:
-        src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log("calibration copy: 1073741824 bytes read, 1073741824 bytes written")
-        del src, dst
+        calibration_copy(torch, dev)
     if keep:
         return res, st
     close_state(torch, st)
@@ -967,6 +973,8 @@ def main():
                                    keep=True)
         rows = build_rows(args, torch, termezo, synth, dev, [args.only], head_state=state,
                           head_fwd=fwd)
+        if args.calib_copy:
+            calibration_copy(torch, dev)
         _emit({"rows": rows, "wall_s": time.perf_counter() - t_start})
         return
     if args.config == "layer":
