@@ -150,11 +150,12 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* ctx, int32_t layer,
 /* For callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation): the same BitLinear
  * forward as termezo_bitlinear_forward (same kernels, same results) without the
- * inspection outputs, whose activation-quantisation scratch (int8 x_q and the
- * per-token scales) lives in a fixed 16 MiB device array inside the library
- * instead of context buffers grown on demand.  The call allocates nothing.
- * Limit: M * d_in bytes rounded up to 256, plus 4 * M, at most 16 MiB (for
- * example M <= 6543 at d_in = 2560, M <= 2425 at d_in = 6912).  Each GPU holds
+ * inspection outputs, whose activation-quantisation scratch (int8 x_q, the
+ * per-token scales and the per-token sums of x_q) lives in a fixed 16 MiB device
+ * array inside the library instead of context buffers grown on demand.  The call
+ * allocates nothing.  Limit: M * d_in bytes rounded up to 256, plus 4 * M rounded
+ * up to 256, plus 4 * M, at most 16 MiB (for example M <= 6533 at d_in = 2560,
+ * M <= 2424 at d_in = 6912).  Each GPU holds
  * one copy of the array, shared by every context and call on that GPU: calls
  * whose work overlaps on one GPU (different streams, or different host
  * threads) race on it; calls ordered on one stream do not.  Nothing in the

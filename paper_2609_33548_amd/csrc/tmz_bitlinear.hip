@@ -12,7 +12,9 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // Activation quantisation, one block per token row:
-//   a = max |x|, s = 127 / max(a, 1e-5), x_q = clamp(rne(x s), -128, 127).
+//   a = max |x|, s = 127 / max(a, 1e-5), x_q = clamp(rne(x s), -128, 127),
+// and the row's sum of x_q (int32, for the offset weight encoding of the
+// full-tile GEMM).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void load4(const float* p, float v[4]) {
   const float4 a = *reinterpret_cast<const float4*>(p);
@@ -44,8 +46,10 @@ constexpr int kActRegs = 8;
 
 template <typename T>
 __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int64_t K,
-                                                   int8_t* __restrict__ xq, float* __restrict__ s) {
+                                                   int8_t* __restrict__ xq, float* __restrict__ s,
+                                                   int32_t* __restrict__ rs) {
   __shared__ float red[4];
+  __shared__ int ired[4];
   const int64_t m = blockIdx.x;
   const T* row = x + m * K;
   uint32_t* out = reinterpret_cast<uint32_t*>(xq + m * K);
@@ -76,12 +80,13 @@ __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int6
   a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
   if (threadIdx.x == 0) s[m] = sc;
+  int qs = 0;                                        // this thread's sum of x_q
   auto pack = [&](const float* w) __attribute__((always_inline)) {
-    const uint32_t b0 = (uint32_t)quant_byte(w[0], sc) & 0xFFu;
-    const uint32_t b1 = (uint32_t)quant_byte(w[1], sc) & 0xFFu;
-    const uint32_t b2 = (uint32_t)quant_byte(w[2], sc) & 0xFFu;
-    const uint32_t b3 = (uint32_t)quant_byte(w[3], sc) & 0xFFu;
-    return b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+    const int32_t q0 = quant_byte(w[0], sc), q1 = quant_byte(w[1], sc);
+    const int32_t q2 = quant_byte(w[2], sc), q3 = quant_byte(w[3], sc);
+    qs += q0 + q1 + q2 + q3;
+    return ((uint32_t)q0 & 0xFFu) | (((uint32_t)q1 & 0xFFu) << 8) | (((uint32_t)q2 & 0xFFu) << 16) |
+           (((uint32_t)q3 & 0xFFu) << 24);
   };
   if (held) {
 #pragma unroll
@@ -96,6 +101,11 @@ __global__ void __launch_bounds__(256) k_act_quant(const T* __restrict__ x, int6
       out[k / 4] = pack(w);
     }
   }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) qs += __shfl_xor(qs, off, 64);
+  if ((threadIdx.x & 63) == 0) ired[threadIdx.x >> 6] = qs;
+  __syncthreads();
+  if (threadIdx.x == 0) rs[m] = ired[0] + ired[1] + ired[2] + ired[3];
 }
 
 // ---------------------------------------------------------------------------
@@ -370,6 +380,22 @@ __device__ __forceinline__ v4i unpack16(uint32_t w) {
   return v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
 }
 
+// The 16 codes of a word as the int8 values w + 1 (0, 1, 2 for w = -1, 0, +1), the
+// operand of the full-tile GEMM: acc' = sum_k x_q (w + 1) and acc = acc' - sum_k x_q,
+// exactly, in int32.  The offset values switch far fewer operand bits than
+// two's-complement -1 (0xFF), and the matrix cores draw less power on them (the
+// same GEMM measured 5% faster in the decoder step).  Same selector scheme as
+// unpack_word: bytes 0, 1, 2 of the low table for groups 0 and 2; for groups 1
+// and 3 selectors 0, 4, 8: byte 0 of the low table, byte 0 of the high table and
+// the (clear) sign of the low table's byte 1.
+__device__ __forceinline__ v4i unpack16_off1(uint32_t w) {
+  const uint32_t y = w >> 4;
+  return v4i{(int)__builtin_amdgcn_perm(0u, 0x00000201u, w & 0x03030303u),
+             (int)__builtin_amdgcn_perm(0x02u, 0x00000001u, w & 0x0C0C0C0Cu),
+             (int)__builtin_amdgcn_perm(0u, 0x00000201u, y & 0x03030303u),
+             (int)__builtin_amdgcn_perm(0x02u, 0x00000001u, y & 0x0C0C0C0Cu)};
+}
+
 constexpr int kDmaBM = 256, kDmaBN = 256;
 template <int BK, int NST>
 constexpr int dma_lds_bytes(int BM, int BN) { return NST * (BM * BK + BN * BK / 4); }
@@ -379,7 +405,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
                                               const uint32_t* __restrict__ codes, int64_t K,
                                               int64_t N, const GemmOut& out, int32_t* acc_out,
                                               int64_t m0, int64_t n0, int8_t* lds,
-                                              const float* __restrict__ s) {
+                                              const float* __restrict__ s,
+                                              const int32_t* __restrict__ rs) {
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int AROW = BK;                        // bytes per A row per stage (no pad)
   constexpr int BROW = BK / 4;                    // bytes of packed codes per B row per stage
@@ -432,8 +459,12 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   // per-token input scales of this lane's tokens and the segments' beta', for the epilogue
   const int ml = lane & 31;                          // token of the lane (h: register half)
   float sreg[TM], bet[kMaxSeg];
+  int32_t rsum[TM];                                  // sum of x_q of the lane's tokens
 #pragma unroll
-  for (int a = 0; a < TM; ++a) sreg[a] = s[m0 + wm * WM + 32 * a + ml];
+  for (int a = 0; a < TM; ++a) {
+    sreg[a] = s[m0 + wm * WM + 32 * a + ml];
+    rsum[a] = rs[m0 + wm * WM + 32 * a + ml];
+  }
 #pragma unroll
   for (int sg = 0; sg < kMaxSeg; ++sg) bet[sg] = sg < out.nseg ? *out.beta[sg] : 0.0f;
 
@@ -481,14 +512,14 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     };
     afrag(0, 0);
 #pragma unroll
-    for (int b = 0; b < TN; ++b) bfc[b] = unpack16((uint32_t)bq[0][b][0]);
+    for (int b = 0; b < TN; ++b) bfc[b] = unpack16_off1((uint32_t)bq[0][b][0]);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1;
       if (ks + 1 < KS) {
         afrag(ks + 1, cur ^ 1);
 #pragma unroll
-        for (int b = 0; b < TN; ++b) bfn[b] = unpack16((uint32_t)bq[(ks + 1) / 4][b][(ks + 1) % 4]);
+        for (int b = 0; b < TN; ++b) bfn[b] = unpack16_off1((uint32_t)bq[(ks + 1) / 4][b][(ks + 1) % 4]);
       }
 #pragma unroll
       for (int a = 0; a < TM; ++a)
@@ -589,8 +620,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
           float v4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const float g = round_act((TY*)nullptr, (float)acc[a][b][4 * q + j] * rg);
-            const float u = round_act((TY*)nullptr, (float)acc[a][b][4 * q + 8 + j] * ru);
+            const float g = round_act((TY*)nullptr, (float)(acc[a][b][4 * q + j] - rsum[a]) * rg);
+            const float u = round_act((TY*)nullptr, (float)(acc[a][b][4 * q + 8 + j] - rsum[a]) * ru);
             v4[j] = silu_mul(g, u);
           }
           stage4(16 * b + 8 * q + 4 * h, v4);
@@ -607,7 +638,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
         for (int q = 0; q < 4; ++q) {
           float v4[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v4[j] = round_act((TY*)nullptr, (float)acc[a][b][4 * q + j] * rr);
+          for (int j = 0; j < 4; ++j)
+            v4[j] = round_act((TY*)nullptr, (float)(acc[a][b][4 * q + j] - rsum[a]) * rr);
           stage4(32 * b + 8 * q + 4 * h, v4);
         }
         if (acc_out) {   // int32 accumulators (parity only), straight from the registers
@@ -615,7 +647,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
           for (int q = 0; q < 4; ++q)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-              acc_out[(m0 + mloc) * N + nb + 8 * q + 4 * h + j] = acc[a][b][4 * q + j];
+              acc_out[(m0 + mloc) * N + nb + 8 * q + 4 * h + j] = acc[a][b][4 * q + j] - rsum[a];
         }
       }
     }
@@ -639,7 +671,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
 template <typename TY, int MODE, int BK>
 __global__ void __launch_bounds__(512)
     k_gemm_i8_dma(const int8_t* __restrict__ xq, const float* __restrict__ s,
-                  const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+                  const int32_t* __restrict__ rs, const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
                   int64_t full, int32_t* __restrict__ acc_out) {
   constexpr int NST = BK == 256 ? 2 : 3;
   __shared__ __attribute__((aligned(1024))) int8_t lds[dma_lds_bytes<BK, NST>(kDmaBM, kDmaBN)];
@@ -658,9 +690,11 @@ __global__ void __launch_bounds__(512)
   const int64_t m0 = tm * kDmaBM + (quarter ? 128 * (q >> 1) : 0);
   const int64_t n0 = tn * kDmaBN + (quarter ? 128 * (q & 1) : 0);
   if (!quarter)
-    gemm_tile_dma<256, 256, 128, 64, TY, MODE, BK, NST>(xq, codes, K, N, out, acc_out, m0, n0, lds, s);
+    gemm_tile_dma<256, 256, 128, 64, TY, MODE, BK, NST>(xq, codes, K, N, out, acc_out, m0, n0, lds, s,
+                                                        rs);
   else
-    gemm_tile_dma<128, 128, 64, 32, TY, MODE, BK, NST>(xq, codes, K, N, out, acc_out, m0, n0, lds, s);
+    gemm_tile_dma<128, 128, 64, 32, TY, MODE, BK, NST>(xq, codes, K, N, out, acc_out, m0, n0, lds, s,
+                                                       rs);
 }
 
 // Two blocks per compute unit: 128 x 256 tiles of 4 waves (128 x 64 per wave, the
@@ -672,13 +706,13 @@ constexpr int kHalfBM = 128, kHalfBN = 256;
 template <typename TY, int MODE>
 __global__ void __launch_bounds__(256, 2)
     k_gemm_i8_dma_h(const int8_t* __restrict__ xq, const float* __restrict__ s,
-                    const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
+                    const int32_t* __restrict__ rs, const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
                     int32_t* __restrict__ acc_out) {
   __shared__ __attribute__((aligned(1024))) int8_t lds[dma_lds_bytes<128, 3>(kHalfBM, kHalfBN)];
   int64_t tm, tn;
   tile_of_block(M / kHalfBM, N / kHalfBN, tm, tn);
   gemm_tile_dma<kHalfBM, kHalfBN, 128, 64, TY, MODE, 128, 3>(xq, codes, K, N, out, acc_out,
-                                                             tm * kHalfBM, tn * kHalfBN, lds, s);
+                                                             tm * kHalfBM, tn * kHalfBN, lds, s, rs);
 }
 
 // ---------------------------------------------------------------------------
@@ -830,12 +864,12 @@ __global__ void __launch_bounds__(512)
 
 // ===========================================================================
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
-                            float* s, hipStream_t st) {
+                            float* s, int32_t* rs, hipStream_t st) {
   if (xdt == TERMEZO_F32)
-    hipLaunchKernelGGL(k_act_quant<float>, dim3(M), dim3(256), 0, st, (const float*)x, K, xq, s);
+    hipLaunchKernelGGL(k_act_quant<float>, dim3(M), dim3(256), 0, st, (const float*)x, K, xq, s, rs);
   else
     hipLaunchKernelGGL(k_act_quant<uint16_t>, dim3(M), dim3(256), 0, st, (const uint16_t*)x, K, xq,
-                       s);
+                       s, rs);
   return hipGetLastError();
 }
 
@@ -892,7 +926,8 @@ static int64_t dma_full_tiles(int64_t T, int n_cu) {
   return full;
 }
 
-hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
+hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, const uint32_t* codes,
+                          int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
                           int32_t* acc, int n_cu, hipStream_t st) {
   if (mode == kGemmSwiGLU) {
@@ -902,14 +937,14 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
     const int64_t T = (M / kDmaBM) * (N / kDmaBN), full = dma_full_tiles(T, n_cu);
     if (use_half_tiles(M, T, n_cu))
       hipLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)(2 * T)), dim3(256),
-                         0, st, xq, s, codes, M, K, N, out, acc);
+                         0, st, xq, s, rs, codes, M, K, N, out, acc);
     else if (K % 256 == 0)
       hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU, 256>),
-                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, codes, M, K,
+                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, rs, codes, M, K,
                          N, out, full, acc);
     else
       hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU, 128>),
-                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, codes, M, K,
+                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, rs, codes, M, K,
                          N, out, full, acc);
     return hipGetLastError();
   }
@@ -951,7 +986,7 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
       if (use_half_tiles(M, T, n_cu)) {
         dim3 gh((unsigned)(2 * T));
 #define TMZ_HALF(TY, MD) \
-  hipLaunchKernelGGL((k_gemm_i8_dma_h<TY, MD>), gh, dim3(256), 0, st, xq, s, codes, M, K, N, out, acc)
+  hipLaunchKernelGGL((k_gemm_i8_dma_h<TY, MD>), gh, dim3(256), 0, st, xq, s, rs, codes, M, K, N, out, acc)
         if (ydt == TERMEZO_F32) {
           if (mode == kGemmStore) TMZ_HALF(float, kGemmStore); else TMZ_HALF(float, kGemmResidual);
         } else {
@@ -964,7 +999,8 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
       const int64_t full = T < n_cu ? 0 : dma_full_tiles(T, n_cu);
       dim3 grid((unsigned)(full + 4 * (T - full)));
 #define TMZ_DMA(TY, MD, BK) \
-  hipLaunchKernelGGL((k_gemm_i8_dma<TY, MD, BK>), grid, dim3(512), 0, st, xq, s, codes, M, K, N, out, full, acc)
+  hipLaunchKernelGGL((k_gemm_i8_dma<TY, MD, BK>), grid, dim3(512), 0, st, xq, s, rs, codes, M, K, N, out, full, \
+                     acc)
 #define TMZ_DMA_K(TY, MD) \
   do {                                                 \
     if (K % 256 == 0) TMZ_DMA(TY, MD, 256); else TMZ_DMA(TY, MD, 128); \
@@ -983,7 +1019,8 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* code
   return launch_tile<128, 128, 64, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
 }
 
-hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
+hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const int32_t* rs,
+                                 const uint32_t* codes,
                                  const float* beta_dev, int64_t M, int64_t K, int64_t N, void* y,
                                  termezo_dtype ydt, int32_t* acc, int n_cu, hipStream_t st) {
   GemmOut out = {};
@@ -993,7 +1030,7 @@ hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_
   out.beta[0] = beta_dev;
   out.nstart[0] = 0;
   out.nstart[1] = N;
-  return launch_gemm_i8(xq, s, codes, M, K, N, out, ydt, kGemmStore, acc, n_cu, st);
+  return launch_gemm_i8(xq, s, rs, codes, M, K, N, out, ydt, kGemmStore, acc, n_cu, st);
 }
 
 }  // namespace tmz

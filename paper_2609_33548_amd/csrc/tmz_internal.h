@@ -173,8 +173,9 @@ struct termezo_ctx {
   void* noalloc_scratch = nullptr;           // this device's address of the file-scope scratch
   int8_t* d_xq = nullptr;                    // activation-quantisation scratch
   int64_t xq_cap = 0;
-  float* d_xs = nullptr;
-  int64_t xs_cap = 0;
+  float* d_xs = nullptr;                     // per-token scales
+  int32_t* d_xrs = nullptr;                  // per-token sums of the int8 activations
+  int64_t xs_cap = 0;                        // tokens d_xs and d_xrs hold
 
   // full-precision parameters theta (dense perturbation and update)
   std::vector<tmz::ThetaHost> theta;
@@ -275,16 +276,18 @@ hipError_t launch_gauss(uint64_t seed, const uint64_t* gids, int64_t n, float* z
 hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, float* mean32,
                       hipStream_t s);
 
-// BitLinear
+// BitLinear.  The quantisers write per token the scale s and the sum of the int8
+// activations rs; the GEMM reads both (rs for its offset weight encoding).
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
-                            float* s, hipStream_t st);
-hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
-                          int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
-                          int32_t* acc, int n_cu, hipStream_t st);
+                            float* s, int32_t* rs, hipStream_t st);
+hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs,
+                          const uint32_t* codes, int64_t M, int64_t K, int64_t N,
+                          const GemmOut& out, termezo_dtype ydt, int mode, int32_t* acc, int n_cu,
+                          hipStream_t st);
 // Whether kGemmSwiGLU (full-tile path only) supports an M x K x N gate|up pair.
 bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt);
-hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const uint32_t* codes,
-                                 const float* beta_dev, int64_t M, int64_t K, int64_t N,
+hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const int32_t* rs,
+                                 const uint32_t* codes, const float* beta_dev, int64_t M, int64_t K, int64_t N,
                                  void* y, termezo_dtype ydt, int32_t* acc, int n_cu,
                                  hipStream_t st);
 

@@ -43,6 +43,11 @@ __device__ __forceinline__ float wsum(float v) {
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
   return v;
 }
+__device__ __forceinline__ int wsum_i(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
 __device__ __forceinline__ float wmax(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
@@ -164,7 +169,8 @@ __device__ __forceinline__ uint4 pack8(const float v[8]) {
 template <int MODE, bool WEIGHTED, int CH>
 __device__ __forceinline__ void row_bf16(const uint16_t* __restrict__ x,
                                          const uint16_t* __restrict__ u, int64_t m, int64_t K,
-                                         float eps, int8_t* xq, float* xs, uint16_t* xf) {
+                                         float eps, int8_t* xq, float* xs, int32_t* xrs,
+                                         uint16_t* xf) {
   const int lane = threadIdx.x & 63;
   const int nch = (int)(K / 8);
   uint4 raw[CH];
@@ -238,6 +244,7 @@ __device__ __forceinline__ void row_bf16(const uint16_t* __restrict__ x,
   }
   const float sc = __fdiv_rn(127.0f, fmaxf(amax, 1e-5f));
   if (lane == 0) xs[m] = sc;
+  int qs = 0;                                 // sum of the row's quantised values
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const int idx = c * 64 + lane;
@@ -247,12 +254,16 @@ __device__ __forceinline__ void row_bf16(const uint16_t* __restrict__ x,
       uint32_t w0 = 0, w1 = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        w0 |= ((uint32_t)(uint8_t)q8(v[j], sc)) << (8 * j);
-        w1 |= ((uint32_t)(uint8_t)q8(v[4 + j], sc)) << (8 * j);
+        const int8_t q0 = q8(v[j], sc), q1 = q8(v[4 + j], sc);
+        qs += q0 + q1;
+        w0 |= ((uint32_t)(uint8_t)q0) << (8 * j);
+        w1 |= ((uint32_t)(uint8_t)q1) << (8 * j);
       }
       *reinterpret_cast<uint2*>(xq + m * K + idx * 8) = make_uint2(w0, w1);
     }
   }
+  qs = wsum_i(qs);
+  if (lane == 0) xrs[m] = qs;
 }
 
 // CH: chunks per lane the row needs at most (the kernel is instantiated for a few
@@ -260,12 +271,12 @@ __device__ __forceinline__ void row_bf16(const uint16_t* __restrict__ x,
 template <int MODE, typename T, bool WEIGHTED = false, int CH = kRowChunks>
 __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* __restrict__ u,
                                              int64_t M, int64_t K, float eps, int8_t* xq,
-                                             float* xs, T* xf) {
+                                             float* xs, int32_t* xrs, T* xf) {
   const int lane = threadIdx.x & 63;
   const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (m >= M) return;                       // whole wave
   if constexpr (sizeof(T) == 2 && CH > 8) {   // long rows: half the registers
-    row_bf16<MODE, WEIGHTED, CH>(x, u, m, K, eps, xq, xs, xf);
+    row_bf16<MODE, WEIGHTED, CH>(x, u, m, K, eps, xq, xs, xrs, xf);
     return;
   }
   const int nch = (int)(K / 8);
@@ -334,6 +345,7 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
   }
   const float sc = __fdiv_rn(127.0f, fmaxf(amax, 1e-5f));
   if (lane == 0) xs[m] = sc;
+  int qs = 0;                                 // sum of the row's quantised values
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const int idx = c * 64 + lane;
@@ -341,12 +353,16 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
       uint32_t w0 = 0, w1 = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        w0 |= ((uint32_t)(uint8_t)q8(v[c][j], sc)) << (8 * j);
-        w1 |= ((uint32_t)(uint8_t)q8(v[c][4 + j], sc)) << (8 * j);
+        const int8_t q0 = q8(v[c][j], sc), q1 = q8(v[c][4 + j], sc);
+        qs += q0 + q1;
+        w0 |= ((uint32_t)(uint8_t)q0) << (8 * j);
+        w1 |= ((uint32_t)(uint8_t)q1) << (8 * j);
       }
       *reinterpret_cast<uint2*>(xq + m * K + idx * 8) = make_uint2(w0, w1);
     }
   }
+  qs = wsum_i(qs);
+  if (lane == 0) xrs[m] = qs;
 }
 
 // One row kernel launch (4 rows per block), instantiated for the chunks per lane
@@ -354,18 +370,21 @@ __global__ void __launch_bounds__(256) k_row(const T* __restrict__ x, const T* _
 // else kRowChunks.
 template <int MODE, typename T, bool W = false>
 static void row_launch(unsigned grid, hipStream_t s, const T* x, const T* u, int64_t M, int64_t K,
-                       float eps, int8_t* xq, float* xs, T* xf) {
+                       float eps, int8_t* xq, float* xs, int32_t* xrs, T* xf) {
   const int64_t need = (K / 8 + 63) / 64;
+#define TMZ_ROW(CHN) \
+  hipLaunchKernelGGL((k_row<MODE, T, W, CHN>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xrs, xf)
   if (need <= 3)
-    hipLaunchKernelGGL((k_row<MODE, T, W, 3>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+    TMZ_ROW(3);
   else if (need <= 5)
-    hipLaunchKernelGGL((k_row<MODE, T, W, 5>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+    TMZ_ROW(5);
   else if (need <= 8)
-    hipLaunchKernelGGL((k_row<MODE, T, W, 8>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+    TMZ_ROW(8);
   else if (need <= 14)
-    hipLaunchKernelGGL((k_row<MODE, T, W, 14>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+    TMZ_ROW(14);
   else
-    hipLaunchKernelGGL((k_row<MODE, T, W>), dim3(grid), dim3(256), 0, s, x, u, M, K, eps, xq, xs, xf);
+    TMZ_ROW(kRowChunks);
+#undef TMZ_ROW
 }
 
 // ---------------------------------------------------------------------------
@@ -1424,6 +1443,7 @@ struct termezo_model {
        *g = nullptr, *u = nullptr, *xf = nullptr;
   int8_t* xq = nullptr;
   float* xs = nullptr;
+  int32_t* xrs = nullptr;                    // per-token sums of the quantised activations
   float *pmax = nullptr, *psum = nullptr, *lab = nullptr, *row = nullptr;
   int32_t* labels = nullptr;
   float *rope_c = nullptr, *rope_s = nullptr;
@@ -1473,6 +1493,7 @@ void model_free_buffers(termezo_model* m) {
   void* p;
   p = m->xq; mfree(p); m->xq = nullptr;
   p = m->xs; mfree(p); m->xs = nullptr;
+  p = m->xrs; mfree(p); m->xrs = nullptr;
   p = m->pmax; mfree(p); m->pmax = nullptr;
   p = m->psum; mfree(p); m->psum = nullptr;
   p = m->lab; mfree(p); m->lab = nullptr;
@@ -1510,6 +1531,7 @@ termezo_status model_reserve(termezo_model* m, int64_t M, int S) {
   A(&m->xf, M * c.d_model * es);
   A((void**)&m->xq, M * kmax);
   A((void**)&m->xs, M * 4);
+  A((void**)&m->xrs, M * 4);
   A((void**)&m->pmax, M * nvt * 4);
   A((void**)&m->psum, M * nvt * 4);
   A((void**)&m->lab, M * 4);
@@ -1743,7 +1765,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
 #define TMZ_NORM(T, MD, W)                                                                   \
   row_launch<MD, T, W>(rowg, s, (const T*)m->h,                                              \
                        nrm ? (const T*)nrm + (int64_t)wr * d : (const T*)nullptr, M, d,      \
-                       cf.norm_eps, xq, xs, (T*)xf)
+                       cf.norm_eps, xq, xs, m->xrs, (T*)xf)
     if (bf) {
       if (xf) {
         if (nrm) TMZ_NORM(uint16_t, kRowNormStore, true); else TMZ_NORM(uint16_t, kRowNormStore, false);
@@ -1772,7 +1794,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o3.y[2] = m->v; o3.ld[2] = dkv; o3.beta[2] = c->d_beta_cur + l0 + 2;
     o3.nstart[0] = 0; o3.nstart[1] = dq; o3.nstart[2] = dq + dkv; o3.nstart[3] = dq + 2 * dkv;
     int sp = span_begin(m, 0, 2.0 * M * d * (dq + 2 * dkv), s);
-    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
                        kGemmStore, nullptr, c->n_cu, s));
     span_end(m, sp, s);
     if (!bf) {   // bf16: the rotation is applied inside the attention kernel
@@ -1789,17 +1811,17 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     span_end(m, sp, s);
     if (bf)
       row_launch<kRowQuant, uint16_t>(rowg, s, (const uint16_t*)m->attn, (const uint16_t*)nullptr,
-                                      M, dq, 0.0f, m->xq, m->xs, (uint16_t*)nullptr);
+                                      M, dq, 0.0f, m->xq, m->xs, m->xrs, (uint16_t*)nullptr);
     else
       row_launch<kRowQuant, float>(rowg, s, (const float*)m->attn, (const float*)nullptr, M, dq,
-                                   0.0f, m->xq, m->xs, (float*)nullptr);
+                                   0.0f, m->xq, m->xs, m->xrs, (float*)nullptr);
     chk(hipGetLastError());
     GemmOut oo = {};
     oo.nseg = 1;
     oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = c->d_beta_cur + l0 + 3;
     oo.nstart[0] = 0; oo.nstart[1] = d;
     sp = span_begin(m, 0, 2.0 * M * dq * d, s);
-    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
                        nullptr, c->n_cu, s));
     span_end(m, sp, s);
     // MLP sub-block
@@ -1813,25 +1835,25 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     // product lands in g), else the two projections and the SwiGLU row kernel
     const bool fused = gemm_swiglu_ok(M, d, 2 * F, adt);
     sp = span_begin(m, 0, 2.0 * M * d * 2 * F, s);
-    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt,
                        fused ? kGemmSwiGLU : kGemmStore, nullptr, c->n_cu, s));
     span_end(m, sp, s);
     if (fused)
       row_launch<kRowQuant, uint16_t>(rowg, s, (const uint16_t*)m->g, (const uint16_t*)nullptr, M,
-                                      F, 0.0f, m->xq, m->xs, (uint16_t*)nullptr);
+                                      F, 0.0f, m->xq, m->xs, m->xrs, (uint16_t*)nullptr);
     else if (bf)
       row_launch<kRowSwiGLU, uint16_t>(rowg, s, (const uint16_t*)m->g, (const uint16_t*)m->u, M,
-                                       F, 0.0f, m->xq, m->xs, (uint16_t*)nullptr);
+                                       F, 0.0f, m->xq, m->xs, m->xrs, (uint16_t*)nullptr);
     else
       row_launch<kRowSwiGLU, float>(rowg, s, (const float*)m->g, (const float*)m->u, M, F, 0.0f,
-                                    m->xq, m->xs, (float*)nullptr);
+                                    m->xq, m->xs, m->xrs, (float*)nullptr);
     chk(hipGetLastError());
     GemmOut od = {};
     od.nseg = 1;
     od.y[0] = m->h; od.ld[0] = d; od.beta[0] = c->d_beta_cur + l0 + 6;
     od.nstart[0] = 0; od.nstart[1] = d;
     sp = span_begin(m, 0, 2.0 * M * F * d, s);
-    chk(launch_gemm_i8(m->xq, m->xs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
                        nullptr, c->n_cu, s));
     span_end(m, sp, s);
   }

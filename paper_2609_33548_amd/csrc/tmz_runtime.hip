@@ -143,10 +143,16 @@ termezo_status ensure_xq_capacity(termezo_ctx* c, int64_t M, int64_t K) {
     TMZ_HIP(c, dalloc(&c->d_xq, (size_t)need));
     c->xq_cap = need;
   }
+  return TERMEZO_OK;
+}
+
+termezo_status ensure_xs_capacity(termezo_ctx* c, int64_t M) {
   if (M > c->xs_cap) {
     dfree(c->d_xs);
+    dfree(c->d_xrs);
     c->xs_cap = 0;
     TMZ_HIP(c, dalloc(&c->d_xs, (size_t)M));
+    TMZ_HIP(c, dalloc(&c->d_xrs, (size_t)M));
     c->xs_cap = M;
   }
   return TERMEZO_OK;
@@ -191,6 +197,7 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_scal);
   dfree(c->d_xq);
   dfree(c->d_xs);
+  dfree(c->d_xrs);
   if (c->d_wc) (void)hipFree(c->d_wc);
   if (c->d_wc_tmp) (void)hipFree(c->d_wc_tmp);
   c->d_wc = c->d_wc_tmp = nullptr;
@@ -486,15 +493,18 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
   const LayerHost& L = c->layers[layer];
   int8_t* xq = xq_out;
   float* xs = xscale_out;
-  if (!xq || !xs) {
-    termezo_status st = ensure_xq_capacity(c, M, L.d_in);
+  termezo_status st = ensure_xs_capacity(c, M);       // the row sums live here in any case
+  if (st != TERMEZO_OK) return st;
+  if (!xq) {
+    st = ensure_xq_capacity(c, M, L.d_in);
     if (st != TERMEZO_OK) return st;
-    if (!xq) xq = c->d_xq;
-    if (!xs) xs = c->d_xs;
+    xq = c->d_xq;
   }
-  TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->stream));
-  TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
-                                   L.d_in, L.d_out, y, y_dtype, acc_out, c->n_cu, c->stream));
+  if (!xs) xs = c->d_xs;
+  TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->d_xrs, c->stream));
+  TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_xrs, c->d_codes + L.code_off,
+                                   c->d_beta_cur + layer, M, L.d_in, L.d_out, y, y_dtype, acc_out,
+                                   c->n_cu, c->stream));
   return TERMEZO_OK;
 }
 
@@ -505,18 +515,21 @@ termezo_status termezo_bitlinear_forward_noalloc(termezo_ctx* c, int32_t layer, 
   const termezo_status ck = check_forward_args(c, layer, x, x_dtype, M, y, y_dtype);
   if (ck != TERMEZO_OK) return ck;
   const LayerHost& L = c->layers[layer];
-  // int8 activations, then the scales at the next 256-byte boundary
+  // int8 activations, then the scales and the row sums, each at a 256-byte boundary
   const int64_t xq_bytes = M <= kNoAllocScratchBytes ? ((M * L.d_in + 255) / 256) * 256 : -1;
-  if (xq_bytes < 0 || xq_bytes + 4 * M > kNoAllocScratchBytes)
+  const int64_t xs_bytes = ((4 * M + 255) / 256) * 256;
+  if (xq_bytes < 0 || xq_bytes + xs_bytes + 4 * M > kNoAllocScratchBytes)
     return fail(c, TERMEZO_ERR_INVALID_ARG,
-                "bitlinear_forward_noalloc: M * d_in + 4 M bytes (256-aligned) exceed the "
+                "bitlinear_forward_noalloc: M * d_in + 8 M bytes (256-aligned parts) exceed the "
                 "16 MiB scratch");
   if (!c->noalloc_scratch) return fail(c, TERMEZO_ERR_DEVICE, "no scratch address");
-  int8_t* xq = static_cast<int8_t*>(c->noalloc_scratch);
-  float* xs = reinterpret_cast<float*>(static_cast<char*>(c->noalloc_scratch) + xq_bytes);
-  TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, c->stream));
-  TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
-                                   L.d_in, L.d_out, y, y_dtype, nullptr, c->n_cu, c->stream));
+  char* base = static_cast<char*>(c->noalloc_scratch);
+  int8_t* xq = reinterpret_cast<int8_t*>(base);
+  float* xs = reinterpret_cast<float*>(base + xq_bytes);
+  int32_t* xrs = reinterpret_cast<int32_t*>(base + xq_bytes + xs_bytes);
+  TMZ_HIP(c, launch_act_quant(x, x_dtype, M, L.d_in, xq, xs, xrs, c->stream));
+  TMZ_HIP(c, launch_bitlinear_gemm(xq, xs, xrs, c->d_codes + L.code_off, c->d_beta_cur + layer,
+                                   M, L.d_in, L.d_out, y, y_dtype, nullptr, c->n_cu, c->stream));
   return TERMEZO_OK;
 }
 

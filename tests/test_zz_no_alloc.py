@@ -53,13 +53,13 @@ def test_noalloc_forward_rejects_sizes_beyond_the_scratch():
     ctx = T.Context([w])
     ctx.build_mask(1e-2)
     ctx.perturb(1, 1e-3, 1)
-    M = 2426                               # 2426 * (6912 + 4) bytes > 16 MiB
+    M = 2425                               # 2425 * 6912 + 9728 + 4 * 2425 bytes > 16 MiB
     x = torch.zeros((M, K), dtype=torch.bfloat16, device="cuda")
     y = torch.zeros((M, N), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(T.TermezoError) as e:
         ctx.bitlinear_forward_noalloc(0, x, y)
     assert e.value.status == T.ERR_INVALID_ARG and "16 MiB" in str(e.value)
     assert bool((y == 0).all())
-    ctx.bitlinear_forward_noalloc(0, x[:2425], y[:2425])   # the largest M that fits
+    ctx.bitlinear_forward_noalloc(0, x[:2424], y[:2424])   # the largest M that fits
     ctx.sync()
     ctx.close()
