@@ -50,6 +50,8 @@ CONFIGS = {
 LAYER = dict(d_out=256, d_in=256, tokens=8, rho=1e-2, eps=1e-3, lr=1e-4)
 PEAK_INT8_TOPS = 5000.0          # MI355X dense int8 MFMA, TOP/s
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA, TFLOP/s
+PEAK_FP32_TFLOPS = 157.3         # MI355X fp32 vector, TFLOP/s
 # HBM traffic of the GEMM launches measured with rocprofv3 counters (FETCH_SIZE,
 # WRITE_SIZE), valid only for the kernel source it was measured on.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bitlinear_gemm_traffic_2b_step.txt")
@@ -610,6 +612,8 @@ def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=Fal
                                 "lm_head_ce": h_ms / steps,
                                 "perturb_update_calls": latent_ms,
                                 "event_timed_step_ms": timed_ms},
+        "step_roofline": step_roofline(c, g_ops / steps, a_ops / steps, h_ops / steps, k0,
+                                       K if not es else es, ms_per_step),
         "attention_tflops": a_ops / (a_ms * 1e-3) / 1e12 if a_ms else None,
         "lm_head_tflops": h_ops / (h_ms * 1e-3) / 1e12 if h_ms else None,
         "mask_build_ms": mask_ms,
@@ -618,6 +622,39 @@ def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=Fal
                    "eq_memory_latent_side_bytes": int(eq_mem),
                    "torch_allocated_bytes": int(torch.cuda.memory_allocated())},
     }
+
+
+def step_roofline(c, gemm_ops, attn_flops, lm_flops, k, dirs, ms_per_step):
+    """The whole step against the rooflines: sum over its kernel classes of algorithmic
+    work / peak (matrix-core classes at their dense peak, attention at the larger of its
+    flop and HBM times, the bandwidth-bound classes at 8 TB/s), over the measured step."""
+    el = 4 if c.get("fp32") else 2                       # bytes per stored activation
+    peak_mm = PEAK_FP32_TFLOPS if c.get("fp32") else PEAK_BF16_TFLOPS   # attention, LM head
+    M = c["batch"] * c["seq"]
+    d, F = c["d_model"], c["d_ffn"]
+    hd = d // c["n_heads"]
+    dkv = c["n_kv_heads"] * hd
+    evals = 2 * dirs                                     # forwards per step
+    # per forward: quantising row kernels read the activation and write int8 (+ 8 B scale and
+    # row sum per token); K rotation and V transposition read and write K and V; the
+    # embedding gather and the stored final norm read and write one activation row each
+    row_b = c["n_blocks"] * (3 * M * ((el + 1) * d + 8) + M * ((el + 1) * F + 8)
+                             + 4 * el * M * dkv) + 4 * el * M * d
+    attn_b = c["n_blocks"] * (2 * el * M * d + 2 * el * M * dkv)
+    attn_f = attn_flops / max(1, evals)
+    attn_ms = evals * max(attn_f / (peak_mm * 1e12),
+                          attn_b / (HBM_PEAK_GBS * 1e9)) * 1e3
+    # latent side: perturbation pair (index, w' of both signs, code word read and write per
+    # active) and update (index, latent read and write, new value)
+    lat_b = dirs * 2 * 26 * k + 16 * k
+    parts = {"bitlinear_gemm": gemm_ops / (PEAK_INT8_TOPS * 1e12) * 1e3,
+             "lm_head_ce": lm_flops / (peak_mm * 1e12) * 1e3,
+             "attention": attn_ms,
+             "row_kernels": evals * row_b / (HBM_PEAK_GBS * 1e9) * 1e3,
+             "latent_side": lat_b / (HBM_PEAK_GBS * 1e9) * 1e3}
+    ideal = sum(parts.values())
+    return {"ideal_ms": ideal, "measured_ms": ms_per_step, "frac": ideal / ms_per_step,
+            "ideal_ms_parts": parts}
 
 
 def _hbm(gbs):
