@@ -753,10 +753,11 @@ __global__ void __launch_bounds__(512) k_attn_bf16(const uint16_t* __restrict__ 
 //    is one 16-byte chunk of a V^T row.  The row sum is taken from the bf16
 //    probabilities that enter the product (v_dot2 with ones).
 //  * K and V^T tiles stream through 2 LDS stages with direct global -> LDS
-//    loads; 16-byte chunk c of a K row r sits at c ^ (r & 15) (128-dim rows)
-//    or c ^ ((r >> 1) & 7) (64-dim rows), of a V^T row at c ^ ((r >> 1) & 7),
-//    so the fragment reads of 16 lanes hit distinct banks; staging rows put
-//    chunk c at c ^ (r & (CPR - 1)).
+//    loads; 16-byte chunk c of a K row r sits at c ^ (r & 15) (128-dim rows),
+//    c ^ ((r >> 1) & 7) (64-dim rows) or c ^ ((r >> 2) & 3) (96-dim rows of 12
+//    chunks: the swap stays inside aligned groups of 4 chunks), of a V^T row at
+//    c ^ ((r >> 1) & 7), so the fragment reads of 16 lanes hit distinct banks;
+//    staging rows put chunk c at c ^ (r & (CPR - 1)) (96-dim rows: c ^ (r & 3)).
 //  * 32-key blocks entirely in a wave's causal future are skipped and only
 //    the diagonal block is masked.  The running maximum is raised only when a
 //    tile's maximum exceeds it by more than 2^8 (in exp2 units); the
@@ -778,15 +779,20 @@ __global__ void __launch_bounds__(512) k_attn_gqa(const uint16_t* __restrict__ q
   constexpr int KROWB = 2 * HD, CPR = HD / 8; // bytes and 16-byte chunks per K / Q row
   constexpr int TB = KT * KROWB;              // bytes per K tile (= per V^T tile)
   constexpr int QB = 256 * KROWB;             // Q / O staging: 256 (query, head) rows
-  constexpr int LPW = TB / 1024 / 8;          // 1 KB loads per wave per operand per stage
+  constexpr int NLD = TB / 1024;              // 1 KB loads per operand per stage
+  constexpr int LPW = (NLD + 7) / 8;          // per wave (load L = 8 j + wave, L < NLD)
   constexpr int NS = HD / 16;                 // 16-dim K steps of S^T
   constexpr int ND = HD / 32;                 // 32-dim blocks of O^T
-  static_assert(HD == 64 || HD == 128, "head dim");
+  static_assert(HD == 64 || HD == 96 || HD == 128, "head dim");
+  static_assert(TB % 1024 == 0, "tile");
   static_assert(G == 1 || G == 2 || G == 4 || G == 8, "group");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * TB + QB];
   uint8_t* stg = lds + 4 * TB;                // Q / O staging rows (query r, head g) -> r G + g
   auto swk = [](int r) __attribute__((always_inline)) {
-    return CPR == 16 ? (r & 15) : ((r >> 1) & 7);
+    return CPR == 16 ? (r & 15) : CPR == 12 ? ((r >> 2) & 3) : ((r >> 1) & 7);
+  };
+  auto sws = [](int r) __attribute__((always_inline)) {   // staging rows
+    return CPR == 12 ? (r & 3) : (r & (CPR - 1));
   };
   auto swv = [](int r) __attribute__((always_inline)) { return (r >> 1) & 7; };
 
@@ -806,24 +812,27 @@ __global__ void __launch_bounds__(512) k_attn_gqa(const uint16_t* __restrict__ q
   const int qpos = q0 + rq;                   // this lane's query
   const int srow = rq * G + wid % G;          // this lane's staging row
 
-  // direct-load sources: load j of wave w fills LDS chunks (w LPW + j) 64 + lane
+  // direct-load sources: load L = 8 j + w (wave w, L < NLD) fills LDS chunks 64 L + lane
   const uint8_t* ksrc[LPW];
   const uint8_t* vsrc[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
-    const int c = (wid * LPW + j) * 64 + lane;
+    const int L = 8 * j + wid;
+    const int c = (L < NLD ? L : 0) * 64 + lane;
     const int kr = c / CPR, kc = (c % CPR) ^ swk(kr);
     ksrc[j] = reinterpret_cast<const uint8_t*>(k + (base + kr) * rowkv + (int64_t)kvh * HD) + 16 * kc;
     const int vr = c / 8, vc = (c % 8) ^ swv(vr);
     vsrc[j] = reinterpret_cast<const uint8_t*>(vt + (((int64_t)b * Hkv + kvh) * HD + vr) * S) + 16 * vc;
   }
-  const uint32_t wbase = wid * LPW * 1024u;
   auto issue = [&](int kt, int st) __attribute__((always_inline)) {
-    const uint32_t kb = lds_offset(lds + st * 2 * TB) + wbase, vb = kb + TB;
+    const uint32_t kb = lds_offset(lds + st * 2 * TB), vb = kb + TB;
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
-      dma16(ksrc[j] + (int64_t)kt * KT * rowkv * 2, kb + 1024u * j);
-      dma16(vsrc[j] + (int64_t)kt * KT * 2, vb + 1024u * j);
+      const int L = 8 * j + wid;                   // wave-uniform
+      if (NLD % 8 == 0 || L < NLD) {
+        dma16(ksrc[j] + (int64_t)kt * KT * rowkv * 2, kb + 1024u * L);
+        dma16(vsrc[j] + (int64_t)kt * KT * 2, vb + 1024u * L);
+      }
     }
   };
 
@@ -842,7 +851,7 @@ __global__ void __launch_bounds__(512) k_attn_gqa(const uint16_t* __restrict__ q
       hi[g] = *reinterpret_cast<const uint4*>(qr + g * HD + HALF);
     }
     const int ti = pos * HALF + 8 * cg;
-    const int sw = r & (CPR - 1);
+    const int sw = sws(r);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       uint8_t* row = stg + (r * G + g) * KROWB;
@@ -858,7 +867,7 @@ __global__ void __launch_bounds__(512) k_attn_gqa(const uint16_t* __restrict__ q
     const uint8_t* row = stg + srow * KROWB;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-      qf[s] = __builtin_bit_cast(v8bf, *reinterpret_cast<const uint4*>(row + 16 * ((2 * s + h) ^ (rq & (CPR - 1)))));
+      qf[s] = __builtin_bit_cast(v8bf, *reinterpret_cast<const uint4*>(row + 16 * ((2 * s + h) ^ sws(rq))));
   }
 
   v16f ot[ND];
@@ -978,13 +987,13 @@ __global__ void __launch_bounds__(512) k_attn_gqa(const uint16_t* __restrict__ q
       for (int g = 0; g < 4; ++g) {
         const uint32_t w0 = pack_bf16x2(ot[d][4 * g] * inv, ot[d][4 * g + 1] * inv);
         const uint32_t w1 = pack_bf16x2(ot[d][4 * g + 2] * inv, ot[d][4 * g + 3] * inv);
-        *reinterpret_cast<uint2*>(row + 16 * ((4 * d + g) ^ (rq & (CPR - 1))) + 8 * h) = make_uint2(w0, w1);
+        *reinterpret_cast<uint2*>(row + 16 * ((4 * d + g) ^ sws(rq)) + 8 * h) = make_uint2(w0, w1);
       }
   }
   __syncthreads();
   for (int it = tid; it < QT * (CPR / 2); it += 512) {
     const int r = it / (CPR / 2), cg = it % (CPR / 2);
-    const int sw = r & (CPR - 1);
+    const int sw = sws(r);
     uint16_t* orow = o + (base + q0 + r) * rowq + (int64_t)hq0 * HD + 8 * cg;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -1585,12 +1594,17 @@ hipError_t run_attention(termezo_model* m, int B, int S, hipStream_t st) {
                      (const uint16_t*)m->k, (const uint16_t*)m->vt, (uint16_t*)m->attn, S,     \
                      c.n_heads, c.n_kv_heads, sl2, m->rope_c, m->rope_s)
   const int G = c.n_heads / c.n_kv_heads;
-  const bool gqa = (m->hd == 64 || m->hd == 128) && (G == 1 || G == 2 || G == 4 || G == 8) &&
+  const bool gqa = (m->hd == 64 || m->hd == 96 || m->hd == 128) &&
+                   (G == 1 || G == 2 || G == 4 || G == 8) &&
                    S % 64 == 0 && S % (256 / G) == 0;
   if (gqa) {
     const int nbh = B * c.n_kv_heads, nqt = S / (256 / G);
     if (m->hd == 128)
       hipLaunchKernelGGL(k_kv_prep<128>, pgrid, dim3(256), 0, st, (uint16_t*)m->k,
+                         (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads, m->rope_c,
+                         m->rope_s);
+    else if (m->hd == 96)
+      hipLaunchKernelGGL(k_kv_prep<96>, pgrid, dim3(256), 0, st, (uint16_t*)m->k,
                          (const uint16_t*)m->v, (uint16_t*)m->vt, S, c.n_kv_heads, m->rope_c,
                          m->rope_s);
     else
@@ -1606,6 +1620,10 @@ hipError_t run_attention(termezo_model* m, int B, int S, hipStream_t st) {
       case 128 * 16 + 2: TMZ_GQA(128, 2); break;
       case 128 * 16 + 4: TMZ_GQA(128, 4); break;
       case 128 * 16 + 8: TMZ_GQA(128, 8); break;
+      case 96 * 16 + 1: TMZ_GQA(96, 1); break;
+      case 96 * 16 + 2: TMZ_GQA(96, 2); break;
+      case 96 * 16 + 4: TMZ_GQA(96, 4); break;
+      case 96 * 16 + 8: TMZ_GQA(96, 8); break;
       case 64 * 16 + 1: TMZ_GQA(64, 1); break;
       case 64 * 16 + 2: TMZ_GQA(64, 2); break;
       case 64 * 16 + 4: TMZ_GQA(64, 4); break;

@@ -137,6 +137,8 @@ def test_tiny_decoder_fp32_projected_gradient(orc):
     (512, 8, 1, 256, 300, 64, 2),      # GQA 8:1, head_dim 64 (32-query tiles)
     (256, 2, 2, 256, 300, 256, 1),     # MHA, head_dim 128 (256-query tiles)
     (256, 4, 2, 256, 300, 128, 2),     # GQA 2:1, head_dim 64
+    (192, 2, 2, 192, 300, 256, 1),     # MHA, head_dim 96 (grouped-query kernel, 12-chunk rows)
+    (384, 4, 2, 256, 300, 128, 2),     # GQA 2:1, head_dim 96
 ])
 def test_bf16_decoder_loss(orc, d, H, Hkv, F, V, S, B):
     torch = _torch()
