@@ -862,6 +862,168 @@ __global__ void __launch_bounds__(512)
   }
 }
 
+// ---------------------------------------------------------------------------
+// One token (M = 1) with the activation quantisation fused in: every block reads the
+// whole activation row (at most 8192 values), forms a = max |x| and
+// s = 127 / max(a, 1e-5) and quantises the row into LDS exactly as k_act_quant does,
+// then runs the contraction of k_gemv_i8 for its 16 output features (token 0 of the
+// 16-token MFMA group).  One launch per call instead of two; the code words are
+// loaded first so that their latency overlaps the row's.
+// ---------------------------------------------------------------------------
+constexpr int kGemv1MaxK = 8192;
+
+__device__ __forceinline__ void load8x(const float* p, float v[8]) {
+  load4(p, v);
+  load4(p + 4, v + 4);
+}
+__device__ __forceinline__ void load8x(const uint16_t* p, float v[8]) {
+  const uint4 a = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = __uint_as_float(w[j] << 16);
+    v[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+  }
+}
+
+template <typename TX, typename TY, bool CVEC>
+__global__ void __launch_bounds__(512)
+    k_gemv1_fused(const TX* __restrict__ x, const uint32_t* __restrict__ codes, int64_t K,
+                  int64_t N, const float* __restrict__ beta, TY* __restrict__ y, int yvec) {
+  constexpr int NW = 8;
+  constexpr int CPW = kGemv1MaxK / (256 * NW);        // 256-k chunks per wave at most
+  constexpr int XI = kGemv1MaxK / (8 * 512);           // 8-value items of the row per thread
+  __shared__ __attribute__((aligned(16))) int8_t xql[kGemv1MaxK];
+  __shared__ int32_t red[NW][4][64];
+  __shared__ float amx[NW];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t n0 = (int64_t)blockIdx.x * 16;
+  const int64_t KW = K / 16;
+  const int nchunk = (int)((KW + 15) / 16);
+  const int fr = lane & 15, g = lane >> 4;
+  const bool row_ok = n0 + fr < N;
+  const uint32_t* crow = codes + (row_ok ? n0 + fr : 0) * KW;
+  // this wave's code words (chunks wid, wid + NW, ...), zero outside the matrix
+  uint32_t cw[CPW][4];
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int64_t w0 = (int64_t)(wid + NW * i) * 16 + 4 * g;
+    if (CVEC) {
+      const v4u v = *reinterpret_cast<const v4u*>(crow + (w0 < KW ? w0 : 0));
+      const bool ok = row_ok && w0 < KW;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cw[i][j] = ok ? v[j] : 0u;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t v = crow[w0 + j < KW ? w0 + j : 0];
+        cw[i][j] = (row_ok && w0 + j < KW) ? v : 0u;
+      }
+    }
+  }
+  // the activation row: max |x|, then the quantised row into LDS
+  float xv[XI][8];
+  float a = 0.0f;
+#pragma unroll
+  for (int it = 0; it < XI; ++it) {
+    const int64_t k = ((int64_t)it * 512 + tid) * 8;
+    if (k < K) {
+      load8x(x + k, xv[it]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) xv[it][j] = 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a = fmaxf(a, fabsf(xv[it][j]));
+  }
+  a = wave_max(a);
+  if (lane == 0) amx[wid] = a;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < NW; ++w) a = fmaxf(a, amx[w]);
+  const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
+#pragma unroll
+  for (int it = 0; it < XI; ++it) {
+    const int64_t k = ((int64_t)it * 512 + tid) * 8;
+    if (k < K) {
+      uint32_t w[2];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        uint32_t b = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b |= ((uint32_t)quant_byte(xv[it][4 * h2 + j], sc) & 0xFFu) << (8 * j);
+        w[h2] = b;
+      }
+      *reinterpret_cast<uint2*>(xql + k) = make_uint2(w[0], w[1]);
+    }
+  }
+  __syncthreads();
+  // contraction: token fr of the MFMA group is the row for fr == 0, zero otherwise
+  v4i acc = v4i{0, 0, 0, 0};
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int c = wid + NW * i;
+    if (c < nchunk) {                                   // wave-uniform
+      const int64_t kb = ((int64_t)c * 16 + 4 * g) * 16;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t k = kb + 16 * j;
+        v4i b = *reinterpret_cast<const v4i*>(xql + (k < K ? k : 0));
+        if (!(fr == 0 && k < K)) b = v4i{0, 0, 0, 0};
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack16(cw[i][j]), b, acc, 0, 0, 0);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) red[wid][i][lane] = acc[i];
+  __syncthreads();
+  if (wid == 0 && fr == 0) {                            // lanes 0, 16, 32, 48: features 4 g ..
+    const int64_t n = n0 + 4 * g;
+    if (n < N) {
+      const float rr = __fdiv_rn(*beta, sc);
+      float y4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int32_t v = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) v += red[w][i][lane];
+        y4[i] = (float)v * rr;
+      }
+      if (yvec && n + 3 < N) {
+        store4(y + n, y4);
+      } else {
+        for (int i = 0; i < 4 && n + i < N; ++i) store_act(y + n + i, y4[i]);
+      }
+    }
+  }
+}
+
+bool gemv1_fused_ok(int64_t M, int64_t K) { return M == 1 && K <= kGemv1MaxK; }
+
+hipError_t launch_gemv1_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
+                              const float* beta_dev, int64_t K, int64_t N, void* y,
+                              termezo_dtype ydt, hipStream_t st) {
+  if (K > kGemv1MaxK || K % 16 != 0) return hipErrorInvalidValue;
+  const bool cvec = (K / 16) % 4 == 0 && reinterpret_cast<uintptr_t>(codes) % 16 == 0;
+  const int yvec = reinterpret_cast<uintptr_t>(y) % (ydt == TERMEZO_F32 ? 16 : 8) == 0;
+  const dim3 grid((unsigned)((N + 15) / 16));
+#define TMZ_G1(TX, TY, CV)                                                                     \
+  hipLaunchKernelGGL((k_gemv1_fused<TX, TY, CV>), grid, dim3(512), 0, st, (const TX*)x, codes, K, \
+                     N, beta_dev, (TY*)y, yvec)
+#define TMZ_G1X(TX, CV)                                        \
+  do {                                                          \
+    if (ydt == TERMEZO_F32) TMZ_G1(TX, float, CV); else TMZ_G1(TX, uint16_t, CV); \
+  } while (0)
+  if (xdt == TERMEZO_F32) {
+    if (cvec) TMZ_G1X(float, true); else TMZ_G1X(float, false);
+  } else {
+    if (cvec) TMZ_G1X(uint16_t, true); else TMZ_G1X(uint16_t, false);
+  }
+#undef TMZ_G1X
+#undef TMZ_G1
+  return hipGetLastError();
+}
+
 // ===========================================================================
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, int32_t* rs, hipStream_t st) {

@@ -284,6 +284,12 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs,
                           const uint32_t* codes, int64_t M, int64_t K, int64_t N,
                           const GemmOut& out, termezo_dtype ydt, int mode, int32_t* acc, int n_cu,
                           hipStream_t st);
+// One token with the activation quantisation fused in (no x_q, scale or row-sum
+// buffers): gemv1_fused_ok(M, K) tells whether it applies.
+bool gemv1_fused_ok(int64_t M, int64_t K);
+hipError_t launch_gemv1_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
+                              const float* beta_dev, int64_t K, int64_t N, void* y,
+                              termezo_dtype ydt, hipStream_t st);
 // Whether kGemmSwiGLU (full-tile path only) supports an M x K x N gate|up pair.
 bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt);
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const int32_t* rs,

@@ -491,6 +491,11 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
   const termezo_status ck = check_forward_args(c, layer, x, x_dtype, M, y, y_dtype);
   if (ck != TERMEZO_OK) return ck;
   const LayerHost& L = c->layers[layer];
+  if (!xq_out && !xscale_out && !acc_out && gemv1_fused_ok(M, L.d_in)) {
+    TMZ_HIP(c, launch_gemv1_fused(x, x_dtype, c->d_codes + L.code_off, c->d_beta_cur + layer,
+                                  L.d_in, L.d_out, y, y_dtype, c->stream));
+    return TERMEZO_OK;
+  }
   int8_t* xq = xq_out;
   float* xs = xscale_out;
   termezo_status st = ensure_xs_capacity(c, M);       // the row sums live here in any case
@@ -515,6 +520,11 @@ termezo_status termezo_bitlinear_forward_noalloc(termezo_ctx* c, int32_t layer, 
   const termezo_status ck = check_forward_args(c, layer, x, x_dtype, M, y, y_dtype);
   if (ck != TERMEZO_OK) return ck;
   const LayerHost& L = c->layers[layer];
+  if (gemv1_fused_ok(M, L.d_in)) {                    // one token: no scratch at all
+    TMZ_HIP(c, launch_gemv1_fused(x, x_dtype, c->d_codes + L.code_off, c->d_beta_cur + layer,
+                                  L.d_in, L.d_out, y, y_dtype, c->stream));
+    return TERMEZO_OK;
+  }
   // int8 activations, then the scales and the row sums, each at a 256-byte boundary
   const int64_t xq_bytes = M <= kNoAllocScratchBytes ? ((M * L.d_in + 255) / 256) * 256 : -1;
   const int64_t xs_bytes = ((4 * M + 255) / 256) * 256;

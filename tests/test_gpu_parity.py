@@ -152,6 +152,34 @@ def test_bitlinear_matches_oracle(orc, M, K, N, xdt, ydt):
     assert np.array_equal(y.float().cpu().numpy(), ry)
 
 
+@pytest.mark.parametrize("K,N", [(256, 256), (2560, 6912), (6912, 2560), (7168, 64), (256, 37),
+                                 (16, 48), (688, 100), (8192, 32),
+                                 (8208, 16)])    # beyond the fused kernel's row: two kernels
+@pytest.mark.parametrize("xdt,ydt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+def test_single_token_forward_matches_oracle(orc, K, N, xdt, ydt):
+    """One token without inspection outputs: the activation quantisation runs inside the
+    contraction kernel (one launch); the output must still be the oracle's bit for bit."""
+    torch = _torch()
+    print(f"bitlinear M=1 K={K} N={N} x={xdt} y={ydt} (fused)", flush=True)
+    ref, ctx, _ = _setup(orc, [(N, K)], bf16=False, seed=5)
+    ctx.build_mask(0.01)
+    ref.build_mask(0.01)
+    ctx.perturb(13, 1e-3, -1)
+    codes, _, betas = ref.perturb(13, 1e-3, -1)
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16}
+    for seed in (6, 7):
+        x = synth.activations(seed, 1, K, bf16=(xdt == "bf16"))
+        xd = torch.from_numpy(x).cuda().to(tdt[xdt])
+        y = torch.empty((1, N), dtype=tdt[ydt], device="cuda")
+        ctx.bitlinear_forward(0, xd, y)
+        torch.cuda.synchronize()
+        rxq, rs = orc.act_quant(x)
+        _, ry = orc.bitlinear(rxq, rs, codes[0], betas[0])
+        if ydt == "bf16":
+            ry = orc.bf16_round(ry)
+        assert np.array_equal(y.float().cpu().numpy(), ry), f"seed {seed}"
+
+
 @pytest.mark.parametrize("M,K,N,ydt", [(8192, 2560, 2560, "bf16"),   # 320 tiles: last 64 cut in quarters
                                        (8192, 1024, 2816, "bf16"),   # 352 tiles: last 96 cut in quarters
                                        (8192, 2560, 3840, "bf16"),   # 480 tiles: whole tiles only
