@@ -146,6 +146,11 @@ struct termezo_ctx {
   uint64_t pair_seed = 0;
   float pair_eps = 0.f;
   int pair_sign = 0;                 // sign whose values d_wp / d_S_cur hold
+  // the draws z of the last pair pass, list order: valid for z_seed until the active list
+  // changes; a single-direction update of that seed reads them instead of drawing again
+  float* d_zs = nullptr;
+  bool z_valid = false;
+  uint64_t z_seed = 0;
   // compact mode: the active latents in list order (latent dtype), library-owned; the
   // caller's latent tensors are no longer read or written
   bool compact = false;

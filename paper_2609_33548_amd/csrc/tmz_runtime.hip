@@ -103,15 +103,18 @@ termezo_status ensure_active_capacity(termezo_ctx* c, int64_t k) {
   dfree(c->d_act_tmp);
   dfree(c->d_wp);
   dfree(c->d_wpm);
+  dfree(c->d_zs);
   dfree(c->d_blk_cnt);
   dfree(c->d_shrink_flags);
   c->act_cap = 0;
   c->pair_valid = false;
+  c->z_valid = false;
   const int64_t cap = k > 0 ? k : 1;
   TMZ_HIP(c, dalloc(&c->d_act, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_act_tmp, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_wp, (size_t)cap));
   TMZ_HIP(c, dalloc(&c->d_wpm, (size_t)cap));
+  TMZ_HIP(c, dalloc(&c->d_zs, (size_t)cap));
   c->blk_cap = cap / 1024 + 2;   // shrink blocks hold at least 1024 entries (4 per thread)
   TMZ_HIP(c, dalloc(&c->d_blk_cnt, (size_t)c->blk_cap));
   // shrink flags, one word per thread: at most 2048 blocks below 64 entries per thread
@@ -186,6 +189,7 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_act_off_tmp);
   dfree(c->d_wp);
   dfree(c->d_wpm);
+  dfree(c->d_zs);
   dfree(c->d_hist);
   dfree(c->d_sel);
   dfree(c->d_tile_cnt);
@@ -361,6 +365,7 @@ termezo_status termezo_build_mask(termezo_ctx* c, float rho0, float delta, int32
 
   c->has_mask = false;
   c->pair_valid = false;
+  c->z_valid = false;
   c->codes_valid = false;
   c->pending_perturb = false;
   c->delta = delta;
@@ -432,11 +437,14 @@ termezo_status termezo_perturb(termezo_ctx* c, uint64_t seed, float eps, int32_t
     }
   } else {
     c->pair_valid = false;
+    if (sign != 0) c->z_valid = false;          // the pair pass below rewrites the draws
     TMZ_HIP(c, launch_copy_i64(c->d_S_cur, c->d_S_clean, c->L, c->stream));
     if (sign != 0) TMZ_HIP(c, launch_copy_i64(c->d_S_alt, c->d_S_clean, c->L, c->stream));
     TMZ_HIP(c, launch_perturb_delta(c, c->k_bound, seed, se, sign != 0));
     if (sign != 0) {
       c->pair_valid = true;
+      c->z_valid = true;
+      c->z_seed = seed;
       c->pair_seed = seed;
       c->pair_eps = eps;
       c->pair_sign = sign;
@@ -562,6 +570,7 @@ SeedList seed_list(const uint64_t* s, int32_t K) {
 termezo_status finish_update(termezo_ctx* c, const SeedList& seeds, int64_t* k_out) {
   TMZ_HIP(c, launch_update(c, c->k_bound, seeds));
   c->pair_valid = false;
+  c->z_valid = false;                          // the shrink below changes the list
   c->theta_pair_valid = false;
   c->theta_sign = 0;
   for (const ThetaHost& t : c->theta) TMZ_HIP(c, launch_theta_update(c, t, seeds));
@@ -706,6 +715,7 @@ termezo_status termezo_compact(termezo_ctx* c) {
   c->mirror = true;
   c->compact = true;
   c->pair_valid = false;
+  c->z_valid = false;
   c->k_bound = k;
   return TERMEZO_OK;
 }
@@ -742,11 +752,12 @@ termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
   int64_t b = c->D / 4;                                          // 2-bit codes
   b += L * (8 * 8 + 4 * 4 + 4 + 8 + 4 + 8) + 3 * (L + 1) * 8;    // per-layer state, offsets
   b += T * (4 + 8 + 8 + 8 + 8 + 8) + 8;                          // tile tables and scratch
-  b += cap * (4 + 4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;  // lists, w' of both signs, shrink
+  b += cap * (4 + 4 + 4 + 4 + 4) + c->blk_cap * 8 + c->flag_cap * 8;  // lists, w' of both
+                                                                    // signs, z, shrink
   b += L * 8;                                                    // |w| sums of the other sign
   if (c->mirror) b += 2 * c->wc_cap * dsz;                       // active latents (list order)
   b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;
-  b += c->xq_cap + c->xs_cap * 4;                                // activation-quant scratch
+  b += c->xq_cap + c->xs_cap * 8;                                // activation-quant scratch
   for (const ThetaHost& t : c->theta) b += 2 * t.n * (int64_t)dtype_size(t.dtype);
   if (library_bytes) *library_bytes = b;
   if (latent_bytes) *latent_bytes = c->compact ? 0 : c->D * dsz;

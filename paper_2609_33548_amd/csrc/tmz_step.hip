@@ -703,7 +703,9 @@ __device__ __forceinline__ void list4(const uint16_t* wc, int64_t j0, int n, flo
 
 // PAIR: both signs of the perturbation from one pass -- w' at +se to wp with its
 // delta in S_cur, w' at -se to wpm with its delta in S_alt (list order), so the other
-// sign of the pair needs no generator pass.  z itself is never stored.
+// sign of the pair needs no generator pass; with zs the draws z themselves go to zs
+// (list order), from which a single-direction update of the same seed reads them
+// instead of drawing again.
 template <typename T, bool PAIR>
 __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
                                                        const uint32_t* __restrict__ act,
@@ -711,7 +713,7 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
                                                        float se, float* __restrict__ wp,
                                                        const T* __restrict__ wc,
                                                        float* __restrict__ wpm,
-                                                       int64_t* S_alt) {
+                                                       int64_t* S_alt, float* __restrict__ zs) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const int64_t k = aoff[st.L];
@@ -772,6 +774,7 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
       any = true;
       put4(wp, j0, 4, v);
       if (PAIR) put4(wpm, j0, 4, vm);
+      if (PAIR && zs) put4(zs, j0, 4, z);
       continue;
     }
     for (int r = 0; r < n; ++r) {
@@ -798,6 +801,7 @@ __global__ void __launch_bounds__(256) k_perturb_delta(DevState st,
     }
     put4(wp, j0, n, v);
     if (PAIR) put4(wpm, j0, n, vm);
+    if (PAIR && zs) put4(zs, j0, n, z);
   }
   flush_delta((long long*)st.S_cur, l, acc, any);
   if (PAIR) flush_delta((long long*)S_alt, l, acc2, any);
@@ -993,7 +997,8 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
                                                 const int64_t* act_off, SeedList seeds,
                                                 const float* scal, T* __restrict__ wn,
                                                 T* __restrict__ wc,
-                                                int write_latents) {
+                                                int write_latents,
+                                                const float* __restrict__ zs) {
   __shared__ int64_t aoff[kMaxLayers + 1];
   load_offsets(aoff, act_off, st.L);
   const float a = scal[0];
@@ -1036,7 +1041,12 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       for (int r = 0; r < 4; ++r) nv[r] = wv[r];
       if (a_ok) {
         float z[4], v[4];
-        gauss_quad(seed, g0 >> 2, 0u, z);
+        if (zs) {                               // the pair pass's draws (K = 1)
+          const float4 zz = *reinterpret_cast<const float4*>(zs + j0);
+          z[0] = zz.x; z[1] = zz.y; z[2] = zz.z; z[3] = zz.w;
+        } else {
+          gauss_quad(seed, g0 >> 2, 0u, z);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] = fmaf(a, z[r], wv[r]);
         for (int q = 1; q < K; ++q) {
@@ -1073,7 +1083,7 @@ __global__ void __launch_bounds__(256) k_update(DevState st, const uint32_t* __r
       nv[r] = wv[r];
       if (a_ok) {
         const uint64_t gid = (uint64_t)(st.gid0[l] + i[r]);
-        float v = fmaf(a, zc.get(seed, gid), wv[r]);
+        float v = fmaf(a, zs ? zs[j] : zc.get(seed, gid), wv[r]);
         for (int q = 1; q < K; ++q) v = fmaf(scal[q], gauss_at(seeds.s[q], gid), v);
         nv[r] = storage_round(w, v);
         if (wc) store1(wc, j, nv[r]);
@@ -1753,24 +1763,25 @@ hipError_t launch_perturb_delta(termezo_ctx* c, int64_t k, uint64_t seed, float 
   const void* wcp = c->mirror ? c->d_wc : nullptr;
   float* wpm = pair ? c->d_wpm : nullptr;
   int64_t* sa = pair ? c->d_S_alt : nullptr;
+  float* zs = pair ? c->d_zs : nullptr;
   if (c->dtype == TERMEZO_F32) {
     if (pair)
       hipLaunchKernelGGL((k_perturb_delta<float, true>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const float*)wcp, wpm, sa);
+                         (const float*)wcp, wpm, sa, zs);
     else
       hipLaunchKernelGGL((k_perturb_delta<float, false>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const float*)wcp, wpm, sa);
+                         (const float*)wcp, wpm, sa, zs);
   } else {
     if (pair)
       hipLaunchKernelGGL((k_perturb_delta<uint16_t, true>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const uint16_t*)wcp, wpm, sa);
+                         (const uint16_t*)wcp, wpm, sa, zs);
     else
       hipLaunchKernelGGL((k_perturb_delta<uint16_t, false>), dim3(g), dim3(256), 0, c->stream,
                          c->dev(), c->d_act, c->d_act_off, seed, se, c->d_wp,
-                         (const uint16_t*)wcp, wpm, sa);
+                         (const uint16_t*)wcp, wpm, sa, zs);
   }
   return hipGetLastError();
 }
@@ -1792,14 +1803,17 @@ hipError_t launch_update(termezo_ctx* c, int64_t k, const SeedList& seeds) {
   const int64_t g = sparse_grid(k);
   void* wcp = c->mirror ? c->d_wc : nullptr;
   const int wl = c->compact ? 0 : 1;           // the caller's latents, unless dropped
+  // one direction whose draws the pair pass kept for the same active list: read them
+  const float* zs =
+      (seeds.K == 1 && c->z_valid && c->z_seed == seeds.s[0]) ? c->d_zs : nullptr;
   if (c->dtype == TERMEZO_F32)
     hipLaunchKernelGGL(k_update<float>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
                        c->d_act_off, seeds, (const float*)c->d_scal, c->d_wp, (float*)wcp,
-                       wl);
+                       wl, zs);
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(g), dim3(256), 0, c->stream, c->dev(), c->d_act,
                        c->d_act_off, seeds, (const float*)c->d_scal, (uint16_t*)c->d_wp,
-                       (uint16_t*)wcp, wl);
+                       (uint16_t*)wcp, wl, zs);
   return hipGetLastError();
 }
 
