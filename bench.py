@@ -646,7 +646,7 @@ def step_roofline(c, gemm_ops, attn_flops, lm_flops, k, dirs, ms_per_step):
                           attn_b / (HBM_PEAK_GBS * 1e9)) * 1e3
     # latent side: perturbation pair (index, w' of both signs, code word read and write per
     # active) and update (index, latent read and write, new value)
-    lat_b = dirs * 2 * 26 * k + 16 * k
+    lat_b = dirs * 2 * 26 * k + 20 * k
     parts = {"bitlinear_gemm": gemm_ops / (PEAK_INT8_TOPS * 1e12) * 1e3,
              "lm_head_ce": lm_flops / (peak_mm * 1e12) * 1e3,
              "attention": attn_ms,
@@ -710,7 +710,10 @@ def sweep_latent(torch, termezo, synth, dev, cpu, compact_mode=True, reps=10):
         t_u = up / reps
         k_after = ctx.active_count()
         b_p = D * (2 + 0.25) + k * (4 + 2)
-        b_u = 16 * k
+        # update + shrink per active: 4 B index, 2 B latent read and written, 4 B z (the pair
+        # pass's draws, read instead of drawn again), 2 B new value; the shrink reads the new
+        # value and the index and writes the index: 20 B in all
+        b_u = 20 * k
         # default path: the same codes; only the actives' codes are rewritten while the
         # threshold-drift guard holds (per active: 4 B index + 2 B latent read, 4 B w' written,
         # index and w' read again, the code word read and, where the code changes, written)
@@ -736,7 +739,10 @@ def sweep_latent(torch, termezo, synth, dev, cpu, compact_mode=True, reps=10):
             u_roof = {"bound": "latency", "frac": None, "frac_hbm": upd_gbs / HBM_PEAK_GBS,
                       "note": "microsecond-scale kernels over a few MB; reported in us"}
         else:
-            u_roof = {**valu, "frac_hbm": upd_gbs / HBM_PEAK_GBS}
+            u_roof = {**_hbm(upd_gbs),
+                      "note": "the draws come from the pair pass (no generator in the update); "
+                              "VALU busy about 65% (SQ counters in "
+                              "profiles/latent_valu_2p4e9_latents.md)"}
         u = {"ratio": r, "k": k, "k_after": k_after, "latents": D, "us": t_u * 1e6,
              "algorithmic_bytes": b_u, "GB/s": upd_gbs, "roofline": u_roof}
         if cpu:
@@ -895,8 +901,9 @@ def build_rows(args, torch, termezo, synth, dev, which, head_state=None, head_fw
         res = measure_steps(torch, head_state, 1.0, args.eps, c["lr"], steps=5, warmup=2)
         res["metric"] = "ZO steps/sec at the 2B shape with every latent active (dense MeZO)"
         res["config"]["workload"] = "termezo_zo_step_bitnet_2b_rho1"
-        res["bound_note"] = ("the GEMMs as in the headline step; the perturbation pair and the "
-                             "update (perturb_update_calls) are generator-bound at this ratio")
+        res["bound_note"] = ("the GEMMs as in the headline step; at this ratio the perturbation "
+                             "pair is generator-bound and the update (which reads the pair's "
+                             "draws) and shrink stream every latent (perturb_update_calls)")
         if cpu:
             fwd_st, fwd_mt = head_fwd if head_fwd else (None, None)
             res["cpu_baseline"] = two_legs(
@@ -1074,6 +1081,7 @@ def main():
         "config": {"workload": workload, **head["config"], "parallelism": "single_gpu"},
         "roofline": head["roofline"],
         "kernels_ms_per_step": head["kernels_ms_per_step"],
+        "step_roofline": head["step_roofline"],
         "attention_tflops": head["attention_tflops"], "lm_head_tflops": head["lm_head_tflops"],
         "mask_build_ms": head["mask_build_ms"], "memory": head["memory"],
         "cpu_baseline": cpu_head,
