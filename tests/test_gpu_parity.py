@@ -411,6 +411,32 @@ def test_guarded_requant_equals_dense_requant(orc, bf16, rho0, eps):
 
 @pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
 @pytest.mark.parametrize("rho0", [0.01, 1.0])
+def test_update_reads_kept_draws_only_for_their_seed(orc, bf16, rho0):
+    """The pair pass keeps its draws z for an update of the same seed over the same
+    active list.  An update whose last perturbation had another seed (here a sign-0
+    call after the pair) must draw z again; one whose seed matches reads them.  Both
+    give the oracle's latents, over steps that shrink the list in between."""
+    print(f"kept draws bf16={bf16} rho0={rho0}", flush=True)
+    shapes = [(256, 256), (128, 512), (64, 128)]
+    ref, ctx, tensors = _setup(orc, shapes, bf16, seed=23)
+    assert ctx.build_mask(rho0) == ref.build_mask(rho0)
+    steps = [((5, 1), (6, 0)),       # pair of seed 5, then a sign-0 call of seed 6: draw again
+             ((7, 1), (7, -1)),      # the pair of seed 7: the kept draws apply
+             ((8, -1), (8, 0)),      # sign 0 of the same seed after the pair: still apply
+             ((9, 1), (10, 0))]
+    for t, calls in enumerate(steps):
+        for sd, sign in calls:
+            ctx.perturb(sd, 1e-3, sign)
+            ref.perturb(sd, 1e-3, sign)
+        g = 30.0 - 17.0 * t
+        assert ctx.update(g, 1e-2) == ref.update(g, 1e-2)
+        assert np.array_equal(_latents_host(tensors), ref.w), f"step {t}: latents"
+        _check_mask(ref, ctx)
+    ctx.close()
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("rho0", [0.01, 1.0])
 def test_perturbation_pair_reuse(orc, bf16, rho0):
     """The first call of a (seed, eps) pair also produces the other sign's values;
     the other sign, a repeat of either sign, a pair that starts with -1, a new eps
