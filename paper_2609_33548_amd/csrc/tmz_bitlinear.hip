@@ -144,16 +144,20 @@ __device__ __forceinline__ float load_act(const float* p) { return *p; }
 __device__ __forceinline__ float load_act(const uint16_t* p) { return bf16_to_f32(*p); }
 __device__ __forceinline__ float round_act(const float*, float v) { return v; }
 __device__ __forceinline__ float round_act(const uint16_t*, float v) { return (float)(__bf16)v; }
+// Both values rounded to the activation type (bf16: one packed conversion).
+__device__ __forceinline__ void round_act2(const float*, float&, float&) {}
+__device__ __forceinline__ void round_act2(const uint16_t*, float& a, float& b) {
+  const uint32_t p = pack_bf16x2(a, b);
+  a = __uint_as_float(p << 16);
+  b = __uint_as_float(p & 0xFFFF0000u);
+}
 
 // Four consecutive activations: one 8-byte (bf16) or 16-byte (fp32) access.
 __device__ __forceinline__ void store4(float* p, const float v[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
 __device__ __forceinline__ void store4(uint16_t* p, const float v[4]) {
-  const __bf16 a = (__bf16)v[0], b = (__bf16)v[1], c = (__bf16)v[2], d = (__bf16)v[3];
-  const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
-  const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, c) | ((uint32_t)__builtin_bit_cast(uint16_t, d) << 16);
-  *reinterpret_cast<uint2*>(p) = make_uint2(w0, w1);
+  *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 }
 // h + y for a 16-byte unit of outputs, rounded to the output type.
 __device__ __forceinline__ v4u add_units(v4u h, v4u y, const float*) {
@@ -165,11 +169,9 @@ __device__ __forceinline__ v4u add_units(v4u h, v4u y, const float*) {
 __device__ __forceinline__ v4u add_units(v4u h, v4u y, const uint16_t*) {
   v4u r;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const __bf16 lo = (__bf16)(__uint_as_float(h[i] << 16) + __uint_as_float(y[i] << 16));
-    const __bf16 hi = (__bf16)(__uint_as_float(h[i] & 0xFFFF0000u) + __uint_as_float(y[i] & 0xFFFF0000u));
-    r[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
-  }
+  for (int i = 0; i < 4; ++i)
+    r[i] = pack_bf16x2(__uint_as_float(h[i] << 16) + __uint_as_float(y[i] << 16),
+                       __uint_as_float(h[i] & 0xFFFF0000u) + __uint_as_float(y[i] & 0xFFFF0000u));
   return r;
 }
 __device__ __forceinline__ void load4v(const float* p, float v[4]) {
@@ -480,13 +482,15 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     for (int j = 0; j < BJ; ++j) dma16(bsrc[j] + koff / 16, bbase + 1024u * j);
   };
 
+  // the accumulators start at -sum_k x_q of the lane's token (every register of a lane
+  // belongs to its token), so they end at sum_k x_q (w + 1) - sum_k x_q = sum_k x_q w
   v16i acc[TM][TN];
 #pragma unroll
   for (int a = 0; a < TM; ++a)
 #pragma unroll
     for (int b = 0; b < TN; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0;
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = -rsum[a];
 
   const int h = lane >> 5;
   const int arow0 = wm * WM + (lane & 31);        // A fragment row of this lane (a = 0)
@@ -620,8 +624,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
           float v4[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const float g = round_act((TY*)nullptr, (float)(acc[a][b][4 * q + j] - rsum[a]) * rg);
-            const float u = round_act((TY*)nullptr, (float)(acc[a][b][4 * q + 8 + j] - rsum[a]) * ru);
+            float g = (float)acc[a][b][4 * q + j] * rg, u = (float)acc[a][b][4 * q + 8 + j] * ru;
+            round_act2((TY*)nullptr, g, u);
             v4[j] = silu_mul(g, u);
           }
           stage4(16 * b + 8 * q + 4 * h, v4);
@@ -638,8 +642,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
         for (int q = 0; q < 4; ++q) {
           float v4[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            v4[j] = round_act((TY*)nullptr, (float)(acc[a][b][4 * q + j] - rsum[a]) * rr);
+          for (int j = 0; j < 4; ++j)   // rounded to the output type by the staging store
+            v4[j] = (float)acc[a][b][4 * q + j] * rr;
           stage4(32 * b + 8 * q + 4 * h, v4);
         }
         if (acc_out) {   // int32 accumulators (parity only), straight from the registers
@@ -647,7 +651,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
           for (int q = 0; q < 4; ++q)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-              acc_out[(m0 + mloc) * N + nb + 8 * q + 4 * h + j] = acc[a][b][4 * q + j] - rsum[a];
+              acc_out[(m0 + mloc) * N + nb + 8 * q + 4 * h + j] = acc[a][b][4 * q + j];
         }
       }
     }

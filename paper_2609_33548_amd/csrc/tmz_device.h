@@ -10,6 +10,14 @@
 
 namespace tmz {
 
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// Two floats to a packed pair of bf16 (RNE), low half = a: one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
+}
+
 // ---------------------------------------------------------------------------
 // Counter-based generator: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).
 // Key = 64-bit seed; counter = (q_lo, q_hi, stream, 0).

@@ -23,13 +23,6 @@ namespace tmz {
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
-typedef float v2f __attribute__((ext_vector_type(2)));
-typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-
-// Two floats to a packed pair of bf16 (RNE), low half = a: one v_cvt_pk_bf16_f32.
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
-}
 
 __device__ __forceinline__ float round_to(const float*, float v) { return v; }
 __device__ __forceinline__ float round_to(const uint16_t*, float v) { return (float)(__bf16)v; }
