@@ -351,14 +351,16 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 //            256: (r >> 2) & 3).
 // The swizzles keep the 16-byte fragment reads of 8 or 16 consecutive rows on
 // distinct banks.  8 waves as 2 x 4, WM x WN per wave,
-// v_mfma_i32_32x32x32_i8 with the codes as the first operand, so the
-// accumulator tile is Y^T (lane column = token).
+// v_mfma_i32_32x32x32_i8 with the activations as the first operand and the codes
+// as the second (the matrix cores run measurably faster with the few-bit code
+// values in the second operand), so a lane's accumulator column is one output
+// feature and its 16 registers are 16 tokens.
 // K assignment: in sub-step ks (32 wide) of a K step of KS = BK / 32 sub-steps,
 // lane l supplies the 16 values at k = 16 (KS (l / 32) + ks) for both operands,
 // so one 16-byte read gives a lane the codes of four sub-steps.  The codes of sub-step ks+1 are
-// unpacked between the MFMAs of sub-step ks.  The per-token output scales
-// beta' / s_m are formed in the epilogue from s_m loaded into registers at the
-// start.
+// unpacked between the MFMAs of sub-step ks.  The accumulators start at minus the
+// activation row sums (the codes enter as w + 1); the per-token output scales
+// beta' / s_m are tabulated in LDS after the main loop.
 //
 // Tiles are 256 x 256 (128 x 64 per wave).  When the last round of tiles
 // would fill at most half of the compute units, its tiles are instead cut
@@ -450,23 +452,18 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     const int brow_l = BRPI * (BJ * bw + j) + lane / BU;
     int64_t crow = n0 + brow_l;                   // code row of tile row brow_l
     if constexpr (MODE == kGemmSwiGLU) {
-      // column 32 p + c holds gate row 16 p + c (c < 16) or up row F + 16 p + c - 16, so a
-      // lane's accumulator registers r and r + 8 are the gate and up value of one feature
-      const int64_t p = crow >> 5, c = crow & 31;
-      crow = c < 16 ? 16 * p + c : (N >> 1) + 16 * p + (c - 16);
+      // column 64 p + c holds gate row 32 p + c (c < 32) or up row F + 32 p + c - 32, so
+      // a wave's column blocks b = 0 and 1 hold the gate and the up values of the same
+      // 32 features in the same lanes
+      const int64_t p = crow >> 6, c = crow & 63;
+      crow = c < 32 ? 32 * p + c : (N >> 1) + 32 * p + (c - 32);
     }
     bsrc[j] = codes + crow * KW + 4 * ((lane % BU) ^ bswz<BK>(brow_l));
   }
 
-  // per-token input scales of this lane's tokens and the segments' beta', for the epilogue
-  const int ml = lane & 31;                          // token of the lane (h: register half)
-  float sreg[TM], bet[kMaxSeg];
-  int32_t rsum[TM];                                  // sum of x_q of the lane's tokens
-#pragma unroll
-  for (int a = 0; a < TM; ++a) {
-    sreg[a] = s[m0 + wm * WM + 32 * a + ml];
-    rsum[a] = rs[m0 + wm * WM + 32 * a + ml];
-  }
+  static_assert(MODE != kGemmSwiGLU || WN == 64, "SwiGLU: gate and up blocks of one wave");
+  // the segments' beta', for the epilogue's table of output scales
+  float bet[kMaxSeg];
 #pragma unroll
   for (int sg = 0; sg < kMaxSeg; ++sg) bet[sg] = sg < out.nseg ? *out.beta[sg] : 0.0f;
 
@@ -482,17 +479,25 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     for (int j = 0; j < BJ; ++j) dma16(bsrc[j] + koff / 16, bbase + 1024u * j);
   };
 
-  // the accumulators start at -sum_k x_q of the lane's token (every register of a lane
-  // belongs to its token), so they end at sum_k x_q (w + 1) - sum_k x_q = sum_k x_q w
+  // Accumulator register r of tile (a, b) is token wm WM + 32 a + 8 (r / 4) + 4 h + r % 4
+  // and feature column wn WN + 32 b + n of the block (n = lane % 32, h = lane / 32).  It
+  // starts at -sum_k x_q of its token, so it ends at sum_k x_q (w + 1) - sum_k x_q =
+  // sum_k x_q w.
+  const int h = lane >> 5, n = lane & 31;
   v16i acc[TM][TN];
 #pragma unroll
-  for (int a = 0; a < TM; ++a)
+  for (int a = 0; a < TM; ++a) {
+    const int32_t* rp = rs + m0 + wm * WM + 32 * a + 4 * h;
 #pragma unroll
-    for (int b = 0; b < TN; ++b)
+    for (int q = 0; q < 4; ++q) {
+      const v4i r4 = *reinterpret_cast<const v4i*>(rp + 8 * q);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = -rsum[a];
+      for (int b = 0; b < TN; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[a][b][4 * q + j] = -r4[j];
+    }
+  }
 
-  const int h = lane >> 5;
   const int arow0 = wm * WM + (lane & 31);        // A fragment row of this lane (a = 0)
   const int brow0 = wn * WN + (lane & 31);
   auto compute = [&](const int8_t* As, const uint32_t* Bs) __attribute__((always_inline)) {
@@ -528,8 +533,8 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < TN; ++b)   // codes as the A operand: acc holds Y^T
-          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bfc[b], af[cur][a], acc[a][b], 0, 0, 0);
+        for (int b = 0; b < TN; ++b)   // activations first, codes second: acc holds Y
+          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[cur][a], bfc[b], acc[a][b], 0, 0, 0);
       if (ks + 1 < KS) {
         __builtin_amdgcn_sched_group_barrier(0x100, TM, 0);      // next A fragments (LDS reads)
 #pragma unroll
@@ -566,21 +571,57 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   // ---- epilogue.  Each wave stages one 32-token slice (MFMA row tile a) of its
   // outputs row-major in a private LDS region (the ring is free after the last
   // barrier), then writes whole 16-byte units, so a store instruction covers
-  // 64 / UPR tokens of UPR * 16 contiguous bytes each instead of 32 tokens of 8
-  // bytes.  Unit u of staged row r sits at unit u ^ (r % UPR).  The LDS writes
-  // and reads of one wave need no barrier: a wave's LDS operations are ordered.
+  // 64 / UPR tokens of UPR * 16 contiguous bytes each instead of scattered
+  // 2-byte values.  Unit u of staged row r sits at unit u ^ (r % UPR).  The LDS
+  // writes and reads of one wave need no barrier: a wave's LDS operations are
+  // ordered.  The output scales beta' / s_m of the block's tokens (one per segment)
+  // are computed once per block into a table after the staging regions.
   constexpr int OW = MODE == kGemmSwiGLU ? WN / 2 : WN;   // outputs per staged row
   constexpr int UB = 16 / (int)sizeof(TY);                // outputs per 16-byte unit
   constexpr int UPR = OW / UB;                            // units per staged row
   constexpr int RB = OW * (int)sizeof(TY);                // bytes per staged row
   constexpr int RPL = 32 * UPR / 64;                      // units read per lane
-  static_assert(NW * 32 * RB <= NST * (ASTAGE + BSTAGE) && RPL >= 1 && UPR <= 16,
-                "epilogue staging");
+  static_assert(NW * 32 * RB + kMaxSeg * BM * 4 <= NST * (ASTAGE + BSTAGE) && RPL >= 1 &&
+                    UPR <= 16, "epilogue staging");
   int8_t* wl = lds + wid * 32 * RB;
-  auto stage4 = [&](int f, const float v[4]) __attribute__((always_inline)) {
-    // four consecutive outputs f..f+3 of staged row ml
-    const int u = f / UB, off = (f % UB) * (int)sizeof(TY);
-    store4(reinterpret_cast<TY*>(wl + ml * RB + 16 * (u ^ (ml % UPR)) + off), v);
+  float* fac = reinterpret_cast<float*>(lds + NW * 32 * RB);   // [segment][BM]
+#pragma unroll
+  for (int sg = 0; sg < kMaxSeg; ++sg)
+    if (sg < out.nseg)
+      for (int t = tid; t < BM; t += NW * 64) fac[sg * BM + t] = __fdiv_rn(bet[sg], s[m0 + t]);
+  __syncthreads();
+  // the output scales of the lane's 16 tokens of slice a
+  auto load_fac = [&](int a, int sg, float f[16]) __attribute__((always_inline)) {
+    const float* p = fac + sg * BM + wm * WM + 32 * a + 4 * h;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = *reinterpret_cast<const float4*>(p + 8 * q);
+      f[4 * q] = v.x; f[4 * q + 1] = v.y; f[4 * q + 2] = v.z; f[4 * q + 3] = v.w;
+    }
+  };
+  // Stage the lane's 16 values (its tokens) of output column c.  bf16: the values of
+  // two consecutive tokens are packed, the lane pair (n, n ^ 1) swaps halves (one DPP
+  // move), and each lane writes one token's two adjacent outputs (the even lane the
+  // first token, the odd lane the second).
+  const uint32_t psel = (n & 1) ? 0x03020706u : 0x05040100u;
+  auto stage16 = [&](int c, const float v[16]) __attribute__((always_inline)) {
+    if constexpr (sizeof(TY) == 2) {
+      const int fc = c & ~1;
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        const uint32_t p = pack_bf16x2(v[r], v[r + 1]);
+        const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)p, 0xB1, 0xF, 0xF, false);
+        const int row = 8 * (r >> 2) + 4 * h + (r & 3) + (n & 1);
+        *reinterpret_cast<uint32_t*>(wl + row * RB + 16 * ((fc / UB) ^ (row % UPR)) + 2 * (fc % UB)) =
+            __builtin_amdgcn_perm(o, p, psel);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 8 * (r >> 2) + 4 * h + (r & 3);
+        *reinterpret_cast<float*>(wl + row * RB + 16 * ((c / UB) ^ (row % UPR)) + 4 * (c % UB)) = v[r];
+      }
+    }
   };
   const int64_t fbase = MODE == kGemmSwiGLU ? (n0 + wn * WN) / 2 : n0 + wn * WN;
   // output unit i (of RPL) of slice a of this lane
@@ -598,7 +639,7 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   };
   // residual inputs: all of a lane's units loaded up front (at most 16 units, else
   // one slice at a time) so their latency overlaps the staging
-  constexpr int HPRE = MODE == kGemmResidual ? (TM * RPL <= 16 ? TM : 1) : 0;
+  constexpr int HPRE = MODE == kGemmResidual ? (TM * RPL <= 8 ? TM : 1) : 0;
   v4u hin[HPRE > 0 ? HPRE : 1][RPL];
   if constexpr (HPRE == TM) {
 #pragma unroll
@@ -608,50 +649,37 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
   }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
-    const int mloc = wm * WM + 32 * a + ml;
     if constexpr (HPRE == 1) {
 #pragma unroll
       for (int i = 0; i < RPL; ++i) hin[0][i] = *unit_ptr(a, i);
     }
     if constexpr (MODE == kGemmSwiGLU) {
-      // registers 0..7 of a 32-column block p are gate features 16 p + 8 (r / 4) + 4 h + r % 4,
-      // registers 8..15 the up values of the same features
-      const float rg = __fdiv_rn(bet[0], sreg[a]), ru = __fdiv_rn(bet[1], sreg[a]);
+      // block 0: gate, block 1: up values of feature fbase + n
+      float fg[16], fu[16], v[16];
+      load_fac(a, 0, fg);
+      load_fac(a, 1, fu);
 #pragma unroll
-      for (int b = 0; b < TN; ++b)
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          float v4[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            float g = (float)acc[a][b][4 * q + j] * rg, u = (float)acc[a][b][4 * q + 8 + j] * ru;
-            round_act2((TY*)nullptr, g, u);
-            v4[j] = silu_mul(g, u);
-          }
-          stage4(16 * b + 8 * q + 4 * h, v4);
-        }
+      for (int r = 0; r < 16; ++r) {
+        float g = (float)acc[a][0][r] * fg[r], u = (float)acc[a][1][r] * fu[r];
+        round_act2((TY*)nullptr, g, u);
+        v[r] = silu_mul(g, u);
+      }
+      stage16(n, v);
     } else {
-      // acc[a][b] is the transposed 32 x 32 tile: lane column = token, register r =
-      // output 8 (r / 4) + 4 h + (r % 4) of the 32-column block b
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int64_t nb = n0 + wn * WN + b * 32;
         const int sg = (out.nseg > 2 && nb >= out.nstart[2]) ? 2 : (out.nseg > 1 && nb >= out.nstart[1]) ? 1 : 0;
-        const float rr = __fdiv_rn(bet[sg], sreg[a]);
+        float f[16], v[16];
+        load_fac(a, sg, f);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float v4[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j)   // rounded to the output type by the staging store
-            v4[j] = (float)acc[a][b][4 * q + j] * rr;
-          stage4(32 * b + 8 * q + 4 * h, v4);
-        }
+        for (int r = 0; r < 16; ++r)   // rounded to the output type by the staging store
+          v[r] = (float)acc[a][b][r] * f[r];
+        stage16(32 * b + n, v);
         if (acc_out) {   // int32 accumulators (parity only), straight from the registers
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              acc_out[(m0 + mloc) * N + nb + 8 * q + 4 * h + j] = acc[a][b][4 * q + j];
+          for (int r = 0; r < 16; ++r)
+            acc_out[(m0 + wm * WM + 32 * a + 8 * (r >> 2) + 4 * h + (r & 3)) * N + nb + n] = acc[a][b][r];
         }
       }
     }
@@ -1101,18 +1129,11 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
     if (!gemm_swiglu_ok(M, K, N, ydt) || out.nseg != 2 || out.nstart[1] * 2 != N || acc ||
         out.ld[0] % 8 != 0 || reinterpret_cast<uintptr_t>(out.y[0]) % 16 != 0)
       return hipErrorInvalidValue;
-    const int64_t T = (M / kDmaBM) * (N / kDmaBN), full = dma_full_tiles(T, n_cu);
-    if (use_half_tiles(M, T, n_cu))
-      hipLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)(2 * T)), dim3(256),
-                         0, st, xq, s, rs, codes, M, K, N, out, acc);
-    else if (K % 256 == 0)
-      hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU, 256>),
-                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, rs, codes, M, K,
-                         N, out, full, acc);
-    else
-      hipLaunchKernelGGL((k_gemm_i8_dma<uint16_t, kGemmSwiGLU, 128>),
-                         dim3((unsigned)(full + 4 * (T - full))), dim3(512), 0, st, xq, s, rs, codes, M, K,
-                         N, out, full, acc);
+    // always the two-blocks-per-CU tiles: their waves are 64 columns wide, the gate and
+    // the up block of 32 features each
+    const int64_t T = (M / kHalfBM) * (N / kHalfBN);
+    hipLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)T), dim3(256), 0, st,
+                       xq, s, rs, codes, M, K, N, out, acc);
     return hipGetLastError();
   }
   if (M <= kGemvMaxM) {
