@@ -1124,7 +1124,8 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
                           int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
                           int32_t* acc, int n_cu, hipStream_t st) {
-  if (!rs && M > kGemvMaxM) return hipErrorInvalidValue;   // the full-tile paths read the row sums
+  // the full-tile paths read the row sums, four tokens per 16-byte load
+  if (M > kGemvMaxM && (!rs || reinterpret_cast<uintptr_t>(rs) % 16 != 0)) return hipErrorInvalidValue;
   if (mode == kGemmSwiGLU) {
     if (!gemm_swiglu_ok(M, K, N, ydt) || out.nseg != 2 || out.nstart[1] * 2 != N || acc ||
         out.ld[0] % 8 != 0 || reinterpret_cast<uintptr_t>(out.y[0]) % 16 != 0)

@@ -282,7 +282,8 @@ hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, fl
                       hipStream_t s);
 
 // BitLinear.  The quantisers write per token the scale s and the sum of the int8
-// activations rs; the GEMM reads both (rs for its offset weight encoding).
+// activations rs; the GEMM reads both (rs, 16-byte aligned, for its offset weight
+// encoding; the full-tile paths reject a null or misaligned rs).
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, int32_t* rs, hipStream_t st);
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs,
