@@ -1091,11 +1091,15 @@ static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* 
   return hipGetLastError();
 }
 
-// Tile choice: the small-M kernel up to kGemvMaxM tokens; 256 x 256 blocks of 8 waves (128 x 64 per wave, two waves per
-// SIMD) when the grid fills the chip, 128 x 128 blocks of 4 waves otherwise;
-// the direct-to-LDS variant when every tile is in bounds and the outputs allow
-// 4-wide stores, with its last round cut into 128 x 128 quarter tiles when it
-// would fill at most half of the n_cu compute units (n_cu = 0: never).
+// Tile choice: the small-M kernel up to kGemvMaxM tokens.  When every tile is in bounds
+// and the outputs allow 4-wide stores, the direct-to-LDS kernels: 128 x 256 tiles, two
+// blocks per compute unit (k_gemm_i8_dma_h), when the 256 x 256 grid is below one round
+// of the n_cu compute units or spans at least three rounds, and always for the SwiGLU
+// gate|up product; otherwise 256 x 256 tiles of 8 waves (128 x 64 per wave, two waves per
+// SIMD) with the last round cut into 128 x 128 quarter tiles when it would fill at most
+// half of the compute units (n_cu = 0: never).  Other shapes: the register-staged
+// kernel, 256 x 256 blocks of 8 waves when the grid fills the chip, 128 x 128 blocks of 4
+// waves otherwise.
 bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt) {
   return ydt == TERMEZO_BF16 && M % kDmaBM == 0 && N % kDmaBN == 0 && K % kBK == 0 && M > 0 &&
          K > 0;
