@@ -11,9 +11,9 @@ Workload: 30 blocks, d = 2560, 20 query / 5 KV heads (head dim 128), SwiGLU FFN
 The mask is built once before the timed steps (its time is reported apart).
 
 The default run prints ONE JSON line: the headline step (steps/s, the roofline
-of the dominant kernel -- the int8 BitLinear GEMM, timed with HIP events on the
-library's stream -- and the oracle baseline on the host cores), and under
-"rows" every other measured workload of the hot path, each with its own
+of the dominant kernel -- the int8 BitLinear GEMM, each launch timed by HIP events
+that take the kernel's own start and end on the library's stream -- and the
+oracle baseline on the host cores), and under "rows" every other measured workload of the hot path, each with its own
 roofline fraction and oracle baseline (single-threaded and on all host cores):
   d1  single BitLinear layer (256 x 256, fp32, MSE), 100 steps
   d2  tiny fp32 decoder (2 blocks, d 256)

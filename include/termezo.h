@@ -364,8 +364,10 @@ termezo_status termezo_model_loss(termezo_model* model, const int32_t* tokens, i
 
 /* Event timing of the model's matrix-core kernels, for measurement: with
  * enable != 0 every following termezo_model_loss records a HIP event pair on
- * the context's stream around each launch of class 0 (BitLinear int8 GEMM),
- * 1 (attention) and 2 (LM head with cross-entropy partials); enabling or
+ * the context's stream for each launch of class 0 (BitLinear int8 GEMM) and 2
+ * (LM head with cross-entropy partials), whose events take the kernel's own
+ * start and end (hipExtLaunchKernel), and around each launch pair of class 1
+ * (attention: K/V preparation, then the attention kernel); enabling or
  * disabling clears the records.  termezo_model_timing waits for the stream and
  * returns, for one class, the summed kernel time in ms, the number of launches
  * and their algorithmic operation count (2 M K N per GEMM; 4 B H hd S(S+1)/2

@@ -1,6 +1,8 @@
 // BitLinear forward on gfx950: per-token absmax int8 activation quantisation
 // and the int8 x ternary contraction on the int8 matrix cores
 // (v_mfma_i32_32x32x32_i8), int32 accumulation, per-row rescale epilogue.
+#include <hip/hip_ext.h>
+
 #include "tmz_device.h"
 #include "tmz_internal.h"
 
@@ -762,12 +764,13 @@ __global__ void __launch_bounds__(256, 2)
 // ---------------------------------------------------------------------------
 constexpr int kGemvMaxM = 128;
 
-template <typename TY, int MODE, bool CVEC>
-__global__ void __launch_bounds__(512)
+template <typename TY, int MODE, bool CVEC, int G, int CPW>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     k_gemv_i8(const int8_t* __restrict__ xq, const float* __restrict__ s,
               const uint32_t* __restrict__ codes, int64_t M, int64_t K, int64_t N, GemmOut out,
               int yvec, int32_t* __restrict__ acc_out) {
-  constexpr int NW = 8, G = kGemvMaxM / 16;
+  constexpr int NW = 8;
+  static_assert(16 * G <= kGemvMaxM, "token groups");
   __shared__ int32_t red[NW][G][4][64];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t n0 = (int64_t)blockIdx.x * 16;
@@ -777,9 +780,9 @@ __global__ void __launch_bounds__(512)
   const int fr = lane & 15, g = lane >> 4;
   const bool row_ok = n0 + fr < N;
   const uint32_t* crow = codes + (row_ok ? n0 + fr : 0) * KW;
-  // Every load below is unconditional, from a clamped in-bounds address, and
-  // out-of-range values are zeroed afterwards: no load sits in a branch, so
-  // all of them are in flight together.
+  // Every load below reads a clamped in-bounds address and out-of-range values are
+  // zeroed afterwards; the only branches around loads are wave-uniform, so all the
+  // loads of a pass are in flight together.
   v4i acc[G];
 #pragma unroll
   for (int tg = 0; tg < G; ++tg) acc[tg] = v4i{0, 0, 0, 0};
@@ -815,30 +818,37 @@ __global__ void __launch_bounds__(512)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc_ = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[j], b[j], acc_, 0, 0, 0);
   };
-  // Two chunks per pass (c and c + NW; the second may lie beyond the matrix
-  // and then contributes zero): both chunks' loads are in flight together.
-  for (int c = wid; c < nchunk; c += 2 * NW) {
-    uint32_t cw0[4], cw1[4];
-    v4i b0[4], b1[4];
-    cload(c, cw0);
-    cload(c + NW, cw1);
-    xload(c, 0, b0);
-    xload(c + NW, 0, b1);
-    v4i a0[4], a1[4];
+  // Passes of up to CPW chunks per wave (CPW * 2048 k per pass): every code load of a
+  // pass is issued first, then the activations of each token group, so a pass costs
+  // one memory round trip.  Chunk indices are wave-uniform: chunks beyond the matrix
+  // issue no loads and contribute nothing.
+  for (int c0 = wid; c0 < nchunk; c0 += CPW * NW) {
+    uint32_t cw[CPW][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) a0[j] = unpack16(cw0[j]);
+    for (int i = 0; i < CPW; ++i) {
+      if (c0 + NW * i < nchunk) {
+        cload(c0 + NW * i, cw[i]);
+      } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) a1[j] = unpack16(cw1[j]);
-    mfma4(a0, b0, acc[0]);
-    mfma4(a1, b1, acc[0]);
-    __builtin_amdgcn_sched_barrier(0);
+        for (int j = 0; j < 4; ++j) cw[i][j] = 0u;
+      }
+    }
 #pragma unroll
-    for (int tg = 1; tg < G; ++tg) {
+    for (int tg = 0; tg < G; ++tg) {
       if (tg < ng) {
-        xload(c, tg, b0);
-        xload(c + NW, tg, b1);
-        mfma4(a0, b0, acc[tg]);
-        mfma4(a1, b1, acc[tg]);
+        v4i b[CPW][4];
+#pragma unroll
+        for (int i = 0; i < CPW; ++i)
+          if (c0 + NW * i < nchunk) xload(c0 + NW * i, tg, b[i]);
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) {
+          if (c0 + NW * i < nchunk) {
+            v4i a4[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) a4[j] = unpack16(cw[i][j]);
+            mfma4(a4, b[i], acc[tg]);
+          }
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -1030,6 +1040,224 @@ __global__ void __launch_bounds__(512)
   }
 }
 
+// ---------------------------------------------------------------------------
+// Two to sixteen tokens with the activation quantisation fused in.  Every block
+// issues its code loads first, then reads all M activation rows (half a wave per
+// row, the row held in registers), forms each row's a = max |x| and
+// s = 127 / max(a, 1e-5) with a half-wave reduction and quantises the rows into LDS
+// with the operations of k_act_quant, then contracts its FG groups of 16 output
+// features as k_gemv_i8 does (one 16-token MFMA group, activations read from LDS).
+// One launch per call instead of two, and no x_q, scale or row-sum buffers.  Every
+// block quantises all M rows itself (VALU work that grows with M K), so the launcher
+// takes this kernel only for small M K, and two feature groups per block where one
+// would need more than a round of blocks.  Rows are held packed (bf16: 8 values per
+// 16 bytes) up to KMAX values, at most ROWS rows; LDS rows are padded by 16 bytes so
+// the 16 token rows of a fragment read fall in distinct banks.
+// ---------------------------------------------------------------------------
+constexpr int kGemvFusedMaxM = 16;
+constexpr int64_t kGemvFusedMaxMK = 16 * 2560;      // rows x values quantised per block
+
+template <typename TX> struct RowChunk;            // 8 activations as loaded
+template <> struct RowChunk<uint16_t> {
+  uint4 v;
+  __device__ __forceinline__ void load(const uint16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void zero() { v = make_uint4(0u, 0u, 0u, 0u); }
+  __device__ __forceinline__ void launder() {
+    asm volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+  }
+  __device__ __forceinline__ void get(float o[8]) const {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      o[2 * j] = __uint_as_float(w[j] << 16);
+      o[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+    }
+  }
+};
+template <> struct RowChunk<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ void zero() { a = b = make_float4(0.f, 0.f, 0.f, 0.f); }
+  __device__ __forceinline__ void launder() {}
+  __device__ __forceinline__ void get(float o[8]) const {
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+};
+
+template <typename TX, typename TY, bool CVEC, int KMAX, int ROWS, int FG>
+__global__ void __launch_bounds__(512)
+    k_gemv_fused(const TX* __restrict__ x, const uint32_t* __restrict__ codes, int64_t M,
+                 int64_t K, int64_t N, const float* __restrict__ beta, TY* __restrict__ y,
+                 int yvec) {
+  constexpr int NW = 8;
+  constexpr int CPW = (KMAX + 256 * NW - 1) / (256 * NW);  // 256-k chunks per wave at most
+  constexpr int XI = KMAX / (8 * 32);                       // 8-value chunks of a row per lane
+  constexpr int LROW = KMAX + 16;                           // LDS row stride in bytes
+  static_assert(KMAX % 256 == 0 && ROWS <= 2 * NW && FG <= NW, "row layout");
+  __shared__ __attribute__((aligned(16))) int8_t xql[ROWS * LROW];
+  __shared__ int32_t red[NW][FG][4][64];
+  __shared__ float scl[ROWS];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t n0 = (int64_t)blockIdx.x * 16 * FG;
+  const int64_t KW = K / 16;
+  const int nchunk = (int)((KW + 15) / 16);
+  const int fr = lane & 15, g = lane >> 4;
+  // this wave's code words (chunks wid, wid + NW, ...) of each feature group, zero
+  // outside the matrix
+  uint32_t cw[FG][CPW][4];
+#pragma unroll
+  for (int f = 0; f < FG; ++f) {
+    const bool row_ok = n0 + 16 * f + fr < N;
+    const uint32_t* crow = codes + (row_ok ? n0 + 16 * f + fr : 0) * KW;
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int64_t w0 = (int64_t)(wid + NW * i) * 16 + 4 * g;
+      if (CVEC) {
+        const v4u v = *reinterpret_cast<const v4u*>(crow + (w0 < KW ? w0 : 0));
+        const bool ok = row_ok && w0 < KW;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cw[f][i][j] = ok ? v[j] : 0u;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t v = crow[w0 + j < KW ? w0 + j : 0];
+          cw[f][i][j] = (row_ok && w0 + j < KW) ? v : 0u;
+        }
+      }
+    }
+  }
+  // token row r = 2 wid + (lane / 32), chunk (it * 32 + lane % 32) of 8 values
+  const int r = 2 * wid + (lane >> 5), j32 = lane & 31;
+  const bool rok = r < M;
+  const TX* xr = x + (rok ? r : 0) * K;
+  RowChunk<TX> xv[XI];
+  float a = 0.0f;
+#pragma unroll
+  for (int it = 0; it < XI; ++it) {
+    const int64_t k = ((int64_t)it * 32 + j32) * 8;
+    if (rok && k < K) xv[it].load(xr + k); else xv[it].zero();
+    float v[8];
+    xv[it].get(v);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) a = fmaxf(a, fabsf(v[t]));
+  }
+#pragma unroll
+  for (int off = 16; off > 0; off >>= 1) a = fmaxf(a, __shfl_xor(a, off, 32));
+  const float sc = __fdiv_rn(127.0f, fmaxf(a, 1e-5f));
+  if (rok) {
+    if (j32 == 0) scl[r] = sc;
+#pragma unroll
+    for (int it = 0; it < XI; ++it) {
+      const int64_t k = ((int64_t)it * 32 + j32) * 8;
+      if (k < K) {
+        float v[8];
+        xv[it].launder();                               // keep the row packed until here
+        xv[it].get(v);
+        uint32_t w[2];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          uint32_t b = 0;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) b |= ((uint32_t)quant_byte(v[4 * h2 + t], sc) & 0xFFu) << (8 * t);
+          w[h2] = b;
+        }
+        *reinterpret_cast<uint2*>(xql + r * LROW + k) = make_uint2(w[0], w[1]);
+      }
+    }
+  }
+  __syncthreads();
+  // contraction: token fr of the MFMA group (token rows at or beyond M only feed their
+  // own accumulator column, which is never stored)
+  v4i acc[FG];
+#pragma unroll
+  for (int f = 0; f < FG; ++f) acc[f] = v4i{0, 0, 0, 0};
+  const int8_t* xl = xql + (fr < ROWS ? fr : 0) * LROW;
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int c = wid + NW * i;
+    if (c < nchunk) {                                   // wave-uniform
+      const int64_t kb = ((int64_t)c * 16 + 4 * g) * 16;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int64_t k = kb + 16 * jj;
+        v4i b = *reinterpret_cast<const v4i*>(xl + (k < K ? k : 0));
+        if (!(k < K)) b = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int f = 0; f < FG; ++f)
+          acc[f] = __builtin_amdgcn_mfma_i32_16x16x64_i8(unpack16(cw[f][i][jj]), b, acc[f], 0, 0, 0);
+      }
+    }
+  }
+#pragma unroll
+  for (int f = 0; f < FG; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wid][f][i][lane] = acc[f][i];
+  __syncthreads();
+  if (wid < FG && fr < M) {                             // wave f: token fr, features 4 g ..
+    const int64_t n = n0 + 16 * wid + 4 * g;
+    if (n < N) {
+      const float rr = __fdiv_rn(*beta, scl[fr]);
+      float y4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int32_t v = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) v += red[w][wid][i][lane];
+        y4[i] = (float)v * rr;
+      }
+      TY* yr = y + (int64_t)fr * N;
+      if (yvec && n + 3 < N) {
+        store4(yr + n, y4);
+      } else {
+        for (int i = 0; i < 4 && n + i < N; ++i) store_act(yr + n + i, y4[i]);
+      }
+    }
+  }
+}
+
+// Longer rows are held for at most 5 tokens (5 x 8192 values quantised per block).
+bool gemv_fused_ok(int64_t M, int64_t K, termezo_dtype xdt) {
+  return M >= 2 && M <= kGemvFusedMaxM && M * K <= kGemvFusedMaxMK &&
+         (K <= 4096 || (xdt == TERMEZO_BF16 && K <= 8192));
+}
+
+hipError_t launch_gemv_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
+                             const float* beta_dev, int64_t M, int64_t K, int64_t N, void* y,
+                             termezo_dtype ydt, int n_cu, hipStream_t st) {
+  if (!gemv_fused_ok(M, K, xdt) || K % 16 != 0) return hipErrorInvalidValue;
+  const bool cvec = (K / 16) % 4 == 0 && reinterpret_cast<uintptr_t>(codes) % 16 == 0;
+  const int yvec =
+      N % 4 == 0 && reinterpret_cast<uintptr_t>(y) % (ydt == TERMEZO_F32 ? 16 : 8) == 0;
+  const bool two = (N + 15) / 16 > (n_cu > 0 ? n_cu : 256);   // two feature groups per block
+  const dim3 grid((unsigned)(two ? (N + 31) / 32 : (N + 15) / 16));
+#define TMZ_GF(TX, TY, CV, KM, RW, FGV)                                                         \
+  hipLaunchKernelGGL((k_gemv_fused<TX, TY, CV, KM, RW, FGV>), grid, dim3(512), 0, st,           \
+                     (const TX*)x, codes, M, K, N, beta_dev, (TY*)y, yvec)
+#define TMZ_GFG(TX, TY, CV, KM, RW)                                     \
+  do {                                                                  \
+    if (two) TMZ_GF(TX, TY, CV, KM, RW, 2); else TMZ_GF(TX, TY, CV, KM, RW, 1); \
+  } while (0)
+#define TMZ_GFY(TX, CV, KM, RW)                                                               \
+  do {                                                                                        \
+    if (ydt == TERMEZO_F32) TMZ_GFG(TX, float, CV, KM, RW); else TMZ_GFG(TX, uint16_t, CV, KM, RW); \
+  } while (0)
+  if (xdt == TERMEZO_F32) {
+    if (cvec) TMZ_GFY(float, true, 4096, 16); else TMZ_GFY(float, false, 4096, 16);
+  } else if (K <= 4096) {
+    if (cvec) TMZ_GFY(uint16_t, true, 4096, 16); else TMZ_GFY(uint16_t, false, 4096, 16);
+  } else {
+    if (cvec) TMZ_GFY(uint16_t, true, 8192, 5); else TMZ_GFY(uint16_t, false, 8192, 5);
+  }
+#undef TMZ_GFY
+#undef TMZ_GFG
+#undef TMZ_GF
+  return hipGetLastError();
+}
+
 bool gemv1_fused_ok(int64_t M, int64_t K) { return M == 1 && K <= kGemv1MaxK; }
 
 hipError_t launch_gemv1_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
@@ -1070,23 +1298,23 @@ hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t
 template <int BM, int BN, int WM, int WN, bool FULL>
 static hipError_t launch_tile(const int8_t* xq, const float* s, const uint32_t* codes, int64_t M,
                               int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
-                              int32_t* acc, hipStream_t st) {
+                              int32_t* acc, hipStream_t st, LaunchEvents ev) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   dim3 grid((unsigned)(((N + BN - 1) / BN) * ((M + BM - 1) / BM)));
   if (ydt == TERMEZO_F32) {
     if (mode == kGemmStore)
-      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, float, kGemmStore>), grid, dim3(NT), 0, st,
-                         xq, s, codes, M, K, N, out, acc);
+      hipExtLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, float, kGemmStore>), grid, dim3(NT), 0,
+                            st, ev.start, ev.stop, 0, xq, s, codes, M, K, N, out, acc);
     else
-      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, float, kGemmResidual>), grid, dim3(NT), 0,
-                         st, xq, s, codes, M, K, N, out, acc);
+      hipExtLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, float, kGemmResidual>), grid, dim3(NT),
+                            0, st, ev.start, ev.stop, 0, xq, s, codes, M, K, N, out, acc);
   } else {
     if (mode == kGemmStore)
-      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, uint16_t, kGemmStore>), grid, dim3(NT), 0,
-                         st, xq, s, codes, M, K, N, out, acc);
+      hipExtLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, uint16_t, kGemmStore>), grid, dim3(NT),
+                            0, st, ev.start, ev.stop, 0, xq, s, codes, M, K, N, out, acc);
     else
-      hipLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, uint16_t, kGemmResidual>), grid, dim3(NT),
-                         0, st, xq, s, codes, M, K, N, out, acc);
+      hipExtLaunchKernelGGL((k_gemm_i8<BM, BN, WM, WN, FULL, uint16_t, kGemmResidual>), grid,
+                            dim3(NT), 0, st, ev.start, ev.stop, 0, xq, s, codes, M, K, N, out, acc);
   }
   return hipGetLastError();
 }
@@ -1127,7 +1355,7 @@ static int64_t dma_full_tiles(int64_t T, int n_cu) {
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, const uint32_t* codes,
                           int64_t M,
                           int64_t K, int64_t N, const GemmOut& out, termezo_dtype ydt, int mode,
-                          int32_t* acc, int n_cu, hipStream_t st) {
+                          int32_t* acc, int n_cu, hipStream_t st, LaunchEvents ev) {
   // the full-tile paths read the row sums, four tokens per 16-byte load
   if (M > kGemvMaxM && (!rs || reinterpret_cast<uintptr_t>(rs) % 16 != 0)) return hipErrorInvalidValue;
   if (mode == kGemmSwiGLU) {
@@ -1137,8 +1365,8 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
     // always the two-blocks-per-CU tiles: their waves are 64 columns wide, the gate and
     // the up block of 32 features each
     const int64_t T = (M / kHalfBM) * (N / kHalfBN);
-    hipLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)T), dim3(256), 0, st,
-                       xq, s, rs, codes, M, K, N, out, acc);
+    hipExtLaunchKernelGGL((k_gemm_i8_dma_h<uint16_t, kGemmSwiGLU>), dim3((unsigned)T), dim3(256), 0,
+                          st, ev.start, ev.stop, 0, xq, s, rs, codes, M, K, N, out, acc);
     return hipGetLastError();
   }
   if (M <= kGemvMaxM) {
@@ -1151,9 +1379,16 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
       for (int i = 0; i < out.nseg; ++i)
         yvec = yvec && out.ld[i] % 4 == 0 && reinterpret_cast<uintptr_t>(out.y[i]) % vec == 0;
       dim3 grid((unsigned)((N + 15) / 16));
+      // up to 16 tokens: one token group, 8192 k per pass; more: 8 groups, 4096 k
 #define TMZ_GEMV(TY, MD, CV)                                                                    \
-  hipLaunchKernelGGL((k_gemv_i8<TY, MD, CV>), grid, dim3(512), 0, st, xq, s, codes, M, K, N, out, \
-                     yvec, acc)
+  do {                                                                                          \
+    if (M <= 16)                                                                                \
+      hipExtLaunchKernelGGL((k_gemv_i8<TY, MD, CV, 1, 4>), grid, dim3(512), 0, st, ev.start,    \
+                            ev.stop, 0, xq, s, codes, M, K, N, out, yvec, acc);                 \
+    else                                                                                        \
+      hipExtLaunchKernelGGL((k_gemv_i8<TY, MD, CV, kGemvMaxM / 16, 2>), grid, dim3(512), 0, st, \
+                            ev.start, ev.stop, 0, xq, s, codes, M, K, N, out, yvec, acc);       \
+  } while (0)
       const bool f32 = ydt == TERMEZO_F32, store = mode == kGemmStore;
       if (cvec) {
         if (f32) { if (store) TMZ_GEMV(float, kGemmStore, true); else TMZ_GEMV(float, kGemmResidual, true); }
@@ -1179,7 +1414,8 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
       if (use_half_tiles(M, T, n_cu)) {
         dim3 gh((unsigned)(2 * T));
 #define TMZ_HALF(TY, MD) \
-  hipLaunchKernelGGL((k_gemm_i8_dma_h<TY, MD>), gh, dim3(256), 0, st, xq, s, rs, codes, M, K, N, out, acc)
+  hipExtLaunchKernelGGL((k_gemm_i8_dma_h<TY, MD>), gh, dim3(256), 0, st, ev.start, ev.stop, 0, xq, s, rs, \
+                        codes, M, K, N, out, acc)
         if (ydt == TERMEZO_F32) {
           if (mode == kGemmStore) TMZ_HALF(float, kGemmStore); else TMZ_HALF(float, kGemmResidual);
         } else {
@@ -1192,8 +1428,8 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
       const int64_t full = T < n_cu ? 0 : dma_full_tiles(T, n_cu);
       dim3 grid((unsigned)(full + 4 * (T - full)));
 #define TMZ_DMA(TY, MD, BK) \
-  hipLaunchKernelGGL((k_gemm_i8_dma<TY, MD, BK>), grid, dim3(512), 0, st, xq, s, rs, codes, M, K, N, out, full, \
-                     acc)
+  hipExtLaunchKernelGGL((k_gemm_i8_dma<TY, MD, BK>), grid, dim3(512), 0, st, ev.start, ev.stop, 0, xq, s, \
+                        rs, codes, M, K, N, out, full, acc)
 #define TMZ_DMA_K(TY, MD) \
   do {                                                 \
     if (K % 256 == 0) TMZ_DMA(TY, MD, 256); else TMZ_DMA(TY, MD, 128); \
@@ -1207,9 +1443,9 @@ hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs, c
 #undef TMZ_DMA
       return hipGetLastError();
     }
-    return launch_tile<256, 256, 128, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
+    return launch_tile<256, 256, 128, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st, ev);
   }
-  return launch_tile<128, 128, 64, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st);
+  return launch_tile<128, 128, 64, 64, false>(xq, s, codes, M, K, N, out, ydt, mode, acc, st, ev);
 }
 
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const int32_t* rs,

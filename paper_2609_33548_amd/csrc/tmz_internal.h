@@ -286,16 +286,27 @@ hipError_t launch_mse(const float* y, const float* t, int64_t n, double* acc, fl
 // encoding; the full-tile paths reject a null or misaligned rs).
 hipError_t launch_act_quant(const void* x, termezo_dtype xdt, int64_t M, int64_t K, int8_t* xq,
                             float* s, int32_t* rs, hipStream_t st);
+// Optional timing of one GEMM launch: non-null events take the start and the end of the
+// kernel's own execution (hipExtLaunchKernel), not the time around the launch.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
 hipError_t launch_gemm_i8(const int8_t* xq, const float* s, const int32_t* rs,
                           const uint32_t* codes, int64_t M, int64_t K, int64_t N,
                           const GemmOut& out, termezo_dtype ydt, int mode, int32_t* acc, int n_cu,
-                          hipStream_t st);
+                          hipStream_t st, LaunchEvents ev = LaunchEvents());
 // One token with the activation quantisation fused in (no x_q, scale or row-sum
 // buffers): gemv1_fused_ok(M, K) tells whether it applies.
 bool gemv1_fused_ok(int64_t M, int64_t K);
 hipError_t launch_gemv1_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
                               const float* beta_dev, int64_t K, int64_t N, void* y,
                               termezo_dtype ydt, hipStream_t st);
+// Two to sixteen tokens with the activation quantisation fused in (no inspection
+// outputs): gemv_fused_ok(M, K, xdt) tells whether it applies.
+bool gemv_fused_ok(int64_t M, int64_t K, termezo_dtype xdt);
+hipError_t launch_gemv_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
+                             const float* beta_dev, int64_t M, int64_t K, int64_t N, void* y,
+                             termezo_dtype ydt, int n_cu, hipStream_t st);
 // Whether kGemmSwiGLU (full-tile path only) supports an M x K x N gate|up pair.
 bool gemm_swiglu_ok(int64_t M, int64_t K, int64_t N, termezo_dtype ydt);
 hipError_t launch_bitlinear_gemm(const int8_t* xq, const float* s, const int32_t* rs,

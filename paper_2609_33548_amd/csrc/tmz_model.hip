@@ -15,6 +15,8 @@
 #include <type_traits>
 #include <vector>
 
+#include <hip/hip_ext.h>
+
 #include "tmz_device.h"
 #include "tmz_internal.h"
 
@@ -1643,6 +1645,23 @@ void span_end(termezo_model* m, int idx, hipStream_t s) {
   if (idx >= 0) (void)hipEventRecord(m->spans[idx].b, s);
 }
 
+// A span whose events the launch itself sets to its kernel's start and end (GEMMs).
+LaunchEvents span_kernel(termezo_model* m, int cls, double ops) {
+  LaunchEvents ev;
+  if (!m->timing) return ev;
+  if (m->used == m->spans.size()) {
+    termezo_model::Span sp{};
+    if (hipEventCreate(&sp.a) != hipSuccess || hipEventCreate(&sp.b) != hipSuccess) return ev;
+    m->spans.push_back(sp);
+  }
+  termezo_model::Span& sp = m->spans[m->used++];
+  sp.cls = cls;
+  sp.ops = ops;
+  ev.start = sp.a;
+  ev.stop = sp.b;
+  return ev;
+}
+
 void model_free_buffers(termezo_model* m) {
   mfree(m->h); mfree(m->q); mfree(m->k); mfree(m->v); mfree(m->vt); mfree(m->attn); mfree(m->g);
   mfree(m->u);
@@ -1959,10 +1978,9 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     o3.y[1] = m->k; o3.ld[1] = dkv; o3.beta[1] = c->d_beta_cur + l0 + 1;
     o3.y[2] = m->v; o3.ld[2] = dkv; o3.beta[2] = c->d_beta_cur + l0 + 2;
     o3.nstart[0] = 0; o3.nstart[1] = dq; o3.nstart[2] = dq + dkv; o3.nstart[3] = dq + 2 * dkv;
-    int sp = span_begin(m, 0, 2.0 * M * d * (dq + 2 * dkv), s);
     chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
-                       kGemmStore, nullptr, c->n_cu, s));
-    span_end(m, sp, s);
+                       kGemmStore, nullptr, c->n_cu, s,
+                       span_kernel(m, 0, 2.0 * M * d * (dq + 2 * dkv))));
     if (!bf) {   // bf16: the rotation is applied inside the attention kernel
       const unsigned rg =
           (unsigned)std::min<int64_t>(8192, (M * cf.n_heads * (m->hd / 2) + 255) / 256);
@@ -1972,7 +1990,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                          cf.n_kv_heads, m->hd, seq, m->rope_c, m->rope_s);
       chk(hipGetLastError());
     }
-    sp = span_begin(m, 1, 4.0 * batch * cf.n_heads * m->hd * (0.5 * seq * (seq + 1.0)), s);
+    const int sp = span_begin(m, 1, 4.0 * batch * cf.n_heads * m->hd * (0.5 * seq * (seq + 1.0)), s);
     chk(run_attention(m, batch, seq, s));
     span_end(m, sp, s);
     if (bf)
@@ -1987,10 +2005,9 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     oo.nseg = 1;
     oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = c->d_beta_cur + l0 + 3;
     oo.nstart[0] = 0; oo.nstart[1] = d;
-    sp = span_begin(m, 0, 2.0 * M * dq * d, s);
     chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
-                       nullptr, c->n_cu, s));
-    span_end(m, sp, s);
+                       nullptr, c->n_cu, s,
+                       span_kernel(m, 0, 2.0 * M * dq * d)));
     // MLP sub-block
     rmsq(m->xq, m->xs, nullptr, 2 * blk + 1);
     GemmOut o2 = {};
@@ -2001,10 +2018,9 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     // gate|up with the SwiGLU in the epilogue where the full-tile path applies (the
     // product lands in g), else the two projections and the SwiGLU row kernel
     const bool fused = gemm_swiglu_ok(M, d, 2 * F, adt);
-    sp = span_begin(m, 0, 2.0 * M * d * 2 * F, s);
     chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt,
-                       fused ? kGemmSwiGLU : kGemmStore, nullptr, c->n_cu, s));
-    span_end(m, sp, s);
+                       fused ? kGemmSwiGLU : kGemmStore, nullptr, c->n_cu, s,
+                       span_kernel(m, 0, 2.0 * M * d * 2 * F)));
     if (fused)
       row_launch<kRowQuant, uint16_t>(rowg, s, (const uint16_t*)m->g, (const uint16_t*)nullptr, M,
                                       F, 0.0f, m->xq, m->xs, m->xrs, (uint16_t*)nullptr, c->n_cu);
@@ -2019,31 +2035,29 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     od.nseg = 1;
     od.y[0] = m->h; od.ld[0] = d; od.beta[0] = c->d_beta_cur + l0 + 6;
     od.nstart[0] = 0; od.nstart[1] = d;
-    sp = span_begin(m, 0, 2.0 * M * F * d, s);
     chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
-                       nullptr, c->n_cu, s));
-    span_end(m, sp, s);
+                       nullptr, c->n_cu, s,
+                       span_kernel(m, 0, 2.0 * M * F * d)));
   }
   rmsq(nullptr, nullptr, m->xf, 2 * cf.n_blocks);
-  const int sp_lm = span_begin(m, 2, 2.0 * M * d * cf.vocab, s);
+  const LaunchEvents ev_lm = span_kernel(m, 2, 2.0 * M * d * cf.vocab);
   if (bf) {
     const unsigned nb = (unsigned)(nvt * ((M + kLmTile - 1) / kLmTile));
     if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % 64 == 0)
-      hipLaunchKernelGGL((k_lmhead_dma<kLmDmaStages, kLmDmaBK, kLmDmaNWN>), dim3(nb), dim3(128 * kLmDmaNWN), 0, s,
-                         (const uint16_t*)m->xf,
-                         (const uint16_t*)emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
-                         m->psum, m->lab, nvt);
+      hipExtLaunchKernelGGL((k_lmhead_dma<kLmDmaStages, kLmDmaBK, kLmDmaNWN>), dim3(nb),
+                            dim3(128 * kLmDmaNWN), 0, s, ev_lm.start, ev_lm.stop, 0,
+                            (const uint16_t*)m->xf, (const uint16_t*)emb, M, d, (int64_t)cf.vocab,
+                            m->labels, m->pmax, m->psum, m->lab, nvt);
     else
-      hipLaunchKernelGGL(k_lmhead_bf16<false>, dim3(nb), dim3(512), 0, s, (const uint16_t*)m->xf,
-                         (const uint16_t*)emb, M, d, (int64_t)cf.vocab, m->labels, m->pmax,
-                         m->psum, m->lab, nvt);
+      hipExtLaunchKernelGGL(k_lmhead_bf16<false>, dim3(nb), dim3(512), 0, s, ev_lm.start,
+                            ev_lm.stop, 0, (const uint16_t*)m->xf, (const uint16_t*)emb, M, d,
+                            (int64_t)cf.vocab, m->labels, m->pmax, m->psum, m->lab, nvt);
   }
   else
-    hipLaunchKernelGGL(k_lmhead_f32, dim3((unsigned)nvt, (unsigned)((M + 1) / 2)), dim3(256), 0, s,
-                       (const float*)m->xf, (const float*)emb, M, d, (int64_t)cf.vocab,
-                       m->labels, m->pmax, m->psum, m->lab, nvt);
+    hipExtLaunchKernelGGL(k_lmhead_f32, dim3((unsigned)nvt, (unsigned)((M + 1) / 2)), dim3(256), 0,
+                          s, ev_lm.start, ev_lm.stop, 0, (const float*)m->xf, (const float*)emb, M,
+                          d, (int64_t)cf.vocab, m->labels, m->pmax, m->psum, m->lab, nvt);
   chk(hipGetLastError());
-  span_end(m, sp_lm, s);
   float* rows = row_loss_dev ? row_loss_dev : m->row;
   hipLaunchKernelGGL(k_ce_combine, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, m->pmax,
                      m->psum, m->lab, M, nvt, seq, rows);

@@ -504,6 +504,11 @@ termezo_status termezo_bitlinear_forward(termezo_ctx* c, int32_t layer, const vo
                                   L.d_in, L.d_out, y, y_dtype, c->stream));
     return TERMEZO_OK;
   }
+  if (!xq_out && !xscale_out && !acc_out && gemv_fused_ok(M, L.d_in, x_dtype)) {
+    TMZ_HIP(c, launch_gemv_fused(x, x_dtype, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
+                                 L.d_in, L.d_out, y, y_dtype, c->n_cu, c->stream));
+    return TERMEZO_OK;
+  }
   int8_t* xq = xq_out;
   float* xs = xscale_out;
   termezo_status st = ensure_xs_capacity(c, M);       // the row sums live here in any case
@@ -531,6 +536,11 @@ termezo_status termezo_bitlinear_forward_noalloc(termezo_ctx* c, int32_t layer, 
   if (gemv1_fused_ok(M, L.d_in)) {                    // one token: no scratch at all
     TMZ_HIP(c, launch_gemv1_fused(x, x_dtype, c->d_codes + L.code_off, c->d_beta_cur + layer,
                                   L.d_in, L.d_out, y, y_dtype, c->stream));
+    return TERMEZO_OK;
+  }
+  if (gemv_fused_ok(M, L.d_in, x_dtype)) {             // up to 16 tokens: none either
+    TMZ_HIP(c, launch_gemv_fused(x, x_dtype, c->d_codes + L.code_off, c->d_beta_cur + layer, M,
+                                 L.d_in, L.d_out, y, y_dtype, c->n_cu, c->stream));
     return TERMEZO_OK;
   }
   // int8 activations, then the scales and the row sums, each at a 256-byte boundary

@@ -180,6 +180,42 @@ def test_single_token_forward_matches_oracle(orc, K, N, xdt, ydt):
         assert np.array_equal(y.float().cpu().numpy(), ry), f"seed {seed}"
 
 
+@pytest.mark.parametrize("M,K,N", [(2, 256, 256), (16, 2560, 2560), (5, 688, 100), (9, 256, 37),
+                                   (3, 16, 48),
+                                   (16, 2560, 6912),    # two feature groups per block
+                                   (2, 2560, 6912),
+                                   (16, 2048, 8200),    # two groups, the last one ragged
+                                   (16, 6912, 2560),    # M K above the fused bound: two kernels
+                                   (10, 4096, 64),      # the longest fp32 row of the fused kernel
+                                   (2, 4112, 48),       # fp32: two kernels; bf16: fused
+                                   (5, 8192, 32),       # the longest bf16 row of the fused kernel
+                                   (7, 8208, 16)])      # beyond it: two kernels
+@pytest.mark.parametrize("xdt,ydt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+def test_few_token_forward_matches_oracle(orc, M, K, N, xdt, ydt):
+    """Two to sixteen tokens without inspection outputs: every block quantises the token
+    rows itself and contracts its features in one launch; the outputs must be the
+    oracle's bit for bit, two calls in a row with new activations."""
+    torch = _torch()
+    print(f"bitlinear M={M} K={K} N={N} x={xdt} y={ydt} (fused, few tokens)", flush=True)
+    ref, ctx, _ = _setup(orc, [(N, K)], bf16=False, seed=9)
+    ctx.build_mask(0.01)
+    ref.build_mask(0.01)
+    ctx.perturb(17, 1e-3, 1)
+    codes, _, betas = ref.perturb(17, 1e-3, 1)
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16}
+    for seed in (21, 22):
+        x = synth.activations(seed, M, K, bf16=(xdt == "bf16"))
+        xd = torch.from_numpy(x).cuda().to(tdt[xdt])
+        y = torch.empty((M, N), dtype=tdt[ydt], device="cuda")
+        ctx.bitlinear_forward(0, xd, y)
+        torch.cuda.synchronize()
+        rxq, rs = orc.act_quant(x)
+        _, ry = orc.bitlinear(rxq, rs, codes[0], betas[0])
+        if ydt == "bf16":
+            ry = orc.bf16_round(ry)
+        assert np.array_equal(y.float().cpu().numpy(), ry), f"seed {seed}"
+
+
 @pytest.mark.parametrize("M,K,N,ydt", [(8192, 2560, 2560, "bf16"),   # 320 tiles: last 64 cut in quarters
                                        (8192, 1024, 2816, "bf16"),   # 352 tiles: last 96 cut in quarters
                                        (8192, 2560, 3840, "bf16"),   # 480 tiles: whole tiles only

@@ -19,7 +19,7 @@ def _torch():
 
 
 @pytest.mark.parametrize("shape,Ms,dt", [
-    ((2560, 2560), (1000, 16), "bf16"),
+    ((2560, 2560), (1000, 40), "bf16"),
     ((640, 688), (300, 37), "f32"),
     ((6912, 2560), (2048, 1), "bf16"),
 ])
