@@ -502,9 +502,23 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
 
   const int arow0 = wm * WM + (lane & 31);        // A fragment row of this lane (a = 0)
   const int brow0 = wn * WN + (lane & 31);
-  auto compute = [&](const int8_t* As, const uint32_t* Bs) __attribute__((always_inline)) {
-    v4i af[2][TM];
-    v4i bq[HK][TN], bfc[TN], bfn[TN];
+  // Fragments live across K steps: the first A fragments and the packed codes of the
+  // next stage are read right after the barrier that ends a stage, ahead of that
+  // stage's last MFMA sub-step (whose operands are already in registers), so their LDS
+  // latency and the first code unpacking fall under MFMAs instead of stalling both
+  // waves of each SIMD at every stage boundary.
+  v4i af[2][TM];
+  v4i bq[HK][TN], bfc[TN], bfn[TN];
+  auto afrag = [&](const int8_t* As, int ks, int slot) __attribute__((always_inline)) {
+    const int c = (ACH / 2) * h + ks;                // logical 16-byte chunk
+#pragma unroll
+    for (int a = 0; a < TM; ++a) {
+      const int row = arow0 + 32 * a;
+      af[slot][a] = *reinterpret_cast<const v4i*>(As + row * AROW + 16 * (c ^ aswz<BK>(row)));
+    }
+  };
+  // the packed codes of a stage and its first A fragments
+  auto first = [&](const int8_t* As, const uint32_t* Bs) __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < HK; ++q)
 #pragma unroll
@@ -513,37 +527,32 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
         bq[q][b] = *reinterpret_cast<const v4i*>(Bs + row * (BROW / 4) +
                                                  4 * ((HK * h + q) ^ bswz<BK>(row)));
       }
-    auto afrag = [&](int ks, int slot) __attribute__((always_inline)) {
-      const int c = (ACH / 2) * h + ks;              // logical 16-byte chunk
+    afrag(As, 0, 0);
+  };
+  auto mfmas = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
-      for (int a = 0; a < TM; ++a) {
-        const int row = arow0 + 32 * a;
-        af[slot][a] = *reinterpret_cast<const v4i*>(As + row * AROW + 16 * (c ^ aswz<BK>(row)));
-      }
-    };
-    afrag(0, 0);
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b)   // activations first, codes second: acc holds Y
+        acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[slot][a], bfc[b], acc[a][b], 0, 0, 0);
+  };
+  // sub-steps 0 .. KS-2 of a stage (reading the fragments of the next sub-step during
+  // each); the operands of sub-step KS-1 are left in af[(KS-1) & 1] and bfc
+  auto steps = [&](const int8_t* As) __attribute__((always_inline)) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) bfc[b] = unpack16_off1((uint32_t)bq[0][b][0]);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    for (int ks = 0; ks + 1 < KS; ++ks) {
       const int cur = ks & 1;
-      if (ks + 1 < KS) {
-        afrag(ks + 1, cur ^ 1);
+      afrag(As, ks + 1, cur ^ 1);
 #pragma unroll
-        for (int b = 0; b < TN; ++b) bfn[b] = unpack16_off1((uint32_t)bq[(ks + 1) / 4][b][(ks + 1) % 4]);
-      }
+      for (int b = 0; b < TN; ++b) bfn[b] = unpack16_off1((uint32_t)bq[(ks + 1) / 4][b][(ks + 1) % 4]);
+      mfmas(cur);
+      __builtin_amdgcn_sched_group_barrier(0x100, TM, 0);      // next A fragments (LDS reads)
 #pragma unroll
-      for (int a = 0; a < TM; ++a)
-#pragma unroll
-        for (int b = 0; b < TN; ++b)   // activations first, codes second: acc holds Y
-          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[cur][a], bfc[b], acc[a][b], 0, 0, 0);
-      if (ks + 1 < KS) {
-        __builtin_amdgcn_sched_group_barrier(0x100, TM, 0);      // next A fragments (LDS reads)
-#pragma unroll
-        for (int i = 0; i < TM * TN; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);     // then unpack work (VALU)
-        }
+      for (int i = 0; i < TM * TN; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);     // then unpack work (VALU)
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -559,15 +568,24 @@ __device__ __forceinline__ void gemm_tile_dma(const int8_t* __restrict__ xq,
     if (p < nk) issue(p, Ast(p), Bst(p));
   if (NST == 3 && nk > 1) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  first(Ast(0), Bst(0));
   int cur = 0;
   for (int kt = 0; kt < nk; ++kt) {
     const int nxt = cur == 0 ? NST - 1 : cur - 1;     // (kt + NST - 1) % NST
+    const int nst = cur == NST - 1 ? 0 : cur + 1;      // stage of step kt + 1
+    // the buffer of step kt - 1: every wave finished reading it before the last barrier
     if (kt + NST - 1 < nk) issue(kt + NST - 1, Ast(nxt), Bst(nxt));
-    compute(Ast(cur), Bst(cur));
+    steps(Ast(cur));
+#pragma unroll
+    for (int b = 0; b < TN; ++b)   // the last sub-step's codes unpacked before the barrier
+      asm volatile("" : "+v"(bfc[b]));
     // the loads of step kt + 1 have landed (NST = 3: those of kt + 2 may still be in flight)
     if (NST == 3 && kt + 2 < nk) wait_vmcnt_le<DJ>(); else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    cur = cur == NST - 1 ? 0 : cur + 1;
+    if (kt + 1 < nk) first(Ast(nst), Bst(nst));
+    mfmas((KS - 1) & 1);                              // the last sub-step of step kt
+    __builtin_amdgcn_sched_barrier(0);
+    cur = nst;
   }
 
   // ---- epilogue.  Each wave stages one 32-token slice (MFMA row tile a) of its
