@@ -450,6 +450,11 @@ def row_single_layer(torch, termezo, synth, dev, steps=100, warmup=5, cpu=True):
     return out
 
 
+# the two evaluations of a pair run at the same time in the timed pass (--sequential: one
+# after the other on the context's stream, as in the per-kernel timing pass)
+PAIR_STREAMS = True
+
+
 def run_decoder(torch, termezo, synth, dev, c, rho, eps, lr, steps, warmup, theta=False, K=1,
                 es=0, compact=False, calib_copy=False, keep=False):
     """The decoder step of configuration c: builds the workload, times `steps` steps
@@ -474,15 +479,25 @@ def run_decoder(torch, termezo, synth, dev, c, rho, eps, lr, steps, warmup, thet
     ctx = termezo.Context(layers)
     model = termezo.Model(ctx, c["n_blocks"], c["d_model"], c["n_heads"], c["n_kv_heads"],
                           c["d_ffn"], c["vocab"], E)
+    # the F+ evaluation of each pair: a second model on a stream of its own, reading a
+    # snapshot of the + codes while the context computes and evaluates the - side
+    pair = None
+    if K == 1 and not es and PAIR_STREAMS:
+        pair = termezo.Model(ctx, c["n_blocks"], c["d_model"], c["n_heads"], c["n_kv_heads"],
+                             c["d_ffn"], c["vocab"], E)
+        pair.set_stream(torch.cuda.Stream())
+        pair.use_snapshot(True)
     n_theta = 0
     if theta:
         NW = torch.ones((2 * c["n_blocks"] + 1, c["d_model"]), dtype=adt, device=dev)
         model.set_norm_weights(NW)
+        if pair is not None:
+            pair.set_norm_weights(NW)
         ctx.theta_register([E, NW])
         n_theta = E.numel() + NW.numel()
         log(f"theta: {n_theta} full-precision parameters perturbed and updated")
-    st = {"ctx": ctx, "model": model, "tok": tok, "lat": lat, "layers": layers, "E": E,
-          "D": D, "c": c, "n_theta": n_theta}
+    st = {"ctx": ctx, "model": model, "pair": pair, "tok": tok, "lat": lat, "layers": layers,
+          "E": E, "D": D, "c": c, "n_theta": n_theta}
     res = measure_steps(torch, st, rho, eps, lr, steps, warmup, K=K, es=es, compact=compact)
     if calib_copy:
         calibration_copy(torch, dev)
@@ -493,6 +508,8 @@ def run_decoder(torch, termezo, synth, dev, c, rho, eps, lr, steps, warmup, thet
 
 
 def close_state(torch, st):
+    if st.get("pair") is not None:
+        st["pair"].close()
     st["model"].close()
     st["ctx"].close()
     st.clear()
@@ -502,6 +519,7 @@ def close_state(torch, st):
 
 def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=False):
     ctx, model, tok, c, D = st["ctx"], st["model"], st["tok"], st["c"], st["D"]
+    pair = st.get("pair")
     fp32 = c.get("fp32", False)
     t0 = time.perf_counter()
     k0, xi0 = ctx.build_mask(rho)
@@ -542,6 +560,16 @@ def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=Fal
                 model.loss(tok, loss_dev=F[n: n + 1], host=False)
             # the losses are the rewards of the descent: -lr ascends on -loss
             timed(lambda: ctx.es_update_from_rewards(seeds, F[:es], -lr))
+            return
+        if K == 1 and pair is not None and not record[0]:
+            # F+ on the pair model's stream from the snapshot, F- on the context's stream
+            ctx.perturb(t, eps, 1)
+            ctx.codes_snapshot()
+            pair.loss(tok, loss_dev=F[0:1], host=False)
+            ctx.perturb(t, eps, -1)
+            model.loss(tok, loss_dev=F[1:2], host=False)
+            pair.join()
+            ctx.update_from_losses(F[0:1], F[1:2], eps, lr)
             return
         if K == 1:
             timed(lambda: ctx.perturb(t, eps, 1))
@@ -595,6 +623,7 @@ def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=Fal
         "ms_per_step": ms_per_step,
         "dtype": "int8xternary+f32" if fp32 else "int8xternary+bf16",
         "config": {"theta_params": st["n_theta"], "directions_per_step": es if es else K,
+                   "pair_evaluation": "two_streams" if pair is not None else "sequential",
                    "estimator": "es_one_sided" if es else "spsa_two_point",
                    "storage": "compact" if compact else "full_latents",
                    **{k: v for k, v in c.items() if k not in ("rho", "lr", "fp32")},
@@ -982,10 +1011,15 @@ def main():
     ap.add_argument("--theta", action="store_true",
                     help="also perturb and update the full-precision parameters (tied embedding and "
                          "RMSNorm weights) with the latents, as Algorithm 1 does")
+    ap.add_argument("--sequential", action="store_true",
+                    help="evaluate the two sides of each perturbation pair one after the other "
+                         "(default: the + side on a second stream from a snapshot of its codes)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the measurement, copy 1 GiB device to device (a kernel of known "
                          "traffic, for scaling hardware byte counters)")
     args = ap.parse_args()
+    global PAIR_STREAMS
+    PAIR_STREAMS = not args.sequential
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the TerMeZO step "
               "here is measured on a single MI355X", file=sys.stderr)

@@ -362,6 +362,26 @@ termezo_status termezo_model_loss(termezo_model* model, const int32_t* tokens, i
                                   int32_t seq, float* loss_dev, float* row_loss_dev,
                                   float* loss_host);
 
+/* The two evaluations of a perturbation pair, F(w + eps z) and F(w - eps z) on the
+ * same batch (Algorithm 1), depend on nothing but the pair's codes, so they may run
+ * at the same time.  termezo_codes_snapshot copies the current codes and output
+ * scales (those of the last termezo_perturb) into a library-owned buffer (allocated
+ * on the first call: 4 bytes per 16 latents plus 4 per layer), stream-ordered on the
+ * context's stream; a model set to read the snapshot (termezo_model_use_snapshot)
+ * evaluates that perturbation while the next termezo_perturb rewrites the current
+ * codes.  termezo_model_set_stream runs a model's forwards on a stream of the
+ * caller's (NULL: the context's stream, the default): each termezo_model_loss then
+ * starts after the work queued on the context's stream, and termezo_model_join
+ * makes the context's stream wait for the model's work before anything queued after
+ * it (the update that reads the losses).  A snapshot stays valid until the next
+ * snapshot; the caller orders a snapshot after the forwards that read the previous
+ * one (a join does).  Errors: INVALID_ARG (null), STATE (no current codes; a
+ * snapshot model before any snapshot), OOM, DEVICE. */
+termezo_status termezo_codes_snapshot(termezo_ctx* ctx);
+termezo_status termezo_model_set_stream(termezo_model* model, void* hip_stream);
+termezo_status termezo_model_use_snapshot(termezo_model* model, int32_t on);
+termezo_status termezo_model_join(termezo_model* model);
+
 /* Event timing of the model's matrix-core kernels, for measurement: with
  * enable != 0 every following termezo_model_loss records a HIP event pair on
  * the context's stream for each launch of class 0 (BitLinear int8 GEMM) and 2

@@ -115,6 +115,12 @@ struct termezo_ctx {
   int64_t* d_tile0 = nullptr;
   int64_t* d_tile_act = nullptr;             // T + 1
   uint32_t* d_codes = nullptr;
+  int64_t code_words = 0;            // 32-bit code words of all layers
+  // copy of the codes and output scales of one perturbation (termezo_codes_snapshot), for a
+  // forward that runs while the next perturbation rewrites the current codes
+  uint32_t* d_codes_snap = nullptr;
+  float* d_beta_snap = nullptr;
+  bool snap_valid = false;
   int64_t* d_S_clean = nullptr;
   int64_t* d_S_cur = nullptr;
   float* d_tau = nullptr;

@@ -1591,7 +1591,11 @@ using namespace tmz;
 
 struct termezo_model {
   termezo_ctx* ctx = nullptr;
-  hipStream_t stream = nullptr;   // copy of the context's stream (destroy never reads ctx)
+  hipStream_t stream = nullptr;   // the context's stream, or the model's own (destroy never reads ctx)
+  bool own_stream = false;        // forwards run on a stream of their own (ordered after the
+                                  // context's work at entry, joined back by termezo_model_join)
+  hipEvent_t ev_in = nullptr, ev_out = nullptr;
+  bool use_snap = false;          // read the context's codes snapshot instead of its current codes
   termezo_model_config cfg{};
   const void* emb = nullptr;
   const void* normw = nullptr;    // RMSNorm weights [2 n_blocks + 1][d] (null: one)
@@ -1896,8 +1900,45 @@ void termezo_model_destroy(termezo_model* m) {
     (void)hipEventDestroy(sp.a);
     (void)hipEventDestroy(sp.b);
   }
+  if (m->ev_in) (void)hipEventDestroy(m->ev_in);
+  if (m->ev_out) (void)hipEventDestroy(m->ev_out);
   model_free_buffers(m);
   delete m;
+}
+
+termezo_status termezo_model_set_stream(termezo_model* m, void* hip_stream) {
+  if (!m) return TERMEZO_ERR_INVALID_ARG;
+  termezo_ctx* c = m->ctx;
+  hipStream_t s = hip_stream ? static_cast<hipStream_t>(hip_stream) : c->stream;
+  if (s != c->stream && !m->ev_in) {
+    if (hipEventCreateWithFlags(&m->ev_in, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&m->ev_out, hipEventDisableTiming) != hipSuccess) {
+      c->last_error = "model_set_stream: event creation";
+      return TERMEZO_ERR_DEVICE;
+    }
+  }
+  if (hipStreamSynchronize(m->stream) != hipSuccess) return TERMEZO_ERR_DEVICE;
+  m->stream = s;
+  m->own_stream = s != c->stream;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_model_use_snapshot(termezo_model* m, int32_t on) {
+  if (!m) return TERMEZO_ERR_INVALID_ARG;
+  m->use_snap = on != 0;
+  return TERMEZO_OK;
+}
+
+termezo_status termezo_model_join(termezo_model* m) {
+  if (!m) return TERMEZO_ERR_INVALID_ARG;
+  if (!m->own_stream) return TERMEZO_OK;
+  termezo_ctx* c = m->ctx;
+  if (hipEventRecord(m->ev_out, m->stream) != hipSuccess ||
+      hipStreamWaitEvent(c->stream, m->ev_out, 0) != hipSuccess) {
+    c->last_error = "model_join: event record / wait";
+    return TERMEZO_ERR_DEVICE;
+  }
+  return TERMEZO_OK;
 }
 
 termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32_t batch,
@@ -1905,15 +1946,24 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
                                   float* loss_host) {
   if (!m || !tokens || batch <= 0 || seq < 2) return TERMEZO_ERR_INVALID_ARG;
   termezo_ctx* c = m->ctx;
-  if (!c->codes_valid) {
-    c->last_error = "model_loss: no current codes (perturb first)";
+  if (m->use_snap ? !c->snap_valid : !c->codes_valid) {
+    c->last_error = m->use_snap ? "model_loss: no codes snapshot" :
+                                  "model_loss: no current codes (perturb first)";
     return TERMEZO_ERR_STATE;
   }
   const termezo_model_config& cf = m->cfg;
   const int64_t M = (int64_t)batch * seq;
   termezo_status st = model_reserve(m, M, seq);
   if (st != TERMEZO_OK) return st;
-  hipStream_t s = c->stream;
+  hipStream_t s = m->stream;
+  if (m->own_stream &&   // everything queued on the context's stream so far comes first
+      (hipEventRecord(m->ev_in, c->stream) != hipSuccess ||
+       hipStreamWaitEvent(s, m->ev_in, 0) != hipSuccess)) {
+    c->last_error = "model_loss: event record / wait";
+    return TERMEZO_ERR_DEVICE;
+  }
+  const uint32_t* codes = m->use_snap ? c->d_codes_snap : c->d_codes;
+  const float* betas = m->use_snap ? c->d_beta_snap : c->d_beta_cur;
   const bool bf = cf.act_dtype == TERMEZO_BF16;
   // full-precision parameters: a registered theta tensor is read at its current
   // (possibly perturbed) values
@@ -1974,11 +2024,11 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     rmsq(m->xq, m->xs, nullptr, 2 * blk);
     GemmOut o3 = {};
     o3.nseg = 3;
-    o3.y[0] = m->q; o3.ld[0] = dq; o3.beta[0] = c->d_beta_cur + l0;
-    o3.y[1] = m->k; o3.ld[1] = dkv; o3.beta[1] = c->d_beta_cur + l0 + 1;
-    o3.y[2] = m->v; o3.ld[2] = dkv; o3.beta[2] = c->d_beta_cur + l0 + 2;
+    o3.y[0] = m->q; o3.ld[0] = dq; o3.beta[0] = betas + l0;
+    o3.y[1] = m->k; o3.ld[1] = dkv; o3.beta[1] = betas + l0 + 1;
+    o3.y[2] = m->v; o3.ld[2] = dkv; o3.beta[2] = betas + l0 + 2;
     o3.nstart[0] = 0; o3.nstart[1] = dq; o3.nstart[2] = dq + dkv; o3.nstart[3] = dq + 2 * dkv;
-    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, codes + Ls[0].code_off, M, d, dq + 2 * dkv, o3, adt,
                        kGemmStore, nullptr, c->n_cu, s,
                        span_kernel(m, 0, 2.0 * M * d * (dq + 2 * dkv))));
     if (!bf) {   // bf16: the rotation is applied inside the attention kernel
@@ -2003,22 +2053,22 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     chk(hipGetLastError());
     GemmOut oo = {};
     oo.nseg = 1;
-    oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = c->d_beta_cur + l0 + 3;
+    oo.y[0] = m->h; oo.ld[0] = d; oo.beta[0] = betas + l0 + 3;
     oo.nstart[0] = 0; oo.nstart[1] = d;
-    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, codes + Ls[3].code_off, M, dq, d, oo, adt, kGemmResidual,
                        nullptr, c->n_cu, s,
                        span_kernel(m, 0, 2.0 * M * dq * d)));
     // MLP sub-block
     rmsq(m->xq, m->xs, nullptr, 2 * blk + 1);
     GemmOut o2 = {};
     o2.nseg = 2;
-    o2.y[0] = m->g; o2.ld[0] = F; o2.beta[0] = c->d_beta_cur + l0 + 4;
-    o2.y[1] = m->u; o2.ld[1] = F; o2.beta[1] = c->d_beta_cur + l0 + 5;
+    o2.y[0] = m->g; o2.ld[0] = F; o2.beta[0] = betas + l0 + 4;
+    o2.y[1] = m->u; o2.ld[1] = F; o2.beta[1] = betas + l0 + 5;
     o2.nstart[0] = 0; o2.nstart[1] = F; o2.nstart[2] = 2 * F;
     // gate|up with the SwiGLU in the epilogue where the full-tile path applies (the
     // product lands in g), else the two projections and the SwiGLU row kernel
     const bool fused = gemm_swiglu_ok(M, d, 2 * F, adt);
-    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[4].code_off, M, d, 2 * F, o2, adt,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, codes + Ls[4].code_off, M, d, 2 * F, o2, adt,
                        fused ? kGemmSwiGLU : kGemmStore, nullptr, c->n_cu, s,
                        span_kernel(m, 0, 2.0 * M * d * 2 * F)));
     if (fused)
@@ -2033,9 +2083,9 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     chk(hipGetLastError());
     GemmOut od = {};
     od.nseg = 1;
-    od.y[0] = m->h; od.ld[0] = d; od.beta[0] = c->d_beta_cur + l0 + 6;
+    od.y[0] = m->h; od.ld[0] = d; od.beta[0] = betas + l0 + 6;
     od.nstart[0] = 0; od.nstart[1] = d;
-    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, c->d_codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
+    chk(launch_gemm_i8(m->xq, m->xs, m->xrs, codes + Ls[6].code_off, M, F, d, od, adt, kGemmResidual,
                        nullptr, c->n_cu, s,
                        span_kernel(m, 0, 2.0 * M * F * d)));
   }
@@ -2072,6 +2122,7 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
     double v = 0.0;
     if (hipMemcpyAsync(&v, m->loss64, 8, hipMemcpyDeviceToHost, s) != hipSuccess)
       return TERMEZO_ERR_DEVICE;
+    if (m->own_stream && hipStreamSynchronize(s) != hipSuccess) return TERMEZO_ERR_DEVICE;
     const termezo_status ds = termezo_sync(c);     // waits; reports deferred errors
     if (ds != TERMEZO_OK) return ds;
     *loss_host = (float)v;

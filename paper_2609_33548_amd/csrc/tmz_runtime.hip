@@ -171,6 +171,8 @@ void free_all(termezo_ctx* c) {
   dfree(c->d_tile0);
   dfree(c->d_tile_act);
   dfree(c->d_codes);
+  dfree(c->d_codes_snap);
+  dfree(c->d_beta_snap);
   dfree(c->d_S_clean);
   dfree(c->d_S_cur);
   dfree(c->d_S_alt);
@@ -272,6 +274,7 @@ termezo_status termezo_create(const termezo_layer* layers, int32_t n_layers,
   }
   c->D = D;
   c->T = (int64_t)tile_layer.size();
+  c->code_words = words;
 
   termezo_status st = TERMEZO_OK;
   auto chk = [&](hipError_t e, const char* what) {
@@ -896,6 +899,24 @@ termezo_status termezo_codes_export(termezo_ctx* c, int32_t layer, int8_t* codes
   (void)hipFree(tmp);
   if (e != hipSuccess) return hip_fail(c, e, "codes export");
   return sync_and_check(c);
+}
+
+termezo_status termezo_codes_snapshot(termezo_ctx* c) {
+  if (!c) return TERMEZO_ERR_INVALID_ARG;
+  if (!c->codes_valid) return fail(c, TERMEZO_ERR_STATE, "codes_snapshot: no current codes");
+  if (!c->d_codes_snap) {
+    TMZ_HIP(c, dalloc(&c->d_codes_snap, (size_t)c->code_words));
+    if (dalloc(&c->d_beta_snap, (size_t)c->L) != hipSuccess) {
+      dfree(c->d_codes_snap);
+      return fail(c, TERMEZO_ERR_OOM, "codes_snapshot: allocation");
+    }
+  }
+  TMZ_HIP(c, hipMemcpyAsync(c->d_codes_snap, c->d_codes, (size_t)c->code_words * 4,
+                            hipMemcpyDeviceToDevice, c->stream));
+  TMZ_HIP(c, hipMemcpyAsync(c->d_beta_snap, c->d_beta_cur, (size_t)c->L * 4,
+                            hipMemcpyDeviceToDevice, c->stream));
+  c->snap_valid = true;
+  return TERMEZO_OK;
 }
 
 termezo_status termezo_layer_stats(termezo_ctx* c, int32_t layer, float* tau, float* beta,

@@ -89,6 +89,10 @@ _SIGS = {
     "termezo_model_set_timing": [_P, _i32],
     "termezo_model_timing": [_P, _i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64),
                              ctypes.POINTER(ctypes.c_double)],
+    "termezo_codes_snapshot": [_P],
+    "termezo_model_set_stream": [_P, _P],
+    "termezo_model_use_snapshot": [_P, _i32],
+    "termezo_model_join": [_P],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -345,6 +349,10 @@ class Context:
                                                         int(bool(standardize))),
                     "es_update_from_rewards")
 
+    def codes_snapshot(self):
+        """Copy the current codes and output scales into the library's snapshot (no wait)."""
+        self._check(_lib.termezo_codes_snapshot(self.handle), "codes_snapshot")
+
     def mse_loss(self, y, target) -> float:
         out = _f32()
         self._check(_lib.termezo_mse_loss(self.handle, _ptr(y), _ptr(target), y.numel(),
@@ -391,6 +399,18 @@ class Model:
                                      _ptr(row_loss_dev), ctypes.byref(out) if host else None)
         self.ctx._check(st, "model_loss")
         return float(np.float32(out.value)) if host else None
+
+    def set_stream(self, stream):
+        """Run this model's forwards on ``stream`` (a torch stream; None: the context's)."""
+        self.stream = stream                      # kept alive with the model
+        self.ctx._check(_lib.termezo_model_set_stream(
+            self.handle, None if stream is None else int(stream.cuda_stream)), "model_set_stream")
+
+    def use_snapshot(self, on: bool):
+        self.ctx._check(_lib.termezo_model_use_snapshot(self.handle, int(on)), "model_use_snapshot")
+
+    def join(self):
+        self.ctx._check(_lib.termezo_model_join(self.handle), "model_join")
 
     GEMM, ATTENTION, LM_HEAD = 0, 1, 2
 

@@ -206,3 +206,66 @@ def test_out_of_range_token_ids_are_reported(orc):
         assert model.loss(tokd) == clean
     model.close()
     ctx.close()
+
+
+def test_pair_forwards_on_two_streams_match_sequential(orc):
+    """F(w + eps z) evaluated on a second stream from a snapshot of its codes while the
+    context computes and evaluates w - eps z (Algorithm 1's two evaluations of a pair
+    run at the same time) gives the losses of the sequential order bit for bit, and the
+    same latents after three updates; a snapshot model before any snapshot is refused."""
+    torch = _torch()
+    from oracle import decoder_ref as dec
+    from paper_2609_33548_amd import termezo
+    cfg = dec.DecoderConfig(n_blocks=2, d_model=256, n_heads=2, n_kv_heads=1, d_ffn=256, vocab=512,
+                            bf16=True)
+    B, S = 2, 128
+    _, ctx, model, tensors, _, E, _, tokd = _build(orc, dec, cfg, 41, B, S)
+    tensors2 = [t.clone() for t in tensors]
+    ctx2 = termezo.Context(tensors2)
+    m_main = termezo.Model(ctx2, cfg.n_blocks, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.d_ffn,
+                           cfg.vocab, E)
+    m_pair = termezo.Model(ctx2, cfg.n_blocks, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.d_ffn,
+                           cfg.vocab, E)
+    side = torch.cuda.Stream()
+    m_pair.set_stream(side)
+    m_pair.use_snapshot(True)
+    assert ctx.build_mask(0.01) == ctx2.build_mask(0.01)
+    Fs, Fc = torch.zeros(2, device="cuda"), torch.zeros(2, device="cuda")
+    eps, lr = 1e-3, 5e-2
+    for t in range(3):
+        print(f"  pair step {t}", flush=True)
+        ctx.perturb(t, eps, 1)
+        model.loss(tokd, loss_dev=Fs[0:1], host=False)
+        ctx.perturb(t, eps, -1)
+        model.loss(tokd, loss_dev=Fs[1:2], host=False)
+        ctx.update_from_losses(Fs[0:1], Fs[1:2], eps, lr)
+
+        ctx2.perturb(t, eps, 1)
+        ctx2.codes_snapshot()
+        m_pair.loss(tokd, loss_dev=Fc[0:1], host=False)
+        ctx2.perturb(t, eps, -1)
+        m_main.loss(tokd, loss_dev=Fc[1:2], host=False)
+        m_pair.join()
+        ctx2.update_from_losses(Fc[0:1], Fc[1:2], eps, lr)
+        torch.cuda.synchronize()
+        assert torch.equal(Fs.view(torch.int32), Fc.view(torch.int32)), (Fs.tolist(), Fc.tolist())
+        assert Fs[0] != Fs[1]
+    ctx.sync()
+    ctx2.sync()
+    for a, b in zip(tensors, tensors2):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    for m in (m_pair, m_main, model):
+        m.close()
+    ctx2.close()
+    ctx.close()
+    ctx3 = termezo.Context(tensors2)
+    m3 = termezo.Model(ctx3, cfg.n_blocks, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.d_ffn,
+                       cfg.vocab, E)
+    m3.use_snapshot(True)
+    ctx3.build_mask(0.01)
+    ctx3.perturb(0, eps, 1)
+    with pytest.raises(termezo.TermezoError) as e:
+        m3.loss(tokd)                          # no snapshot taken on this context
+    assert e.value.status == termezo.ERR_STATE
+    m3.close()
+    ctx3.close()
