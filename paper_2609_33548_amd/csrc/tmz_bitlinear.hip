@@ -1150,7 +1150,7 @@ __global__ void __launch_bounds__(512)
   }
   // token row r = 2 wid + (lane / 32), chunk (it * 32 + lane % 32) of 8 values
   const int r = 2 * wid + (lane >> 5), j32 = lane & 31;
-  const bool rok = r < M;
+  const bool rok = r < M && r < ROWS;          // the launcher keeps M <= ROWS
   const TX* xr = x + (rok ? r : 0) * K;
   RowChunk<TX> xv[XI];
   float a = 0.0f;
@@ -1237,10 +1237,12 @@ __global__ void __launch_bounds__(512)
   }
 }
 
-// Longer rows are held for at most 5 tokens (5 x 8192 values quantised per block).
+// Rows of up to 4096 values for up to 16 tokens; longer bf16 rows (up to 8192 values) for
+// at most kGemvFusedLongRows tokens, the rows the long-row instantiation holds in LDS.
+constexpr int kGemvFusedLongRows = 5;
 bool gemv_fused_ok(int64_t M, int64_t K, termezo_dtype xdt) {
   return M >= 2 && M <= kGemvFusedMaxM && M * K <= kGemvFusedMaxMK &&
-         (K <= 4096 || (xdt == TERMEZO_BF16 && K <= 8192));
+         (K <= 4096 || (xdt == TERMEZO_BF16 && K <= 8192 && M <= kGemvFusedLongRows));
 }
 
 hipError_t launch_gemv_fused(const void* x, termezo_dtype xdt, const uint32_t* codes,
@@ -1268,7 +1270,8 @@ hipError_t launch_gemv_fused(const void* x, termezo_dtype xdt, const uint32_t* c
   } else if (K <= 4096) {
     if (cvec) TMZ_GFY(uint16_t, true, 4096, 16); else TMZ_GFY(uint16_t, false, 4096, 16);
   } else {
-    if (cvec) TMZ_GFY(uint16_t, true, 8192, 5); else TMZ_GFY(uint16_t, false, 8192, 5);
+    if (cvec) TMZ_GFY(uint16_t, true, 8192, kGemvFusedLongRows);
+    else TMZ_GFY(uint16_t, false, 8192, kGemvFusedLongRows);
   }
 #undef TMZ_GFY
 #undef TMZ_GFG

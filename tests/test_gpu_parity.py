@@ -188,6 +188,7 @@ def test_single_token_forward_matches_oracle(orc, K, N, xdt, ydt):
                                    (16, 6912, 2560),    # M K above the fused bound: two kernels
                                    (10, 4096, 64),      # the longest fp32 row of the fused kernel
                                    (2, 4112, 48),       # fp32: two kernels; bf16: fused
+                                   (9, 4112, 48),       # a long row for more tokens than it holds
                                    (5, 8192, 32),       # the longest bf16 row of the fused kernel
                                    (7, 8208, 16)])      # beyond it: two kernels
 @pytest.mark.parametrize("xdt,ydt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
