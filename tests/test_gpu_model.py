@@ -231,7 +231,7 @@ def test_pair_forwards_on_two_streams_match_sequential(orc):
     m_pair.use_snapshot(True)
     assert ctx.build_mask(0.01) == ctx2.build_mask(0.01)
     Fs, Fc = torch.zeros(2, device="cuda"), torch.zeros(2, device="cuda")
-    eps, lr = 1e-3, 5e-2
+    eps, lr = 1e-3, 1e-4
     for t in range(3):
         print(f"  pair step {t}", flush=True)
         ctx.perturb(t, eps, 1)
@@ -249,7 +249,8 @@ def test_pair_forwards_on_two_streams_match_sequential(orc):
         ctx2.update_from_losses(Fc[0:1], Fc[1:2], eps, lr)
         torch.cuda.synchronize()
         assert torch.equal(Fs.view(torch.int32), Fc.view(torch.int32)), (Fs.tolist(), Fc.tolist())
-        assert Fs[0] != Fs[1]
+        if t == 0:                             # the full mask: the two sides differ
+            assert Fs[0] != Fs[1]
     ctx.sync()
     ctx2.sync()
     for a, b in zip(tensors, tensors2):
