@@ -208,11 +208,13 @@ def test_out_of_range_token_ids_are_reported(orc):
     ctx.close()
 
 
-def test_pair_forwards_on_two_streams_match_sequential(orc):
+@pytest.mark.parametrize("theta", [False, True])
+def test_pair_forwards_on_two_streams_match_sequential(orc, theta):
     """F(w + eps z) evaluated on a second stream from a snapshot of its codes while the
     context computes and evaluates w - eps z (Algorithm 1's two evaluations of a pair
     run at the same time) gives the losses of the sequential order bit for bit, and the
-    same latents after three updates; a snapshot model before any snapshot is refused."""
+    same latents (and theta: embedding and RMSNorm weights, when registered) after three
+    updates; a snapshot model before any snapshot is refused."""
     torch = _torch()
     from oracle import decoder_ref as dec
     from paper_2609_33548_amd import termezo
@@ -222,10 +224,23 @@ def test_pair_forwards_on_two_streams_match_sequential(orc):
     _, ctx, model, tensors, _, E, _, tokd = _build(orc, dec, cfg, 41, B, S)
     tensors2 = [t.clone() for t in tensors]
     ctx2 = termezo.Context(tensors2)
+    E2 = E.clone()
     m_main = termezo.Model(ctx2, cfg.n_blocks, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.d_ffn,
-                           cfg.vocab, E)
+                           cfg.vocab, E2)
     m_pair = termezo.Model(ctx2, cfg.n_blocks, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.d_ffn,
-                           cfg.vocab, E)
+                           cfg.vocab, E2)
+    th1 = th2 = None
+    if theta:
+        NW = torch.from_numpy(synth.latents(45, [(2 * cfg.n_blocks + 1) * cfg.d_model], bf16=True)
+                              ).cuda().to(torch.bfloat16).view(2 * cfg.n_blocks + 1, cfg.d_model) + 1.0
+        NW2 = NW.clone()
+        model.set_norm_weights(NW)
+        m_main.set_norm_weights(NW2)
+        m_pair.set_norm_weights(NW2)
+        th1, th2 = [E, NW], [E2, NW2]
+        E0 = E.clone()
+        ctx.theta_register(th1)
+        ctx2.theta_register(th2)
     side = torch.cuda.Stream()
     m_pair.set_stream(side)
     m_pair.use_snapshot(True)
@@ -255,6 +270,10 @@ def test_pair_forwards_on_two_streams_match_sequential(orc):
     ctx2.sync()
     for a, b in zip(tensors, tensors2):
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    if theta:
+        for a, b in zip(th1, th2):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        assert not torch.equal(E.view(torch.int16), E0.view(torch.int16))   # theta was updated
     for m in (m_pair, m_main, model):
         m.close()
     ctx2.close()
