@@ -614,6 +614,7 @@ def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=Fal
     model.set_timing(False)
     latent_ms = sum(a.elapsed_time(b) for a, b in lat_ev) / steps
     k_final = ctx.active_count()
+    lib_s, _ = ctx.memory_footprint()   # while stepping: the codes snapshot of the pair included
     gemm_tops = g_ops / (g_ms * 1e-3) / 1e12
     log(f"gemm {g_n} launches, {g_ms / g_n * 1e3:.1f} us avg, {gemm_tops:.1f} TOP/s; attention "
         f"{a_ms / max(1, a_n) * 1e3:.1f} us avg; lm head {h_ms / max(1, h_n) * 1e3:.1f} us avg; "
@@ -646,8 +647,8 @@ def measure_steps(torch, st, rho, eps, lr, steps, warmup, K=1, es=0, compact=Fal
         "attention_tflops": a_ops / (a_ms * 1e-3) / 1e12 if a_ms else None,
         "lm_head_tflops": h_ops / (h_ms * 1e-3) / 1e12 if h_ms else None,
         "mask_build_ms": mask_ms,
-        "memory": {"library_bytes": lib_b, "latent_bytes_needed": lat_b,
-                   "method_state_bytes": lib_b + lat_b,
+        "memory": {"library_bytes": lib_s, "library_bytes_after_mask_build": lib_b,
+                   "latent_bytes_needed": lat_b, "method_state_bytes": lib_s + lat_b,
                    "eq_memory_latent_side_bytes": int(eq_mem),
                    "torch_allocated_bytes": int(torch.cuda.memory_allocated())},
     }

@@ -214,8 +214,9 @@ termezo_status termezo_active_values(termezo_ctx* ctx, int32_t layer, float* val
 /* Device memory of the method's state (host values, nullable): library_bytes =
  * the library-owned buffers (codes, mask lists, thresholds, tile tables, the
  * list-order copy of the active latents -- kept for sets of at most 1/8 of the
- * latents and in compact mode --, theta copies, scratch); latent_bytes = the
- * caller's latent tensors the context still needs (0 in compact mode). */
+ * latents and in compact mode --, theta copies, the codes snapshot once taken,
+ * scratch); latent_bytes = the caller's latent tensors the context still needs
+ * (0 in compact mode). */
 termezo_status termezo_memory_footprint(termezo_ctx* ctx, int64_t* library_bytes,
                                         int64_t* latent_bytes);
 

@@ -772,6 +772,7 @@ termezo_status termezo_memory_footprint(termezo_ctx* c, int64_t* library_bytes,
   b += (int64_t)kHistBins * 8 + (int64_t)sizeof(SelectState) + 4 * 8 + kScalLen * 4 + 4;
   b += c->xq_cap + c->xs_cap * 8;                                // activation-quant scratch
   for (const ThetaHost& t : c->theta) b += 2 * t.n * (int64_t)dtype_size(t.dtype);
+  if (c->d_codes_snap) b += c->code_words * 4 + L * 4;               // codes snapshot
   if (library_bytes) *library_bytes = b;
   if (latent_bytes) *latent_bytes = c->compact ? 0 : c->D * dsz;
   return TERMEZO_OK;
