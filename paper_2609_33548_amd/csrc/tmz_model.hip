@@ -1381,8 +1381,9 @@ __global__ void __launch_bounds__(128 * NWN) k_lmhead_dma(const uint16_t* __rest
   constexpr int KS = CPR / 2;                     // MFMA sub-steps per stage
   constexpr int IPW = BM * CPR / NT;              // loads per operand per wave per stage
   static_assert(CPR == 8 || CPR == 4, "stage width");
-  static_assert(STAGES >= 2 && STAGES * 2 * OPB <= 152 * 1024, "LDS");
+  static_assert(STAGES >= 2 && STAGES * 2 * OPB + BN / WN * BM * 8 <= 152 * 1024, "LDS");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES * 2 * OPB];
+  __shared__ float red[BN / WN][BM][2];           // per wave column: token max and sum of exp
   __shared__ int32_t lbl[BM];
   auto sw = [](int row) __attribute__((always_inline)) {
     return CPR == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
@@ -1390,11 +1391,8 @@ __global__ void __launch_bounds__(128 * NWN) k_lmhead_dma(const uint16_t* __rest
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid / (BN / WN), wn = wid % (BN / WN);
-  int64_t tm, tn;
-  tile_of_block(M / BM, nvt, tm, tn);
-  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t ntiles = (M / BM) * nvt;
   const int nk = (int)(d / BK);
-  for (int i = tid; i < BM; i += NT) lbl[i] = labels[m0 + i];
 
   // load j of wave w fills the 64 LDS chunks (w * IPW + j) * 64 .. + 63 of an operand:
   // RPL rows of CPR chunks.  The chunk swizzle of those rows depends on j only through
@@ -1404,12 +1402,19 @@ __global__ void __launch_bounds__(128 * NWN) k_lmhead_dma(const uint16_t* __rest
   static_assert(IPW % 2 == 0, "loads per wave");
   const uint8_t* asrc[2];
   const uint8_t* bsrc[2];
+  // tile it of the grouped (XCD-aware) order: its origin and the load sources
+  auto tile = [&](int64_t it, int64_t& m0, int64_t& n0) __attribute__((always_inline)) {
+    int64_t tm, tn;
+    tile_of_linear(xcd_linear(it, ntiles), M / BM, nvt, tm, tn);
+    m0 = tm * BM;
+    n0 = tn * BN;
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const int row = (wid * IPW + p) * RPL + lane / CPR, lc = (lane % CPR) ^ sw(row);
-    asrc[p] = reinterpret_cast<const uint8_t*>(x) + (m0 + row) * d * 2 + 16 * lc;
-    bsrc[p] = reinterpret_cast<const uint8_t*>(E) + (n0 + row) * d * 2 + 16 * lc;
-  }
+    for (int p = 0; p < 2; ++p) {
+      const int row = (wid * IPW + p) * RPL + lane / CPR, lc = (lane % CPR) ^ sw(row);
+      asrc[p] = reinterpret_cast<const uint8_t*>(x) + (m0 + row) * d * 2 + 16 * lc;
+      bsrc[p] = reinterpret_cast<const uint8_t*>(E) + (n0 + row) * d * 2 + 16 * lc;
+    }
+  };
   const uint32_t wbase = __builtin_amdgcn_readfirstlane(wid) * IPW * 1024u;
   auto Ast = [&](int st) { return lds + st * 2 * OPB; };
   auto issue = [&](int kt, int st) __attribute__((always_inline)) {
@@ -1423,17 +1428,10 @@ __global__ void __launch_bounds__(128 * NWN) k_lmhead_dma(const uint16_t* __rest
     }
   };
 
-  v16f acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
-
   typedef uint32_t v4u __attribute__((ext_vector_type(4)));
   const int h = lane >> 5;
   const int arow0 = wm * WM + (lane & 31), brow0 = wn * WN + (lane & 31);
+  v16f acc[TM][TN];
   auto compute = [&](const uint8_t* As, const uint8_t* Bs) __attribute__((always_inline)) {
     v8bf af[2][TM], bfr[2][TN];
     auto frag = [&](int ks, int slot) __attribute__((always_inline)) {
@@ -1466,60 +1464,91 @@ __global__ void __launch_bounds__(128 * NWN) k_lmhead_dma(const uint16_t* __rest
     }
   };
 
-  // prologue: STAGES - 1 stages in flight, stage 0 complete
+  // Blocks walk the tiles it = blockIdx.x, + gridDim.x, ...  The first stages of the next
+  // tile are issued right after the last barrier of the current one (the ring is free
+  // then), so their loads land while the current tile's epilogue runs.
+  int64_t it = blockIdx.x;
+  if (it >= ntiles) return;                       // whole block
+  int64_t m0, n0;
+  tile(it, m0, n0);
+  for (int i = tid; i < BM; i += NT) lbl[i] = labels[m0 + i];
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < nk) issue(st, st);
-  if (nk >= STAGES - 1) wait_vmcnt_le<(STAGES - 2) * 2 * IPW>(); else __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt % STAGES;
-    const bool more = kt + STAGES - 1 < nk;
-    if (more) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);   // the stage freed at kt-1
-    compute(Ast(st), Ast(st) + OPB);
-    if (more) wait_vmcnt_le<(STAGES - 2) * 2 * IPW>(); else __builtin_amdgcn_s_waitcnt(0);
+  while (true) {
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+    // prologue: stages 0 .. STAGES-2 issued, stage 0 complete
+    if (nk >= STAGES - 1) wait_vmcnt_le<(STAGES - 2) * 2 * IPW>(); else __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-  }
-
-  // ---- epilogue: per token, max and sum of exp over the block's 256 columns ----
-  float* red = reinterpret_cast<float*>(lds);     // [4 waves along N][BM][2]
-  const float L2E = 1.4426950408889634f;
-#pragma unroll
-  for (int a = 0; a < TM; ++a) {
-    const int li = wm * WM + 32 * a + (lane & 31);
-    const int lb = lbl[li];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[a][b][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float se = 0.0f;
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        se += __builtin_amdgcn_exp2f((acc[a][b][r] - mx) * L2E);
-        const int64_t col = n0 + wn * WN + 32 * b + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (col == lb) lab[m0 + li] = acc[a][b][r];
-      }
-    se += __shfl_xor(se, 32, 64);
-    if (h == 0) {
-      red[(wn * BM + li) * 2 + 0] = mx;
-      red[(wn * BM + li) * 2 + 1] = se;
+    for (int kt = 0; kt < nk; ++kt) {
+      const int st = kt % STAGES;
+      const bool more = kt + STAGES - 1 < nk;
+      if (more) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);   // the stage freed at kt-1
+      compute(Ast(st), Ast(st) + OPB);
+      if (more) wait_vmcnt_le<(STAGES - 2) * 2 * IPW>(); else __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
     }
-  }
-  __syncthreads();
-  if (tid < BM) {
-    float mx = -INFINITY;
+    const int64_t cm0 = m0, cn0 = n0, ctn = cn0 / BN;
+    const int64_t nit = it + gridDim.x;
+    if (nit < ntiles) {                           // next tile's first stages
+      tile(nit, m0, n0);
 #pragma unroll
-    for (int w = 0; w < BN / WN; ++w) mx = fmaxf(mx, red[(w * BM + tid) * 2]);
-    float se = 0.0f;
+      for (int st = 0; st < STAGES - 1; ++st)
+        if (st < nk) issue(st, st);
+    }
+
+    // ---- epilogue: per token, max and sum of exp over the block's 256 columns ----
+    const float L2E = 1.4426950408889634f;
 #pragma unroll
-    for (int w = 0; w < BN / WN; ++w)
-      se += red[(w * BM + tid) * 2 + 1] * __builtin_amdgcn_exp2f((red[(w * BM + tid) * 2] - mx) * L2E);
-    pmax[(m0 + tid) * nvt + tn] = mx;
-    psum[(m0 + tid) * nvt + tn] = se;
+    for (int a = 0; a < TM; ++a) {
+      const int li = wm * WM + 32 * a + (lane & 31);
+      const int lb = lbl[li];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[a][b][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float se = 0.0f;
+#pragma unroll
+      for (int b = 0; b < TN; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          se += __builtin_amdgcn_exp2f((acc[a][b][r] - mx) * L2E);
+          const int64_t col = cn0 + wn * WN + 32 * b + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (col == lb) lab[cm0 + li] = acc[a][b][r];
+        }
+      se += __shfl_xor(se, 32, 64);
+      if (h == 0) {
+        red[wn][li][0] = mx;
+        red[wn][li][1] = se;
+      }
+    }
+    __syncthreads();
+    if (tid < BM) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < BN / WN; ++w) mx = fmaxf(mx, red[w][tid][0]);
+      float se = 0.0f;
+#pragma unroll
+      for (int w = 0; w < BN / WN; ++w)
+        se += red[w][tid][1] * __builtin_amdgcn_exp2f((red[w][tid][0] - mx) * L2E);
+      pmax[(cm0 + tid) * nvt + ctn] = mx;
+      psum[(cm0 + tid) * nvt + ctn] = se;
+    }
+    if (nit >= ntiles) break;
+    it = nit;
+    // the load sources again (computed afresh rather than held through the epilogue)
+    int64_t itr = it;
+    asm volatile("" : "+s"(itr));
+    tile(itr, m0, n0);
+    __syncthreads();                              // red and lbl read by every wave
+    for (int i = tid; i < BM; i += NT) lbl[i] = labels[m0 + i];
   }
 }
 
@@ -2093,8 +2122,10 @@ termezo_status termezo_model_loss(termezo_model* m, const int32_t* tokens, int32
   const LaunchEvents ev_lm = span_kernel(m, 2, 2.0 * M * d * cf.vocab);
   if (bf) {
     const unsigned nb = (unsigned)(nvt * ((M + kLmTile - 1) / kLmTile));
+    // the direct-load kernel walks its tiles with one block per compute unit
+    const unsigned nbp = c->n_cu > 0 && nb > (unsigned)c->n_cu ? (unsigned)c->n_cu : nb;
     if (M % kLmTile == 0 && cf.vocab % kLmTile == 0 && d % 64 == 0)
-      hipExtLaunchKernelGGL((k_lmhead_dma<kLmDmaStages, kLmDmaBK, kLmDmaNWN>), dim3(nb),
+      hipExtLaunchKernelGGL((k_lmhead_dma<kLmDmaStages, kLmDmaBK, kLmDmaNWN>), dim3(nbp),
                             dim3(128 * kLmDmaNWN), 0, s, ev_lm.start, ev_lm.stop, 0,
                             (const uint16_t*)m->xf, (const uint16_t*)emb, M, d, (int64_t)cf.vocab,
                             m->labels, m->pmax, m->psum, m->lab, nvt);
